@@ -1,0 +1,349 @@
+"""Oracle for one ProxyFormer layer: forward (Algorithm 1) and backward.
+
+Test infrastructure only (see the package docstring). All arithmetic is
+float64 numpy; matrix products use ``@`` as a library primitive.
+
+Notation: a linear map is y = x W^T + b with W stored [out, in]. d_0 is the
+local-stream width d_fine, d_M the proxy width d_proxy, R_j = L/(k_1...k_j)
+and m = R_M = L/P the number of proxies (Sec. 3.1, Eq. 15).
+
+Readings of points the paper leaves open (each is also a flag or default of
+the C-ABI):
+* Causality of the injection. Algorithm 1 injects the contextualised proxy
+  of block i into block i. Under the causal proxy mask of Eq. 9 a token
+  would then see later tokens of its own block, while the language model
+  only needs block causality (Sec. 3.7). TOKEN_CAUSAL (default) injects
+  the proxy of block i-1 into block i and zero into block 0, so token t
+  depends only on tokens <= t; BLOCK_CAUSAL is the literal reading
+  (block i gets proxy i, causal proxy mask); BIDIRECTIONAL sets M = 0.
+* The interaction F of Eq. 9 is multi-head attention with Q/K/V/O linear
+  maps (with biases), heads taking contiguous column slices of width
+  d_head, scale 1/sqrt(d_head), masked entries excluded, no positional
+  encoding (NoPE, Sec. 5.1), no norm or residual inside F.
+* The proxy stream returned by Algorithm 1 is H after the update of Eq. 8
+  (before interaction).
+* Flatten / grouping order: token-major, so grouping k consecutive rows of
+  a row-major [R, d] matrix is a zero-copy reshape to [R/k, k*d].
+* C and D are shared across blocks (and across groups of a level).
+* The gate g of Eq. 12 is a d_fine-wide linear map of the concatenation
+  [X, Delta]: G = X W_gx^T + Delta W_gd^T + b_g with W_g = [W_gx | W_gd].
+* Intermediate level widths d_j default to d_proxy; there is no
+  non-linearity between levels (the cascade is reshape -> project).
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+TOKEN_CAUSAL = 0
+BLOCK_CAUSAL = 1
+BIDIRECTIONAL = 2
+
+_ROW_CHUNK = 512  # query rows per chunk; rows are independent (Eq. 9)
+
+
+def _f64(a):
+    return None if a is None else np.asarray(a, dtype=np.float64)
+
+
+def sigmoid(z):
+    """Logistic function sigma(z) = 1 / (1 + exp(-z)), evaluated without overflow."""
+    z = np.asarray(z, dtype=np.float64)
+    out = np.empty_like(z)
+    pos = z >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-z[pos]))
+    e = np.exp(z[~pos])
+    out[~pos] = e / (1.0 + e)
+    return out
+
+
+def linear(x, w, b):
+    """y = x W^T + b (W stored [out, in]; b may be None)."""
+    y = x @ _f64(w).T
+    if b is not None:
+        y = y + _f64(b)
+    return y
+
+
+def group_rows(z, k: int):
+    """Partition of Eq. 2 / grouping step of Eq. 16.
+
+    Groups k consecutive rows of z [R*k, d] and concatenates their channels:
+    out[r, q*d + c] = z[r*k + q, c]. For row-major storage this index map is
+    exactly a reshape.
+    """
+    rows, d = z.shape
+    if rows % k:
+        raise ValueError("row count must be a multiple of the group factor")
+    return z.reshape(rows // k, k * d)
+
+
+def ungroup_rows(t, k: int):
+    """Unflatten of Eq. 10 / the reverse reshape of Eq. 17.
+
+    out[r*k + q, c] = t[r, q*d + c] for t [R, k*d].
+    """
+    rows, kd = t.shape
+    return t.reshape(rows * k, kd // k)
+
+
+def compress(x, factors: Sequence[int], comp):
+    """Bottom-up compression C of one sequence (Eq. 7; cascade of Eq. 16).
+
+    x: [L, d_0]. comp: list of (W_cj [d_j, k_j d_{j-1}], b_cj) for j = 1..M.
+    Level j groups k_j consecutive rows of Z_{j-1} and projects them:
+    Z_j = group(Z_{j-1}, k_j) W_cj^T + b_cj. Returns c = Z_M [L/P, d_M] and the
+    list of level inputs group(Z_{j-1}, k_j) (needed by the backward).
+    """
+    z = _f64(x)
+    inputs = []
+    for k, (w, b) in zip(factors, comp):
+        v = group_rows(z, k)
+        inputs.append(v)
+        z = linear(v, w, b)
+    return z, inputs
+
+
+def decompress(s, factors: Sequence[int], dec):
+    """Top-down decompression D = D_1 o ... o D_M of proxy rows (Eq. 10, Eq. 17).
+
+    s: [R_M, d_M]. dec: list of (W_dj [k_j d_{j-1}, d_j], b_dj) for j = 1..M.
+    Level j (applied for j = M down to 1) projects U_j up to k_j d_{j-1}
+    channels and unflattens to k_j rows: U_{j-1} = ungroup(U_j W_dj^T + b_dj).
+    Returns Delta = U_0 and the list of level inputs [U_M, ..., U_1].
+    """
+    u = _f64(s)
+    inputs = []
+    for j in reversed(range(len(factors))):
+        w, b = dec[j]
+        inputs.append(u)
+        u = ungroup_rows(linear(u, w, b), factors[j])
+    return u, inputs
+
+
+def attention_rows(q, k, v, rows, n_heads: int, mask: int):
+    """Multi-head proxy attention (Eq. 9) for selected query rows.
+
+    q, k, v: [m, d_p], head h in columns [h*d_head, (h+1)*d_head).
+    For query row i: s_ij = Q_i . K_j / sqrt(d_head); the causal mask keeps
+    j <= i (both causal modes), BIDIRECTIONAL keeps every j; p_i = softmax_j(s_i)
+    and O_i = sum_j p_ij V_j. Returns O [len(rows), d_p] and the natural-log
+    log-sum-exp of the scores, LSE [n_heads, len(rows)].
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    m, d = q.shape
+    dh = d // n_heads
+    scale = 1.0 / np.sqrt(dh)
+    rows = np.asarray(rows, dtype=np.int64)
+    out = np.zeros((rows.size, d))
+    lse = np.zeros((n_heads, rows.size))
+    for s0 in range(0, rows.size, _ROW_CHUNK):
+        r = rows[s0:s0 + _ROW_CHUNK]
+        kmax = m if mask == BIDIRECTIONAL else int(r.max()) + 1
+        for h in range(n_heads):
+            cs = slice(h * dh, (h + 1) * dh)
+            sc = (q[r, cs] @ k[:kmax, cs].T) * scale
+            if mask != BIDIRECTIONAL:
+                sc[np.arange(kmax)[None, :] > r[:, None]] = -np.inf
+            mx = sc.max(axis=1, keepdims=True)
+            p = np.exp(sc - mx)
+            den = p.sum(axis=1, keepdims=True)
+            out[s0:s0 + r.size, cs] = (p @ v[:kmax, cs]) / den
+            lse[h, s0:s0 + r.size] = (mx + np.log(den))[:, 0]
+    return out, lse
+
+
+def proxies_and_attention_inputs(x, weights, factors, h_in=None):
+    """Steps 1-5 of Algorithm 1 up to the interaction inputs, one sequence.
+
+    Returns c (Eq. 7/16), H = H_in + c (Eq. 8), and the projections Q, K, V of H.
+    """
+    c, cin = compress(x, factors, weights["compress"])
+    h = c if h_in is None else _f64(h_in) + c
+    q = linear(h, *weights["q"])
+    k = linear(h, *weights["k"])
+    v = linear(h, *weights["v"])
+    return c, cin, h, q, k, v
+
+
+def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
+                  mask: int = TOKEN_CAUSAL, h_in=None,
+                  sample_blocks: Optional[Sequence[int]] = None,
+                  keep: bool = False) -> Dict[str, object]:
+    """One ProxyFormer layer (Algorithm 1) on x [B, L, d_fine].
+
+    Steps: partition and compress every block (Eq. 2, 7, 15-16); residual
+    proxy update H = H_in + c (Eq. 8); causal multi-head attention over the
+    m proxies (Eq. 9) followed by the output map W_o; decompress the proxy
+    each block receives (Eq. 10, 17); gated injection
+    Y = X + sigmoid(G) * Delta with G = [X, Delta] W_g^T + b_g (Eq. 12).
+
+    Returns x_out [B, L, d_fine] and h_out = H [B, m, d_proxy]. With
+    ``sample_blocks`` only those blocks are decompressed and injected
+    (x_out then has shape [B, len(sample_blocks), P, d_fine]); H is still
+    computed for every block. With ``keep`` the intermediates needed by the
+    backward are returned per sequence.
+    """
+    x = _f64(x)
+    bsz, seq, d_f = x.shape
+    p_blk = int(np.prod(factors))
+    m = seq // p_blk
+    if m * p_blk != seq:
+        raise ValueError("seq_len must be a multiple of the block size P")
+    d_p = weights["q"][0].shape[0]
+    h_out = np.zeros((bsz, m, d_p))
+    if sample_blocks is None:
+        blocks = np.arange(m)
+        x_out = np.zeros_like(x)
+    else:
+        blocks = np.asarray(sample_blocks, dtype=np.int64)
+        x_out = np.zeros((bsz, blocks.size, p_blk, d_f))
+    kept: List[Dict[str, object]] = []
+    lse_all = np.zeros((bsz, n_heads, m)) if sample_blocks is None else None
+    for b in range(bsz):
+        hin_b = None if h_in is None else _f64(h_in)[b]
+        c, cin, h, q, k, v = proxies_and_attention_inputs(x[b], weights, factors, hin_b)
+        h_out[b] = h
+        # which contextualised proxy feeds each block: TOKEN_CAUSAL gives
+        # block i proxy i-1 (block 0 gets zero); the other modes give proxy i
+        if mask == TOKEN_CAUSAL:
+            src = blocks - 1
+        else:
+            src = blocks.copy()
+        need = np.unique(src[src >= 0])
+        o_need, lse = attention_rows(q, k, v, need, n_heads, mask)
+        hbar_need = linear(o_need, *weights["o"])
+        s = np.zeros((blocks.size, d_p))
+        pos = np.searchsorted(need, src[src >= 0])
+        s[src >= 0] = hbar_need[pos]
+        delta, dinputs = decompress(s, factors, weights["decompress"])
+        xb = x[b].reshape(m, p_blk, d_f)[blocks].reshape(-1, d_f)
+        wg, bg = _f64(weights["gate"][0]), _f64(weights["gate"][1])
+        g = xb @ wg[:, :d_f].T + delta @ wg[:, d_f:].T + bg
+        y = xb + sigmoid(g) * delta
+        if sample_blocks is None:
+            x_out[b] = y
+            lse_full = np.zeros((n_heads, m))
+            lse_full[:, need] = lse
+            lse_all[b] = lse_full
+        else:
+            x_out[b] = y.reshape(blocks.size, p_blk, d_f)
+        if keep:
+            if sample_blocks is not None:
+                raise ValueError("keep requires the full forward")
+            hbar = np.zeros((m, d_p))
+            hbar[need] = hbar_need
+            o_full = np.zeros((m, d_p))
+            o_full[need] = o_need
+            kept.append(dict(cin=cin, h=h, q=q, k=k, v=v, o=o_full, hbar=hbar,
+                             s=s, dinputs=dinputs, delta=delta, g=g, x=x[b]))
+    res: Dict[str, object] = {"x_out": x_out, "h_out": h_out}
+    if lse_all is not None:
+        res["lse"] = lse_all
+    if keep:
+        res["kept"] = kept
+    return res
+
+
+def _attention_backward(q, k, v, o, do, n_heads, mask):
+    """Chain rule through Eq. 9 for one sequence (all rows, dense per head).
+
+    With P = softmax(S), S = Q K^T / sqrt(d_head) + M: dV = P^T dO,
+    dP = dO V^T, dS = P * (dP - rowsum(dO * O)), dQ = dS K / sqrt(d_head),
+    dK = dS^T Q / sqrt(d_head).
+    """
+    m, d = q.shape
+    dh = d // n_heads
+    scale = 1.0 / np.sqrt(dh)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for h in range(n_heads):
+        cs = slice(h * dh, (h + 1) * dh)
+        sc = (q[:, cs] @ k[:, cs].T) * scale
+        if mask != BIDIRECTIONAL:
+            sc[np.triu(np.ones((m, m), dtype=bool), 1)] = -np.inf
+        mx = sc.max(axis=1, keepdims=True)
+        p = np.exp(sc - mx)
+        p /= p.sum(axis=1, keepdims=True)
+        dv[:, cs] = p.T @ do[:, cs]
+        dp = do[:, cs] @ v[:, cs].T
+        dsm = p * (dp - np.sum(do[:, cs] * o[:, cs], axis=1, keepdims=True))
+        dq[:, cs] = (dsm @ k[:, cs]) * scale
+        dk[:, cs] = (dsm.T @ q[:, cs]) * scale
+    return dq, dk, dv
+
+
+def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
+                   mask: int = TOKEN_CAUSAL, h_in=None, dh_out=None) -> Dict[str, object]:
+    """Gradients of the layer forward (chain rule of Eq. 7-17 as read above).
+
+    Given dY = dL/dX_out [B, L, d_fine] and optionally dH_out [B, m, d_proxy],
+    returns dx, dh_in (None when h_in is None) and every weight and bias
+    gradient summed over the batch, in the layout of the weights.
+    """
+    fwd = layer_forward(x, weights, factors, n_heads, mask, h_in, keep=True)
+    dy = _f64(dy)
+    bsz, seq, d_f = dy.shape
+    p_blk = int(np.prod(factors))
+    m = seq // p_blk
+    nlev = len(factors)
+
+    def zgrad(w):
+        w0 = _f64(w[0])
+        return [np.zeros_like(w0), np.zeros(w0.shape[0])]
+
+    gr = {"compress": [zgrad(w) for w in weights["compress"]],
+          "q": zgrad(weights["q"]), "k": zgrad(weights["k"]), "v": zgrad(weights["v"]),
+          "o": zgrad(weights["o"]),
+          "decompress": [zgrad(w) for w in weights["decompress"]],
+          "gate": zgrad(weights["gate"])}
+    dx = np.zeros_like(dy)
+    dh_in = None if h_in is None else np.zeros((bsz, m, weights["q"][0].shape[0]))
+    wg = _f64(weights["gate"][0])
+    for b in range(bsz):
+        kp = fwd["kept"][b]
+        xb, delta, g = kp["x"], kp["delta"], kp["g"]
+        sg = sigmoid(g)
+        # Eq. 12: Y = X + sigmoid(G) * Delta, G = X W_gx^T + Delta W_gd^T + b_g
+        dg = dy[b] * delta * sg * (1.0 - sg)
+        ddelta = dy[b] * sg + dg @ wg[:, d_f:]
+        dxb = dy[b] + dg @ wg[:, :d_f]
+        gr["gate"][0] += dg.T @ np.concatenate([xb, delta], axis=1)
+        gr["gate"][1] += dg.sum(axis=0)
+        # Eq. 17 in reverse: level j = 1..M (the forward ran M..1)
+        du = ddelta
+        for j in range(nlev):
+            u_in = kp["dinputs"][nlev - 1 - j]          # input U_j of level j
+            dt = group_rows(du, factors[j])             # gradient of U_j W^T + b
+            gr["decompress"][j][0] += dt.T @ u_in
+            gr["decompress"][j][1] += dt.sum(axis=0)
+            du = dt @ _f64(weights["decompress"][j][0])
+        ds = du
+        # undo the shift that chose which proxy feeds each block
+        if mask == TOKEN_CAUSAL:
+            dhbar = np.zeros_like(ds)
+            dhbar[:-1] = ds[1:]
+        else:
+            dhbar = ds
+        gr["o"][0] += dhbar.T @ kp["o"]
+        gr["o"][1] += dhbar.sum(axis=0)
+        do = dhbar @ _f64(weights["o"][0])
+        dq, dk, dv = _attention_backward(kp["q"], kp["k"], kp["v"], kp["o"], do, n_heads, mask)
+        dh = np.zeros_like(kp["h"]) if dh_out is None else _f64(dh_out)[b].copy()
+        for name, dz in (("q", dq), ("k", dk), ("v", dv)):
+            gr[name][0] += dz.T @ kp["h"]
+            gr[name][1] += dz.sum(axis=0)
+            dh += dz @ _f64(weights[name][0])
+        if dh_in is not None:
+            dh_in[b] = dh
+        # Eq. 8 passes dH to c unchanged; then Eq. 16 in reverse, level M..1
+        dz = dh
+        for j in reversed(range(nlev)):
+            v_in = kp["cin"][j]
+            gr["compress"][j][0] += dz.T @ v_in
+            gr["compress"][j][1] += dz.sum(axis=0)
+            dz = ungroup_rows(dz @ _f64(weights["compress"][j][0]), factors[j])
+        dx[b] = dxb + dz
+    return {"dx": dx, "dh_in": dh_in, "grads": gr}

@@ -1,0 +1,133 @@
+"""Pins for the oracle's layer backward (CPU only).
+
+Central finite differences in float64 check every gradient the backward
+returns, in every mask mode and with a factorised cascade; the dual
+causality test checks that the gradient respects the forward's causal
+structure.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from test_oracle_layer import rand_weights
+
+
+def _loss(x, w, factors, nh, mask, h_in, dy, dh):
+    r = oracle.layer_forward(x, w, factors, nh, mask, h_in)
+    val = float(np.sum(r["x_out"] * dy))
+    if dh is not None:
+        val += float(np.sum(r["h_out"] * dh))
+    return val
+
+
+def _param_paths(w):
+    paths = []
+    for name in ("q", "k", "v", "o", "gate"):
+        paths += [((name, 0),), ((name, 1),)]
+    for lvl in range(len(w["compress"])):
+        paths += [("compress", (lvl, 0)), ("compress", (lvl, 1))]
+        paths += [("decompress", (lvl, 0)), ("decompress", (lvl, 1))]
+    return paths
+
+
+def _get(w, path):
+    if len(path) == 1:
+        name, idx = path[0]
+        return w[name][idx]
+    name, (lvl, idx) = path
+    return w[name][lvl][idx]
+
+
+def _set(w, path, val):
+    import copy
+    w2 = copy.deepcopy(w)
+    if len(path) == 1:
+        name, idx = path[0]
+        t = list(w2[name])
+        t[idx] = val
+        w2[name] = tuple(t)
+    else:
+        name, (lvl, idx) = path
+        t = list(w2[name][lvl])
+        t[idx] = val
+        w2[name][lvl] = tuple(t)
+    return w2
+
+
+def _grad_of(gr, path):
+    if len(path) == 1:
+        name, idx = path[0]
+        return gr[name][idx]
+    name, (lvl, idx) = path
+    return gr[name][lvl][idx]
+
+
+@pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BLOCK_CAUSAL, oracle.BIDIRECTIONAL])
+@pytest.mark.parametrize("factors", [(4,), (2, 4), (4, 2)])
+def test_backward_finite_differences(mask, factors):
+    rng = np.random.default_rng(20 + mask)
+    d_f, d_p, nh, L, B = 4, 6, 2, 16, 2
+    dims = [d_f] + [5] * (len(factors) - 1) + [d_p]   # d_1 differs from d_0 and d_M
+    w = rand_weights(rng, d_f, d_p, factors, dims=dims, std=0.4)
+    x = rng.standard_normal((B, L, d_f))
+    m = L // int(np.prod(factors))
+    h_in = rng.standard_normal((B, m, d_p))
+    dy = rng.standard_normal((B, L, d_f))
+    dh = rng.standard_normal((B, m, d_p))
+    res = oracle.layer_backward(x, w, factors, nh, dy, mask, h_in, dh)
+    eps = 1e-5
+
+    def fd(fplus, fminus):
+        return (fplus - fminus) / (2 * eps)
+
+    # input gradients along random directions
+    for _ in range(3):
+        vx = rng.standard_normal(x.shape)
+        num = fd(_loss(x + eps * vx, w, factors, nh, mask, h_in, dy, dh),
+                 _loss(x - eps * vx, w, factors, nh, mask, h_in, dy, dh))
+        ana = float(np.sum(res["dx"] * vx))
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (num, ana)
+        vh = rng.standard_normal(h_in.shape)
+        num = fd(_loss(x, w, factors, nh, mask, h_in + eps * vh, dy, dh),
+                 _loss(x, w, factors, nh, mask, h_in - eps * vh, dy, dh))
+        ana = float(np.sum(res["dh_in"] * vh))
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (num, ana)
+    # every weight and bias
+    for path in _param_paths(w):
+        p0 = _get(w, path)
+        v = rng.standard_normal(p0.shape)
+        num = fd(_loss(x, _set(w, path, p0 + eps * v), factors, nh, mask, h_in, dy, dh),
+                 _loss(x, _set(w, path, p0 - eps * v), factors, nh, mask, h_in, dy, dh))
+        ana = float(np.sum(_grad_of(res["grads"], path) * v))
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (path, num, ana)
+
+
+def test_backward_without_h_in_and_dh_out():
+    rng = np.random.default_rng(30)
+    d_f, d_p, nh, L = 3, 4, 2, 12
+    w = rand_weights(rng, d_f, d_p, (3,))
+    x = rng.standard_normal((1, L, d_f))
+    dy = rng.standard_normal((1, L, d_f))
+    res = oracle.layer_backward(x, w, (3,), nh, dy)
+    assert res["dh_in"] is None
+    eps = 1e-5
+    vx = rng.standard_normal(x.shape)
+    num = (_loss(x + eps * vx, w, (3,), nh, 0, None, dy, None)
+           - _loss(x - eps * vx, w, (3,), nh, 0, None, dy, None)) / (2 * eps)
+    assert abs(num - float(np.sum(res["dx"] * vx))) < 1e-6 * max(1.0, abs(num))
+
+
+def test_backward_dual_causality():
+    """Token-causal forward: dY[t] can only reach dX[s] for s <= t."""
+    rng = np.random.default_rng(31)
+    d_f, d_p, nh, L = 4, 6, 2, 24
+    w = rand_weights(rng, d_f, d_p, (2, 2))
+    x = rng.standard_normal((1, L, d_f))
+    dy = rng.standard_normal((1, L, d_f))
+    base = oracle.layer_backward(x, w, (2, 2), nh, dy)["dx"]
+    for t in (3, 10, 17):
+        dy2 = dy.copy()
+        dy2[0, t] += 1.0
+        r = oracle.layer_backward(x, w, (2, 2), nh, dy2)["dx"]
+        assert np.array_equal(r[0, t + 1:], base[0, t + 1:])
+        assert not np.array_equal(r[0, t], base[0, t])
