@@ -1,0 +1,212 @@
+/*
+ * proxyformer.h - C ABI of the MI355X (gfx950) ProxyFormer hot-path library.
+ *
+ * The library computes one ProxyFormer layer (Algorithm 1 of the paper:
+ * block compression, causal multi-head attention over the L/P proxies,
+ * decompression and gated injection back into every token), its backward,
+ * and the proxy-only KV-cache decode step with its block-triggered append
+ * (Sec. 3.8, Eq. 19-21). Every step runs in hand-written HIP kernels.
+ *
+ * Conventions shared by every entry point
+ *  - Tensor arguments are DEVICE pointers owned by the caller: contiguous,
+ *    row-major, 16-byte aligned. The library never allocates or frees device
+ *    memory; scratch space is the caller's `workspace` (size from the
+ *    matching *_workspace_size query, alignment 256 bytes).
+ *  - Activations and weights use the dtype of the config (PF_BF16: bfloat16,
+ *    PF_FP32: float). Accumulation is always fp32. Weight gradients are
+ *    always fp32.
+ *  - Linear maps follow y = x W^T + b with W stored [out, in]; a NULL bias
+ *    means zero.
+ *  - `stream` is a hipStream_t passed as void* (NULL = null stream). Calls
+ *    only enqueue work and return without synchronising.
+ *  - Every argument is checked on the host before the first launch. A status
+ *    other than PF_OK means nothing was enqueued and no buffer was touched,
+ *    except PF_ERR_HIP, which reports a failed launch (text in
+ *    proxy_last_error()).
+ *  - Calls are re-entrant; all state lives in caller-owned structs/buffers.
+ */
+#ifndef PROXYFORMER_H
+#define PROXYFORMER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PF_MAX_LEVELS 4
+
+enum pf_status {
+  PF_OK = 0,
+  PF_ERR_INVALID_ARG = -1, /* inconsistent sizes, NULL required pointer */
+  PF_ERR_UNSUPPORTED = -2, /* valid but not implemented shape/dtype */
+  PF_ERR_CAPACITY = -3,    /* proxy KV cache would overflow n_cap */
+  PF_ERR_WORKSPACE = -4,   /* workspace NULL or smaller than required */
+  PF_ERR_HIP = -5          /* a HIP launch failed */
+};
+
+enum pf_dtype { PF_FP32 = 0, PF_BF16 = 1 };
+
+/* Which contextualised proxy feeds each block (Algorithm 1 with Eq. 9).
+ * PF_TOKEN_CAUSAL: block i receives proxy i-1 (block 0 receives zero), so
+ *   output token t depends only on input tokens <= t.
+ * PF_BLOCK_CAUSAL: block i receives proxy i under the causal proxy mask
+ *   (the literal reading; a token sees its whole block).
+ * PF_BIDIRECTIONAL: block i receives proxy i, mask M = 0 in Eq. 9. */
+enum pf_mask { PF_TOKEN_CAUSAL = 0, PF_BLOCK_CAUSAL = 1, PF_BIDIRECTIONAL = 2 };
+
+typedef struct {
+  const void* w; /* [out, in] */
+  const void* b; /* [out] or NULL */
+} pf_linear;
+
+/* One layer call (Algorithm 1 inputs; factorisation of Eq. 15).
+ *  batch     B >= 1 sequences, processed independently.
+ *  seq_len   L tokens per sequence; must be a multiple of P.
+ *  d_fine    local-stream width d_0.
+ *  d_proxy   proxy width d_M = n_heads * head_dim.
+ *  n_levels  M in 1..4; factors[0..M-1] = k_1..k_M, P = prod k_j.
+ *  level_dims[j] = d_{j+1} for j < M-1 (0 -> d_proxy); level_dims[M-1] is
+ *            ignored (d_M = d_proxy).
+ *  head_dim  64 or 128.
+ *  dtype     pf_dtype; mask pf_mask. */
+typedef struct {
+  int32_t batch;
+  int64_t seq_len;
+  int32_t d_fine, d_proxy, n_heads, head_dim;
+  int32_t n_levels;
+  int32_t factors[PF_MAX_LEVELS];
+  int32_t level_dims[PF_MAX_LEVELS];
+  int32_t dtype, mask;
+} pf_layer_config;
+
+/* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)
+ * q, k, v, o : W [d_proxy, d_proxy]     (Eq. 9 and its output map)
+ * decompress[j]: W [k_{j+1} d_j, d_{j+1}] (Eq. 10, Eq. 17)
+ * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12) */
+typedef struct {
+  pf_linear compress[PF_MAX_LEVELS];
+  pf_linear q, k, v, o;
+  pf_linear decompress[PF_MAX_LEVELS];
+  pf_linear gate;
+} pf_layer_weights;
+
+typedef struct {
+  void* dw; /* fp32, same shape as W, overwritten */
+  void* db; /* fp32 [out], overwritten; may be NULL (not computed) */
+} pf_linear_grad;
+
+typedef struct {
+  pf_linear_grad compress[PF_MAX_LEVELS];
+  pf_linear_grad q, k, v, o;
+  pf_linear_grad decompress[PF_MAX_LEVELS];
+  pf_linear_grad gate;
+} pf_layer_grads;
+
+/* Bytes of scratch the forward (for_backward = 0) or backward
+ * (for_backward = 1) needs; 0 for an invalid config. */
+size_t proxy_layer_workspace_size(const pf_layer_config* cfg, int for_backward);
+
+/* Bytes of the `saved` buffer the forward fills for the backward
+ * (activations of every step); 0 for an invalid config. */
+size_t proxy_layer_saved_size(const pf_layer_config* cfg);
+
+/* Layer forward, Algorithm 1 (Eq. 2, 7, 8, 9, 10, 12, 15-17).
+ *  x      [B, L, d_fine]  local stream X^(l-1)
+ *  h_in   [B, m, d_proxy] proxy stream H^(l-1), or NULL for zero (Eq. 8
+ *         then reduces to direct compression)
+ *  x_out  [B, L, d_fine]  X^(l) = X + sigmoid(G) * Delta   (may not alias x)
+ *  h_out  [B, m, d_proxy] H^(l) = H^(l-1) + C(X)            (returned by Alg. 1)
+ *  saved  NULL, or proxy_layer_saved_size() bytes to keep activations for
+ *         proxy_layer_backward.
+ * Returns PF_OK or an error status (see the conventions above). */
+int proxy_layer_forward(const pf_layer_config* cfg, const pf_layer_weights* w,
+                        const void* x, const void* h_in, void* x_out, void* h_out,
+                        void* saved, void* workspace, size_t ws_bytes, void* stream);
+
+/* Layer backward: the chain rule through every forward step.
+ *  saved   the buffer a forward with the same cfg/weights/x/h_in filled
+ *  dy      [B, L, d_fine] gradient of x_out
+ *  dh_out  [B, m, d_proxy] gradient of h_out, or NULL for zero
+ *  dx      [B, L, d_fine] gradient of x (dtype of cfg), overwritten
+ *  dh_in   [B, m, d_proxy] gradient of h_in (dtype of cfg), or NULL
+ *  grads   fp32 weight/bias gradients summed over the batch, overwritten;
+ *          a NULL dw skips that map's weight gradient. */
+int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w,
+                         const void* x, const void* h_in, const void* saved,
+                         const void* dy, const void* dh_out, void* dx, void* dh_in,
+                         const pf_layer_grads* grads, void* workspace, size_t ws_bytes,
+                         void* stream);
+
+/* Decode (generation block of Eq. 19-20 against the proxy cache of Eq. 21).
+ *  d_model = n_heads * head_dim; head_dim 64 or 128.
+ *  n_levels/factors/level_dims describe the compression C of the append
+ *  (as in pf_layer_config with d_fine = d_proxy = d_model). */
+typedef struct {
+  int32_t batch, d_model, n_heads, head_dim, n_levels;
+  int32_t factors[PF_MAX_LEVELS];
+  int32_t level_dims[PF_MAX_LEVELS];
+  int32_t dtype;
+  float rms_eps;
+} pf_decode_config;
+
+/* rms_gamma [d_model]; q,k,v,o W [d,d]; alpha W [n_heads, d] (MLP_alpha of
+ * Eq. 20, followed by a sigmoid); compress as in pf_layer_weights;
+ * k_proxy, v_proxy W [d,d]: the proxy-attention K/V maps whose outputs are
+ * the cached rows (Eq. 21). */
+typedef struct {
+  const void* rms_gamma;
+  pf_linear q, k, v, o, alpha;
+  pf_linear compress[PF_MAX_LEVELS];
+  pf_linear k_proxy, v_proxy;
+} pf_decode_weights;
+
+/* Whole inference state (caller-owned device buffers, host counters).
+ *  k_cache, v_cache [B, n_heads, n_cap, head_dim]: rows 0..n-1 valid.
+ *  x_blk [B, P, d]: inputs of the current block; k_loc, v_loc
+ *  [B, n_heads, P, head_dim]: its keys/values; slots 0..j-1 valid.
+ * The batch moves in lockstep (one n and one j for all sequences). */
+typedef struct {
+  void* k_cache;
+  void* v_cache;
+  int64_t n_cap, n;
+  void* x_blk;
+  void* k_loc;
+  void* v_loc;
+  int32_t j;
+} pf_decode_state;
+
+size_t proxy_decode_workspace_size(const pf_decode_config* cfg);
+
+/* One decode step for the token at block position j of every sequence.
+ *  x_t [B, d] layer input of the new token; y_t [B, d] output
+ *  y = x + (A_x + alpha * A_h) W_o^T + b_o, where A_x attends over the
+ *  current block's slots 0..j and A_h over the n cached proxies.
+ * Writes x/k/v of the token into slot j; on success j += 1, and when j
+ * reaches P the block is appended (as proxy_cache_append) in the same call,
+ * n += 1 and j = 0. A full cache (n == n_cap when the block completes)
+ * returns PF_ERR_CAPACITY before any launch. */
+int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w,
+                      pf_decode_state* st, const void* x_t, void* y_t,
+                      void* workspace, size_t ws_bytes, void* stream);
+
+/* Append nblk whole blocks to the cache (prefill path and the streaming
+ * update of Sec. 3.8): for each block h = C(x_block) (Eq. 7 / 16), then
+ * K_p[n] = h W_kp^T + b, V_p[n] = h W_vp^T + b, n += 1 (Eq. 21).
+ *  x_blocks [B, nblk * P, d]. PF_ERR_CAPACITY if n + nblk > n_cap. */
+int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w,
+                       pf_decode_state* st, const void* x_blocks, int64_t nblk,
+                       void* workspace, size_t ws_bytes, void* stream);
+
+/* Message of the last non-OK status on the calling thread. */
+const char* proxy_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+int proxy_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PROXYFORMER_H */

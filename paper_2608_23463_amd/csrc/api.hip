@@ -1,0 +1,221 @@
+// C-ABI entry points: argument validation on the host, then dispatch to the
+// dtype-specific launch sequences. Nothing is enqueued unless every check
+// passes.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "common.hpp"
+#include "decode.hpp"
+#include "layer.hpp"
+
+namespace pf {
+size_t layer_forward_gemm_ws(const LayerDims& d);
+size_t layer_backward_gemm_ws(const LayerDims& d);
+
+size_t layer_gemm_ws_bytes(const LayerDims& d, bool for_backward) {
+  return for_backward ? layer_backward_gemm_ws(d) : layer_forward_gemm_ws(d);
+}
+}  // namespace pf
+
+using namespace pf;
+
+static thread_local std::string g_last_error;
+
+static int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+static int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+static int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return PF_OK;
+  return fail(PF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+static bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const char* pa = reinterpret_cast<const char*>(a);
+  const char* pb = reinterpret_cast<const char*>(b);
+  return a && b && pa < pb + nb && pb < pa + na;
+}
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+extern "C" {
+
+int proxy_version(void) { return 100; }
+
+const char* proxy_last_error(void) { return g_last_error.c_str(); }
+
+size_t proxy_layer_workspace_size(const pf_layer_config* cfg, int for_backward) {
+  LayerDims d;
+  const char* why;
+  if (layer_dims(cfg, &d, &why) != PF_OK) return 0;
+  return layer_ws(d, for_backward != 0).bytes;
+}
+
+size_t proxy_layer_saved_size(const pf_layer_config* cfg) {
+  LayerDims d;
+  const char* why;
+  if (layer_dims(cfg, &d, &why) != PF_OK) return 0;
+  return layer_acts(d, true).bytes;
+}
+
+static int check_weights(const LayerDims& d, const pf_layer_weights* w) {
+  if (!w) return fail(PF_ERR_INVALID_ARG, "weights struct is NULL");
+  for (int j = 0; j < d.M; ++j) {
+    if (!w->compress[j].w) return fail(PF_ERR_INVALID_ARG, "compress[%d].w is NULL", j);
+    if (!w->decompress[j].w) return fail(PF_ERR_INVALID_ARG, "decompress[%d].w is NULL", j);
+    if (!aligned16(w->compress[j].w) || !aligned16(w->decompress[j].w))
+      return fail(PF_ERR_INVALID_ARG, "level %d weights must be 16-byte aligned", j);
+  }
+  const pf_linear* maps[5] = {&w->q, &w->k, &w->v, &w->o, &w->gate};
+  const char* names[5] = {"q", "k", "v", "o", "gate"};
+  for (int i = 0; i < 5; ++i) {
+    if (!maps[i]->w) return fail(PF_ERR_INVALID_ARG, "%s.w is NULL", names[i]);
+    if (!aligned16(maps[i]->w)) return fail(PF_ERR_INVALID_ARG, "%s.w must be 16-byte aligned", names[i]);
+  }
+  return PF_OK;
+}
+
+int proxy_layer_forward(const pf_layer_config* cfg, const pf_layer_weights* w, const void* x, const void* h_in,
+                        void* x_out, void* h_out, void* saved, void* workspace, size_t ws_bytes, void* stream) {
+  LayerDims d;
+  const char* why;
+  int st = layer_dims(cfg, &d, &why);
+  if (st != PF_OK) return fail(st, "invalid layer config: %s", why);
+  if ((st = check_weights(d, w)) != PF_OK) return st;
+  if (!x || !x_out || !h_out) return fail(PF_ERR_INVALID_ARG, "x, x_out and h_out must be non-NULL");
+  if (!aligned16(x) || !aligned16(x_out) || !aligned16(h_out) || (h_in && !aligned16(h_in)) ||
+      (saved && !aligned16(saved)))
+    return fail(PF_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  const size_t tok_bytes = (size_t)d.B * d.L * d.d_f * d.esize;
+  const size_t prox_bytes = (size_t)d.B * d.m * d.d_p * d.esize;
+  if (overlaps(x, tok_bytes, x_out, tok_bytes)) return fail(PF_ERR_INVALID_ARG, "x_out must not alias x");
+  if (overlaps(h_out, prox_bytes, x_out, tok_bytes) || overlaps(h_out, prox_bytes, x, tok_bytes))
+    return fail(PF_ERR_INVALID_ARG, "h_out must not alias x or x_out");
+  const LayerWs W = layer_ws(d, false);
+  if (W.bytes && (!workspace || ws_bytes < W.bytes))
+    return fail(PF_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", W.bytes, workspace ? ws_bytes : 0);
+  char* ws = reinterpret_cast<char*>(workspace);
+  char* acts = saved ? reinterpret_cast<char*>(saved) : ws + W.acts;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = cfg->dtype == PF_BF16
+                     ? layer_forward_run<bf16>(d, cfg, w, x, h_in, x_out, h_out, acts, saved != nullptr, ws, s)
+                     : layer_forward_run<float>(d, cfg, w, x, h_in, x_out, h_out, acts, saved != nullptr, ws, s);
+  return hip_status(e, "proxy_layer_forward launch");
+}
+
+int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w, const void* x, const void* h_in,
+                         const void* saved, const void* dy, const void* dh_out, void* dx, void* dh_in,
+                         const pf_layer_grads* grads, void* workspace, size_t ws_bytes, void* stream) {
+  LayerDims d;
+  const char* why;
+  int st = layer_dims(cfg, &d, &why);
+  if (st != PF_OK) return fail(st, "invalid layer config: %s", why);
+  if ((st = check_weights(d, w)) != PF_OK) return st;
+  if (!x || !saved || !dy || !dx || !grads)
+    return fail(PF_ERR_INVALID_ARG, "x, saved, dy, dx and grads must be non-NULL");
+  if ((h_in == nullptr) != (dh_in == nullptr))
+    return fail(PF_ERR_INVALID_ARG, "dh_in must be given exactly when h_in is given");
+  if (!aligned16(x) || !aligned16(saved) || !aligned16(dy) || !aligned16(dx) || (dh_out && !aligned16(dh_out)) ||
+      (dh_in && !aligned16(dh_in)) || (h_in && !aligned16(h_in)))
+    return fail(PF_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  const size_t tok_bytes = (size_t)d.B * d.L * d.d_f * d.esize;
+  if (overlaps(dx, tok_bytes, dy, tok_bytes)) return fail(PF_ERR_INVALID_ARG, "dx must not alias dy");
+  const LayerWs W = layer_ws(d, true);
+  if (W.bytes && (!workspace || ws_bytes < W.bytes))
+    return fail(PF_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", W.bytes, workspace ? ws_bytes : 0);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const char* sv = reinterpret_cast<const char*>(saved);
+  char* ws = reinterpret_cast<char*>(workspace);
+  hipError_t e = cfg->dtype == PF_BF16
+                     ? layer_backward_run<bf16>(d, cfg, w, x, h_in, sv, dy, dh_out, dx, dh_in, grads, ws, s)
+                     : layer_backward_run<float>(d, cfg, w, x, h_in, sv, dy, dh_out, dx, dh_in, grads, ws, s);
+  if (e == hipErrorNotSupported) return fail(PF_ERR_UNSUPPORTED, "backward not available for this config");
+  return hip_status(e, "proxy_layer_backward launch");
+}
+
+// ---------------------------------------------------------------- decode
+
+size_t proxy_decode_workspace_size(const pf_decode_config* cfg) {
+  DecodeDims d;
+  const char* why;
+  if (decode_dims(cfg, &d, &why) != PF_OK) return 0;
+  return decode_ws(d).bytes;
+}
+
+static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weights* w, const pf_decode_state* st,
+                               DecodeDims* d, void* workspace, size_t ws_bytes) {
+  const char* why;
+  int s = decode_dims(cfg, d, &why);
+  if (s != PF_OK) return fail(s, "invalid decode config: %s", why);
+  if (!w || !st) return fail(PF_ERR_INVALID_ARG, "weights and state must be non-NULL");
+  if (!w->rms_gamma || !w->q.w || !w->k.w || !w->v.w || !w->o.w || !w->alpha.w || !w->k_proxy.w || !w->v_proxy.w)
+    return fail(PF_ERR_INVALID_ARG, "a required decode weight is NULL");
+  for (int j = 0; j < d->M; ++j)
+    if (!w->compress[j].w) return fail(PF_ERR_INVALID_ARG, "compress[%d].w is NULL", j);
+  if (!st->k_cache || !st->v_cache || !st->x_blk || !st->k_loc || !st->v_loc)
+    return fail(PF_ERR_INVALID_ARG, "a decode state buffer is NULL");
+  if (st->n < 0 || st->n_cap < 0 || st->n > st->n_cap) return fail(PF_ERR_INVALID_ARG, "state n must be in 0..n_cap");
+  if (st->n_cap > INT32_MAX) return fail(PF_ERR_UNSUPPORTED, "n_cap above 2^31 - 1");
+  if (st->j < 0 || st->j >= d->P) return fail(PF_ERR_INVALID_ARG, "state j must be in 0..P-1");
+  const DecodeWs W = decode_ws(*d);
+  if (!workspace || ws_bytes < W.bytes)
+    return fail(PF_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", W.bytes, workspace ? ws_bytes : 0);
+  return PF_OK;
+}
+
+int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, pf_decode_state* st, const void* x_t,
+                      void* y_t, void* workspace, size_t ws_bytes, void* stream) {
+  DecodeDims d;
+  int s = check_decode_common(cfg, w, st, &d, workspace, ws_bytes);
+  if (s != PF_OK) return s;
+  if (!x_t || !y_t) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be non-NULL");
+  if (overlaps(x_t, (size_t)d.B * d.d * d.esize, y_t, (size_t)d.B * d.d * d.esize))
+    return fail(PF_ERR_INVALID_ARG, "y_t must not alias x_t");
+  const bool completes = st->j + 1 == d.P;
+  if (completes && st->n + 1 > st->n_cap)
+    return fail(PF_ERR_CAPACITY, "proxy cache full: n = %lld, n_cap = %lld", (long long)st->n, (long long)st->n_cap);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, w, *st, x_t, y_t, reinterpret_cast<char*>(workspace), hs)
+                              : decode_step_run<float>(d, w, *st, x_t, y_t, reinterpret_cast<char*>(workspace), hs);
+  if (e != hipSuccess) return hip_status(e, "proxy_decode_step launch");
+  if (completes) {
+    e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, st->x_blk, 1, reinterpret_cast<char*>(workspace), hs)
+                     : cache_append_run<float>(d, w, *st, st->x_blk, 1, reinterpret_cast<char*>(workspace), hs);
+    if (e != hipSuccess) return hip_status(e, "proxy_decode_step append launch");
+    st->n += 1;
+    st->j = 0;
+  } else {
+    st->j += 1;
+  }
+  return PF_OK;
+}
+
+int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w, pf_decode_state* st,
+                       const void* x_blocks, int64_t nblk, void* workspace, size_t ws_bytes, void* stream) {
+  DecodeDims d;
+  int s = check_decode_common(cfg, w, st, &d, workspace, ws_bytes);
+  if (s != PF_OK) return s;
+  if (nblk < 0) return fail(PF_ERR_INVALID_ARG, "nblk must be >= 0");
+  if (nblk == 0) return PF_OK;
+  if (!x_blocks) return fail(PF_ERR_INVALID_ARG, "x_blocks is NULL");
+  if (st->n + nblk > st->n_cap)
+    return fail(PF_ERR_CAPACITY, "append of %lld blocks overflows the cache (n = %lld, n_cap = %lld)",
+                (long long)nblk, (long long)st->n, (long long)st->n_cap);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, x_blocks, nblk, reinterpret_cast<char*>(workspace), hs)
+                              : cache_append_run<float>(d, w, *st, x_blocks, nblk, reinterpret_cast<char*>(workspace), hs);
+  if (e != hipSuccess) return hip_status(e, "proxy_cache_append launch");
+  st->n += nblk;
+  return PF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,105 @@
+// Device-side building blocks shared by every kernel of the library:
+// element types, 16-byte vector access, fp32<->bf16 conversion and the
+// MFMA fragment abstraction for gfx950 (CDNA4, 64-wide wavefronts).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pf {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;  // MI355X: 8 accelerator complex dies, workgroups dealt round-robin
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float v);
+template <>
+__device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }  // round to nearest even
+
+template <typename T>
+__device__ __forceinline__ float load_f32(const T* p, int64_t i) {
+  return p ? to_f32(p[i]) : 0.0f;
+}
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+// ---------------------------------------------------------------------------
+// MFMA fragments. One "k16 step" multiplies a 32x16 slice of A by a 16x32
+// slice of B into a 32x32 fp32 tile held as 16 floats per lane.
+// Lane l supplies row (l % 32) of A / column (l % 32) of B and the eight
+// reduction indices (l / 32) * 8 .. +7 of the step. Because A and B use the
+// same lane->index assignment, the product is exact regardless of how the
+// hardware orders the reduction inside the instruction.
+//  bf16: one v_mfma_f32_32x32x16_bf16 (8 bf16 per lane per operand).
+//  fp32: eight v_mfma_f32_32x32x2_f32; slot s of lane group g is index g*8+s.
+// Output layout of a 32x32 tile: lane l holds column l % 32, register r holds
+// row (r / 4) * 8 + (l / 32) * 4 + (r % 4).
+// ---------------------------------------------------------------------------
+template <typename T>
+struct Mma;
+
+template <>
+struct Mma<bf16> {
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ f32x16 mma(const frag& a, const frag& b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ frag load(const bf16* p) {
+    return *reinterpret_cast<const frag*>(p);
+  }
+  static __device__ __forceinline__ frag pack(const float* v) {
+    frag f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = (bf16)v[i];
+    return f;
+  }
+};
+
+template <>
+struct Mma<float> {
+  typedef f32x8 frag;
+  static __device__ __forceinline__ f32x16 mma(const frag& a, const frag& b, f32x16 c) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], c, 0, 0, 0);
+    return c;
+  }
+  static __device__ __forceinline__ frag load(const float* p) {
+    // two 16-byte reads: fragment addresses are only 16-byte aligned
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(p);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(p + 4);
+    frag f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[i] = lo[i];
+      f[i + 4] = hi[i];
+    }
+    return f;
+  }
+  static __device__ __forceinline__ frag pack(const float* v) {
+    frag f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = v[i];
+    return f;
+  }
+};
+
+__device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
+
+}  // namespace pf

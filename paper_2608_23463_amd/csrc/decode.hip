@@ -1,0 +1,518 @@
+// Proxy-KV-cache decode step and block-triggered append (Eq. 19-21, Sec. 3.8).
+//
+// Step (one token per sequence, the batch in lockstep):
+//  1. rmsnorm_kernel: u = RMSNorm(x) * gamma, and x is stored in block slot j.
+//  2. GEMMs of u with W_q, W_k, W_v (k, v written straight into slot j of the
+//     local block) and W_alpha (sigmoid in the epilogue).
+//  3. decode_attn_kernel: the only HBM-heavy step. Cache rows of every
+//     (sequence, head) are cut into slices; a workgroup streams one slice of
+//     K and V with 16-byte loads (eight lanes per 64-channel row), keeps an
+//     online softmax per row slot, and writes an unnormalised partial
+//     (max, sum, weighted values). One extra slice per (sequence, head)
+//     handles the current block's slots 0..j.
+//  4. decode_combine_kernel: merges the cache slices in a fixed order (A_h),
+//     normalises the local part (A_x) and forms A = A_x + alpha * A_h.
+//  5. GEMM with W_o plus the residual x (y = x + A W_o^T + b_o).
+// Append: compression GEMMs over whole blocks (the block is a zero-copy
+// [rows, P*d] view), then the K/V proxy maps write straight into cache row n.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+#include "decode.hpp"
+#include "epilogues.hpp"
+#include "layer.hpp"
+#include "runner.hpp"
+
+namespace pf {
+
+int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why) {
+  *why = nullptr;
+  if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
+  if (c->dtype != PF_FP32 && c->dtype != PF_BF16) return *why = "dtype must be PF_FP32 or PF_BF16", PF_ERR_INVALID_ARG;
+  if (c->batch < 1 || c->d_model < 1 || c->n_heads < 1 || c->head_dim < 1)
+    return *why = "sizes must be >= 1", PF_ERR_INVALID_ARG;
+  if ((int64_t)c->n_heads * c->head_dim != c->d_model) return *why = "n_heads * head_dim must equal d_model", PF_ERR_INVALID_ARG;
+  if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
+  if (!(c->rms_eps >= 0.0f)) return *why = "rms_eps must be >= 0", PF_ERR_INVALID_ARG;
+  d->B = c->batch;
+  d->d = c->d_model;
+  d->nh = c->n_heads;
+  d->dh = c->head_dim;
+  d->M = c->n_levels;
+  d->P = 1;
+  for (int j = 0; j < d->M; ++j) {
+    if (c->factors[j] < 1) return *why = "every factor k_j must be >= 1", PF_ERR_INVALID_ARG;
+    d->k[j] = c->factors[j];
+    d->P *= c->factors[j];
+    if (d->P > (1 << 16)) return *why = "block size P too large", PF_ERR_INVALID_ARG;
+  }
+  d->dl[0] = d->d;
+  for (int j = 1; j < d->M; ++j) d->dl[j] = c->level_dims[j - 1] > 0 ? c->level_dims[j - 1] : d->d;
+  d->dl[d->M] = d->d;
+  d->esize = c->dtype == PF_BF16 ? 2 : 4;
+  d->eps = c->rms_eps;
+  if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
+  for (int j = 0; j <= d->M; ++j)
+    if (d->dl[j] % 8 != 0) return *why = "every channel width must be a multiple of 8", PF_ERR_UNSUPPORTED;
+  const int64_t lvl1_rows_per_block = d->P / d->k[0];
+  d->append_rows = (int)std::max<int64_t>(1, std::min<int64_t>(4096, 65536 / lvl1_rows_per_block));
+  return PF_OK;
+}
+
+// Offsets of every scratch buffer except the split-K partials.
+static DecodeWs decode_ws_layout(const DecodeDims& d) {
+  DecodeWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t es = d.esize;
+  w.u = take((size_t)d.B * d.d * es);
+  w.q = take((size_t)d.B * d.d * es);
+  w.alpha = take((size_t)d.B * d.nh * 4);
+  w.attn = take((size_t)d.B * d.d * es);
+  const size_t nparts = (size_t)d.B * d.nh * (kDecodeMaxSplits + 1);
+  w.part_m = take(nparts * 4);
+  w.part_l = take(nparts * 4);
+  w.part_acc = take(nparts * d.dh * 4);
+  int64_t per_block = d.P;  // rows of level j per block
+  for (int j = 1; j <= d.M; ++j) {
+    per_block /= d.k[j - 1];
+    w.z[j] = take((size_t)d.append_rows * per_block * d.dl[j] * es);
+  }
+  w.gemm = off;
+  w.bytes = off;
+  return w;
+}
+
+// ---- kernels ------------------------------------------------------------------
+
+template <typename T>
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ gamma, T* u,
+                                                      T* x_blk, int d, int64_t blk_stride, int j, float eps) {
+  const int b = blockIdx.x;
+  const T* xr = x + (int64_t)b * d;
+  float ss = 0.0f;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    const float v = to_f32(xr[c]);
+    ss += v * v;
+  }
+  __shared__ float red[256];
+  red[threadIdx.x] = ss;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    const T xv = xr[c];
+    u[(int64_t)b * d + c] = from_f32<T>(to_f32(xv) * inv * to_f32(gamma[c]));
+    x_blk[(int64_t)b * blk_stride + (int64_t)j * d + c] = xv;
+  }
+}
+
+struct DecodeAttnParams {
+  const void* q;       // [B, d]
+  const void* kc;      // [B, h, n_cap, dh]
+  const void* vc;
+  const void* kl;      // [B, h, P, dh]
+  const void* vl;
+  float* part_m;       // [B*h, S+1]
+  float* part_l;
+  float* part_acc;     // [B*h, S+1, dh]
+  int64_t n, n_cap, P;
+  int j;               // local slots 0..j are valid
+  int nh, splits, chunk;
+  float scale_log2;
+};
+
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) decode_attn_kernel(const DecodeAttnParams p) {
+  constexpr int kVec = 16 / sizeof(T);
+  constexpr int LPR = DH / kVec;        // lanes per row
+  constexpr int RPW = kWave / LPR;      // rows per wave per load
+  constexpr int U = 4;                  // row groups in flight per lane
+  const int s = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int b = bh / p.nh, h = bh % p.nh;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane % LPR, rslot = lane / LPR;
+
+  const T* base_k;
+  const T* base_v;
+  int64_t r0, r1;
+  if (s < p.splits) {
+    base_k = reinterpret_cast<const T*>(p.kc) + (int64_t)bh * p.n_cap * DH;
+    base_v = reinterpret_cast<const T*>(p.vc) + (int64_t)bh * p.n_cap * DH;
+    r0 = (int64_t)s * p.chunk;
+    r1 = std::min<int64_t>(p.n, r0 + p.chunk);
+  } else {
+    base_k = reinterpret_cast<const T*>(p.kl) + (int64_t)bh * p.P * DH;
+    base_v = reinterpret_cast<const T*>(p.vl) + (int64_t)bh * p.P * DH;
+    r0 = 0;
+    r1 = p.j + 1;
+  }
+
+  float qv[kVec];
+  {
+    const T* qp = reinterpret_cast<const T*>(p.q) + (int64_t)b * p.nh * DH + h * DH + sub * kVec;
+#pragma unroll
+    for (int i = 0; i < kVec; ++i) qv[i] = to_f32(qp[i]) * p.scale_log2;
+  }
+  float mrun = -INFINITY, lrun = 0.0f;
+  float acc[kVec];
+#pragma unroll
+  for (int i = 0; i < kVec; ++i) acc[i] = 0.0f;
+
+  const int64_t step = (int64_t)4 * U * RPW;
+  for (int64_t rb = r0 + (int64_t)wave * U * RPW; rb < r1; rb += step) {
+    u32x4 kraw[U], vraw[U];
+    bool valid[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t row = rb + u * RPW + rslot;
+      valid[u] = row < r1;
+      u32x4 zero = {0u, 0u, 0u, 0u};
+      kraw[u] = valid[u] ? ld16(base_k + row * DH + sub * kVec) : zero;
+      vraw[u] = valid[u] ? ld16(base_v + row * DH + sub * kVec) : zero;
+    }
+    float sc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const T* kt = reinterpret_cast<const T*>(&kraw[u]);
+      float dot = 0.0f;
+#pragma unroll
+      for (int i = 0; i < kVec; ++i) dot += qv[i] * to_f32(kt[i]);
+#pragma unroll
+      for (int off = 1; off < LPR; off <<= 1) dot += __shfl_xor(dot, off);
+      sc[u] = valid[u] ? dot : -INFINITY;
+    }
+    float mt = sc[0];
+#pragma unroll
+    for (int u = 1; u < U; ++u) mt = fmaxf(mt, sc[u]);
+    const float mnew = fmaxf(mrun, mt);
+    if (mnew == -INFINITY) continue;
+    const float alpha = fast_exp2(mrun - mnew);
+    mrun = mnew;
+    lrun *= alpha;
+#pragma unroll
+    for (int i = 0; i < kVec; ++i) acc[i] *= alpha;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float pu = fast_exp2(sc[u] - mnew);
+      lrun += pu;
+      const T* vt = reinterpret_cast<const T*>(&vraw[u]);
+#pragma unroll
+      for (int i = 0; i < kVec; ++i) acc[i] += pu * to_f32(vt[i]);
+    }
+  }
+
+  // merge the 4 * RPW row slots of the workgroup (fixed order)
+  __shared__ float sm[4 * RPW];
+  __shared__ float sl[4 * RPW];
+  __shared__ float sacc[4 * RPW][DH];
+  const int slot = wave * RPW + rslot;
+  if (sub == 0) {
+    sm[slot] = mrun;
+    sl[slot] = lrun;
+  }
+#pragma unroll
+  for (int i = 0; i < kVec; ++i) sacc[slot][sub * kVec + i] = acc[i];
+  __syncthreads();
+  if (tid < DH) {
+    float mx = -INFINITY;
+    for (int i = 0; i < 4 * RPW; ++i) mx = fmaxf(mx, sm[i]);
+    float l = 0.0f, a = 0.0f;
+    if (mx != -INFINITY) {
+      for (int i = 0; i < 4 * RPW; ++i) {
+        const float f = fast_exp2(sm[i] - mx);
+        l += sl[i] * f;
+        a += sacc[i][tid] * f;
+      }
+    }
+    const int64_t pidx = (int64_t)bh * (p.splits + 1) + s;
+    p.part_acc[pidx * DH + tid] = a;
+    if (tid == 0) {
+      p.part_m[pidx] = mx;
+      p.part_l[pidx] = l;
+    }
+  }
+}
+
+template <typename T, int DH>
+__global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restrict__ part_m,
+                                                            const float* __restrict__ part_l,
+                                                            const float* __restrict__ part_acc,
+                                                            const float* __restrict__ alpha, T* attn, int nh,
+                                                            int splits) {
+  const int bh = blockIdx.x;
+  const int b = bh / nh, h = bh % nh;
+  const int64_t base = (int64_t)bh * (splits + 1);
+  float mx = -INFINITY;
+  for (int s = 0; s < splits; ++s) mx = fmaxf(mx, part_m[base + s]);
+  const float a = alpha[(int64_t)b * nh + h];
+  for (int c = threadIdx.x; c < DH; c += 64) {
+    float ah = 0.0f;
+    if (mx != -INFINITY) {
+      float l = 0.0f, acc = 0.0f;
+      for (int s = 0; s < splits; ++s) {
+        const float f = fast_exp2(part_m[base + s] - mx);
+        l += part_l[base + s] * f;
+        acc += part_acc[(base + s) * DH + c] * f;
+      }
+      ah = acc / l;
+    }
+    const float ax = part_acc[(base + splits) * DH + c] / part_l[base + splits];
+    attn[(int64_t)b * nh * DH + h * DH + c] = from_f32<T>(ax + a * ah);
+  }
+}
+
+// k/v of the new token into slot j of the local block: out [B, h, P, dh].
+template <typename T>
+struct EpiSlot {
+  T* out;
+  const T* bias;
+  int nh, dh;
+  int64_t P;
+  int j;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    if (bias) v += to_f32(bias[c]);
+    const int hd = c / dh, e = c - hd * dh;
+    out[(((int64_t)r * nh + hd) * P + j) * dh + e] = from_f32<T>(v);
+  }
+};
+
+template <typename T>
+struct EpiSigmoidF32 {
+  float* out;
+  const T* bias;
+  int ldo;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    if (bias) v += to_f32(bias[c]);
+    out[(int64_t)r * ldo + c] = sigmoidf(v);
+  }
+};
+
+// Proxy K/V rows into the cache: row rr = r0 + r is (sequence rr / nblk,
+// block rr % nblk) and lands at cache row n0 + block.
+template <typename T>
+struct EpiCache {
+  T* cache;
+  const T* bias;
+  int64_t n_cap, n0, nblk, r0;
+  int nh, dh;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    if (bias) v += to_f32(bias[c]);
+    const int64_t rr = r0 + r;
+    const int64_t b = rr / nblk, i = rr - b * nblk;
+    const int hd = c / dh, e = c - hd * dh;
+    cache[(((int64_t)b * nh + hd) * n_cap + n0 + i) * dh + e] = from_f32<T>(v);
+  }
+};
+
+// ---- launch sequences ---------------------------------------------------------
+
+template <typename T>
+static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
+                        const void* x_blocks, int64_t nblk, char* ws) {
+  const DecodeWs W = decode_ws_layout(d);
+  const int64_t total = (int64_t)d.B * nblk;   // (sequence, block) rows of the [B*nblk, P*d] view
+  const int64_t row_elems = d.P * d.d;
+  for (int64_t r0 = 0; r0 < total; r0 += d.append_rows) {
+    const int rows = (int)std::min<int64_t>(d.append_rows, total - r0);
+    const T* zin = reinterpret_cast<const T*>(x_blocks) + r0 * row_elems;
+    int64_t lvl_rows = (int64_t)rows * d.P;
+    for (int j = 0; j < d.M; ++j) {  // compression C (Eq. 7, 16)
+      lvl_rows /= d.k[j];
+      GemmProblem pr{};
+      pr.a = zin;
+      pr.lda = (int64_t)d.k[j] * d.dl[j];
+      pr.b = w->compress[j].w;
+      pr.ldb = pr.lda;
+      pr.M = (int)lvl_rows;
+      pr.N = d.dl[j + 1];
+      pr.K = (int)pr.lda;
+      T* out = reinterpret_cast<T*>(ws + W.z[j + 1]);
+      EpiLinear<T> e{out, pr.N, reinterpret_cast<const T*>(w->compress[j].b), nullptr, 0, nullptr};
+      run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+      zin = out;
+    }
+    const pf_linear* maps[2] = {&w->k_proxy, &w->v_proxy};
+    void* caches[2] = {st.k_cache, st.v_cache};
+    for (int i = 0; i < 2; ++i) {  // cached rows K_p, V_p (Eq. 21)
+      GemmProblem pr{};
+      pr.a = zin;
+      pr.lda = d.d;
+      pr.b = maps[i]->w;
+      pr.ldb = d.d;
+      pr.M = rows;
+      pr.N = d.d;
+      pr.K = d.d;
+      EpiCache<T> e{reinterpret_cast<T*>(caches[i]), reinterpret_cast<const T*>(maps[i]->b), st.n_cap, st.n, nblk, r0,
+                    d.nh, d.dh};
+      run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    }
+  }
+}
+
+static void split_plan(int64_t n, int* splits, int* chunk) {
+  if (n <= 0) {
+    *splits = 0;
+    *chunk = kDecodeRowsPerSplit;
+    return;
+  }
+  int64_t c = kDecodeRowsPerSplit;
+  if ((n + c - 1) / c > kDecodeMaxSplits) c = (n + kDecodeMaxSplits - 1) / kDecodeMaxSplits;
+  *chunk = (int)c;
+  *splits = (int)((n + c - 1) / c);
+}
+
+template <typename T>
+static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
+                      const void* x_t, void* y_t, char* ws) {
+  const DecodeWs W = decode_ws_layout(d);
+  T* u = reinterpret_cast<T*>(ws + W.u);
+  T* q = reinterpret_cast<T*>(ws + W.q);
+  float* alpha = reinterpret_cast<float*>(ws + W.alpha);
+  T* attn = reinterpret_cast<T*>(ws + W.attn);
+  run.launch([&] {
+    hipLaunchKernelGGL((rmsnorm_kernel<T>), dim3(d.B), dim3(256), 0, run.stream, reinterpret_cast<const T*>(x_t),
+                       reinterpret_cast<const T*>(w->rms_gamma), u, reinterpret_cast<T*>(st.x_blk), d.d,
+                       (int64_t)(d.P * d.d), st.j, d.eps);
+    return hipGetLastError();
+  });
+  GemmProblem pr{};
+  pr.a = u;
+  pr.lda = d.d;
+  pr.ldb = d.d;
+  pr.M = d.B;
+  pr.N = d.d;
+  pr.K = d.d;
+  pr.b = w->q.w;
+  run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, EpiLinear<T>{q, d.d, reinterpret_cast<const T*>(w->q.b), nullptr, 0, nullptr});
+  pr.b = w->k.w;
+  run.gemm<T, LAYOUT_K, LAYOUT_K>(
+      pr, EpiSlot<T>{reinterpret_cast<T*>(st.k_loc), reinterpret_cast<const T*>(w->k.b), d.nh, d.dh, d.P, st.j});
+  pr.b = w->v.w;
+  run.gemm<T, LAYOUT_K, LAYOUT_K>(
+      pr, EpiSlot<T>{reinterpret_cast<T*>(st.v_loc), reinterpret_cast<const T*>(w->v.b), d.nh, d.dh, d.P, st.j});
+  pr.b = w->alpha.w;
+  pr.N = d.nh;
+  run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, EpiSigmoidF32<T>{alpha, reinterpret_cast<const T*>(w->alpha.b), d.nh});
+
+  int splits, chunk;
+  split_plan(st.n, &splits, &chunk);
+  DecodeAttnParams ap{};
+  ap.q = q;
+  ap.kc = st.k_cache;
+  ap.vc = st.v_cache;
+  ap.kl = st.k_loc;
+  ap.vl = st.v_loc;
+  ap.part_m = reinterpret_cast<float*>(ws + W.part_m);
+  ap.part_l = reinterpret_cast<float*>(ws + W.part_l);
+  ap.part_acc = reinterpret_cast<float*>(ws + W.part_acc);
+  ap.n = st.n;
+  ap.n_cap = st.n_cap;
+  ap.P = d.P;
+  ap.j = st.j;
+  ap.nh = d.nh;
+  ap.splits = splits;
+  ap.chunk = chunk;
+  ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  run.launch([&] {
+    const dim3 grid(splits + 1, d.B * d.nh);
+    if (d.dh == 64)
+      hipLaunchKernelGGL((decode_attn_kernel<T, 64>), grid, dim3(256), 0, run.stream, ap);
+    else
+      hipLaunchKernelGGL((decode_attn_kernel<T, 128>), grid, dim3(256), 0, run.stream, ap);
+    return hipGetLastError();
+  });
+  run.launch([&] {
+    if (d.dh == 64)
+      hipLaunchKernelGGL((decode_combine_kernel<T, 64>), dim3(d.B * d.nh), dim3(64), 0, run.stream, ap.part_m,
+                         ap.part_l, ap.part_acc, alpha, attn, d.nh, splits);
+    else
+      hipLaunchKernelGGL((decode_combine_kernel<T, 128>), dim3(d.B * d.nh), dim3(64), 0, run.stream, ap.part_m,
+                         ap.part_l, ap.part_acc, alpha, attn, d.nh, splits);
+    return hipGetLastError();
+  });
+  pr.a = attn;
+  pr.b = w->o.w;
+  pr.N = d.d;
+  run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, EpiLinear<T>{reinterpret_cast<T*>(y_t), d.d, reinterpret_cast<const T*>(w->o.b),
+                                                   reinterpret_cast<const T*>(x_t), d.d, nullptr});
+}
+
+// Split-K need of every GEMM a step or an append can issue (any chunk size).
+static size_t decode_gemm_need(const DecodeDims& d) {
+  Runner dry(true);
+  pf_decode_weights nw{};
+  pf_decode_state ns{};
+  ns.n_cap = 1;
+  for (int rows = 1; rows <= d.append_rows; ++rows) {
+    // one append of `rows` blocks of a single sequence exercises every chunk size
+    DecodeDims d1 = d;
+    d1.B = 1;
+    if (d.esize == 2)
+      append_impl<bf16>(dry, d1, &nw, ns, nullptr, rows, nullptr);
+    else
+      append_impl<float>(dry, d1, &nw, ns, nullptr, rows, nullptr);
+  }
+  if (d.esize == 2)
+    step_impl<bf16>(dry, d, &nw, ns, nullptr, nullptr, nullptr);
+  else
+    step_impl<float>(dry, d, &nw, ns, nullptr, nullptr, nullptr);
+  return dry.gemm_need;
+}
+
+DecodeWs decode_ws(const DecodeDims& d) {
+  // memoised: the sizing sweep is pure arithmetic but runs on every call
+  static thread_local DecodeDims last{};
+  static thread_local size_t last_need = 0;
+  static thread_local bool have = false;
+  DecodeWs w = decode_ws_layout(d);
+  size_t need;
+  if (have && memcmp(&last, &d, sizeof(d)) == 0) {
+    need = last_need;
+  } else {
+    need = decode_gemm_need(d);
+    last = d;
+    last_need = need;
+    have = true;
+  }
+  w.bytes = w.gemm + align256(need);
+  return w;
+}
+
+template <typename T>
+hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
+                           const void* x_t, void* y_t, char* ws, hipStream_t stream) {
+  const DecodeWs W = decode_ws_layout(d);
+  Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
+  step_impl<T>(run, d, w, st, x_t, y_t, ws);
+  return run.err;
+}
+
+template <typename T>
+hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
+                            const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream) {
+  const DecodeWs W = decode_ws_layout(d);
+  Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
+  append_impl<T>(run, d, w, st, x_blocks, nblk, ws);
+  return run.err;
+}
+
+template hipError_t decode_step_run<bf16>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
+                                          const void*, void*, char*, hipStream_t);
+template hipError_t decode_step_run<float>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
+                                           const void*, void*, char*, hipStream_t);
+template hipError_t cache_append_run<bf16>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
+                                           const void*, int64_t, char*, hipStream_t);
+template hipError_t cache_append_run<float>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
+                                            const void*, int64_t, char*, hipStream_t);
+
+}  // namespace pf

@@ -1,0 +1,46 @@
+// Proxy-KV-cache decode (Eq. 19-21, Sec. 3.8): sizes, workspace layout and
+// the launch sequences of the decode step and the cache append.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/proxyformer.h"
+
+namespace pf {
+
+struct DecodeDims {
+  int B, d, nh, dh, M;
+  int k[PF_MAX_LEVELS];
+  int dl[PF_MAX_LEVELS + 1];  // d_0 = d_model ... d_M = d_model
+  int64_t P;
+  int esize;
+  float eps;
+  int append_rows;            // rows (sequence, block) compressed per append GEMM chunk
+};
+
+constexpr int kDecodeMaxSplits = 256;   // cache-row slices per (sequence, head)
+constexpr int kDecodeRowsPerSplit = 1024;
+
+struct DecodeWs {
+  size_t u, q, alpha, attn;         // [B, d], [B, d], fp32 [B, h], [B, d]
+  size_t part_m, part_l, part_acc;  // fp32 partial softmax states
+  size_t z[PF_MAX_LEVELS];          // append: compression level outputs (j = 1..M)
+  size_t gemm;
+  size_t bytes;
+};
+
+int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why);
+DecodeWs decode_ws(const DecodeDims& d);
+
+template <typename T>
+hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
+                           const void* x_t, void* y_t, char* ws, hipStream_t stream);
+
+template <typename T>
+hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
+                            const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream);
+
+}  // namespace pf

@@ -1,0 +1,437 @@
+// Tiled MFMA GEMM for gfx950 with pluggable epilogues.
+//
+// Computes C[m][n] = sum_k A(m, k) * B(n, k) for m < M, n < N, k < K and hands
+// every fp32 result to an epilogue functor epi(row, col, value).
+//  A(m,k): LAYOUT_K  -> A[m * lda + k]  (row-major, reduction contiguous)
+//          LAYOUT_MN -> A[k * lda + m]  (reduction strided)
+//  B(n,k): LAYOUT_K  -> B[n * ldb + k]  (a weight stored [out, in])
+//          LAYOUT_MN -> B[k * ldb + n]
+// Optional A features, both handled in the tile loader:
+//  - concatenation along K: for k >= a_ksplit the values come from A2
+//    (A2[m * lda2 + k - a_ksplit]); used for the gate input [X, Delta].
+//  - row shift: with a_shift_period p > 0, row m reads row m-1 of A, and rows
+//    with m % p == 0 read zeros; used to feed proxy i-1 to block i.
+// Split-K: gridDim.z slices of the reduction range, each slice handing its
+// partial sums to the epilogue (normally a store into an fp32 workspace,
+// reduced afterwards in a fixed order, so results are deterministic).
+//
+// Design: a workgroup owns a BM x BN tile, WM x WN waves each own a
+// (BM/WM) x (BN/WN) sub-tile made of 32x32 MFMA tiles. K advances BK at a
+// time through two LDS buffers; the next K slice is fetched from global
+// memory into registers while the current one is multiplied. Operands in
+// LAYOUT_MN are transposed in registers (VEC x VEC blocks) before they are
+// written to LDS, so LDS always holds rows contiguous along K and every lane
+// reads its MFMA fragment with 16-byte LDS reads. Rows are padded by 16 bytes
+// so that the 32 rows a fragment read touches fall in distinct banks.
+// Workgroups are dealt to the 8 XCDs round-robin; the tile index is remapped
+// so that each XCD works on a contiguous band of tiles (shared L2), and
+// within the band GROUP_M row tiles are visited per column sweep.
+#pragma once
+
+#include <algorithm>
+#include <type_traits>
+
+#include "common.hpp"
+
+namespace pf {
+
+enum { LAYOUT_K = 0, LAYOUT_MN = 1 };
+
+struct GemmParams {
+  const void* a;
+  int64_t lda;
+  const void* a2;
+  int64_t lda2;
+  int a_ksplit;        // K index where A2 starts (>= K: unused)
+  int a_shift_period;  // 0: off
+  const void* b;
+  int64_t ldb;
+  int M, N, K;
+  int k_slice;         // reduction length per gridDim.z slice (multiple of BK)
+  int tiles_m, tiles_n;
+  int group_m;
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN>
+struct GemmShape {
+  static constexpr int kThreads = WM * WN * kWave;
+  static constexpr int kVec = 16 / sizeof(T);  // elements per 16-byte access
+  static constexpr int kStride = BK + kVec;    // LDS row stride (elements)
+  static constexpr int kTM = BM / WM, kTN = BN / WN;
+  static constexpr int kFM = kTM / 32, kFN = kTN / 32;
+  static constexpr int kALoads = BM * BK / (kThreads * kVec);
+  static constexpr int kBLoads = BN * BK / (kThreads * kVec);
+  static constexpr int kStageElems = (BM + BN) * kStride;
+  static constexpr size_t kLdsBytes = 2 * kStageElems * sizeof(T);
+  static_assert(BK % 16 == 0, "BK must hold whole k16 steps");
+  static_assert(kTM % 32 == 0 && kTN % 32 == 0, "wave tile must be whole 32x32 MFMA tiles");
+  static_assert((BM * BK) % (kThreads * kVec) == 0, "A tile must split evenly");
+  static_assert((BN * BK) % (kThreads * kVec) == 0, "B tile must split evenly");
+};
+
+// ---- tile loaders: global -> registers -> LDS ------------------------------
+
+// Rows of the tile are contiguous along K in global memory.
+template <typename T, int ROWS, int BK, int NT, bool IS_A>
+struct LoaderK {
+  static constexpr int kVec = 16 / sizeof(T);
+  static constexpr int kChunks = BK / kVec;  // 16-byte chunks per row
+  static constexpr int kLoads = ROWS * BK / (NT * kVec);
+
+  static __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], const GemmParams& p, int row0,
+                                               int rows_total, int k0, int kend, int tid) {
+    const T* base = reinterpret_cast<const T*>(IS_A ? p.a : p.b);
+    const int64_t ld = IS_A ? p.lda : p.ldb;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int v = tid + i * NT;
+      const int row = v / kChunks;
+      const int k = k0 + (v % kChunks) * kVec;
+      int grow = row0 + row;
+      bool ok = grow < rows_total && k < kend;
+      if (IS_A && p.a_shift_period > 0) {
+        ok = ok && (grow % p.a_shift_period) != 0;
+        grow -= 1;
+      }
+      u32x4 val = {0u, 0u, 0u, 0u};
+      if (ok) {
+        if (IS_A && k >= p.a_ksplit) {
+          const T* a2 = reinterpret_cast<const T*>(p.a2);
+          val = ld16(a2 + (int64_t)grow * p.lda2 + (k - p.a_ksplit));
+        } else {
+          val = ld16(base + (int64_t)grow * ld + k);
+        }
+      }
+      r[i] = val;
+    }
+  }
+
+  static __device__ __forceinline__ void stash(const u32x4 (&r)[kLoads], T* lds, int stride, int tid) {
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int v = tid + i * NT;
+      st16(lds + (v / kChunks) * stride + (v % kChunks) * kVec, r[i]);
+    }
+  }
+};
+
+// Tile rows are contiguous along M (or N) in global memory: element (row, k)
+// sits at base[k * ld + row]. Each thread fetches VEC x VEC blocks and
+// transposes them in registers.
+template <typename T, int ROWS, int BK, int NT, bool IS_A>
+struct LoaderMN {
+  static constexpr int kVec = 16 / sizeof(T);
+  static constexpr int kRowBlocks = ROWS / kVec;
+  static constexpr int kTotalBlocks = ROWS * BK / (kVec * kVec);
+  static constexpr int kBlocks = (kTotalBlocks + NT - 1) / NT;  // blocks per thread (some idle)
+  static constexpr int kLoads = kBlocks * kVec;
+  static_assert(ROWS % kVec == 0 && BK % kVec == 0, "tile must hold whole VEC x VEC blocks");
+
+  static __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], const GemmParams& p, int row0,
+                                               int rows_total, int k0, int kend, int tid) {
+    const T* base = reinterpret_cast<const T*>(IS_A ? p.a : p.b);
+    const int64_t ld = IS_A ? p.lda : p.ldb;
+#pragma unroll
+    for (int bi = 0; bi < kBlocks; ++bi) {
+      const int blk = tid + bi * NT;
+      const int row = row0 + (blk % kRowBlocks) * kVec;
+      const int kb = k0 + (blk / kRowBlocks) * kVec;
+      const bool active = (kTotalBlocks % NT == 0) || blk < kTotalBlocks;
+#pragma unroll
+      for (int t = 0; t < kVec; ++t) {
+        const int k = kb + t;
+        u32x4 val = {0u, 0u, 0u, 0u};
+        if (active && row < rows_total && k < kend) val = ld16(base + (int64_t)k * ld + row);
+        r[bi * kVec + t] = val;
+      }
+    }
+  }
+
+  static __device__ __forceinline__ void stash(const u32x4 (&r)[kLoads], T* lds, int stride, int tid) {
+#pragma unroll
+    for (int bi = 0; bi < kBlocks; ++bi) {
+      const int blk = tid + bi * NT;
+      if ((kTotalBlocks % NT) != 0 && blk >= kTotalBlocks) continue;
+      const int row = (blk % kRowBlocks) * kVec;
+      const int kb = (blk / kRowBlocks) * kVec;
+      const u32x4* in = &r[bi * kVec];
+      if constexpr (sizeof(T) == 2) {
+        // 8x8 block of 16-bit values: in[t] = k-row t, halves = rows.
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          u32x4 o;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t x = in[2 * w][c >> 1];
+            const uint32_t y = in[2 * w + 1][c >> 1];
+            o[w] = (c & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+          }
+          st16(lds + (row + c) * stride + kb, o);
+        }
+      } else {
+        // 4x4 block of 32-bit values.
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          u32x4 o;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) o[w] = in[w][c];
+          st16(lds + (row + c) * stride + kb, o);
+        }
+      }
+    }
+  }
+};
+
+template <typename T, int ROWS, int BK, int NT, bool IS_A, int LAYOUT>
+using Loader = typename std::conditional<LAYOUT == LAYOUT_K, LoaderK<T, ROWS, BK, NT, IS_A>,
+                                         LoaderMN<T, ROWS, BK, NT, IS_A>>::type;
+
+// Tile index remap: contiguous bands per XCD, GROUP_M-row column sweeps.
+__device__ __forceinline__ void tile_coords(const GemmParams& p, int& tm, int& tn) {
+  const int T = p.tiles_m * p.tiles_n;
+  const int wg = blockIdx.x;
+  const int q = T / kNumXcd, rem = T % kNumXcd;
+  const int xcd = wg % kNumXcd, local = wg / kNumXcd;
+  const int t = (xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q) + local;
+  const int gsz = p.group_m * p.tiles_n;
+  const int g = t / gsz;
+  const int first_m = g * p.group_m;
+  const int gm = min(p.tiles_m - first_m, p.group_m);
+  const int w = t % gsz;
+  tm = first_m + w % gm;
+  tn = w / gm;
+}
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, int LA, int LB, class Epi>
+__global__ void __launch_bounds__(WM* WN* kWave)
+    gemm_kernel(const GemmParams p, const Epi epi) {
+  typedef GemmShape<T, BM, BN, BK, WM, WN> S;
+  typedef Loader<T, BM, BK, S::kThreads, true, LA> LdA;
+  typedef Loader<T, BN, BK, S::kThreads, false, LB> LdB;
+  typedef Mma<T> MM;
+  __shared__ __attribute__((aligned(16))) T smem[2 * S::kStageElems];
+
+  int tm, tn;
+  tile_coords(p, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = blockIdx.z * p.k_slice;
+  const int kend = min(p.K, kbeg + p.k_slice);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  f32x16 acc[S::kFM][S::kFN];
+#pragma unroll
+  for (int i = 0; i < S::kFM; ++i)
+#pragma unroll
+    for (int j = 0; j < S::kFN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  u32x4 ra[LdA::kLoads], rb[LdB::kLoads];
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  if (nk > 0) {
+    LdA::fetch(ra, p, m0, p.M, kbeg, kend, tid);
+    LdB::fetch(rb, p, n0, p.N, kbeg, kend, tid);
+    LdA::stash(ra, smem, S::kStride, tid);
+    LdB::stash(rb, smem + BM * S::kStride, S::kStride, tid);
+  }
+  __syncthreads();
+
+  const int frow = lane & 31;
+  const int fk = (lane >> 5) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    T* cur = smem + (kt & 1) * S::kStageElems;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      LdA::fetch(ra, p, m0, p.M, kbeg + (kt + 1) * BK, kend, tid);
+      LdB::fetch(rb, p, n0, p.N, kbeg + (kt + 1) * BK, kend, tid);
+    }
+    const T* sa = cur + (wm * S::kTM + frow) * S::kStride + fk;
+    const T* sb = cur + (BM + wn * S::kTN + frow) * S::kStride + fk;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      typename MM::frag fa[S::kFM], fb[S::kFN];
+#pragma unroll
+      for (int i = 0; i < S::kFM; ++i) fa[i] = MM::load(sa + i * 32 * S::kStride + kk);
+#pragma unroll
+      for (int j = 0; j < S::kFN; ++j) fb[j] = MM::load(sb + j * 32 * S::kStride + kk);
+#pragma unroll
+      for (int i = 0; i < S::kFM; ++i)
+#pragma unroll
+        for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[i], fb[j], acc[i][j]);
+    }
+    if (more) {
+      T* nxt = smem + ((kt + 1) & 1) * S::kStageElems;
+      LdA::stash(ra, nxt, S::kStride, tid);
+      LdB::stash(rb, nxt + BM * S::kStride, S::kStride, tid);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue: lane holds column (lane % 32), rows acc_row(r, lane) of each tile.
+#pragma unroll
+  for (int i = 0; i < S::kFM; ++i) {
+#pragma unroll
+    for (int j = 0; j < S::kFN; ++j) {
+      const int col = n0 + wn * S::kTN + j * 32 + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * S::kTM + i * 32 + acc_row(r, lane);
+        if (row < p.M && col < p.N) epi(row, col, acc[i][j][r]);
+      }
+    }
+  }
+}
+
+// Fixed-order reduction of split-K partials ws[s][M][N], then the epilogue.
+template <class Epi>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(const float* __restrict__ ws, int splits, int M,
+                                                            int N, const Epi epi) {
+  const int64_t total = (int64_t)M * N;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    float s = 0.0f;
+    for (int z = 0; z < splits; ++z) s += ws[(int64_t)z * total + idx];
+    epi((int)(idx / N), (int)(idx % N), s);
+  }
+}
+
+// Epilogue writing split-K partials.
+struct EpiPartial {
+  float* ws;
+  int N;
+  int64_t slice_stride;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    ws[(int64_t)blockIdx.z * slice_stride + (int64_t)r * N + c] = v;
+  }
+};
+
+// ---- host side --------------------------------------------------------------
+
+struct GemmProblem {
+  const void* a;
+  int64_t lda;
+  const void* a2 = nullptr;
+  int64_t lda2 = 0;
+  int a_ksplit = 1 << 30;
+  int a_shift_period = 0;
+  const void* b;
+  int64_t ldb;
+  int M, N, K;
+};
+
+// Tile configuration chosen for a problem.
+enum GemmTile { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x64 = 2 };
+
+struct GemmPlan {
+  int tile;
+  int bm, bn, bk;
+  int splits;
+  int k_slice;
+};
+
+template <typename T>
+inline GemmPlan plan_gemm(const GemmProblem& pr, int num_cu) {
+  GemmPlan pl;
+  const int64_t mn = (int64_t)pr.M * pr.N;
+  if (sizeof(T) == 4) {
+    pl.tile = TILE_128x128;
+    pl.bm = pl.bn = 128;
+    pl.bk = 32;
+  } else if (mn >= (int64_t)256 * 256 * num_cu && pr.M >= 256 && pr.N >= 256) {
+    pl.tile = TILE_256x256;
+    pl.bm = pl.bn = 256;
+    pl.bk = 64;
+  } else if (mn >= (int64_t)128 * 128 * num_cu / 2 || pr.M > 64 || pr.N > 64) {
+    pl.tile = TILE_128x128;
+    pl.bm = pl.bn = 128;
+    pl.bk = 64;
+  } else {
+    pl.tile = TILE_64x64;
+    pl.bm = pl.bn = 64;
+    pl.bk = 64;
+  }
+  const int64_t tiles = (int64_t)((pr.M + pl.bm - 1) / pl.bm) * ((pr.N + pl.bn - 1) / pl.bn);
+  const int kblocks = (pr.K + pl.bk - 1) / pl.bk;
+  int splits = 1;
+  // Deterministic split-K when the tile grid cannot fill the chip and the
+  // reduction is long enough for each slice to stay efficient.
+  while (tiles * splits < num_cu && kblocks / (splits * 2) >= 8) splits *= 2;
+  const int kb_per = (kblocks + splits - 1) / splits;
+  pl.k_slice = kb_per * pl.bk;
+  pl.splits = (kblocks + kb_per - 1) / kb_per;
+  return pl;
+}
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, int LA, int LB, class Epi>
+inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, const Epi& epi,
+                                   hipStream_t stream) {
+  GemmParams p;
+  p.a = pr.a;
+  p.lda = pr.lda;
+  p.a2 = pr.a2;
+  p.lda2 = pr.lda2;
+  p.a_ksplit = pr.a_ksplit;
+  p.a_shift_period = pr.a_shift_period;
+  p.b = pr.b;
+  p.ldb = pr.ldb;
+  p.M = pr.M;
+  p.N = pr.N;
+  p.K = pr.K;
+  p.k_slice = pl.k_slice;
+  p.tiles_m = (pr.M + BM - 1) / BM;
+  p.tiles_n = (pr.N + BN - 1) / BN;
+  p.group_m = 8;
+  dim3 grid(p.tiles_m * p.tiles_n, 1, pl.splits);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, BK, WM, WN, LA, LB, Epi>), grid,
+                     dim3(WM * WN * kWave), 0, stream, p, epi);
+  return hipGetLastError();
+}
+
+template <typename T, int LA, int LB, class Epi>
+inline hipError_t launch_gemm_plan(const GemmProblem& pr, const GemmPlan& pl, const Epi& epi,
+                                   hipStream_t stream) {
+  if constexpr (sizeof(T) == 4) {
+    return launch_gemm_tile<T, 128, 128, 32, 2, 2, LA, LB>(pr, pl, epi, stream);
+  } else {
+    switch (pl.tile) {
+      case TILE_256x256:
+        return launch_gemm_tile<T, 256, 256, 64, 2, 2, LA, LB>(pr, pl, epi, stream);
+      case TILE_128x128:
+        return launch_gemm_tile<T, 128, 128, 64, 2, 2, LA, LB>(pr, pl, epi, stream);
+      default:
+        return launch_gemm_tile<T, 64, 64, 64, 2, 2, LA, LB>(pr, pl, epi, stream);
+    }
+  }
+}
+
+// Bytes of fp32 workspace a problem needs for split-K partials.
+template <typename T>
+inline size_t gemm_workspace_bytes(const GemmProblem& pr, int num_cu) {
+  const GemmPlan pl = plan_gemm<T>(pr, num_cu);
+  return pl.splits > 1 ? (size_t)pl.splits * pr.M * pr.N * sizeof(float) : 0;
+}
+
+// Run C = A B^T through `epi`, splitting K through `ws` when that helps.
+template <typename T, int LA, int LB, class Epi>
+inline hipError_t run_gemm(const GemmProblem& pr, const Epi& epi, float* ws, int num_cu,
+                           hipStream_t stream) {
+  if (pr.M <= 0 || pr.N <= 0) return hipSuccess;
+  GemmPlan pl = plan_gemm<T>(pr, num_cu);
+  if (pl.splits <= 1 || ws == nullptr) {
+    pl.splits = 1;
+    pl.k_slice = ((pr.K + pl.bk - 1) / pl.bk) * pl.bk;
+    if (pl.k_slice == 0) pl.k_slice = pl.bk;
+    return launch_gemm_plan<T, LA, LB>(pr, pl, epi, stream);
+  }
+  EpiPartial part{ws, pr.N, (int64_t)pr.M * pr.N};
+  hipError_t e = launch_gemm_plan<T, LA, LB>(pr, pl, part, stream);
+  if (e != hipSuccess) return e;
+  const int64_t total = (int64_t)pr.M * pr.N;
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL((splitk_reduce_kernel<Epi>), dim3(blocks), dim3(256), 0, stream, ws, pl.splits,
+                     pr.M, pr.N, epi);
+  return hipGetLastError();
+}
+
+}  // namespace pf

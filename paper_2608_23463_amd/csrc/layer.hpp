@@ -1,0 +1,82 @@
+// Host-side planning shared by the layer entry points: derived sizes and the
+// byte layout of the saved-activation region and the workspace.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/proxyformer.h"
+
+namespace pf {
+
+constexpr int kPlanCUs = 256;  // MI355X compute units; fixes split-K plans (and workspace sizes)
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct LayerDims {
+  int B;
+  int64_t L;
+  int d_f, d_p, nh, dh;
+  int M;            // levels
+  int k[PF_MAX_LEVELS];
+  int d[PF_MAX_LEVELS + 1];       // d[0] = d_fine ... d[M] = d_proxy
+  int64_t R[PF_MAX_LEVELS + 1];   // rows per sequence after j levels; R[0] = L, R[M] = m
+  int64_t P, m;
+  int ld_t;         // row stride of transposed per-head tensors (m rounded up to 64)
+  int esize;        // bytes per activation element
+};
+
+// Byte offsets of every activation inside the region that holds them
+// (the caller's `saved` buffer, or the workspace when saved is NULL).
+struct LayerActs {
+  size_t z[PF_MAX_LEVELS];    // Z_j, j = 1..M-1: compression level outputs [B*R_j, d_j]
+  size_t h;                   // H = H_in + c [B*m, d_p] (copy kept for the backward)
+  size_t q, k, v;             // [B, h, m, dh]
+  size_t qt, kt, vt;          // [B, h, dh, ld_t]
+  size_t o;                   // [B*m, d_p]
+  size_t lse;                 // [B, h, m] fp32
+  size_t hbar;                // [B*m, d_p] (output of W_o, before the shift)
+  size_t u[PF_MAX_LEVELS];    // U_j, j = 1..M-1: decompression level outputs [B*R_j, d_j]
+  size_t delta;               // [B*L, d_f]
+  size_t g;                   // gate pre-activation G [B*L, d_f]
+  size_t bytes;
+};
+
+struct LayerWs {
+  size_t acts;      // forward activations when saved == NULL
+  size_t gemm;      // split-K partials
+  // backward scratch
+  size_t dg, ddelta;          // [B*L, d_f]
+  size_t du[PF_MAX_LEVELS];   // dU_j j = 1..M-1 [B*R_j, d_j]
+  size_t ds;                  // dS (shifted) [B*m, d_p]
+  size_t dhbar;               // [B*m, d_p]
+  size_t dO, dOt;             // [B*m, d_p], [B, h, dh, ld_t]
+  size_t delta_rs;            // [B, h, m] fp32
+  size_t dq, dk, dv;          // fp32 [B*m, d_p]
+  size_t dqkv_t;              // dtype copies of dq, dk, dv for the projection GEMMs [3][B*m, d_p]
+  size_t dh;                  // [B*m, d_p]
+  size_t dz[PF_MAX_LEVELS];   // dZ_j j = 1..M-1 [B*R_j, d_j]
+  size_t bytes;
+};
+
+// Validates cfg; on failure returns a status and writes a message.
+int layer_dims(const pf_layer_config* cfg, LayerDims* d, const char** why);
+LayerActs layer_acts(const LayerDims& d, bool for_backward);
+LayerWs layer_ws(const LayerDims& d, bool for_backward);
+
+template <typename T>
+hipError_t layer_forward_run(const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
+                             const void* x, const void* h_in, void* x_out, void* h_out, char* acts,
+                             bool saving, char* ws, hipStream_t stream);
+
+template <typename T>
+hipError_t layer_backward_run(const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
+                              const void* x, const void* h_in, const char* saved, const void* dy,
+                              const void* dh_out, void* dx, void* dh_in, const pf_layer_grads* gr,
+                              char* ws, hipStream_t stream);
+
+size_t layer_gemm_ws_bytes(const LayerDims& d, bool for_backward);
+
+}  // namespace pf

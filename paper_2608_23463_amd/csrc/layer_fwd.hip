@@ -1,0 +1,300 @@
+// ProxyFormer layer forward (Algorithm 1): planning of sizes and buffers,
+// and the sequence of kernels that computes X^(l), H^(l) from X^(l-1), H^(l-1).
+//
+//  1. compression, one GEMM per level (Eq. 7, 15-16); the block partition of
+//     Eq. 2 and the grouping of Eq. 16 are zero-copy views of row-major data,
+//     and the last level's epilogue adds b_c and H_in (Eq. 8) and writes H.
+//  2. Q, K, V projections of H, written per head (V key-contiguous).
+//  3. causal flash attention over the m proxies (Eq. 9).
+//  4. output map W_o -> contextualised proxies.
+//  5. decompression, one GEMM per level from level M down to 1 (Eq. 10, 17);
+//     the first reads proxy i-1 for block i (token-causal injection) through
+//     a row shift in the GEMM's tile loader.
+//  6. gate GEMM over [X, Delta] with the injection X + sigmoid(G) * Delta in
+//     its epilogue (Eq. 12).
+#include <algorithm>
+
+#include "attention.hpp"
+#include "epilogues.hpp"
+#include "layer.hpp"
+#include "runner.hpp"
+
+namespace pf {
+
+__global__ void fill_zero_kernel(u32x4* p, size_t n16) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) p[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
+hipError_t fill_zero(void* p, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  const size_t n16 = bytes / 16;  // every buffer here is a multiple of 16 bytes
+  const int blocks = (int)std::min<size_t>((n16 + 255) / 256, 4096);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, reinterpret_cast<u32x4*>(p), n16);
+  return hipGetLastError();
+}
+
+int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
+  *why = nullptr;
+  if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
+  if (c->dtype != PF_FP32 && c->dtype != PF_BF16) return *why = "dtype must be PF_FP32 or PF_BF16", PF_ERR_INVALID_ARG;
+  if (c->mask < PF_TOKEN_CAUSAL || c->mask > PF_BIDIRECTIONAL) return *why = "unknown mask mode", PF_ERR_INVALID_ARG;
+  if (c->batch < 1 || c->seq_len < 1) return *why = "batch and seq_len must be >= 1", PF_ERR_INVALID_ARG;
+  if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
+  if (c->d_fine < 1 || c->d_proxy < 1 || c->n_heads < 1 || c->head_dim < 1)
+    return *why = "widths and head counts must be >= 1", PF_ERR_INVALID_ARG;
+  if ((int64_t)c->n_heads * c->head_dim != c->d_proxy) return *why = "n_heads * head_dim must equal d_proxy", PF_ERR_INVALID_ARG;
+  d->B = c->batch;
+  d->L = c->seq_len;
+  d->d_f = c->d_fine;
+  d->d_p = c->d_proxy;
+  d->nh = c->n_heads;
+  d->dh = c->head_dim;
+  d->M = c->n_levels;
+  d->P = 1;
+  for (int j = 0; j < d->M; ++j) {
+    if (c->factors[j] < 1) return *why = "every factor k_j must be >= 1", PF_ERR_INVALID_ARG;
+    d->k[j] = c->factors[j];
+    d->P *= c->factors[j];
+    if (d->P > (1 << 20)) return *why = "block size P too large", PF_ERR_INVALID_ARG;
+  }
+  if (d->L % d->P != 0) return *why = "seq_len must be a multiple of P = prod(factors)", PF_ERR_INVALID_ARG;
+  d->d[0] = d->d_f;
+  for (int j = 1; j < d->M; ++j) d->d[j] = c->level_dims[j - 1] > 0 ? c->level_dims[j - 1] : d->d_p;
+  d->d[d->M] = d->d_p;
+  d->R[0] = d->L;
+  for (int j = 1; j <= d->M; ++j) d->R[j] = d->R[j - 1] / d->k[j - 1];
+  d->m = d->R[d->M];
+  d->ld_t = (int)((d->m + 63) / 64 * 64);
+  d->esize = c->dtype == PF_BF16 ? 2 : 4;
+  if ((int64_t)d->B * d->L > INT32_MAX) return *why = "batch * seq_len exceeds 2^31 - 1 rows", PF_ERR_UNSUPPORTED;
+  for (int j = 0; j <= d->M; ++j)
+    if (d->d[j] % 8 != 0) return *why = "every channel width must be a multiple of 8", PF_ERR_UNSUPPORTED;
+  for (int j = 0; j < d->M; ++j)
+    if ((int64_t)d->k[j] * d->d[j] > INT32_MAX / 2) return *why = "k_j * d_j too large", PF_ERR_UNSUPPORTED;
+  if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
+  return PF_OK;
+}
+
+LayerActs layer_acts(const LayerDims& d, bool bwd) {
+  LayerActs a{};
+  size_t off = 0;
+  const size_t es = d.esize;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t prox = (size_t)d.B * d.m * d.d_p * es;
+  const size_t headt = (size_t)d.B * d.nh * d.dh * d.ld_t * es;
+  for (int j = 1; j < d.M; ++j) a.z[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+  a.h = bwd ? take(prox) : 0;
+  a.q = take(prox);
+  a.k = take(prox);
+  a.v = bwd ? take(prox) : 0;
+  a.qt = bwd ? take(headt) : 0;
+  a.kt = bwd ? take(headt) : 0;
+  a.vt = take(headt);
+  a.o = take(prox);
+  a.lse = take((size_t)d.B * d.nh * d.m * 4);
+  a.hbar = take(prox);
+  for (int j = 1; j < d.M; ++j) a.u[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+  a.delta = take((size_t)d.B * d.L * d.d_f * es);
+  a.g = bwd ? take((size_t)d.B * d.L * d.d_f * es) : 0;
+  a.bytes = off;
+  return a;
+}
+
+LayerWs layer_ws(const LayerDims& d, bool bwd) {
+  LayerWs w{};
+  size_t off = 0;
+  const size_t es = d.esize;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t prox = (size_t)d.B * d.m * d.d_p * es;
+  const size_t tok = (size_t)d.B * d.L * d.d_f * es;
+  if (!bwd) {
+    w.acts = take(layer_acts(d, false).bytes);
+  } else {
+    w.dg = take(tok);
+    w.ddelta = take(tok);
+    for (int j = 1; j < d.M; ++j) w.du[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+    w.ds = take(prox);
+    w.dhbar = take(prox);
+    w.dO = take(prox);
+    w.dOt = take((size_t)d.B * d.nh * d.dh * d.ld_t * es);
+    w.delta_rs = take((size_t)d.B * d.nh * d.m * 4);
+    const size_t proxf = (size_t)d.B * d.m * d.d_p * 4;
+    w.dq = take(proxf);
+    w.dk = take(proxf);
+    w.dv = take(proxf);
+    w.dqkv_t = take(3 * prox);
+    w.dh = take(prox);
+    for (int j = 1; j < d.M; ++j) w.dz[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+  }
+  w.gemm = take(layer_gemm_ws_bytes(d, bwd));
+  w.bytes = off;
+  return w;
+}
+
+template <typename T>
+static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
+                         const void* x, const void* h_in, void* x_out, void* h_out, char* act, bool saving) {
+  const LayerActs A = layer_acts(d, saving);
+  auto P = [&](size_t off) { return reinterpret_cast<T*>(act + off); };
+  const int64_t rows_m = (int64_t)d.B * d.m;
+
+  // 1. compression cascade (Eq. 7, 16) and the residual proxy update (Eq. 8)
+  const T* zin = reinterpret_cast<const T*>(x);
+  for (int j = 0; j < d.M; ++j) {
+    GemmProblem pr{};
+    pr.a = zin;
+    pr.lda = (int64_t)d.k[j] * d.d[j];
+    pr.b = w->compress[j].w;
+    pr.ldb = pr.lda;
+    pr.M = (int)(d.B * d.R[j + 1]);
+    pr.N = d.d[j + 1];
+    pr.K = (int)pr.lda;
+    EpiLinear<T> e{};
+    e.bias = reinterpret_cast<const T*>(w->compress[j].b);
+    if (j == d.M - 1) {
+      e.out = reinterpret_cast<T*>(h_out);
+      e.ldo = d.d_p;
+      e.add = reinterpret_cast<const T*>(h_in);
+      e.ld_add = d.d_p;
+      e.out2 = saving ? P(A.h) : nullptr;
+    } else {
+      e.out = P(A.z[j + 1]);
+      e.ldo = d.d[j + 1];
+    }
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    zin = e.out;
+  }
+
+  // 2. projections of H into per-head Q, K (row layout) and V (key-contiguous)
+  const T* hbuf = reinterpret_cast<const T*>(h_out);
+  if (d.ld_t != d.m) {
+    // padding columns of the transposed tensors must read as zero
+    const size_t tb = (size_t)d.B * d.nh * d.dh * d.ld_t * sizeof(T);
+    run.launch([&] { return fill_zero(P(A.vt), tb, run.stream); });
+    if (saving) {
+      run.launch([&] { return fill_zero(P(A.qt), tb, run.stream); });
+      run.launch([&] { return fill_zero(P(A.kt), tb, run.stream); });
+    }
+  }
+  const pf_linear* proj[3] = {&w->q, &w->k, &w->v};
+  T* outs[3] = {P(A.q), P(A.k), saving ? P(A.v) : nullptr};
+  T* outs_t[3] = {saving ? P(A.qt) : nullptr, saving ? P(A.kt) : nullptr, P(A.vt)};
+  for (int i = 0; i < 3; ++i) {
+    GemmProblem pr{};
+    pr.a = hbuf;
+    pr.lda = d.d_p;
+    pr.b = proj[i]->w;
+    pr.ldb = d.d_p;
+    pr.M = (int)rows_m;
+    pr.N = d.d_p;
+    pr.K = d.d_p;
+    EpiHeads<T> e{outs[i], outs_t[i], reinterpret_cast<const T*>(proj[i]->b), (int)d.m, d.dh, d.nh, d.ld_t};
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+  }
+
+  // 3. attention over the proxies (Eq. 9)
+  AttnParams ap{};
+  ap.q = P(A.q);
+  ap.k = P(A.k);
+  ap.vt = P(A.vt);
+  ap.o = P(A.o);
+  ap.lse = reinterpret_cast<float*>(act + A.lse);
+  ap.m = (int)d.m;
+  ap.n_heads = d.nh;
+  ap.ld_t = d.ld_t;
+  ap.causal = cfg->mask != PF_BIDIRECTIONAL;
+  ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  run.launch([&] { return launch_attention_fwd<T>(ap, d.B, d.dh, run.stream); });
+
+  // 4. output map of the interaction
+  {
+    GemmProblem pr{};
+    pr.a = P(A.o);
+    pr.lda = d.d_p;
+    pr.b = w->o.w;
+    pr.ldb = d.d_p;
+    pr.M = (int)rows_m;
+    pr.N = d.d_p;
+    pr.K = d.d_p;
+    EpiLinear<T> e{P(A.hbar), d.d_p, reinterpret_cast<const T*>(w->o.b), nullptr, 0, nullptr};
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+  }
+
+  // 5. decompression, level M down to 1 (Eq. 10, 17)
+  for (int j = d.M - 1; j >= 0; --j) {
+    GemmProblem pr{};
+    if (j == d.M - 1) {
+      pr.a = P(A.hbar);
+      pr.a_shift_period = cfg->mask == PF_TOKEN_CAUSAL ? (int)d.m : 0;
+    } else {
+      pr.a = P(A.u[j + 1]);
+    }
+    pr.lda = d.d[j + 1];
+    pr.b = w->decompress[j].w;
+    pr.ldb = d.d[j + 1];
+    pr.M = (int)(d.B * d.R[j + 1]);
+    pr.N = d.k[j] * d.d[j];
+    pr.K = d.d[j + 1];
+    T* out = j == 0 ? P(A.delta) : P(A.u[j]);
+    EpiLinear<T> e{out, pr.N, reinterpret_cast<const T*>(w->decompress[j].b), nullptr, 0, nullptr};
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+  }
+
+  // 6. gated injection (Eq. 12)
+  {
+    GemmProblem pr{};
+    pr.a = x;
+    pr.lda = d.d_f;
+    pr.a2 = P(A.delta);
+    pr.lda2 = d.d_f;
+    pr.a_ksplit = d.d_f;
+    pr.b = w->gate.w;
+    pr.ldb = 2 * d.d_f;
+    pr.M = (int)(d.B * d.L);
+    pr.N = d.d_f;
+    pr.K = 2 * d.d_f;
+    EpiGate<T> e{reinterpret_cast<const T*>(x), P(A.delta), reinterpret_cast<const T*>(w->gate.b),
+                 reinterpret_cast<T*>(x_out), saving ? P(A.g) : nullptr, d.d_f};
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+  }
+}
+
+template <typename T>
+hipError_t layer_forward_run(const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
+                             const void* x, const void* h_in, void* x_out, void* h_out, char* acts, bool saving,
+                             char* ws, hipStream_t stream) {
+  const LayerWs W = layer_ws(d, false);
+  Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
+  forward_impl<T>(run, d, cfg, w, x, h_in, x_out, h_out, acts, saving);
+  return run.err;
+}
+
+size_t layer_forward_gemm_ws(const LayerDims& d) {
+  pf_layer_config cfg{};
+  cfg.mask = PF_TOKEN_CAUSAL;
+  pf_layer_weights w{};
+  Runner run(true);
+  if (d.esize == 2)
+    forward_impl<bf16>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, true);
+  else
+    forward_impl<float>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, true);
+  return run.gemm_need;
+}
+
+template hipError_t layer_forward_run<bf16>(const LayerDims&, const pf_layer_config*, const pf_layer_weights*,
+                                            const void*, const void*, void*, void*, char*, bool, char*,
+                                            hipStream_t);
+template hipError_t layer_forward_run<float>(const LayerDims&, const pf_layer_config*, const pf_layer_weights*,
+                                             const void*, const void*, void*, void*, char*, bool, char*,
+                                             hipStream_t);
+
+}  // namespace pf

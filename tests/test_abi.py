@@ -1,0 +1,165 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+the header declares, and rejects invalid arguments before any launch.
+No test here touches a GPU (every call fails validation or is a size query).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_23463_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "proxyformer.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(proxy_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libproxyformer.so is not built (run __graft_entry__.build())")
+    return B.load()
+
+
+def test_exports_every_declared_function(lib):
+    names = header_functions()
+    assert set(names) == set(B.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.proxy_version() == 100
+
+
+def _cfg(**kw):
+    base = dict(batch=1, seq_len=4096, d_fine=256, d_proxy=256, n_heads=4, head_dim=64, factors=(64,),
+                dtype="bf16", mask=0)
+    base.update(kw)
+    return B.layer_config(**base)
+
+
+def test_size_queries(lib):
+    cfg = _cfg()
+    ws = B.layer_workspace_size(cfg)
+    saved = B.layer_saved_size(cfg)
+    assert ws > 0 and saved > 0 and ws % 256 == 0 and saved % 256 == 0
+    # saved activations include at least Delta and G for every token
+    assert saved >= 2 * 4096 * 256 * 2
+    assert B.layer_workspace_size(cfg, True) > 0
+    for bad in (dict(seq_len=4000), dict(n_heads=3), dict(factors=()), dict(head_dim=32, n_heads=8),
+                dict(d_fine=100), dict(batch=0), dict(dtype="fp16")):
+        c = _cfg(**bad) if "dtype" not in bad else _cfg()
+        if "dtype" in bad:
+            c.dtype = 7
+        assert B.layer_workspace_size(c) == 0, bad
+        assert B.layer_saved_size(c) == 0, bad
+
+
+def _weights_struct(nlev=1, null=None):
+    w = B.PfLayerWeights()
+    fake = 0x10000  # never dereferenced: every call below fails validation first
+    for i in range(nlev):
+        w.compress[i] = B.PfLinear(fake, None)
+        w.decompress[i] = B.PfLinear(fake, None)
+    for name in ("q", "k", "v", "o", "gate"):
+        setattr(w, name, B.PfLinear(fake, None))
+    if null:
+        setattr(w, null, B.PfLinear(None, None))
+    return w
+
+
+def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 << 40):
+    return lib.proxy_layer_forward(ctypes.byref(cfg), ctypes.byref(w), x, None, xo, ho, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(seq_len=4000), B.PF_ERR_INVALID_ARG),
+    (dict(n_heads=8), B.PF_ERR_INVALID_ARG),
+    (dict(mask=5), B.PF_ERR_INVALID_ARG),
+    (dict(head_dim=32, n_heads=8), B.PF_ERR_UNSUPPORTED),
+    (dict(d_fine=100), B.PF_ERR_UNSUPPORTED),
+])
+def test_forward_rejects_bad_config(lib, bad, status):
+    cfg = _cfg(**bad)
+    assert _fwd(lib, cfg, _weights_struct()) == status
+    assert B.last_error()
+
+
+def test_forward_rejects_bad_pointers(lib):
+    cfg = _cfg()
+    assert _fwd(lib, cfg, _weights_struct(null="gate")) == B.PF_ERR_INVALID_ARG
+    assert "gate" in B.last_error()
+    assert _fwd(lib, cfg, _weights_struct(), x=None) == B.PF_ERR_INVALID_ARG
+    assert _fwd(lib, cfg, _weights_struct(), xo=(2 << 32) + 4096) == B.PF_ERR_INVALID_ARG  # x_out aliases x
+    assert "alias" in B.last_error()
+    assert _fwd(lib, cfg, _weights_struct(), x=(2 << 32) + 8) == B.PF_ERR_INVALID_ARG  # misaligned
+    assert _fwd(lib, cfg, _weights_struct(), ws_bytes=1024) == B.PF_ERR_WORKSPACE
+    assert _fwd(lib, cfg, _weights_struct(), ws=None) == B.PF_ERR_WORKSPACE
+
+
+def test_backward_rejects_bad_arguments(lib):
+    cfg = _cfg()
+    g = B.PfLayerGrads()
+    w = _weights_struct()
+    st = lib.proxy_layer_backward(ctypes.byref(cfg), ctypes.byref(w), 0x20000, None, None, 0x30000, None,
+                                  0x40000, None, ctypes.byref(g), 0x50000, 1 << 40, None)
+    assert st == B.PF_ERR_INVALID_ARG  # saved is NULL
+    st = lib.proxy_layer_backward(ctypes.byref(cfg), ctypes.byref(w), 0x20000, 0x60000, 0x70000, 0x30000, None,
+                                  0x40000, None, ctypes.byref(g), 0x50000, 1 << 40, None)
+    assert st == B.PF_ERR_INVALID_ARG  # h_in given without dh_in
+
+
+def _dcfg(**kw):
+    base = dict(batch=2, d_model=128, n_heads=2, head_dim=64, factors=(4,), dtype="bf16")
+    base.update(kw)
+    return B.decode_config(**base)
+
+
+def _dweights():
+    w = B.PfDecodeWeights()
+    fake = 0x10000
+    w.rms_gamma = fake
+    for name in ("q", "k", "v", "o", "alpha", "k_proxy", "v_proxy"):
+        setattr(w, name, B.PfLinear(fake, None))
+    w.compress[0] = B.PfLinear(fake, None)
+    return w
+
+
+def _dstate(n=0, n_cap=4, j=0):
+    return B.PfDecodeState(0x20000, 0x30000, n_cap, n, 0x40000, 0x50000, 0x60000, j)
+
+
+def test_decode_validation(lib):
+    cfg = _dcfg()
+    ws = int(lib.proxy_decode_workspace_size(ctypes.byref(cfg)))
+    assert ws > 0
+    w = _dweights()
+    # j out of range
+    st = _dstate(j=4)
+    assert lib.proxy_decode_step(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), 0x70000, 0x80000,
+                                 0x90000, ws, None) == B.PF_ERR_INVALID_ARG
+    # block completes with a full cache
+    st = _dstate(n=4, n_cap=4, j=3)
+    assert lib.proxy_decode_step(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), 0x70000, 0x80000,
+                                 0x90000, ws, None) == B.PF_ERR_CAPACITY
+    assert st.n == 4 and st.j == 3  # untouched
+    # append past capacity
+    st = _dstate(n=2, n_cap=4)
+    assert lib.proxy_cache_append(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), 0x70000, 3, 0x90000, ws,
+                                  None) == B.PF_ERR_CAPACITY
+    assert st.n == 2
+    # nothing to append is a no-op
+    assert lib.proxy_cache_append(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), None, 0, 0x90000, ws,
+                                  None) == B.PF_OK
+    # workspace too small
+    assert lib.proxy_decode_step(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(_dstate()), 0x70000, 0x80000,
+                                 0x90000, 16, None) == B.PF_ERR_WORKSPACE
+    # bad config
+    bad = _dcfg(n_heads=3)
+    assert lib.proxy_decode_step(ctypes.byref(bad), ctypes.byref(w), ctypes.byref(_dstate()), 0x70000, 0x80000,
+                                 0x90000, ws, None) == B.PF_ERR_INVALID_ARG
+    assert lib.proxy_decode_workspace_size(ctypes.byref(bad)) == 0

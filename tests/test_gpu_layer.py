@@ -1,0 +1,121 @@
+"""GPU parity of the layer forward against the CPU oracle (through the C ABI).
+
+Every case runs the HIP path and the oracle on the same seeded inputs and
+compares whole output tensors with the infinity-norm relative error
+(1e-4 for fp32, 2e-2 for bf16, fp32 accumulation), plus bit-exact
+invariants (causality, zero decompression, run-to-run determinism).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_23463_amd import synth
+from paper_2608_23463_amd.synth import LayerShape
+from helpers import assert_close, dev, dev_weights, host
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    # ragged: m = 37 proxies (not a multiple of any tile), d = 192 (3 heads)
+    "bf16_ragged_tc": (LayerShape(2, 37 * 16, 192, 192, 3, 64, (16,)), True),
+    "bf16_ragged_bc": (LayerShape(1, 37 * 16, 192, 192, 3, 64, (16,), mask=synth.BLOCK_CAUSAL), False),
+    "bf16_ragged_bi": (LayerShape(1, 37 * 16, 192, 192, 3, 64, (16,), mask=synth.BIDIRECTIONAL), True),
+    "fp32_ragged_tc": (LayerShape(2, 37 * 16, 192, 192, 3, 64, (16,), dtype="fp32"), True),
+    "bf16_factorised": (LayerShape(1, 64 * 70, 128, 256, 2, 128, (4, 2, 8), level_dims=(96, 160)), True),
+    "fp32_factorised": (LayerShape(1, 8 * 40, 64, 128, 1, 128, (2, 4), level_dims=(48,), dtype="fp32"), False),
+    "bf16_dfine_ne_dproxy": (LayerShape(1, 64 * 300, 64, 512, 8, 64, (64,)), False),
+    "bf16_single_block": (LayerShape(1, 64, 128, 128, 2, 64, (64,)), False),
+    "bf16_block1": (LayerShape(1, 200, 64, 128, 2, 64, (1,)), False),
+}
+
+
+def run_gpu(shape, inp, save=False):
+    from paper_2608_23463_amd import binding as B
+    cfg = B.config_from_shape(shape)
+    x = dev(inp["x"], shape.dtype)
+    h_in = dev(inp["h_in"], shape.dtype)
+    w = dev_weights(inp["weights"], shape.dtype)
+    x_out, h_out, saved = B.layer_forward(cfg, w, x, h_in, save=save)
+    import torch
+    torch.cuda.synchronize()
+    return x_out, h_out
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_forward_parity_small(gpu, name):
+    shape, with_h = SMALL[name]
+    print(f"[case {name}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, seed=hash(name) % 1000, with_h_in=with_h)
+    # larger weights than the workload's 0.02 so that attention is not uniform
+    rng = np.random.default_rng(7)
+    for key in ("q", "k"):
+        wq, bq = inp["weights"][key]
+        inp["weights"][key] = (synth.bf16_round(wq * 4) if shape.dtype == "bf16" else wq * 4, bq)
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask, inp["h_in"])
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+
+
+@pytest.mark.parametrize("name", ["layer_fp32_L4k_d256", "layer_bf16_L64k_d1024"])
+def test_forward_parity_workload(gpu, name):
+    shape = synth.WORKLOADS[name]
+    print(f"[workload {name}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+
+
+def test_forward_parity_L1M_sampled(gpu):
+    """Full-size 1M-token layer: every proxy, and 64 sampled blocks of X_out."""
+    name = "layer_bf16_L1M_d1024"
+    shape = synth.WORKLOADS[name]
+    print(f"[workload {name}] generating inputs", flush=True)
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
+    x_out, h_out = run_gpu(shape, inp)
+    m = shape.n_proxies
+    rng = np.random.default_rng(123)
+    blocks = sorted(set([0, 1, m - 2, m - 1] + list(rng.choice(np.arange(2, m - 2), 60, replace=False))))
+    print(f"[workload {name}] oracle on {len(blocks)} sampled blocks", flush=True)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask,
+                               sample_blocks=blocks)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out (all proxies)")
+    got = host(x_out.reshape(1, m, shape.block, shape.d_fine)[:, blocks])
+    assert_close(got, ref["x_out"], shape.dtype, f"{name} x_out (sampled blocks)")
+
+
+def test_zero_decompression_is_identity_bitwise(gpu):
+    shape = synth.WORKLOADS["layer_bf16_L64k_d1024"]
+    inp = synth.layer_inputs(shape, 5)
+    inp["weights"]["decompress"] = [(np.zeros_like(a), b) for a, b in inp["weights"]["decompress"]]
+    x_out, _ = run_gpu(shape, inp)
+    import torch
+    assert torch.equal(x_out, dev(inp["x"], shape.dtype))
+
+
+@pytest.mark.parametrize("factors", [(64,), (8, 8)])
+def test_token_causality_bit_identical(gpu, factors):
+    import torch
+    shape = LayerShape(1, 64 * 96, 256, 256, 4, 64, factors)
+    inp = synth.layer_inputs(shape, 11)
+    x0, h0 = run_gpu(shape, inp)
+    for t in (0, 1000, 64 * 50 + 7, 64 * 96 - 1):
+        inp2 = dict(inp)
+        x = inp["x"].copy()
+        x[0, t] += 1.0
+        inp2["x"] = x
+        x1, h1 = run_gpu(shape, inp2)
+        assert torch.equal(x1[0, :t], x0[0, :t]), t
+        assert torch.equal(h1[0, :t // 64], h0[0, :t // 64]), t
+        assert not torch.equal(x1[0, t], x0[0, t])
+
+
+def test_run_twice_bitwise(gpu):
+    import torch
+    shape = LayerShape(1, 64 * 200, 512, 512, 8, 64, (64,))
+    inp = synth.layer_inputs(shape, 12)
+    a = run_gpu(shape, inp)
+    b = run_gpu(shape, inp)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
