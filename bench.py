@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Throughput of the ProxyFormer hot path on one MI355X; prints one JSON line.
+
+value: layer-forward tokens/s on the 1M-token workload (batch 1, L = 1,048,576,
+d = 1024, 16 heads x 64, P = 64, bf16 with fp32 accumulation), inputs resident
+in HBM, W untimed warmup calls then K timed calls bracketed by
+torch.cuda.synchronize() and HIP events on the launch stream.
+
+Extra objects on the same line:
+  kernels      per-kernel average duration from the library's event tracing
+               (a second pass over K calls) and achieved TFLOP/s or GB/s
+  roofline     the dominant kernel against the MI355X peak of its bound
+  decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
+               rows each, 256 new tokens per sequence including the 4
+               block-triggered appends
+  cpu_baseline the CPU oracle timed on a bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ProxyFormer layer fwd tokens/sec at L=1M, P=64; proxy-KV decode tokens/sec"
+LAYER_WORKLOAD = "layer_bf16_L1M_d1024"
+DECODE_WORKLOAD = "decode_bf16_B32_n16k"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+CPU_SAMPLE_TOKENS = 65536
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_bf16_L1M_d1024.txt")
+KERNEL_SOURCES = ["paper_2608_23463_amd/csrc/gemm.hpp", "paper_2608_23463_amd/csrc/epilogues.hpp",
+                  "paper_2608_23463_amd/csrc/common.hpp", "paper_2608_23463_amd/csrc/attention_fwd.hip",
+                  "paper_2608_23463_amd/csrc/layer_fwd.hip"]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(label: str):
+    """HBM bytes per launch of `label` from the committed counter summary, or
+    None when the summary is missing or the kernel sources changed since."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    v = vals.get(f"{label}_bytes_per_launch")
+    return float(v) if v else None
+
+
+def layer_flops(shape):
+    """Algorithmic flops per launch of each forward kernel (multiply-add = 2)."""
+    B, L, df, dp = shape.batch, shape.seq_len, shape.d_fine, shape.d_proxy
+    P = shape.block
+    m = L // P
+    dims = shape.dims()
+    comp = 0
+    rows = B * L
+    for j, k in enumerate(shape.factors):
+        rows //= k
+        comp += 2 * rows * (k * dims[j]) * dims[j + 1]
+    return {
+        "compress_gemm": comp / len(shape.factors),
+        "qkv_gemm": 2 * B * m * dp * dp,
+        "attention_fwd": 2.0 * B * dp * m * (m + 1),   # QK^T and PV over the causal triangle
+        "o_gemm": 2 * B * m * dp * dp,
+        "decompress_gemm": comp / len(shape.factors),
+        "gate_gemm": 2 * B * L * df * 2 * df,
+    }
+
+
+def to_dev(a, dt):
+    import numpy as np
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
+    return t.to(torch.bfloat16 if dt == "bf16" else torch.float32)
+
+
+def dev_weights(w, dt):
+    out = {}
+    for k, v in w.items():
+        if isinstance(v, list):
+            out[k] = [(to_dev(a, dt), to_dev(b, dt)) for a, b in v]
+        elif isinstance(v, tuple):
+            out[k] = (to_dev(v[0], dt), to_dev(v[1], dt))
+        else:
+            out[k] = to_dev(v, dt)
+    return out
+
+
+def bench_layer(steps, warmup):
+    import torch
+    from paper_2608_23463_amd import binding as B
+    from paper_2608_23463_amd import synth
+    shape = synth.WORKLOADS[LAYER_WORKLOAD]
+    log(f"generating {LAYER_WORKLOAD} inputs")
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[LAYER_WORKLOAD])
+    sample = {"x": inp["x"][:, :CPU_SAMPLE_TOKENS].copy(), "weights": inp["weights"]}
+    x = to_dev(inp["x"], shape.dtype)
+    del inp["x"]
+    w = dev_weights(inp["weights"], shape.dtype)
+    cfg = B.config_from_shape(shape)
+    ws = torch.empty(B.layer_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    m = shape.n_proxies
+    x_out = torch.empty_like(x)
+    h_out = torch.empty((1, m, shape.d_proxy), dtype=x.dtype, device="cuda")
+    wst = B.layer_weights(w)
+
+    def call():
+        B.layer_forward_raw(cfg, wst, x, None, x_out, h_out, None, ws)
+
+    log(f"warmup {warmup}")
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {steps} forward calls")
+    start.record()
+    for _ in range(steps):
+        call()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+
+    log("tracing per-kernel durations")
+    B.trace_reset()
+    B.trace_enable(True)
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    tr = B.trace_collect()
+    B.trace_enable(False)
+    flops = layer_flops(shape)
+    kernels = {}
+    for label, (cnt, tot) in tr.items():
+        per_call = cnt / steps
+        avg = tot / cnt
+        ent = {"launches_per_step": per_call, "avg_ms": round(avg, 4)}
+        if label in flops:
+            ent["tflops"] = round(flops[label] / (avg * 1e-3) / 1e12, 1)
+        kernels[label] = ent
+    dom = max((k for k in tr if k in flops), key=lambda k: tr[k][1])
+    dom_ms = tr[dom][1] / tr[dom][0]
+    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
+    traffic = measured_traffic(dom)
+    roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
+    del x, x_out, h_out, ws, w
+    torch.cuda.empty_cache()
+    return shape, ms, kernels, roof, sample
+
+
+def bench_decode():
+    import numpy as np
+    import torch
+    from paper_2608_23463_amd import binding as B
+    from paper_2608_23463_amd import synth
+    shape = synth.WORKLOADS[DECODE_WORKLOAD]
+    log(f"generating {DECODE_WORKLOAD} inputs")
+    inp = synth.decode_inputs(shape, synth.WORKLOAD_SEEDS[DECODE_WORKLOAD])
+    cfg = B.decode_config(shape.batch, shape.d_model, shape.n_heads, shape.head_dim, shape.factors,
+                          shape.level_dims, shape.dtype, shape.rms_eps)
+    kc = to_dev(inp.pop("k_cache"), shape.dtype)
+    vc = to_dev(inp.pop("v_cache"), shape.dtype)
+    xs = to_dev(inp["x"], shape.dtype)
+    sess = B.DecodeSession(cfg, dev_weights(inp["weights"], shape.dtype), kc, vc, n=shape.n0)
+    ys = torch.empty_like(xs)
+
+    def run_all():
+        sess.state.n = shape.n0
+        sess.state.j = 0
+        for t in range(shape.steps):
+            sess.step(xs[t], ys[t])
+
+    log("decode warmup")
+    run_all()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {shape.steps} decode steps")
+    start.record()
+    run_all()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop)
+    B.trace_reset()
+    B.trace_enable(True)
+    run_all()
+    torch.cuda.synchronize()
+    tr = B.trace_collect()
+    B.trace_enable(False)
+    attn = tr.get("decode_attn")
+    out = {"metric": "proxy-KV decode tokens/s", "value": round(shape.batch * shape.steps / (ms * 1e-3), 1),
+           "unit": "tokens/s", "ms_total": round(ms, 3), "ms_per_step": round(ms / shape.steps, 4),
+           "workload": DECODE_WORKLOAD, "batch": shape.batch, "cached_rows": shape.n0, "steps": shape.steps,
+           "appends": shape.steps // shape.block}
+    if attn:
+        avg = attn[1] / attn[0]
+        # K and V rows read per step: every cached row once (n grows by one per block)
+        n_mean = shape.n0 + (shape.steps // shape.block) / 2.0
+        nbytes = 2 * shape.batch * shape.n_heads * n_mean * shape.head_dim * 2
+        gbs = nbytes / (avg * 1e-3) / 1e9
+        out["roofline"] = {"kernel": "decode_attn", "bound": "hbm", "achieved": round(gbs, 1),
+                           "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                           "traffic": None, "avg_ms": round(avg, 4), "work_per_launch": nbytes}
+    out["kernels"] = {k: {"launches": c, "avg_ms": round(t / c, 4)} for k, (c, t) in tr.items()}
+    del kc, vc, xs, ys, sess
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(shape, sample):
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    log(f"oracle on {CPU_SAMPLE_TOKENS} tokens")
+    t0 = time.perf_counter()
+    oracle.layer_forward(sample["x"], sample["weights"], shape.factors, shape.n_heads, shape.mask)
+    dt = time.perf_counter() - t0
+    return {"value": round(CPU_SAMPLE_TOKENS / dt, 1), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"full layer forward (fp64) over the first {CPU_SAMPLE_TOKENS} tokens "
+                      f"({CPU_SAMPLE_TOKENS // shape.block} blocks) of the 1M-token workload",
+            "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build runs the hot path on a single MI355X and has no "
+              "multi-GPU path; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2608_23463_amd import binding as B
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    B.load()
+    shape, ms, kernels, roof, sample = bench_layer(args.steps, args.warmup)
+    result = {
+        "metric": METRIC,
+        "value": round(shape.seq_len * shape.batch / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": LAYER_WORKLOAD, "batch": shape.batch, "seq_len": shape.seq_len,
+                   "d_fine": shape.d_fine, "d_proxy": shape.d_proxy, "n_heads": shape.n_heads,
+                   "head_dim": shape.head_dim, "P": shape.block, "levels": list(shape.factors),
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_decode:
+        result["decode"] = bench_decode()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(shape, sample)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

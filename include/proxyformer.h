@@ -199,6 +199,23 @@ int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w,
                        pf_decode_state* st, const void* x_blocks, int64_t nblk,
                        void* workspace, size_t ws_bytes, void* stream);
 
+/* Launch tracing (profiling aid). While enabled, every kernel launch of the
+ * library is bracketed by two HIP events recorded on its stream and
+ * attributed to a label (e.g. "gate_gemm", "attention_fwd", "decode_attn").
+ *  proxy_trace_enable   1 = on, 0 = off; returns the previous setting.
+ *  proxy_trace_collect  waits for every recorded event, folds it into the
+ *                       per-label totals; returns the number of labels or
+ *                       PF_ERR_HIP.
+ *  proxy_trace_get      label i (first-seen order) into label[label_cap]
+ *                       (NUL-terminated), its launch count and total
+ *                       milliseconds; PF_ERR_INVALID_ARG for a bad index.
+ *  proxy_trace_reset    drops all totals and pending events.
+ * Tracing adds host work per launch; time throughput with it off. */
+int proxy_trace_enable(int on);
+int proxy_trace_collect(void);
+int proxy_trace_get(int i, char* label, size_t label_cap, int64_t* launches, double* total_ms);
+void proxy_trace_reset(void);
+
 /* Message of the last non-OK status on the calling thread. */
 const char* proxy_last_error(void);
 

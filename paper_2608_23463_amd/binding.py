@@ -27,6 +27,7 @@ EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
     "proxy_layer_backward", "proxy_decode_workspace_size", "proxy_decode_step",
     "proxy_cache_append", "proxy_last_error", "proxy_version",
+    "proxy_trace_enable", "proxy_trace_collect", "proxy_trace_get", "proxy_trace_reset",
 )
 
 c_void_p = ctypes.c_void_p
@@ -119,6 +120,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.proxy_last_error.restype = ctypes.c_char_p
     lib.proxy_version.argtypes = []
     lib.proxy_version.restype = c_int32
+    lib.proxy_trace_enable.argtypes = [c_int32]
+    lib.proxy_trace_enable.restype = c_int32
+    lib.proxy_trace_collect.argtypes = []
+    lib.proxy_trace_collect.restype = c_int32
+    lib.proxy_trace_get.argtypes = [c_int32, ctypes.c_char_p, c_size_t, ctypes.POINTER(c_int64),
+                                    ctypes.POINTER(ctypes.c_double)]
+    lib.proxy_trace_get.restype = c_int32
+    lib.proxy_trace_reset.argtypes = []
+    lib.proxy_trace_reset.restype = None
     _lib = lib
     return lib
 
@@ -130,6 +140,30 @@ def last_error() -> str:
 def _check(status: int):
     if status != PF_OK:
         raise ProxyFormerError(status, last_error())
+
+
+def trace_enable(on: bool) -> bool:
+    return bool(load().proxy_trace_enable(int(on)))
+
+
+def trace_reset() -> None:
+    load().proxy_trace_reset()
+
+
+def trace_collect() -> Dict[str, tuple]:
+    """{label: (launches, total_ms)} of everything traced since the last reset."""
+    lib = load()
+    n = lib.proxy_trace_collect()
+    if n < 0:
+        raise ProxyFormerError(n, "trace collection failed")
+    out = {}
+    buf = ctypes.create_string_buffer(128)
+    for i in range(n):
+        cnt = c_int64()
+        ms = ctypes.c_double()
+        _check(lib.proxy_trace_get(i, buf, 128, ctypes.byref(cnt), ctypes.byref(ms)))
+        out[buf.value.decode()] = (int(cnt.value), float(ms.value))
+    return out
 
 
 def _ptr(t) -> Optional[int]:

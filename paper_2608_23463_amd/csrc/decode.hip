@@ -338,7 +338,7 @@ static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weight
       pr.K = (int)pr.lda;
       T* out = reinterpret_cast<T*>(ws + W.z[j + 1]);
       EpiLinear<T> e{out, pr.N, reinterpret_cast<const T*>(w->compress[j].b), nullptr, 0, nullptr};
-      run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+      run.gemm<T, LAYOUT_K, LAYOUT_K>("append_compress_gemm", pr, e);
       zin = out;
     }
     const pf_linear* maps[2] = {&w->k_proxy, &w->v_proxy};
@@ -354,7 +354,7 @@ static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weight
       pr.K = d.d;
       EpiCache<T> e{reinterpret_cast<T*>(caches[i]), reinterpret_cast<const T*>(maps[i]->b), st.n_cap, st.n, nblk, r0,
                     d.nh, d.dh};
-      run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+      run.gemm<T, LAYOUT_K, LAYOUT_K>("append_kv_gemm", pr, e);
     }
   }
 }
@@ -379,7 +379,7 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   T* q = reinterpret_cast<T*>(ws + W.q);
   float* alpha = reinterpret_cast<float*>(ws + W.alpha);
   T* attn = reinterpret_cast<T*>(ws + W.attn);
-  run.launch([&] {
+  run.launch("decode_rmsnorm", [&] {
     hipLaunchKernelGGL((rmsnorm_kernel<T>), dim3(d.B), dim3(256), 0, run.stream, reinterpret_cast<const T*>(x_t),
                        reinterpret_cast<const T*>(w->rms_gamma), u, reinterpret_cast<T*>(st.x_blk), d.d,
                        (int64_t)(d.P * d.d), st.j, d.eps);
@@ -393,16 +393,16 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   pr.N = d.d;
   pr.K = d.d;
   pr.b = w->q.w;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, EpiLinear<T>{q, d.d, reinterpret_cast<const T*>(w->q.b), nullptr, 0, nullptr});
+  run.gemm<T, LAYOUT_K, LAYOUT_K>("decode_q_gemm", pr, EpiLinear<T>{q, d.d, reinterpret_cast<const T*>(w->q.b), nullptr, 0, nullptr});
   pr.b = w->k.w;
   run.gemm<T, LAYOUT_K, LAYOUT_K>(
-      pr, EpiSlot<T>{reinterpret_cast<T*>(st.k_loc), reinterpret_cast<const T*>(w->k.b), d.nh, d.dh, d.P, st.j});
+      "decode_k_gemm", pr, EpiSlot<T>{reinterpret_cast<T*>(st.k_loc), reinterpret_cast<const T*>(w->k.b), d.nh, d.dh, d.P, st.j});
   pr.b = w->v.w;
   run.gemm<T, LAYOUT_K, LAYOUT_K>(
-      pr, EpiSlot<T>{reinterpret_cast<T*>(st.v_loc), reinterpret_cast<const T*>(w->v.b), d.nh, d.dh, d.P, st.j});
+      "decode_v_gemm", pr, EpiSlot<T>{reinterpret_cast<T*>(st.v_loc), reinterpret_cast<const T*>(w->v.b), d.nh, d.dh, d.P, st.j});
   pr.b = w->alpha.w;
   pr.N = d.nh;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, EpiSigmoidF32<T>{alpha, reinterpret_cast<const T*>(w->alpha.b), d.nh});
+  run.gemm<T, LAYOUT_K, LAYOUT_K>("decode_alpha_gemm", pr, EpiSigmoidF32<T>{alpha, reinterpret_cast<const T*>(w->alpha.b), d.nh});
 
   int splits, chunk;
   split_plan(st.n, &splits, &chunk);
@@ -423,7 +423,7 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   ap.splits = splits;
   ap.chunk = chunk;
   ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
-  run.launch([&] {
+  run.launch("decode_attn", [&] {
     const dim3 grid(splits + 1, d.B * d.nh);
     if (d.dh == 64)
       hipLaunchKernelGGL((decode_attn_kernel<T, 64>), grid, dim3(256), 0, run.stream, ap);
@@ -431,7 +431,7 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
       hipLaunchKernelGGL((decode_attn_kernel<T, 128>), grid, dim3(256), 0, run.stream, ap);
     return hipGetLastError();
   });
-  run.launch([&] {
+  run.launch("decode_combine", [&] {
     if (d.dh == 64)
       hipLaunchKernelGGL((decode_combine_kernel<T, 64>), dim3(d.B * d.nh), dim3(64), 0, run.stream, ap.part_m,
                          ap.part_l, ap.part_acc, alpha, attn, d.nh, splits);
@@ -443,7 +443,7 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   pr.a = attn;
   pr.b = w->o.w;
   pr.N = d.d;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, EpiLinear<T>{reinterpret_cast<T*>(y_t), d.d, reinterpret_cast<const T*>(w->o.b),
+  run.gemm<T, LAYOUT_K, LAYOUT_K>("decode_out_gemm", pr, EpiLinear<T>{reinterpret_cast<T*>(y_t), d.d, reinterpret_cast<const T*>(w->o.b),
                                                    reinterpret_cast<const T*>(x_t), d.d, nullptr});
 }
 

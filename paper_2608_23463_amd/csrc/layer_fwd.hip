@@ -170,7 +170,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
       e.out = P(A.z[j + 1]);
       e.ldo = d.d[j + 1];
     }
-    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("compress_gemm", pr, e);
     zin = e.out;
   }
 
@@ -179,10 +179,10 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   if (d.ld_t != d.m) {
     // padding columns of the transposed tensors must read as zero
     const size_t tb = (size_t)d.B * d.nh * d.dh * d.ld_t * sizeof(T);
-    run.launch([&] { return fill_zero(P(A.vt), tb, run.stream); });
+    run.launch("fill_zero", [&] { return fill_zero(P(A.vt), tb, run.stream); });
     if (saving) {
-      run.launch([&] { return fill_zero(P(A.qt), tb, run.stream); });
-      run.launch([&] { return fill_zero(P(A.kt), tb, run.stream); });
+      run.launch("fill_zero", [&] { return fill_zero(P(A.qt), tb, run.stream); });
+      run.launch("fill_zero", [&] { return fill_zero(P(A.kt), tb, run.stream); });
     }
   }
   const pf_linear* proj[3] = {&w->q, &w->k, &w->v};
@@ -198,7 +198,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.N = d.d_p;
     pr.K = d.d_p;
     EpiHeads<T> e{outs[i], outs_t[i], reinterpret_cast<const T*>(proj[i]->b), (int)d.m, d.dh, d.nh, d.ld_t};
-    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("qkv_gemm", pr, e);
   }
 
   // 3. attention over the proxies (Eq. 9)
@@ -213,7 +213,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   ap.ld_t = d.ld_t;
   ap.causal = cfg->mask != PF_BIDIRECTIONAL;
   ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
-  run.launch([&] { return launch_attention_fwd<T>(ap, d.B, d.dh, run.stream); });
+  run.launch("attention_fwd", [&] { return launch_attention_fwd<T>(ap, d.B, d.dh, run.stream); });
 
   // 4. output map of the interaction
   {
@@ -226,7 +226,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.N = d.d_p;
     pr.K = d.d_p;
     EpiLinear<T> e{P(A.hbar), d.d_p, reinterpret_cast<const T*>(w->o.b), nullptr, 0, nullptr};
-    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("o_gemm", pr, e);
   }
 
   // 5. decompression, level M down to 1 (Eq. 10, 17)
@@ -246,7 +246,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.K = d.d[j + 1];
     T* out = j == 0 ? P(A.delta) : P(A.u[j]);
     EpiLinear<T> e{out, pr.N, reinterpret_cast<const T*>(w->decompress[j].b), nullptr, 0, nullptr};
-    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("decompress_gemm", pr, e);
   }
 
   // 6. gated injection (Eq. 12)
@@ -264,7 +264,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.K = 2 * d.d_f;
     EpiGate<T> e{reinterpret_cast<const T*>(x), P(A.delta), reinterpret_cast<const T*>(w->gate.b),
                  reinterpret_cast<T*>(x_out), saving ? P(A.g) : nullptr, d.d_f};
-    run.gemm<T, LAYOUT_K, LAYOUT_K>(pr, e);
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("gate_gemm", pr, e);
   }
 }
 

@@ -43,7 +43,7 @@ class LayerShape:
     n_heads: int
     head_dim: int
     factors: Tuple[int, ...]          # k_1..k_M, product = P (Eq. 15)
-    level_dims: Tuple[int, ...] = ()  # d_1..d_M; empty -> every d_j = d_proxy
+    level_dims: Tuple[int, ...] = ()  # d_1..d_{M-1}; missing or 0 -> d_proxy
     dtype: str = "bf16"               # "bf16" or "fp32"
     mask: int = TOKEN_CAUSAL
 
@@ -59,13 +59,12 @@ class LayerShape:
         return self.seq_len // self.block
 
     def dims(self) -> List[int]:
-        """d_0..d_M: d_0 = d_fine, d_M = d_proxy."""
+        """d_0..d_M: d_0 = d_fine, d_j = level_dims[j-1] (0 or absent -> d_proxy), d_M = d_proxy."""
         m = len(self.factors)
-        if self.level_dims:
-            lv = list(self.level_dims)
-        else:
-            lv = [self.d_proxy] * m
-        lv[-1] = self.d_proxy
+        lv = [self.d_proxy] * m
+        for j, v in enumerate(self.level_dims[:m - 1]):
+            if v:
+                lv[j] = v
         return [self.d_fine] + lv
 
     def weight_shapes(self) -> Dict[str, object]:
@@ -110,9 +109,12 @@ class DecodeShape:
         return self.n_cap if self.n_cap else self.n0 + self.steps // self.block + 1
 
     def dims(self) -> List[int]:
+        """d_0..d_M with d_0 = d_M = d_model and d_j = level_dims[j-1] in between."""
         m = len(self.factors)
-        lv = list(self.level_dims) if self.level_dims else [self.d_model] * m
-        lv[-1] = self.d_model
+        lv = [self.d_model] * m
+        for j, v in enumerate(self.level_dims[:m - 1]):
+            if v:
+                lv[j] = v
         return [self.d_model] + lv
 
 

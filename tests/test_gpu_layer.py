@@ -5,6 +5,8 @@ compares whole output tensors with the infinity-norm relative error
 (1e-4 for fp32, 2e-2 for bf16, fp32 accumulation), plus bit-exact
 invariants (causality, zero decompression, run-to-run determinism).
 """
+import zlib
+
 import numpy as np
 import pytest
 
@@ -45,7 +47,7 @@ def run_gpu(shape, inp, save=False):
 def test_forward_parity_small(gpu, name):
     shape, with_h = SMALL[name]
     print(f"[case {name}] {shape}", flush=True)
-    inp = synth.layer_inputs(shape, seed=hash(name) % 1000, with_h_in=with_h)
+    inp = synth.layer_inputs(shape, seed=zlib.crc32(name.encode()) % 1000, with_h_in=with_h)
     # larger weights than the workload's 0.02 so that attention is not uniform
     rng = np.random.default_rng(7)
     for key in ("q", "k"):
