@@ -45,6 +45,7 @@ static bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return a && b && pa < pb + nb && pb < pa + na;
 }
 
+// NULL counts as aligned (optional pointers are checked for presence elsewhere)
 static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 extern "C" {
@@ -72,14 +73,16 @@ static int check_weights(const LayerDims& d, const pf_layer_weights* w) {
   for (int j = 0; j < d.M; ++j) {
     if (!w->compress[j].w) return fail(PF_ERR_INVALID_ARG, "compress[%d].w is NULL", j);
     if (!w->decompress[j].w) return fail(PF_ERR_INVALID_ARG, "decompress[%d].w is NULL", j);
-    if (!aligned16(w->compress[j].w) || !aligned16(w->decompress[j].w))
-      return fail(PF_ERR_INVALID_ARG, "level %d weights must be 16-byte aligned", j);
+    if (!aligned16(w->compress[j].w) || !aligned16(w->decompress[j].w) || !aligned16(w->compress[j].b) ||
+        !aligned16(w->decompress[j].b))
+      return fail(PF_ERR_INVALID_ARG, "level %d weights and biases must be 16-byte aligned", j);
   }
   const pf_linear* maps[5] = {&w->q, &w->k, &w->v, &w->o, &w->gate};
   const char* names[5] = {"q", "k", "v", "o", "gate"};
   for (int i = 0; i < 5; ++i) {
     if (!maps[i]->w) return fail(PF_ERR_INVALID_ARG, "%s.w is NULL", names[i]);
-    if (!aligned16(maps[i]->w)) return fail(PF_ERR_INVALID_ARG, "%s.w must be 16-byte aligned", names[i]);
+    if (!aligned16(maps[i]->w) || !aligned16(maps[i]->b))
+      return fail(PF_ERR_INVALID_ARG, "%s weights and bias must be 16-byte aligned", names[i]);
   }
   return PF_OK;
 }
@@ -161,6 +164,15 @@ static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weig
     return fail(PF_ERR_INVALID_ARG, "a required decode weight is NULL");
   for (int j = 0; j < d->M; ++j)
     if (!w->compress[j].w) return fail(PF_ERR_INVALID_ARG, "compress[%d].w is NULL", j);
+  {
+    const void* ptrs[] = {w->rms_gamma, w->q.w, w->q.b, w->k.w, w->k.b, w->v.w, w->v.b, w->o.w, w->o.b,
+                          w->alpha.w, w->alpha.b, w->k_proxy.w, w->k_proxy.b, w->v_proxy.w, w->v_proxy.b,
+                          w->compress[0].w, w->compress[0].b, w->compress[1].w, w->compress[1].b,
+                          w->compress[2].w, w->compress[2].b, w->compress[3].w, w->compress[3].b,
+                          st->k_cache, st->v_cache, st->x_blk, st->k_loc, st->v_loc};
+    for (const void* p : ptrs)
+      if (!aligned16(p)) return fail(PF_ERR_INVALID_ARG, "decode weights and state buffers must be 16-byte aligned");
+  }
   if (!st->k_cache || !st->v_cache || !st->x_blk || !st->k_loc || !st->v_loc)
     return fail(PF_ERR_INVALID_ARG, "a decode state buffer is NULL");
   if (st->n < 0 || st->n_cap < 0 || st->n > st->n_cap) return fail(PF_ERR_INVALID_ARG, "state n must be in 0..n_cap");
@@ -178,6 +190,7 @@ int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, p
   int s = check_decode_common(cfg, w, st, &d, workspace, ws_bytes);
   if (s != PF_OK) return s;
   if (!x_t || !y_t) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be non-NULL");
+  if (!aligned16(x_t) || !aligned16(y_t)) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be 16-byte aligned");
   if (overlaps(x_t, (size_t)d.B * d.d * d.esize, y_t, (size_t)d.B * d.d * d.esize))
     return fail(PF_ERR_INVALID_ARG, "y_t must not alias x_t");
   const bool completes = st->j + 1 == d.P;
@@ -207,6 +220,7 @@ int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w, 
   if (nblk < 0) return fail(PF_ERR_INVALID_ARG, "nblk must be >= 0");
   if (nblk == 0) return PF_OK;
   if (!x_blocks) return fail(PF_ERR_INVALID_ARG, "x_blocks is NULL");
+  if (!aligned16(x_blocks)) return fail(PF_ERR_INVALID_ARG, "x_blocks must be 16-byte aligned");
   if (st->n + nblk > st->n_cap)
     return fail(PF_ERR_CAPACITY, "append of %lld blocks overflows the cache (n = %lld, n_cap = %lld)",
                 (long long)nblk, (long long)st->n, (long long)st->n_cap);

@@ -284,6 +284,13 @@ struct EpiSlot {
     const int hd = c / dh, e = c - hd * dh;
     out[(((int64_t)r * nh + hd) * P + j) * dh + e] = from_f32<T>(v);
   }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e] + (bias ? to_f32(bias[c + e]) : 0.0f);
+    const int hd = c / dh, e0 = c - hd * dh;
+    store8(out + (((int64_t)r * nh + hd) * P + j) * dh + e0, v);
+  }
 };
 
 template <typename T>
@@ -294,6 +301,9 @@ struct EpiSigmoidF32 {
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     if (bias) v += to_f32(bias[c]);
     out[(int64_t)r * ldo + c] = sigmoidf(v);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    for (int e = 0; e < 8; ++e) (*this)(r, c + e, v[e]);
   }
 };
 
@@ -311,6 +321,15 @@ struct EpiCache {
     const int64_t b = rr / nblk, i = rr - b * nblk;
     const int hd = c / dh, e = c - hd * dh;
     cache[(((int64_t)b * nh + hd) * n_cap + n0 + i) * dh + e] = from_f32<T>(v);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e] + (bias ? to_f32(bias[c + e]) : 0.0f);
+    const int64_t rr = r0 + r;
+    const int64_t b = rr / nblk, i = rr - b * nblk;
+    const int hd = c / dh, e0 = c - hd * dh;
+    store8(cache + (((int64_t)b * nh + hd) * n_cap + n0 + i) * dh + e0, v);
   }
 };
 

@@ -22,6 +22,23 @@ struct EpiLinear {
     out[(int64_t)r * ldo + c] = o;
     if (out2) out2[(int64_t)r * ldo + c] = o;
   }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float v[8], t[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e];
+    if (bias) {
+      load8(bias + c, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    if (add) {
+      load8(add + (int64_t)r * ld_add + c, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    store8(out + (int64_t)r * ldo + c, v);
+    if (out2) store8(out2 + (int64_t)r * ldo + c, v);
+  }
 };
 
 // Splits a [B*m, h*dh] projection into per-head tensors: row r = b*m + i,
@@ -40,6 +57,26 @@ struct EpiHeads {
     const int64_t bh = (int64_t)b * n_heads + hd;
     if (out) out[(bh * m + i) * dh + e] = o;
     if (out_t) out_t[(bh * dh + e) * ld_t + i] = o;
+  }
+  // 8 consecutive channels stay inside one head (dh is a multiple of 8)
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e];
+    if (bias) {
+      float t[8];
+      load8(bias + c, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    const int b = r / m, i = r - b * m;
+    const int hd = c / dh, e0 = c - hd * dh;
+    const int64_t bh = (int64_t)b * n_heads + hd;
+    if (out) store8(out + (bh * m + i) * dh + e0, v);
+    if (out_t) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out_t[(bh * dh + e0 + e) * ld_t + i] = from_f32<T>(v[e]);
+    }
   }
 };
 
@@ -60,6 +97,24 @@ struct EpiGate {
     y[i] = from_f32<T>(xv + sigmoidf(v) * dv);
     if (gsave) gsave[i] = from_f32<T>(v);
   }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float g[8], xv[8], dv[8], yv[8];
+    const int64_t i = (int64_t)r * ld + c;
+    load8(x + i, xv);
+    load8(delta + i, dv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) g[e] = v0[e];
+    if (bias) {
+      float t[8];
+      load8(bias + c, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) g[e] += t[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) yv[e] = xv[e] + sigmoidf(g[e]) * dv[e];
+    store8(y + i, yv);
+    if (gsave) store8(gsave + i, g);
+  }
 };
 
 // fp32 store with optional accumulation into what is there (fixed order:
@@ -71,6 +126,23 @@ struct EpiF32 {
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     float* p = out + (int64_t)r * ldo + c;
     *p = accumulate ? *p + v : v;
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float* p = out + (int64_t)r * ldo + c;
+    if ((ldo & 3) != 0) {
+      for (int e = 0; e < 8; ++e) (*this)(r, c + e, v0[e]);
+      return;
+    }
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e];
+    if (accumulate) {
+      float t[8];
+      load8(p, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    store8(p, v);
   }
 };
 

@@ -268,28 +268,72 @@ __global__ void __launch_bounds__(WM* WN* kWave)
     __syncthreads();
   }
 
-  // Epilogue: lane holds column (lane % 32), rows acc_row(r, lane) of each tile.
+  // Epilogue through LDS, one band of kTM rows (one wave row) at a time: the
+  // waves of that band park their fp32 accumulators in LDS, then every thread
+  // takes 8 consecutive columns of a row and hands them to the epilogue, so
+  // its global reads and writes are 16-byte and coalesced along rows.
+  float* stage = reinterpret_cast<float*>(smem);
+  constexpr int kSRow = BN + 8;  // +32 bytes: the two lane halves hit disjoint banks
+  static_assert((size_t)S::kTM * kSRow * sizeof(float) <= S::kLdsBytes, "epilogue band must fit in LDS");
+  constexpr int kChunks = S::kTM * BN / 8;
+#pragma unroll 1
+  for (int band = 0; band < WM; ++band) {
+    __syncthreads();
+    if (wm == band) {
 #pragma unroll
-  for (int i = 0; i < S::kFM; ++i) {
+      for (int i = 0; i < S::kFM; ++i)
 #pragma unroll
-    for (int j = 0; j < S::kFN; ++j) {
-      const int col = n0 + wn * S::kTN + j * 32 + (lane & 31);
+        for (int j = 0; j < S::kFN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * S::kTM + i * 32 + acc_row(r, lane);
-        if (row < p.M && col < p.N) epi(row, col, acc[i][j][r]);
+          for (int r = 0; r < 16; ++r)
+            stage[(i * 32 + acc_row(r, lane)) * kSRow + wn * S::kTN + j * 32 + (lane & 31)] = acc[i][j][r];
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int c = tid; c < kChunks; c += S::kThreads) {
+      const int rl = c / (BN / 8), cl = (c % (BN / 8)) * 8;
+      const int row = m0 + band * S::kTM + rl, col = n0 + cl;
+      if (row < p.M && col < p.N) {
+        float v[8];
+        const f32x4 a = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = a[e];
+          v[e + 4] = b[e];
+        }
+        if (col + 8 <= p.N) {
+          epi.vec8(row, col, v);
+        } else {
+          for (int e = 0; col + e < p.N; ++e) epi(row, col + e, v[e]);
+        }
       }
     }
   }
 }
 
-// Fixed-order reduction of split-K partials ws[s][M][N], then the epilogue.
+// Fixed-order reduction of split-K partials ws[s][M][N], then the epilogue
+// (8 consecutive columns per thread when N is a multiple of 8).
 template <class Epi>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(const float* __restrict__ ws, int splits, int M,
                                                             int N, const Epi epi) {
   const int64_t total = (int64_t)M * N;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * blockDim.x) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if ((N & 7) == 0) {
+    for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < total / 8; c += stride) {
+      const int64_t idx = c * 8;
+      float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      for (int z = 0; z < splits; ++z) {
+        float t[8];
+        load8(ws + (int64_t)z * total + idx, t);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += t[e];
+      }
+      epi.vec8((int)(idx / N), (int)(idx % N), v);
+    }
+    return;
+  }
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += stride) {
     float s = 0.0f;
     for (int z = 0; z < splits; ++z) s += ws[(int64_t)z * total + idx];
     epi((int)(idx / N), (int)(idx % N), s);
@@ -303,6 +347,13 @@ struct EpiPartial {
   int64_t slice_stride;
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     ws[(int64_t)blockIdx.z * slice_stride + (int64_t)r * N + c] = v;
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    if ((N & 7) == 0) {
+      store8(ws + (int64_t)blockIdx.z * slice_stride + (int64_t)r * N + c, v);
+    } else {
+      for (int e = 0; e < 8; ++e) (*this)(r, c + e, v[e]);
+    }
   }
 };
 
