@@ -11,9 +11,6 @@
 #include "layer.hpp"
 
 namespace pf {
-size_t layer_forward_gemm_ws(const LayerDims& d);
-size_t layer_backward_gemm_ws(const LayerDims& d);
-
 size_t layer_gemm_ws_bytes(const LayerDims& d, bool for_backward) {
   return for_backward ? layer_backward_gemm_ws(d) : layer_forward_gemm_ws(d);
 }

@@ -25,7 +25,8 @@ hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hi
 
 // Backward of Eq. 9 given dO and the forward's O and LSE. Row tensors q, k, v,
 // do_ and transposed tensors qt, kt, dot (layouts as above). Writes dq, dk, dv
-// as fp32 [B*m, h*dh] row-major (heads are column slices). delta is scratch
+// in the activation dtype as [B*m, h*dh] row-major (heads are column slices);
+// each value is accumulated in fp32 and rounded once. delta is scratch
 // [B, h, m] fp32 for rowsum(dO * O).
 struct AttnBwdParams {
   const void* q;
@@ -34,13 +35,13 @@ struct AttnBwdParams {
   const void* qt;
   const void* kt;
   const void* o;     // [B*m, h*dh]
-  const void* do_;   // [B*m, h*dh]
+  const void* do_;   // [B, h, m, dh]
   const void* dot;   // [B, h, dh, ld_t]
   const float* lse;
   float* delta;
-  float* dq;
-  float* dk;
-  float* dv;
+  void* dq;
+  void* dk;
+  void* dv;
   int m, n_heads, ld_t;
   int causal;
   float scale_log2;

@@ -80,6 +80,43 @@ struct EpiHeads {
   }
 };
 
+// Output map of the interaction with the token-causal shift folded in: row
+// r = b*m + i of H-bar goes to row r + 1 of S (the proxy block i + 1 receives);
+// the row i = m - 1 has no receiver and instead clears row b*m (block 0
+// receives zero). Every row of S is written exactly once.
+template <typename T>
+struct EpiShift {
+  T* out;
+  const T* bias;
+  int m, ld;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    if (bias) v += to_f32(bias[c]);
+    const int i = r % m;
+    if (i < m - 1)
+      out[(int64_t)(r + 1) * ld + c] = from_f32<T>(v);
+    else
+      out[(int64_t)(r - i) * ld + c] = from_f32<T>(0.0f);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e];
+    if (bias) {
+      float t[8];
+      load8(bias + c, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    const int i = r % m;
+    if (i < m - 1) {
+      store8(out + (int64_t)(r + 1) * ld + c, v);
+    } else {
+      const float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      store8(out + (int64_t)(r - i) * ld + c, z);
+    }
+  }
+};
+
 // Gated injection (Eq. 12): G = acc + b_g; Y = X + sigmoid(G) * Delta.
 template <typename T>
 struct EpiGate {

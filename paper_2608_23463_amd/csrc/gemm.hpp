@@ -6,11 +6,9 @@
 //          LAYOUT_MN -> A[k * lda + m]  (reduction strided)
 //  B(n,k): LAYOUT_K  -> B[n * ldb + k]  (a weight stored [out, in])
 //          LAYOUT_MN -> B[k * ldb + n]
-// Optional A features, both handled in the tile loader:
-//  - concatenation along K: for k >= a_ksplit the values come from A2
-//    (A2[m * lda2 + k - a_ksplit]); used for the gate input [X, Delta].
-//  - row shift: with a_shift_period p > 0, row m reads row m-1 of A, and rows
-//    with m % p == 0 read zeros; used to feed proxy i-1 to block i.
+// Optional concatenation of A along K, handled in the tile loader: for
+// k >= a_ksplit the values come from A2 (A2[m * lda2 + k - a_ksplit]); used
+// for the gate input [X, Delta].
 // Split-K: gridDim.z slices of the reduction range, each slice handing its
 // partial sums to the epilogue (normally a store into an fp32 workspace,
 // reduced afterwards in a fixed order, so results are deterministic).
@@ -43,7 +41,6 @@ struct GemmParams {
   const void* a2;
   int64_t lda2;
   int a_ksplit;        // K index where A2 starts (>= K: unused)
-  int a_shift_period;  // 0: off
   const void* b;
   int64_t ldb;
   int M, N, K;
@@ -87,12 +84,8 @@ struct LoaderK {
       const int v = tid + i * NT;
       const int row = v / kChunks;
       const int k = k0 + (v % kChunks) * kVec;
-      int grow = row0 + row;
-      bool ok = grow < rows_total && k < kend;
-      if (IS_A && p.a_shift_period > 0) {
-        ok = ok && (grow % p.a_shift_period) != 0;
-        grow -= 1;
-      }
+      const int grow = row0 + row;
+      const bool ok = grow < rows_total && k < kend;
       u32x4 val = {0u, 0u, 0u, 0u};
       if (ok) {
         if (IS_A && k >= p.a_ksplit) {
@@ -365,7 +358,6 @@ struct GemmProblem {
   const void* a2 = nullptr;
   int64_t lda2 = 0;
   int a_ksplit = 1 << 30;
-  int a_shift_period = 0;
   const void* b;
   int64_t ldb;
   int M, N, K;
@@ -423,7 +415,6 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   p.a2 = pr.a2;
   p.lda2 = pr.lda2;
   p.a_ksplit = pr.a_ksplit;
-  p.a_shift_period = pr.a_shift_period;
   p.b = pr.b;
   p.ldb = pr.ldb;
   p.M = pr.M;

@@ -37,7 +37,7 @@ struct LayerActs {
   size_t qt, kt, vt;          // [B, h, dh, ld_t]
   size_t o;                   // [B*m, d_p]
   size_t lse;                 // [B, h, m] fp32
-  size_t hbar;                // [B*m, d_p] (output of W_o, before the shift)
+  size_t s;                   // S [B*m, d_p]: the contextualised proxy each block receives
   size_t u[PF_MAX_LEVELS];    // U_j, j = 1..M-1: decompression level outputs [B*R_j, d_j]
   size_t delta;               // [B*L, d_f]
   size_t g;                   // gate pre-activation G [B*L, d_f]
@@ -48,23 +48,31 @@ struct LayerWs {
   size_t acts;      // forward activations when saved == NULL
   size_t gemm;      // split-K partials
   // backward scratch
-  size_t dg, ddelta;          // [B*L, d_f]
+  size_t dg, ddelta;          // dG, dDelta [B*L, d_f]
+  size_t dx32;                // fp32 accumulator of dX [B*L, d_f]
   size_t du[PF_MAX_LEVELS];   // dU_j j = 1..M-1 [B*R_j, d_j]
-  size_t ds;                  // dS (shifted) [B*m, d_p]
-  size_t dhbar;               // [B*m, d_p]
-  size_t dO, dOt;             // [B*m, d_p], [B, h, dh, ld_t]
-  size_t delta_rs;            // [B, h, m] fp32
-  size_t dq, dk, dv;          // fp32 [B*m, d_p]
-  size_t dqkv_t;              // dtype copies of dq, dk, dv for the projection GEMMs [3][B*m, d_p]
-  size_t dh;                  // [B*m, d_p]
+  size_t dhbar;               // gradient of the W_o output (shift undone) [B*m, d_p]
+  size_t dO, dOt;             // [B, h, m, dh], [B, h, dh, ld_t]
+  size_t delta_rs;            // rowsum(dO * O) [B, h, m] fp32
+  size_t dq, dk, dv;          // [B*m, d_p]
+  size_t dh32;                // fp32 accumulator of dH [B*m, d_p]
+  size_t dh;                  // dH in the activation dtype [B*m, d_p]
   size_t dz[PF_MAX_LEVELS];   // dZ_j j = 1..M-1 [B*R_j, d_j]
+  size_t colsum;              // bias-gradient partial column sums
   size_t bytes;
 };
+
+constexpr int kColsumChunks = 512;
 
 // Validates cfg; on failure returns a status and writes a message.
 int layer_dims(const pf_layer_config* cfg, LayerDims* d, const char** why);
 LayerActs layer_acts(const LayerDims& d, bool for_backward);
+// Workspace offsets without the split-K region (gemm == bytes == end of the
+// fixed buffers); layer_ws adds the split-K region sized by a dry run.
+LayerWs layer_ws_layout(const LayerDims& d, bool for_backward);
 LayerWs layer_ws(const LayerDims& d, bool for_backward);
+size_t layer_forward_gemm_ws(const LayerDims& d);
+size_t layer_backward_gemm_ws(const LayerDims& d);
 
 template <typename T>
 hipError_t layer_forward_run(const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,

@@ -1,16 +1,382 @@
-// ProxyFormer layer backward (placeholder until the backward kernels land).
-#include "common.hpp"
+// ProxyFormer layer backward: the chain rule through every forward step, in
+// reverse order, from the activations the forward saved.
+//
+//  1. gate: dG = dY * Delta * s(1 - s) with s = sigmoid(G) (elementwise), then
+//     one GEMM [dG W_gx | dG W_gd] whose epilogue forms dX = dY + dG W_gx (fp32
+//     accumulator) and dDelta = s * dY + dG W_gd; dW_g = dG^T [X, Delta].
+//  2. decompression levels 1..M (reverse of Eq. 17): dW_dj = dT^T U_j,
+//     dU_j = dT W_dj; the top level's epilogue undoes the token-causal shift.
+//  3. output map: dO = dHbar W_o (written per head in both layouts for the
+//     attention backward), dW_o = dHbar^T O.
+//  4. attention backward (separate dK/dV and dQ kernels, no atomics).
+//  5. projections: dW_{q,k,v} = d{Q,K,V}^T H; dH = dH_out + dQ W_q + dK W_k
+//     + dV W_v accumulated in fp32, rounded once (this is dH_in, Eq. 8).
+//  6. compression levels M..1 (reverse of Eq. 16): dW_cj = dZ_j^T V_j and
+//     dV_j = dZ_j W_cj; level 1 adds into the fp32 dX and rounds it once.
+// Bias gradients are column sums, reduced in two fixed-order stages. Every
+// GEMM whose reduction runs over tokens (the weight gradients) uses operands
+// contiguous along the output dimensions (LAYOUT_MN), transposed in registers
+// on the way to LDS, so no transposed copy of any activation is made.
+#include <algorithm>
+
+#include "attention.hpp"
+#include "epilogues.hpp"
 #include "layer.hpp"
+#include "runner.hpp"
 
 namespace pf {
 
-size_t layer_backward_gemm_ws(const LayerDims&) { return 0; }
+// dG = dY * Delta * s * (1 - s), s = sigmoid(G); 8 elements per thread.
+template <typename T>
+__global__ void __launch_bounds__(256) gate_bwd_prep_kernel(const T* __restrict__ dy, const T* __restrict__ delta,
+                                                            const T* __restrict__ g, T* __restrict__ dg, int64_t n8) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n8; c += stride) {
+    float a[8], b[8], z[8], o[8];
+    load8(dy + c * 8, a);
+    load8(delta + c * 8, b);
+    load8(g + c * 8, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float s = sigmoidf(z[e]);
+      o[e] = a[e] * b[e] * s * (1.0f - s);
+    }
+    store8(dg + c * 8, o);
+  }
+}
+
+// Column sums in two fixed-order stages: partial sums over row chunks, then
+// the sum of the partials in chunk order.
+template <typename T>
+__global__ void __launch_bounds__(256) colsum_partial_kernel(const T* __restrict__ in, int64_t rows, int n,
+                                                             int64_t ld, int64_t rows_per_chunk,
+                                                             float* __restrict__ part) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  const int chunk = blockIdx.y;
+  if (c >= n) return;
+  const int64_t r0 = (int64_t)chunk * rows_per_chunk;
+  const int64_t r1 = std::min<int64_t>(rows, r0 + rows_per_chunk);
+  float s = 0.0f;
+  for (int64_t r = r0; r < r1; ++r) s += to_f32(in[r * ld + c]);
+  part[(int64_t)chunk * n + c] = s;
+}
+
+__global__ void __launch_bounds__(256) colsum_final_kernel(const float* __restrict__ part, int chunks, int n,
+                                                           float* __restrict__ out) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= n) return;
+  float s = 0.0f;
+  for (int k = 0; k < chunks; ++k) s += part[(int64_t)k * n + c];
+  out[c] = s;
+}
+
+// Gate dgrad epilogue: columns [0, d) are dG W_gx, columns [d, 2d) dG W_gd.
+template <typename T>
+struct EpiGateDgrad {
+  const T* dy;
+  const T* g;
+  float* dx32;
+  T* ddelta;
+  int d;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    if (c < d) {
+      const int64_t i = (int64_t)r * d + c;
+      dx32[i] = to_f32(dy[i]) + v;
+    } else {
+      const int64_t i = (int64_t)r * d + (c - d);
+      ddelta[i] = from_f32<T>(to_f32(dy[i]) * sigmoidf(to_f32(g[i])) + v);
+    }
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    float a[8], o[8];
+    if (c < d) {  // d is a multiple of 8, so a chunk never straddles the halves
+      const int64_t i = (int64_t)r * d + c;
+      load8(dy + i, a);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = a[e] + v[e];
+      store8(dx32 + i, o);
+    } else {
+      const int64_t i = (int64_t)r * d + (c - d);
+      float z[8];
+      load8(dy + i, a);
+      load8(g + i, z);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = a[e] * sigmoidf(z[e]) + v[e];
+      store8(ddelta + i, o);
+    }
+  }
+};
+
+// Gradient of S back to the rows of the W_o output: in token-causal mode
+// dHbar[r - 1] = dS[r] within a sequence and the last proxy (which feeds no
+// block) gets zero; the row r = b*m writes that zero.
+template <typename T>
+struct EpiUnshift {
+  T* out;
+  int m, ld, shift;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    if (!shift) {
+      out[(int64_t)r * ld + c] = from_f32<T>(v);
+      return;
+    }
+    const int i = r % m;
+    if (i > 0)
+      out[(int64_t)(r - 1) * ld + c] = from_f32<T>(v);
+    else
+      out[(int64_t)(r + m - 1) * ld + c] = from_f32<T>(0.0f);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    if (!shift) {
+      store8(out + (int64_t)r * ld + c, v);
+      return;
+    }
+    const int i = r % m;
+    if (i > 0) {
+      store8(out + (int64_t)(r - 1) * ld + c, v);
+    } else {
+      const float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      store8(out + (int64_t)(r + m - 1) * ld + c, z);
+    }
+  }
+};
+
+// fp32 accumulation across several GEMMs into `acc`; the first may start from
+// `add` (dtype T) instead of the accumulator, the last writes the rounded sum
+// to `out` (and `out2`) instead of the accumulator.
+template <typename T>
+struct EpiAccum {
+  float* acc;
+  int64_t ld;
+  const T* add;
+  int first;
+  T* out;
+  T* out2;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    const int64_t i = (int64_t)r * ld + c;
+    const float t = v + (first ? (add ? to_f32(add[i]) : 0.0f) : acc[i]);
+    if (out) {
+      out[i] = from_f32<T>(t);
+      if (out2) out2[i] = from_f32<T>(t);
+    } else {
+      acc[i] = t;
+    }
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    const int64_t i = (int64_t)r * ld + c;
+    float t[8], b[8];
+    if (first) {
+      if (add) {
+        load8(add + i, b);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) b[e] = 0.0f;
+      }
+    } else {
+      load8(acc + i, b);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[e] = v[e] + b[e];
+    if (out) {
+      store8(out + i, t);
+      if (out2) store8(out2 + i, t);
+    } else {
+      store8(acc + i, t);
+    }
+  }
+};
 
 template <typename T>
-hipError_t layer_backward_run(const LayerDims&, const pf_layer_config*, const pf_layer_weights*, const void*,
-                              const void*, const char*, const void*, const void*, void*, void*,
-                              const pf_layer_grads*, char*, hipStream_t) {
-  return hipErrorNotSupported;
+static void colsum(Runner& run, const char* label, const T* in, int64_t rows, int n, int64_t ld, float* part,
+                   float* out) {
+  if (!out || run.dry) return;
+  const int chunks = (int)std::max<int64_t>(1, std::min<int64_t>(kColsumChunks, (rows + 63) / 64));
+  const int64_t rpc = (rows + chunks - 1) / chunks;
+  run.launch(label, [&] {
+    hipLaunchKernelGGL((colsum_partial_kernel<T>), dim3((n + 255) / 256, chunks), dim3(256), 0, run.stream, in,
+                       rows, n, ld, rpc, part);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((n + 255) / 256), dim3(256), 0, run.stream, part, chunks, n, out);
+    return hipGetLastError();
+  });
+}
+
+// dW (fp32 [M, N] with row stride ldo) = sum over rows r of A[r, m] * B[r, n]:
+// both operands are row-major [rows, *] activations, i.e. contiguous along
+// the output dimensions.
+template <typename T>
+static void wgrad(Runner& run, const char* label, const T* a, int64_t lda, const T* b, int64_t ldb, int M, int N,
+                  int64_t rows, float* out, int64_t ldo) {
+  if (!out) return;
+  GemmProblem pr{};
+  pr.a = a;
+  pr.lda = lda;
+  pr.b = b;
+  pr.ldb = ldb;
+  pr.M = M;
+  pr.N = N;
+  pr.K = (int)rows;
+  run.gemm<T, LAYOUT_MN, LAYOUT_MN>(label, pr, EpiF32{out, ldo, 0});
+}
+
+// dA [rows, N] = G [rows, K] W [K, N] for a weight W stored [K (out), N (in)]:
+// the weight is read contiguous along N (LAYOUT_MN).
+template <typename T, class Epi>
+static void dgrad(Runner& run, const char* label, const T* g, int64_t ldg, const void* w, int64_t ldw, int64_t rows,
+                  int N, int K, const Epi& epi) {
+  GemmProblem pr{};
+  pr.a = g;
+  pr.lda = ldg;
+  pr.b = w;
+  pr.ldb = ldw;
+  pr.M = (int)rows;
+  pr.N = N;
+  pr.K = K;
+  run.gemm<T, LAYOUT_K, LAYOUT_MN>(label, pr, epi);
+}
+
+template <typename T>
+static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
+                          const void* x, const char* saved, const void* dy, const void* dh_out, void* dx, void* dh_in,
+                          const pf_layer_grads* gr, char* ws) {
+  const LayerActs A = layer_acts(d, true);
+  const LayerWs W = layer_ws_layout(d, true);
+  auto S = [&](size_t off) { return reinterpret_cast<const T*>(saved + off); };
+  auto WT = [&](size_t off) { return reinterpret_cast<T*>(ws + off); };
+  auto WF = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  float* part = WF(W.colsum);
+  const int64_t BL = (int64_t)d.B * d.L;
+  const int64_t Bm = (int64_t)d.B * d.m;
+  const int df = d.d_f, dp = d.d_p;
+  const T* dyp = reinterpret_cast<const T*>(dy);
+  const T* xp = reinterpret_cast<const T*>(x);
+
+  // 1. gate (Eq. 12)
+  run.launch("gate_bwd_prep", [&] {
+    const int64_t n8 = BL * df / 8;
+    const int blocks = (int)std::min<int64_t>((n8 + 255) / 256, 16384);
+    hipLaunchKernelGGL((gate_bwd_prep_kernel<T>), dim3(blocks), dim3(256), 0, run.stream, dyp, S(A.delta), S(A.g),
+                       WT(W.dg), n8);
+    return hipGetLastError();
+  });
+  dgrad<T>(run, "gate_dgrad_gemm", WT(W.dg), df, w->gate.w, 2 * df, BL, 2 * df, df,
+           EpiGateDgrad<T>{dyp, S(A.g), WF(W.dx32), WT(W.ddelta), df});
+  float* dwg = reinterpret_cast<float*>(gr->gate.dw);
+  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df);
+  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, S(A.delta), df, df, df, BL, dwg ? dwg + df : nullptr, 2 * df);
+  colsum<T>(run, "bias_colsum", WT(W.dg), BL, df, df, part, reinterpret_cast<float*>(gr->gate.db));
+
+  // 2. decompression levels 1..M (reverse of Eq. 17)
+  const T* dT = WT(W.ddelta);  // dU_0 = dDelta
+  for (int j = 0; j < d.M; ++j) {
+    const int64_t rows = (int64_t)d.B * d.R[j + 1];
+    const int kd = d.k[j] * d.d[j];
+    const int dn = d.d[j + 1];
+    const T* u_in = j == d.M - 1 ? S(A.s) : S(A.u[j + 1]);
+    wgrad<T>(run, "decompress_wgrad_gemm", dT, kd, u_in, dn, kd, dn, rows,
+             reinterpret_cast<float*>(gr->decompress[j].dw), dn);
+    colsum<T>(run, "bias_colsum", dT, rows, kd, kd, part, reinterpret_cast<float*>(gr->decompress[j].db));
+    if (j == d.M - 1) {
+      dgrad<T>(run, "decompress_dgrad_gemm", dT, kd, w->decompress[j].w, dn, rows, dn, kd,
+               EpiUnshift<T>{WT(W.dhbar), (int)d.m, dp, cfg->mask == PF_TOKEN_CAUSAL ? 1 : 0});
+    } else {
+      dgrad<T>(run, "decompress_dgrad_gemm", dT, kd, w->decompress[j].w, dn, rows, dn, kd,
+               EpiLinear<T>{WT(W.du[j + 1]), dn, nullptr, nullptr, 0, nullptr});
+      dT = WT(W.du[j + 1]);
+    }
+  }
+
+  // 3. output map of the interaction
+  if (d.ld_t != d.m) {
+    const size_t tb = (size_t)d.B * d.nh * d.dh * d.ld_t * sizeof(T);
+    run.launch("fill_zero", [&] { return fill_zero(WT(W.dOt), tb, run.stream); });
+  }
+  dgrad<T>(run, "o_dgrad_gemm", WT(W.dhbar), dp, w->o.w, dp, Bm, dp, dp,
+           EpiHeads<T>{WT(W.dO), WT(W.dOt), nullptr, (int)d.m, d.dh, d.nh, d.ld_t});
+  wgrad<T>(run, "o_wgrad_gemm", WT(W.dhbar), dp, S(A.o), dp, dp, dp, Bm, reinterpret_cast<float*>(gr->o.dw), dp);
+  colsum<T>(run, "bias_colsum", WT(W.dhbar), Bm, dp, dp, part, reinterpret_cast<float*>(gr->o.db));
+
+  // 4. attention (Eq. 9)
+  AttnBwdParams ap{};
+  ap.q = S(A.q);
+  ap.k = S(A.k);
+  ap.v = S(A.v);
+  ap.qt = S(A.qt);
+  ap.kt = S(A.kt);
+  ap.o = S(A.o);
+  ap.do_ = WT(W.dO);
+  ap.dot = WT(W.dOt);
+  ap.lse = reinterpret_cast<const float*>(saved + A.lse);
+  ap.delta = WF(W.delta_rs);
+  ap.dq = WT(W.dq);
+  ap.dk = WT(W.dk);
+  ap.dv = WT(W.dv);
+  ap.m = (int)d.m;
+  ap.n_heads = d.nh;
+  ap.ld_t = d.ld_t;
+  ap.causal = cfg->mask != PF_BIDIRECTIONAL;
+  ap.scale = (float)(1.0 / std::sqrt((double)d.dh));
+  ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  run.launch("attention_bwd", [&] { return launch_attention_bwd<T>(ap, d.B, d.dh, run.stream); });
+
+  // 5. projections of H (and the residual update of Eq. 8)
+  const T* dqkv[3] = {WT(W.dq), WT(W.dk), WT(W.dv)};
+  const pf_linear* maps[3] = {&w->q, &w->k, &w->v};
+  const pf_linear_grad* grads[3] = {&gr->q, &gr->k, &gr->v};
+  for (int i = 0; i < 3; ++i) {
+    wgrad<T>(run, "qkv_wgrad_gemm", dqkv[i], dp, S(A.h), dp, dp, dp, Bm, reinterpret_cast<float*>(grads[i]->dw), dp);
+    colsum<T>(run, "bias_colsum", dqkv[i], Bm, dp, dp, part, reinterpret_cast<float*>(grads[i]->db));
+  }
+  for (int i = 0; i < 3; ++i) {
+    EpiAccum<T> e{WF(W.dh32), dp, reinterpret_cast<const T*>(dh_out), i == 0, i == 2 ? WT(W.dh) : nullptr,
+                  i == 2 ? reinterpret_cast<T*>(dh_in) : nullptr};
+    dgrad<T>(run, "qkv_dgrad_gemm", dqkv[i], dp, maps[i]->w, dp, Bm, dp, dp, e);
+  }
+
+  // 6. compression levels M..1 (reverse of Eq. 16)
+  const T* dz = WT(W.dh);
+  for (int j = d.M - 1; j >= 0; --j) {
+    const int64_t rows = (int64_t)d.B * d.R[j + 1];
+    const int kd = d.k[j] * d.d[j];
+    const int dn = d.d[j + 1];
+    const T* v_in = j == 0 ? xp : S(A.z[j]);
+    wgrad<T>(run, "compress_wgrad_gemm", dz, dn, v_in, kd, dn, kd, rows,
+             reinterpret_cast<float*>(gr->compress[j].dw), kd);
+    colsum<T>(run, "bias_colsum", dz, rows, dn, dn, part, reinterpret_cast<float*>(gr->compress[j].db));
+    if (j == 0) {
+      dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
+               EpiAccum<T>{WF(W.dx32), kd, nullptr, 0, reinterpret_cast<T*>(dx), nullptr});
+    } else {
+      dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
+               EpiLinear<T>{WT(W.dz[j]), kd, nullptr, nullptr, 0, nullptr});
+      dz = WT(W.dz[j]);
+    }
+  }
+}
+
+template <typename T>
+hipError_t layer_backward_run(const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
+                              const void* x, const void*, const char* saved, const void* dy, const void* dh_out,
+                              void* dx, void* dh_in, const pf_layer_grads* gr, char* ws, hipStream_t stream) {
+  const LayerWs W = layer_ws(d, true);
+  Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
+  backward_impl<T>(run, d, cfg, w, x, saved, dy, dh_out, dx, dh_in, gr, ws);
+  return run.err;
+}
+
+size_t layer_backward_gemm_ws(const LayerDims& d) {
+  pf_layer_config cfg{};
+  cfg.mask = PF_TOKEN_CAUSAL;
+  pf_layer_weights w{};
+  // every weight gradient requested, so every GEMM is planned
+  static float dummy;
+  pf_layer_grads gr{};
+  for (int j = 0; j < PF_MAX_LEVELS; ++j) gr.compress[j].dw = gr.decompress[j].dw = &dummy;
+  gr.q.dw = gr.k.dw = gr.v.dw = gr.o.dw = gr.gate.dw = &dummy;
+  Runner run(true);
+  if (d.esize == 2)
+    backward_impl<bf16>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, &gr, nullptr);
+  else
+    backward_impl<float>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, &gr, nullptr);
+  return run.gemm_need;
 }
 
 template hipError_t layer_backward_run<bf16>(const LayerDims&, const pf_layer_config*, const pf_layer_weights*,
@@ -19,4 +385,5 @@ template hipError_t layer_backward_run<bf16>(const LayerDims&, const pf_layer_co
 template hipError_t layer_backward_run<float>(const LayerDims&, const pf_layer_config*, const pf_layer_weights*,
                                               const void*, const void*, const char*, const void*, const void*, void*,
                                               void*, const pf_layer_grads*, char*, hipStream_t);
+
 }  // namespace pf

@@ -6,10 +6,10 @@
 //     and the last level's epilogue adds b_c and H_in (Eq. 8) and writes H.
 //  2. Q, K, V projections of H, written per head (V key-contiguous).
 //  3. causal flash attention over the m proxies (Eq. 9).
-//  4. output map W_o -> contextualised proxies.
-//  5. decompression, one GEMM per level from level M down to 1 (Eq. 10, 17);
-//     the first reads proxy i-1 for block i (token-causal injection) through
-//     a row shift in the GEMM's tile loader.
+//  4. output map W_o -> contextualised proxies S.
+//  5. decompression, one GEMM per level from level M down to 1 (Eq. 10, 17),
+//     reading S, which the W_o epilogue wrote already shifted (block i
+//     receives proxy i-1 in token-causal mode).
 //  6. gate GEMM over [X, Delta] with the injection X + sigmoid(G) * Delta in
 //     its epilogue (Eq. 12).
 #include <algorithm>
@@ -97,7 +97,7 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   a.vt = take(headt);
   a.o = take(prox);
   a.lse = take((size_t)d.B * d.nh * d.m * 4);
-  a.hbar = take(prox);
+  a.s = take(prox);
   for (int j = 1; j < d.M; ++j) a.u[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
   a.delta = take((size_t)d.B * d.L * d.d_f * es);
   a.g = bwd ? take((size_t)d.B * d.L * d.d_f * es) : 0;
@@ -105,7 +105,7 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   return a;
 }
 
-LayerWs layer_ws(const LayerDims& d, bool bwd) {
+LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
   LayerWs w{};
   size_t off = 0;
   const size_t es = d.esize;
@@ -119,24 +119,34 @@ LayerWs layer_ws(const LayerDims& d, bool bwd) {
   if (!bwd) {
     w.acts = take(layer_acts(d, false).bytes);
   } else {
+    const size_t prox32 = (size_t)d.B * d.m * d.d_p * 4;
     w.dg = take(tok);
     w.ddelta = take(tok);
+    w.dx32 = take((size_t)d.B * d.L * d.d_f * 4);
     for (int j = 1; j < d.M; ++j) w.du[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
-    w.ds = take(prox);
     w.dhbar = take(prox);
     w.dO = take(prox);
     w.dOt = take((size_t)d.B * d.nh * d.dh * d.ld_t * es);
     w.delta_rs = take((size_t)d.B * d.nh * d.m * 4);
-    const size_t proxf = (size_t)d.B * d.m * d.d_p * 4;
-    w.dq = take(proxf);
-    w.dk = take(proxf);
-    w.dv = take(proxf);
-    w.dqkv_t = take(3 * prox);
+    w.dq = take(prox);
+    w.dk = take(prox);
+    w.dv = take(prox);
+    w.dh32 = take(prox32);
     w.dh = take(prox);
     for (int j = 1; j < d.M; ++j) w.dz[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+    // widest bias: max over every linear map's output width
+    int64_t widest = std::max<int64_t>(2 * d.d_f, d.d_p);
+    for (int j = 0; j < d.M; ++j) widest = std::max<int64_t>(widest, (int64_t)d.k[j] * d.d[j]);
+    w.colsum = take((size_t)kColsumChunks * widest * 4);
   }
-  w.gemm = take(layer_gemm_ws_bytes(d, bwd));
+  w.gemm = off;
   w.bytes = off;
+  return w;
+}
+
+LayerWs layer_ws(const LayerDims& d, bool bwd) {
+  LayerWs w = layer_ws_layout(d, bwd);
+  w.bytes = w.gemm + align256(layer_gemm_ws_bytes(d, bwd));
   return w;
 }
 
@@ -215,7 +225,8 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   run.launch("attention_fwd", [&] { return launch_attention_fwd<T>(ap, d.B, d.dh, run.stream); });
 
-  // 4. output map of the interaction
+  // 4. output map of the interaction; in token-causal mode its epilogue also
+  //    applies the shift, so S holds proxy i-1 at row i (zero at row 0)
   {
     GemmProblem pr{};
     pr.a = P(A.o);
@@ -225,19 +236,18 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.M = (int)rows_m;
     pr.N = d.d_p;
     pr.K = d.d_p;
-    EpiLinear<T> e{P(A.hbar), d.d_p, reinterpret_cast<const T*>(w->o.b), nullptr, 0, nullptr};
-    run.gemm<T, LAYOUT_K, LAYOUT_K>("o_gemm", pr, e);
+    const T* bo = reinterpret_cast<const T*>(w->o.b);
+    if (cfg->mask == PF_TOKEN_CAUSAL) {
+      run.gemm<T, LAYOUT_K, LAYOUT_K>("o_gemm", pr, EpiShift<T>{P(A.s), bo, (int)d.m, d.d_p});
+    } else {
+      run.gemm<T, LAYOUT_K, LAYOUT_K>("o_gemm", pr, EpiLinear<T>{P(A.s), d.d_p, bo, nullptr, 0, nullptr});
+    }
   }
 
   // 5. decompression, level M down to 1 (Eq. 10, 17)
   for (int j = d.M - 1; j >= 0; --j) {
     GemmProblem pr{};
-    if (j == d.M - 1) {
-      pr.a = P(A.hbar);
-      pr.a_shift_period = cfg->mask == PF_TOKEN_CAUSAL ? (int)d.m : 0;
-    } else {
-      pr.a = P(A.u[j + 1]);
-    }
+    pr.a = j == d.M - 1 ? P(A.s) : P(A.u[j + 1]);
     pr.lda = d.d[j + 1];
     pr.b = w->decompress[j].w;
     pr.ldb = d.d[j + 1];
