@@ -280,8 +280,9 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
     """Gradients of the layer forward (chain rule of Eq. 7-17 as read above).
 
     Given dY = dL/dX_out [B, L, d_fine] and optionally dH_out [B, m, d_proxy],
-    returns dx, dh_in (None when h_in is None) and every weight and bias
-    gradient summed over the batch, in the layout of the weights.
+    returns dx, dh_in (None when h_in is None), every weight and bias gradient
+    summed over the batch in the layout of the weights, and the gradients of
+    the projections Q, K, V per proxy ("proj_grads", [B, m, d_proxy] each).
     """
     fwd = layer_forward(x, weights, factors, n_heads, mask, h_in, keep=True)
     dy = _f64(dy)
@@ -300,7 +301,9 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
           "decompress": [zgrad(w) for w in weights["decompress"]],
           "gate": zgrad(weights["gate"])}
     dx = np.zeros_like(dy)
-    dh_in = None if h_in is None else np.zeros((bsz, m, weights["q"][0].shape[0]))
+    d_p = weights["q"][0].shape[0]
+    dh_in = None if h_in is None else np.zeros((bsz, m, d_p))
+    proj_grads = {name: np.zeros((bsz, m, d_p)) for name in ("q", "k", "v")}
     wg = _f64(weights["gate"][0])
     for b in range(bsz):
         kp = fwd["kept"][b]
@@ -333,6 +336,7 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
         dq, dk, dv = _attention_backward(kp["q"], kp["k"], kp["v"], kp["o"], do, n_heads, mask)
         dh = np.zeros_like(kp["h"]) if dh_out is None else _f64(dh_out)[b].copy()
         for name, dz in (("q", dq), ("k", dk), ("v", dv)):
+            proj_grads[name][b] = dz
             gr[name][0] += dz.T @ kp["h"]
             gr[name][1] += dz.sum(axis=0)
             dh += dz @ _f64(weights[name][0])
@@ -346,4 +350,4 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             gr["compress"][j][1] += dz.sum(axis=0)
             dz = ungroup_rows(dz @ _f64(weights["compress"][j][0]), factors[j])
         dx[b] = dxb + dz
-    return {"dx": dx, "dh_in": dh_in, "grads": gr}
+    return {"dx": dx, "dh_in": dh_in, "grads": gr, "proj_grads": proj_grads}

@@ -14,7 +14,7 @@ import pytest
 import oracle
 from paper_2608_23463_amd import synth
 from paper_2608_23463_amd.synth import LayerShape
-from helpers import assert_close, dev, dev_weights, host
+from helpers import dev, dev_weights, host
 
 pytestmark = pytest.mark.gpu
 
@@ -34,19 +34,41 @@ def run_gpu_backward(shape, inp, dh_out=None):
 
 
 def compare(shape, inp, res, ref, label):
+    """Every gradient against the oracle; all are reported before asserting.
+
+    The key bias gradient is zero in exact arithmetic (softmax is invariant
+    to adding one constant to every key, so each row of dS sums to zero).
+    Its error is measured against the scale of its summands,
+    max_c sum_rows |dK[row, c]| (oracle), instead of its own ~0 magnitude.
+    """
+    from helpers import TOL
     dx, dh_in, grads = res
     dt = shape.dtype
-    assert_close(host(dx), ref["dx"], dt, f"{label} dx")
+    errs = {}
+
+    def chk(got, want, what, scale=None):
+        e = oracle.max_rel_err(got, want) if scale is None else \
+            float(np.max(np.abs(np.asarray(got, np.float64) - want))) / scale
+        errs[what] = e
+        print(f"  {label} {what}: max rel err {e:.3e} (tol {TOL[dt]:g})", flush=True)
+
+    chk(host(dx), ref["dx"], "dx")
     if ref["dh_in"] is not None:
-        assert_close(host(dh_in), ref["dh_in"], dt, f"{label} dh_in")
+        chk(host(dh_in), ref["dh_in"], "dh_in")
     rg = ref["grads"]
     for name in ("q", "k", "v", "o", "gate"):
-        assert_close(host(grads[name][0]), rg[name][0], dt, f"{label} dW_{name}")
-        assert_close(host(grads[name][1]), rg[name][1], dt, f"{label} db_{name}")
+        chk(host(grads[name][0]), rg[name][0], f"dW_{name}")
+        if name == "k":
+            scale = float(np.max(np.sum(np.abs(ref["proj_grads"]["k"]), axis=(0, 1))))
+            chk(host(grads[name][1]), rg[name][1], "db_k", scale)
+        else:
+            chk(host(grads[name][1]), rg[name][1], f"db_{name}")
     for kind in ("compress", "decompress"):
         for j in range(len(shape.factors)):
-            assert_close(host(grads[kind][j][0]), rg[kind][j][0], dt, f"{label} dW_{kind}[{j}]")
-            assert_close(host(grads[kind][j][1]), rg[kind][j][1], dt, f"{label} db_{kind}[{j}]")
+            chk(host(grads[kind][j][0]), rg[kind][j][0], f"dW_{kind}[{j}]")
+            chk(host(grads[kind][j][1]), rg[kind][j][1], f"db_{kind}[{j}]")
+    bad = {k: v for k, v in errs.items() if not v <= TOL[dt]}
+    assert not bad, f"{label}: gradients above tolerance: {bad}"
 
 
 CASES = {

@@ -131,3 +131,19 @@ def test_backward_dual_causality():
         r = oracle.layer_backward(x, w, (2, 2), nh, dy2)["dx"]
         assert np.array_equal(r[0, t + 1:], base[0, t + 1:])
         assert not np.array_equal(r[0, t], base[0, t])
+
+
+def test_key_bias_gradient_vanishes():
+    """Softmax is invariant to one constant added to every key (Eq. 9), so
+    dL/db_k = sum of dK over proxies is zero up to rounding in every mode."""
+    rng = np.random.default_rng(32)
+    d_f, d_p, nh, L = 4, 6, 2, 24
+    w = rand_weights(rng, d_f, d_p, (4,), std=0.5)
+    x = rng.standard_normal((2, L, d_f))
+    dy = rng.standard_normal((2, L, d_f))
+    for mask in (0, 1, 2):
+        res = oracle.layer_backward(x, w, (4,), nh, dy, mask)
+        scale = np.max(np.sum(np.abs(res["proj_grads"]["k"]), axis=(0, 1)))
+        assert scale > 1e-3
+        assert np.max(np.abs(res["grads"]["k"][1])) < 1e-12 * scale
+        np.testing.assert_allclose(res["grads"]["k"][1], res["proj_grads"]["k"].sum(axis=(0, 1)), atol=1e-14)
