@@ -12,6 +12,8 @@ namespace pf {
 struct AttnParams {
   const void* q;    // [B, h, m, dh]
   const void* k;    // [B, h, m, dh]
+  const void* q_lo; // optional low parts of the two-term split of Q and K
+  const void* k_lo; //   (bf16 only): logits use Qh Kh + Ql Kh + Qh Kl
   const void* vt;   // [B, h, dh, ld_t]
   void* o;          // [B*m, h*dh] row-major (heads are column slices)
   float* lse;       // [B, h, m] natural-log log-sum-exp of the scaled scores
@@ -31,6 +33,8 @@ hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hi
 struct AttnBwdParams {
   const void* q;
   const void* k;
+  const void* q_lo;  // optional, as in AttnParams
+  const void* k_lo;
   const void* v;
   const void* qt;
   const void* kt;

@@ -14,7 +14,8 @@
 // its B operand (same key/query permutation on both operands, as in the
 // forward kernel). The transposed operands (Q^T, K^T, dO^T) are produced
 // key/query-contiguous by the GEMM epilogues, so every MFMA fragment is a
-// plain LDS read.
+// plain LDS read. With SPLIT (bf16 hi/lo parts of Q and K) the recomputed
+// scores are Qh Kh + Ql Kh + Qh Kl, matching the forward's logits.
 #include "attention.hpp"
 
 namespace pf {
@@ -75,7 +76,7 @@ __global__ void __launch_bounds__(256) attn_bwd_delta_kernel(const T* __restrict
   if (lane == 0) delta[row] = s;
 }
 
-template <typename T, int DH>
+template <typename T, int DH, bool SPLIT>
 __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const AttnBwdParams p) {
   typedef Mma<T> MM;
   constexpr int kVec = 16 / sizeof(T);
@@ -83,6 +84,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const AttnBwdParams 
   constexpr int RS = DH + kVec;          // row-layout tile stride
   constexpr int TS = QT + kVec;          // transposed tile stride
   __shared__ __attribute__((aligned(16))) T s_q[QT * RS];
+  __shared__ __attribute__((aligned(16))) T s_ql[SPLIT ? QT * RS : 8];
   __shared__ __attribute__((aligned(16))) T s_do[QT * RS];
   __shared__ __attribute__((aligned(16))) T s_qt[DH * TS];
   __shared__ __attribute__((aligned(16))) T s_dot[DH * TS];
@@ -104,17 +106,23 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const AttnBwdParams 
   const T* dog = reinterpret_cast<const T*>(p.do_) + hoff;
   const T* qtg = reinterpret_cast<const T*>(p.qt) + toff;
   const T* dotg = reinterpret_cast<const T*>(p.dot) + toff;
+  const T* qlg = SPLIT ? reinterpret_cast<const T*>(p.q_lo) + hoff : nullptr;
+  const T* klg = SPLIT ? reinterpret_cast<const T*>(p.k_lo) + hoff : nullptr;
 
   // this wave's keys and values as B operands (column = key)
-  typename MM::frag kf[DH / 16], vf[DH / 16];
+  typename MM::frag kf[DH / 16], kfl[SPLIT ? DH / 16 : 1], vf[DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
     if (mykey < m) {
       kf[kk] = MM::load(kg + (int64_t)mykey * DH + kk * 16 + g * 8);
       vf[kk] = MM::load(vg + (int64_t)mykey * DH + kk * 16 + g * 8);
+      if constexpr (SPLIT) kfl[kk] = MM::load(klg + (int64_t)mykey * DH + kk * 16 + g * 8);
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) kf[kk][i] = vf[kk][i] = (T)0.0f;
+      for (int i = 0; i < 8; ++i) {
+        kf[kk][i] = vf[kk][i] = (T)0.0f;
+        if constexpr (SPLIT) kfl[kk][i] = (T)0.0f;
+      }
     }
   }
   f32x16 dvt[DH / 32], dkt[DH / 32];
@@ -130,6 +138,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const AttnBwdParams 
     const int vq = min(QT, m - q0);
     __syncthreads();
     tile_to_lds<T, QT, DH>(s_q, RS, qg + (int64_t)q0 * DH, DH, vq, DH, tid);
+    if constexpr (SPLIT) tile_to_lds<T, QT, DH>(s_ql, RS, qlg + (int64_t)q0 * DH, DH, vq, DH, tid);
     tile_to_lds<T, QT, DH>(s_do, RS, dog + (int64_t)q0 * DH, DH, vq, DH, tid);
     tile_to_lds<T, DH, QT>(s_qt, TS, qtg + q0, p.ld_t, DH, p.ld_t - q0, tid);
     tile_to_lds<T, DH, QT>(s_dot, TS, dotg + q0, p.ld_t, DH, p.ld_t - q0, tid);
@@ -148,7 +157,12 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const AttnBwdParams 
 #pragma unroll
       for (int kk = 0; kk < DH / 16; ++kk) {
         const int off = (qb * 32 + col) * RS + kk * 16 + g * 8;
-        s = MM::mma(MM::load(s_q + off), kf[kk], s);
+        const typename MM::frag qh = MM::load(s_q + off);
+        s = MM::mma(qh, kf[kk], s);
+        if constexpr (SPLIT) {
+          s = MM::mma(MM::load(s_ql + off), kf[kk], s);
+          s = MM::mma(qh, kfl[kk], s);
+        }
         dp = MM::mma(MM::load(s_do + off), vf[kk], dp);
       }
       float pr[16], dsr[16];
@@ -188,7 +202,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const AttnBwdParams 
   }
 }
 
-template <typename T, int DH>
+template <typename T, int DH, bool SPLIT>
 __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const AttnBwdParams p) {
   typedef Mma<T> MM;
   constexpr int kVec = 16 / sizeof(T);
@@ -196,6 +210,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const AttnBwdParams p)
   constexpr int RS = DH + kVec;
   constexpr int TS = KT + kVec;
   __shared__ __attribute__((aligned(16))) T s_k[KT * RS];
+  __shared__ __attribute__((aligned(16))) T s_kl[SPLIT ? KT * RS : 8];
   __shared__ __attribute__((aligned(16))) T s_v[KT * RS];
   __shared__ __attribute__((aligned(16))) T s_kt[DH * TS];
 
@@ -216,16 +231,22 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const AttnBwdParams p)
   const T* vg = reinterpret_cast<const T*>(p.v) + hoff;
   const T* dog = reinterpret_cast<const T*>(p.do_) + hoff;
   const T* ktg = reinterpret_cast<const T*>(p.kt) + toff;
+  const T* qlg = SPLIT ? reinterpret_cast<const T*>(p.q_lo) + hoff : nullptr;
+  const T* klg = SPLIT ? reinterpret_cast<const T*>(p.k_lo) + hoff : nullptr;
 
-  typename MM::frag qf[DH / 16], dof[DH / 16];
+  typename MM::frag qf[DH / 16], qfl[SPLIT ? DH / 16 : 1], dof[DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
     if (myq < m) {
       qf[kk] = MM::load(qg + (int64_t)myq * DH + kk * 16 + g * 8);
       dof[kk] = MM::load(dog + (int64_t)myq * DH + kk * 16 + g * 8);
+      if constexpr (SPLIT) qfl[kk] = MM::load(qlg + (int64_t)myq * DH + kk * 16 + g * 8);
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) qf[kk][i] = dof[kk][i] = (T)0.0f;
+      for (int i = 0; i < 8; ++i) {
+        qf[kk][i] = dof[kk][i] = (T)0.0f;
+        if constexpr (SPLIT) qfl[kk][i] = (T)0.0f;
+      }
     }
   }
   const float lse2 = myq < m ? p.lse[(int64_t)bh * m + myq] * 1.4426950408889634f : 0.0f;
@@ -243,6 +264,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const AttnBwdParams p)
     const int vk = min(KT, m - kt0);
     __syncthreads();
     tile_to_lds<T, KT, DH>(s_k, RS, kg + (int64_t)kt0 * DH, DH, vk, DH, tid);
+    if constexpr (SPLIT) tile_to_lds<T, KT, DH>(s_kl, RS, klg + (int64_t)kt0 * DH, DH, vk, DH, tid);
     tile_to_lds<T, KT, DH>(s_v, RS, vg + (int64_t)kt0 * DH, DH, vk, DH, tid);
     tile_to_lds<T, DH, KT>(s_kt, TS, ktg + kt0, p.ld_t, DH, p.ld_t - kt0, tid);
     __syncthreads();
@@ -255,7 +277,12 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const AttnBwdParams p)
 #pragma unroll
       for (int kk = 0; kk < DH / 16; ++kk) {
         const int off = (kb * 32 + col) * RS + kk * 16 + g * 8;
-        s = MM::mma(MM::load(s_k + off), qf[kk], s);
+        const typename MM::frag kh = MM::load(s_k + off);
+        s = MM::mma(kh, qf[kk], s);
+        if constexpr (SPLIT) {
+          s = MM::mma(MM::load(s_kl + off), qf[kk], s);
+          s = MM::mma(kh, qfl[kk], s);
+        }
         dp = MM::mma(MM::load(s_v + off), dof[kk], dp);
       }
       float dsr[16];
@@ -291,16 +318,27 @@ hipError_t launch_attention_bwd(const AttnBwdParams& p, int batch, int head_dim,
   const int64_t rows = (int64_t)batch * p.n_heads * p.m;
   const dim3 dgrid((unsigned)((rows + 3) / 4));
   const dim3 kgrid((p.m + 127) / 128, batch * p.n_heads);
+  const bool split = sizeof(T) == 2 && p.q_lo && p.k_lo;
   if (head_dim == 64) {
     hipLaunchKernelGGL((attn_bwd_delta_kernel<T, 64>), dgrid, dim3(256), 0, stream,
                        reinterpret_cast<const T*>(p.do_), reinterpret_cast<const T*>(p.o), p.delta, p.m, p.n_heads, rows);
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, 64>), kgrid, dim3(256), 0, stream, p);
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<T, 64>), kgrid, dim3(256), 0, stream, p);
+    if (split) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, 64, sizeof(T) == 2>), kgrid, dim3(256), 0, stream, p);
+      hipLaunchKernelGGL((attn_bwd_dq_kernel<T, 64, sizeof(T) == 2>), kgrid, dim3(256), 0, stream, p);
+    } else {
+      hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, 64, false>), kgrid, dim3(256), 0, stream, p);
+      hipLaunchKernelGGL((attn_bwd_dq_kernel<T, 64, false>), kgrid, dim3(256), 0, stream, p);
+    }
   } else {
     hipLaunchKernelGGL((attn_bwd_delta_kernel<T, 128>), dgrid, dim3(256), 0, stream,
                        reinterpret_cast<const T*>(p.do_), reinterpret_cast<const T*>(p.o), p.delta, p.m, p.n_heads, rows);
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, 128>), kgrid, dim3(256), 0, stream, p);
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<T, 128>), kgrid, dim3(256), 0, stream, p);
+    if (split) {
+      hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, 128, sizeof(T) == 2>), kgrid, dim3(256), 0, stream, p);
+      hipLaunchKernelGGL((attn_bwd_dq_kernel<T, 128, sizeof(T) == 2>), kgrid, dim3(256), 0, stream, p);
+    } else {
+      hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, 128, false>), kgrid, dim3(256), 0, stream, p);
+      hipLaunchKernelGGL((attn_bwd_dq_kernel<T, 128, false>), kgrid, dim3(256), 0, stream, p);
+    }
   }
   return hipGetLastError();
 }

@@ -9,20 +9,25 @@
 // feed O^T += V^T P^T directly as the B operand; V arrives key-contiguous
 // (the producing GEMM writes V transposed), so the A fragments are plain LDS
 // reads. Exponentials use exp2 with log2(e)/sqrt(d_head) folded into the
-// score scale. Masked scores are -inf and contribute exactly zero, so a query
+// score scale. With SPLIT, Q and K arrive as bf16 hi/lo pairs and the scores
+// are Kh Qh + Kl Qh + Kh Ql (three MFMAs into one accumulator), so a sharp
+// softmax is not moved by one bf16 rounding of its logits. Masked scores are
+// -inf and contribute exactly zero, so a query
 // never depends on later proxies (bit-exact causality).
 #include "attention.hpp"
 
 namespace pf {
 
-template <typename T, int DH>
+template <typename T, int DH, bool SPLIT>
 struct AttnFwdShape {
   static constexpr int kVec = 16 / sizeof(T);
   static constexpr int kKT = 64;                    // keys per tile
   static constexpr int kKStride = DH + kVec;        // K tile row stride
   static constexpr int kVStride = kKT + kVec;       // V^T tile row stride
   static constexpr int kKElems = kKT * kKStride;
-  static constexpr int kStage = kKElems + DH * kVStride;
+  static constexpr int kKParts = SPLIT ? 2 : 1;     // K hi (and lo) tiles
+  static constexpr int kVOff = kKParts * kKElems;
+  static constexpr int kStage = kVOff + DH * kVStride;
   static constexpr int kKLoads = kKT * DH / (256 * kVec);
   static constexpr int kVLoads = DH * kKT / (256 * kVec);
 };
@@ -38,9 +43,9 @@ struct Quad<float> {
   typedef u32x4 type;
 };
 
-template <typename T, int DH>
+template <typename T, int DH, bool SPLIT>
 __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
-  typedef AttnFwdShape<T, DH> S;
+  typedef AttnFwdShape<T, DH, SPLIT> S;
   typedef Mma<T> MM;
   __shared__ __attribute__((aligned(16))) T smem[2 * S::kStage];
 
@@ -56,32 +61,42 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
 
   const T* qp = reinterpret_cast<const T*>(p.q) + (int64_t)bh * p.m * DH;
   const T* kp = reinterpret_cast<const T*>(p.k) + (int64_t)bh * p.m * DH;
+  const T* qlp = SPLIT ? reinterpret_cast<const T*>(p.q_lo) + (int64_t)bh * p.m * DH : nullptr;
+  const T* klp = SPLIT ? reinterpret_cast<const T*>(p.k_lo) + (int64_t)bh * p.m * DH : nullptr;
   const T* vtp = reinterpret_cast<const T*>(p.vt) + (int64_t)bh * DH * p.ld_t;
 
-  typename MM::frag qf[DH / 16];
+  typename MM::frag qf[DH / 16], qfl[SPLIT ? DH / 16 : 1];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
     if (myq < p.m) {
       qf[kk] = MM::load(qp + (int64_t)myq * DH + kk * 16 + g * 8);
+      if constexpr (SPLIT) qfl[kk] = MM::load(qlp + (int64_t)myq * DH + kk * 16 + g * 8);
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) qf[kk][i] = (T)0.0f;
+      for (int i = 0; i < 8; ++i) {
+        qf[kk][i] = (T)0.0f;
+        if constexpr (SPLIT) qfl[kk][i] = (T)0.0f;
+      }
     }
   }
 
   const int kv_end = p.causal ? min(p.m, q0 + 128) : p.m;
   const int ntiles = (kv_end + S::kKT - 1) / S::kKT;
 
-  u32x4 rk[S::kKLoads], rv[S::kVLoads];
+  u32x4 rk[S::kKParts][S::kKLoads], rv[S::kVLoads];
   auto fetch = [&](int kt0) {
     constexpr int kc = DH / S::kVec;
 #pragma unroll
-    for (int i = 0; i < S::kKLoads; ++i) {
-      const int v = tid + i * 256;
-      const int key = kt0 + v / kc;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (key < p.m) val = ld16(kp + (int64_t)key * DH + (v % kc) * S::kVec);
-      rk[i] = val;
+    for (int part = 0; part < S::kKParts; ++part) {
+      const T* src = part == 0 ? kp : klp;
+#pragma unroll
+      for (int i = 0; i < S::kKLoads; ++i) {
+        const int v = tid + i * 256;
+        const int key = kt0 + v / kc;
+        u32x4 val = {0u, 0u, 0u, 0u};
+        if (key < p.m) val = ld16(src + (int64_t)key * DH + (v % kc) * S::kVec);
+        rk[part][i] = val;
+      }
     }
     constexpr int vc = S::kKT / S::kVec;
 #pragma unroll
@@ -93,15 +108,17 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
   auto stash = [&](T* st) {
     constexpr int kc = DH / S::kVec;
 #pragma unroll
-    for (int i = 0; i < S::kKLoads; ++i) {
-      const int v = tid + i * 256;
-      st16(st + (v / kc) * S::kKStride + (v % kc) * S::kVec, rk[i]);
-    }
+    for (int part = 0; part < S::kKParts; ++part)
+#pragma unroll
+      for (int i = 0; i < S::kKLoads; ++i) {
+        const int v = tid + i * 256;
+        st16(st + part * S::kKElems + (v / kc) * S::kKStride + (v % kc) * S::kVec, rk[part][i]);
+      }
     constexpr int vc = S::kKT / S::kVec;
 #pragma unroll
     for (int i = 0; i < S::kVLoads; ++i) {
       const int v = tid + i * 256;
-      st16(st + S::kKElems + (v / vc) * S::kVStride + (v % vc) * S::kVec, rv[i]);
+      st16(st + S::kVOff + (v / vc) * S::kVStride + (v % vc) * S::kVec, rv[i]);
     }
   };
 
@@ -121,7 +138,7 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
     const bool more = t + 1 < ntiles;
     if (more) fetch(kt0 + S::kKT);
     const T* sk = smem + (t & 1) * S::kStage;
-    const T* sv = sk + S::kKElems;
+    const T* sv = sk + S::kVOff;
     const bool active = !p.causal || kt0 <= qw0 + 31;  // uniform across the wave
     if (active) {
       f32x16 s[2];
@@ -130,8 +147,15 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
 #pragma unroll
-        for (int kk = 0; kk < DH / 16; ++kk)
-          s[kb] = MM::mma(MM::load(sk + (kb * 32 + col) * S::kKStride + kk * 16 + g * 8), qf[kk], s[kb]);
+        for (int kk = 0; kk < DH / 16; ++kk) {
+          const int off = (kb * 32 + col) * S::kKStride + kk * 16 + g * 8;
+          const typename MM::frag kh = MM::load(sk + off);
+          s[kb] = MM::mma(kh, qf[kk], s[kb]);
+          if constexpr (SPLIT) {
+            s[kb] = MM::mma(MM::load(sk + S::kKElems + off), qf[kk], s[kb]);
+            s[kb] = MM::mma(kh, qfl[kk], s[kb]);
+          }
+        }
       }
       const bool need_mask = (p.causal && kt0 + S::kKT - 1 > qw0) || kt0 + S::kKT > p.m;
       float mt = -INFINITY;
@@ -206,10 +230,17 @@ template <typename T>
 hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hipStream_t stream) {
   if (p.m <= 0) return hipSuccess;
   dim3 grid((p.m + 127) / 128, batch * p.n_heads);
+  const bool split = sizeof(T) == 2 && p.q_lo && p.k_lo;
   if (head_dim == 64) {
-    hipLaunchKernelGGL((attn_fwd_kernel<T, 64>), grid, dim3(256), 0, stream, p);
+    if (split)
+      hipLaunchKernelGGL((attn_fwd_kernel<T, 64, sizeof(T) == 2>), grid, dim3(256), 0, stream, p);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<T, 64, false>), grid, dim3(256), 0, stream, p);
   } else {
-    hipLaunchKernelGGL((attn_fwd_kernel<T, 128>), grid, dim3(256), 0, stream, p);
+    if (split)
+      hipLaunchKernelGGL((attn_fwd_kernel<T, 128, sizeof(T) == 2>), grid, dim3(256), 0, stream, p);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<T, 128, false>), grid, dim3(256), 0, stream, p);
   }
   return hipGetLastError();
 }

@@ -36,6 +36,11 @@ __device__ __forceinline__ float load_f32(const T* p, int64_t i) {
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
+// Low part of a two-term bf16 split: v = hi + lo with hi = bf16(v) and
+// lo = bf16(v - hi), which together keep ~16 mantissa bits of v. For fp32
+// tensors there is no low part.
+__device__ __forceinline__ float split_lo(float v) { return (float)(bf16)(v - (float)(bf16)v); }
+
 // Eight consecutive elements <-> fp32 (16-byte aligned for bf16, two
 // 16-byte accesses for fp32).
 __device__ __forceinline__ void load8(const bf16* p, float* v) {

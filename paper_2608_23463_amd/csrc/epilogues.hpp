@@ -7,6 +7,7 @@
 namespace pf {
 
 // out[r, c] = acc + bias[c] (+ add[r, c]); optional second copy out2.
+// out_lo (bf16 only, optional): low part of the two-term split of the result.
 template <typename T>
 struct EpiLinear {
   T* out;
@@ -15,12 +16,14 @@ struct EpiLinear {
   const T* add;
   int64_t ld_add;
   T* out2;
+  T* out_lo;
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     if (bias) v += to_f32(bias[c]);
     if (add) v += to_f32(add[(int64_t)r * ld_add + c]);
     const T o = from_f32<T>(v);
     out[(int64_t)r * ldo + c] = o;
     if (out2) out2[(int64_t)r * ldo + c] = o;
+    if (out_lo) out_lo[(int64_t)r * ldo + c] = from_f32<T>(split_lo(v));
   }
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
     float v[8], t[8];
@@ -38,6 +41,11 @@ struct EpiLinear {
     }
     store8(out + (int64_t)r * ldo + c, v);
     if (out2) store8(out2 + (int64_t)r * ldo + c, v);
+    if (out_lo) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = split_lo(v[e]);
+      store8(out_lo + (int64_t)r * ldo + c, t);
+    }
   }
 };
 
@@ -49,6 +57,7 @@ struct EpiHeads {
   T* out_t;
   const T* bias;
   int m, dh, n_heads, ld_t;
+  T* out_lo;  // optional low part of the split, row layout
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     if (bias) v += to_f32(bias[c]);
     const T o = from_f32<T>(v);
@@ -57,6 +66,7 @@ struct EpiHeads {
     const int64_t bh = (int64_t)b * n_heads + hd;
     if (out) out[(bh * m + i) * dh + e] = o;
     if (out_t) out_t[(bh * dh + e) * ld_t + i] = o;
+    if (out_lo) out_lo[(bh * m + i) * dh + e] = from_f32<T>(split_lo(v));
   }
   // 8 consecutive channels stay inside one head (dh is a multiple of 8)
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
@@ -73,6 +83,12 @@ struct EpiHeads {
     const int hd = c / dh, e0 = c - hd * dh;
     const int64_t bh = (int64_t)b * n_heads + hd;
     if (out) store8(out + (bh * m + i) * dh + e0, v);
+    if (out_lo) {
+      float t[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = split_lo(v[e]);
+      store8(out_lo + (bh * m + i) * dh + e0, t);
+    }
     if (out_t) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) out_t[(bh * dh + e0 + e) * ld_t + i] = from_f32<T>(v[e]);

@@ -6,9 +6,11 @@
 //          LAYOUT_MN -> A[k * lda + m]  (reduction strided)
 //  B(n,k): LAYOUT_K  -> B[n * ldb + k]  (a weight stored [out, in])
 //          LAYOUT_MN -> B[k * ldb + n]
-// Optional concatenation of A along K, handled in the tile loader: for
-// k >= a_ksplit the values come from A2 (A2[m * lda2 + k - a_ksplit]); used
-// for the gate input [X, Delta].
+// Optional concatenation along K, handled in the tile loader (LAYOUT_K
+// operands): for k >= a_ksplit the A values come from A2
+// (A2[m * lda2 + k - a_ksplit]), and for k >= b_ksplit the B values from B2.
+// Used for the gate input [X, Delta], and for the split-precision products
+// [X_hi | X_lo] [W | W]^T = X W^T to ~16 mantissa bits.
 // Split-K: gridDim.z slices of the reduction range, each slice handing its
 // partial sums to the epilogue (normally a store into an fp32 workspace,
 // reduced afterwards in a fixed order, so results are deterministic).
@@ -43,6 +45,9 @@ struct GemmParams {
   int a_ksplit;        // K index where A2 starts (>= K: unused)
   const void* b;
   int64_t ldb;
+  const void* b2;
+  int64_t ldb2;
+  int b_ksplit;        // K index where B2 starts (>= K: unused)
   int M, N, K;
   int k_slice;         // reduction length per gridDim.z slice (multiple of BK)
   int tiles_m, tiles_n;
@@ -86,11 +91,12 @@ struct LoaderK {
       const int k = k0 + (v % kChunks) * kVec;
       const int grow = row0 + row;
       const bool ok = grow < rows_total && k < kend;
+      const int ksplit = IS_A ? p.a_ksplit : p.b_ksplit;
       u32x4 val = {0u, 0u, 0u, 0u};
       if (ok) {
-        if (IS_A && k >= p.a_ksplit) {
-          const T* a2 = reinterpret_cast<const T*>(p.a2);
-          val = ld16(a2 + (int64_t)grow * p.lda2 + (k - p.a_ksplit));
+        if (k >= ksplit) {
+          const T* src2 = reinterpret_cast<const T*>(IS_A ? p.a2 : p.b2);
+          val = ld16(src2 + (int64_t)grow * (IS_A ? p.lda2 : p.ldb2) + (k - ksplit));
         } else {
           val = ld16(base + (int64_t)grow * ld + k);
         }
@@ -360,6 +366,9 @@ struct GemmProblem {
   int a_ksplit = 1 << 30;
   const void* b;
   int64_t ldb;
+  const void* b2 = nullptr;
+  int64_t ldb2 = 0;
+  int b_ksplit = 1 << 30;
   int M, N, K;
 };
 
@@ -417,6 +426,9 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   p.a_ksplit = pr.a_ksplit;
   p.b = pr.b;
   p.ldb = pr.ldb;
+  p.b2 = pr.b2;
+  p.ldb2 = pr.ldb2;
+  p.b_ksplit = pr.b_ksplit;
   p.M = pr.M;
   p.N = pr.N;
   p.K = pr.K;

@@ -30,10 +30,18 @@ struct LayerDims {
 
 // Byte offsets of every activation inside the region that holds them
 // (the caller's `saved` buffer, or the workspace when saved is NULL).
+// In bf16 mode the proxy path upstream of the attention logits (Z_j, H, Q, K)
+// also keeps the low part of a two-term bf16 split (the *_lo buffers): a
+// proxy sums P * d_fine products, so its magnitude, and the logits', grow
+// with the compression fan-in, and one bf16 rounding there moves a sharp
+// softmax by several percent. In fp32 mode the *_lo buffers are empty.
 struct LayerActs {
   size_t z[PF_MAX_LEVELS];    // Z_j, j = 1..M-1: compression level outputs [B*R_j, d_j]
+  size_t z_lo[PF_MAX_LEVELS];
   size_t h;                   // H = H_in + c [B*m, d_p] (copy kept for the backward)
+  size_t h_lo;
   size_t q, k, v;             // [B, h, m, dh]
+  size_t q_lo, k_lo;
   size_t qt, kt, vt;          // [B, h, dh, ld_t]
   size_t o;                   // [B*m, d_p]
   size_t lse;                 // [B, h, m] fp32

@@ -4,7 +4,10 @@
 //  1. compression, one GEMM per level (Eq. 7, 15-16); the block partition of
 //     Eq. 2 and the grouping of Eq. 16 are zero-copy views of row-major data,
 //     and the last level's epilogue adds b_c and H_in (Eq. 8) and writes H.
-//  2. Q, K, V projections of H, written per head (V key-contiguous).
+//  2. Q, K, V projections of H, written per head (V key-contiguous). In bf16
+//     mode H, the level outputs Z_j, Q and K keep a bf16 low part as well
+//     (two-term split), and the GEMMs that read them multiply [hi | lo] by
+//     [W | W]: the attention logits then carry ~16 mantissa bits.
 //  3. causal flash attention over the m proxies (Eq. 9).
 //  4. output map W_o -> contextualised proxies S.
 //  5. decompression, one GEMM per level from level M down to 1 (Eq. 10, 17),
@@ -87,10 +90,17 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   };
   const size_t prox = (size_t)d.B * d.m * d.d_p * es;
   const size_t headt = (size_t)d.B * d.nh * d.dh * d.ld_t * es;
-  for (int j = 1; j < d.M; ++j) a.z[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+  const bool split = d.esize == 2;
+  for (int j = 1; j < d.M; ++j) {
+    a.z[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
+    a.z_lo[j] = take(split ? (size_t)d.B * d.R[j] * d.d[j] * es : 0);
+  }
   a.h = bwd ? take(prox) : 0;
+  a.h_lo = take(split ? prox : 0);
   a.q = take(prox);
   a.k = take(prox);
+  a.q_lo = take(split ? prox : 0);
+  a.k_lo = take(split ? prox : 0);
   a.v = bwd ? take(prox) : 0;
   a.qt = bwd ? take(headt) : 0;
   a.kt = bwd ? take(headt) : 0;
@@ -157,17 +167,31 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   auto P = [&](size_t off) { return reinterpret_cast<T*>(act + off); };
   const int64_t rows_m = (int64_t)d.B * d.m;
 
-  // 1. compression cascade (Eq. 7, 16) and the residual proxy update (Eq. 8)
+  const bool split = sizeof(T) == 2;
+
+  // 1. compression cascade (Eq. 7, 16) and the residual proxy update (Eq. 8).
+  //    Levels after the first read their input as [hi | lo] against [W | W].
   const T* zin = reinterpret_cast<const T*>(x);
+  const T* zin_lo = nullptr;
   for (int j = 0; j < d.M; ++j) {
     GemmProblem pr{};
+    const int kd = d.k[j] * d.d[j];
     pr.a = zin;
-    pr.lda = (int64_t)d.k[j] * d.d[j];
+    pr.lda = kd;
     pr.b = w->compress[j].w;
-    pr.ldb = pr.lda;
+    pr.ldb = kd;
     pr.M = (int)(d.B * d.R[j + 1]);
     pr.N = d.d[j + 1];
-    pr.K = (int)pr.lda;
+    pr.K = kd;
+    if (zin_lo) {
+      pr.a2 = zin_lo;
+      pr.lda2 = kd;
+      pr.a_ksplit = kd;
+      pr.b2 = w->compress[j].w;
+      pr.ldb2 = kd;
+      pr.b_ksplit = kd;
+      pr.K = 2 * kd;
+    }
     EpiLinear<T> e{};
     e.bias = reinterpret_cast<const T*>(w->compress[j].b);
     if (j == d.M - 1) {
@@ -176,15 +200,19 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
       e.add = reinterpret_cast<const T*>(h_in);
       e.ld_add = d.d_p;
       e.out2 = saving ? P(A.h) : nullptr;
+      e.out_lo = split ? P(A.h_lo) : nullptr;
     } else {
       e.out = P(A.z[j + 1]);
       e.ldo = d.d[j + 1];
+      e.out_lo = split ? P(A.z_lo[j + 1]) : nullptr;
     }
     run.gemm<T, LAYOUT_K, LAYOUT_K>("compress_gemm", pr, e);
     zin = e.out;
+    zin_lo = e.out_lo;
   }
 
-  // 2. projections of H into per-head Q, K (row layout) and V (key-contiguous)
+  // 2. projections of H into per-head Q, K (row layout, hi and lo parts) and
+  //    V (key-contiguous); Q and K read H as [hi | lo]
   const T* hbuf = reinterpret_cast<const T*>(h_out);
   if (d.ld_t != d.m) {
     // padding columns of the transposed tensors must read as zero
@@ -198,6 +226,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   const pf_linear* proj[3] = {&w->q, &w->k, &w->v};
   T* outs[3] = {P(A.q), P(A.k), saving ? P(A.v) : nullptr};
   T* outs_t[3] = {saving ? P(A.qt) : nullptr, saving ? P(A.kt) : nullptr, P(A.vt)};
+  T* outs_lo[3] = {split ? P(A.q_lo) : nullptr, split ? P(A.k_lo) : nullptr, nullptr};
   for (int i = 0; i < 3; ++i) {
     GemmProblem pr{};
     pr.a = hbuf;
@@ -207,7 +236,17 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.M = (int)rows_m;
     pr.N = d.d_p;
     pr.K = d.d_p;
-    EpiHeads<T> e{outs[i], outs_t[i], reinterpret_cast<const T*>(proj[i]->b), (int)d.m, d.dh, d.nh, d.ld_t};
+    if (outs_lo[i]) {
+      pr.a2 = P(A.h_lo);
+      pr.lda2 = d.d_p;
+      pr.a_ksplit = d.d_p;
+      pr.b2 = proj[i]->w;
+      pr.ldb2 = d.d_p;
+      pr.b_ksplit = d.d_p;
+      pr.K = 2 * d.d_p;
+    }
+    EpiHeads<T> e{outs[i], outs_t[i], reinterpret_cast<const T*>(proj[i]->b), (int)d.m, d.dh, d.nh, d.ld_t,
+                  outs_lo[i]};
     run.gemm<T, LAYOUT_K, LAYOUT_K>("qkv_gemm", pr, e);
   }
 
@@ -215,6 +254,8 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   AttnParams ap{};
   ap.q = P(A.q);
   ap.k = P(A.k);
+  ap.q_lo = split ? P(A.q_lo) : nullptr;
+  ap.k_lo = split ? P(A.k_lo) : nullptr;
   ap.vt = P(A.vt);
   ap.o = P(A.o);
   ap.lse = reinterpret_cast<float*>(act + A.lse);
