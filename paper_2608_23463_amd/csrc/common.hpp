@@ -34,6 +34,18 @@ __device__ __forceinline__ float load_f32(const T* p, int64_t i) {
 }
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Raw buffer access (gfx9 descriptor word 3 = 0x00020000). A load whose byte
+// offset plus size exceeds `bytes` returns zero, so tile edges need no
+// branches; kOOB is an offset that is always out of range.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0);
+}
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
 // Low part of a two-term bf16 split: v = hi + lo with hi = bf16(v) and

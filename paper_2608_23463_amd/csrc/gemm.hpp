@@ -72,6 +72,11 @@ struct GemmShape {
 };
 
 // ---- tile loaders: global -> registers -> LDS ------------------------------
+//
+// Both loaders use buffer loads: the per-thread byte offsets inside a tile are
+// computed once; each K step only rebuilds the (scalar) descriptor whose base
+// is the tile's first element and whose byte range ends at the operand's
+// edge, so out-of-range rows and K rows read as zero in hardware.
 
 // Rows of the tile are contiguous along K in global memory.
 template <typename T, int ROWS, int BK, int NT, bool IS_A>
@@ -80,28 +85,59 @@ struct LoaderK {
   static constexpr int kChunks = BK / kVec;  // 16-byte chunks per row
   static constexpr int kLoads = ROWS * BK / (NT * kVec);
 
-  static __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], const GemmParams& p, int row0,
-                                               int rows_total, int k0, int kend, int tid) {
-    const T* base = reinterpret_cast<const T*>(IS_A ? p.a : p.b);
+  uint32_t voff[kLoads];  // byte offset of each chunk from the tile's first element
+  int kc[kLoads];         // K offset (elements) of each chunk inside the tile
+  const char* src1;       // row row0 of the primary source
+  const char* src2;       // row row0 of the source after the K split
+  int64_t ld_bytes;
+  uint32_t row_bytes_valid;  // bytes spanned by the valid rows of the tile
+  int ksplit;
+
+  __device__ __forceinline__ void init(const GemmParams& p, int row0, int rows_total, int tid) {
     const int64_t ld = IS_A ? p.lda : p.ldb;
+    ld_bytes = ld * (int64_t)sizeof(T);
+    src1 = reinterpret_cast<const char*>(IS_A ? p.a : p.b) + row0 * ld_bytes;
+    const void* s2 = IS_A ? p.a2 : p.b2;
+    src2 = s2 ? reinterpret_cast<const char*>(s2) + row0 * ld_bytes : nullptr;  // same row stride
+    ksplit = IS_A ? p.a_ksplit : p.b_ksplit;
+    const int valid = max(0, min(ROWS, rows_total - row0));
+    row_bytes_valid = (uint32_t)(valid * ld_bytes);
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) {
       const int v = tid + i * NT;
-      const int row = v / kChunks;
-      const int k = k0 + (v % kChunks) * kVec;
-      const int grow = row0 + row;
-      const bool ok = grow < rows_total && k < kend;
-      const int ksplit = IS_A ? p.a_ksplit : p.b_ksplit;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (ok) {
-        if (k >= ksplit) {
-          const T* src2 = reinterpret_cast<const T*>(IS_A ? p.a2 : p.b2);
-          val = ld16(src2 + (int64_t)grow * (IS_A ? p.lda2 : p.ldb2) + (k - ksplit));
-        } else {
-          val = ld16(base + (int64_t)grow * ld + k);
-        }
+      kc[i] = (v % kChunks) * kVec;
+      voff[i] = (uint32_t)((v / kChunks) * ld_bytes + kc[i] * (int)sizeof(T));
+    }
+  }
+
+  // One K step [k0, k0 + BK) clipped to kend.
+  __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], int k0, int kend) const {
+    const bool partial = k0 + BK > kend;
+    if (k0 + BK <= ksplit || k0 >= ksplit) {
+      const bool second = k0 >= ksplit;
+      const int krel = second ? k0 - ksplit : k0;
+      const rsrc_t rs = make_rsrc((second ? src2 : src1) + (int64_t)krel * sizeof(T),
+                                  row_bytes_valid - (uint32_t)(krel * sizeof(T)));
+      if (!partial) {
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) r[i] = buf_ld16(rs, voff[i]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) r[i] = buf_ld16(rs, k0 + kc[i] < kend ? voff[i] : kOOB);
       }
-      r[i] = val;
+    } else {
+      // the tile straddles the split: read each chunk from its source
+      const rsrc_t r1 = make_rsrc(src1 + (int64_t)k0 * sizeof(T), row_bytes_valid - (uint32_t)(k0 * sizeof(T)));
+      const rsrc_t r2 = make_rsrc(src2 + (int64_t)(k0 - ksplit) * (int64_t)sizeof(T),
+                                  row_bytes_valid + (uint32_t)((ksplit - k0) * sizeof(T)));
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        const int k = k0 + kc[i];
+        const bool ok = k < kend;
+        const u32x4 a = buf_ld16(r1, ok && k < ksplit ? voff[i] : kOOB);
+        const u32x4 b = buf_ld16(r2, ok && k >= ksplit ? voff[i] : kOOB);
+        r[i] = a | b;
+      }
     }
   }
 
@@ -126,24 +162,31 @@ struct LoaderMN {
   static constexpr int kLoads = kBlocks * kVec;
   static_assert(ROWS % kVec == 0 && BK % kVec == 0, "tile must hold whole VEC x VEC blocks");
 
-  static __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], const GemmParams& p, int row0,
-                                               int rows_total, int k0, int kend, int tid) {
-    const T* base = reinterpret_cast<const T*>(IS_A ? p.a : p.b);
+  uint32_t voff[kLoads];
+  const char* src;
+  int64_t ld_bytes;
+
+  __device__ __forceinline__ void init(const GemmParams& p, int row0, int rows_total, int tid) {
     const int64_t ld = IS_A ? p.lda : p.ldb;
+    ld_bytes = ld * (int64_t)sizeof(T);
+    src = reinterpret_cast<const char*>(IS_A ? p.a : p.b) + (int64_t)row0 * sizeof(T);
 #pragma unroll
     for (int bi = 0; bi < kBlocks; ++bi) {
       const int blk = tid + bi * NT;
-      const int row = row0 + (blk % kRowBlocks) * kVec;
-      const int kb = k0 + (blk / kRowBlocks) * kVec;
-      const bool active = (kTotalBlocks % NT == 0) || blk < kTotalBlocks;
+      const int row = (blk % kRowBlocks) * kVec;
+      const int kb = (blk / kRowBlocks) * kVec;
+      const bool active = ((kTotalBlocks % NT == 0) || blk < kTotalBlocks) && row0 + row < rows_total;
 #pragma unroll
-      for (int t = 0; t < kVec; ++t) {
-        const int k = kb + t;
-        u32x4 val = {0u, 0u, 0u, 0u};
-        if (active && row < rows_total && k < kend) val = ld16(base + (int64_t)k * ld + row);
-        r[bi * kVec + t] = val;
-      }
+      for (int t = 0; t < kVec; ++t)
+        voff[bi * kVec + t] = active ? (uint32_t)((kb + t) * ld_bytes + row * (int)sizeof(T)) : kOOB;
     }
+  }
+
+  __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], int k0, int kend) const {
+    // K rows at or beyond kend fall outside the descriptor's range
+    const rsrc_t rs = make_rsrc(src + (int64_t)k0 * ld_bytes, (uint32_t)(max(0, kend - k0) * ld_bytes));
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) r[i] = buf_ld16(rs, voff[i]);
   }
 
   static __device__ __forceinline__ void stash(const u32x4 (&r)[kLoads], T* lds, int stride, int tid) {
@@ -201,8 +244,12 @@ __device__ __forceinline__ void tile_coords(const GemmParams& p, int& tm, int& t
   tn = w / gm;
 }
 
+// Occupancy: the two LDS stages of the 256x256 tile admit one workgroup per
+// CU, so the kernel declares that and lets the compiler keep the prefetched
+// fragments in registers instead of scheduling for more waves.
 template <typename T, int BM, int BN, int BK, int WM, int WN, int LA, int LB, class Epi>
 __global__ void __launch_bounds__(WM* WN* kWave)
+    __attribute__((amdgpu_waves_per_eu(1, (BM >= 256 ? 1 : 2))))
     gemm_kernel(const GemmParams p, const Epi epi) {
   typedef GemmShape<T, BM, BN, BK, WM, WN> S;
   typedef Loader<T, BM, BK, S::kThreads, true, LA> LdA;
@@ -226,11 +273,15 @@ __global__ void __launch_bounds__(WM* WN* kWave)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  LdA lda_;
+  LdB ldb_;
+  lda_.init(p, m0, p.M, tid);
+  ldb_.init(p, n0, p.N, tid);
   u32x4 ra[LdA::kLoads], rb[LdB::kLoads];
   const int nk = (kend - kbeg + BK - 1) / BK;
   if (nk > 0) {
-    LdA::fetch(ra, p, m0, p.M, kbeg, kend, tid);
-    LdB::fetch(rb, p, n0, p.N, kbeg, kend, tid);
+    lda_.fetch(ra, kbeg, kend);
+    ldb_.fetch(rb, kbeg, kend);
     LdA::stash(ra, smem, S::kStride, tid);
     LdB::stash(rb, smem + BM * S::kStride, S::kStride, tid);
   }
@@ -242,22 +293,52 @@ __global__ void __launch_bounds__(WM* WN* kWave)
     T* cur = smem + (kt & 1) * S::kStageElems;
     const bool more = kt + 1 < nk;
     if (more) {
-      LdA::fetch(ra, p, m0, p.M, kbeg + (kt + 1) * BK, kend, tid);
-      LdB::fetch(rb, p, n0, p.N, kbeg + (kt + 1) * BK, kend, tid);
+      lda_.fetch(ra, kbeg + (kt + 1) * BK, kend);
+      ldb_.fetch(rb, kbeg + (kt + 1) * BK, kend);
     }
     const T* sa = cur + (wm * S::kTM + frow) * S::kStride + fk;
     const T* sb = cur + (BM + wn * S::kTN + frow) * S::kStride + fk;
+    // fragments of k16 step s + 1 are read from LDS while step s multiplies
+    typename MM::frag fa[2][S::kFM], fb[2][S::kFN];
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      typename MM::frag fa[S::kFM], fb[S::kFN];
+    for (int i = 0; i < S::kFM; ++i) fa[0][i] = MM::load(sa + i * 32 * S::kStride);
 #pragma unroll
-      for (int i = 0; i < S::kFM; ++i) fa[i] = MM::load(sa + i * 32 * S::kStride + kk);
+    for (int j = 0; j < S::kFN; ++j) fb[0][j] = MM::load(sb + j * 32 * S::kStride);
 #pragma unroll
-      for (int j = 0; j < S::kFN; ++j) fb[j] = MM::load(sb + j * 32 * S::kStride + kk);
+    for (int st = 0; st < BK / 16; ++st) {
+      const int cb = st & 1, nb = cb ^ 1;
+      if (st + 1 < BK / 16) {
+#pragma unroll
+        for (int i = 0; i < S::kFM; ++i) fa[nb][i] = MM::load(sa + i * 32 * S::kStride + (st + 1) * 16);
+#pragma unroll
+        for (int j = 0; j < S::kFN; ++j) fb[nb][j] = MM::load(sb + j * 32 * S::kStride + (st + 1) * 16);
+      }
 #pragma unroll
       for (int i = 0; i < S::kFM; ++i)
 #pragma unroll
-        for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[i], fb[j], acc[i][j]);
+        for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[cb][i], fb[cb][j], acc[i][j]);
+    }
+    // Instruction order for the block above: the reads of step 0, then each
+    // step's MFMAs interleaved with the fragment reads of the next step, so
+    // LDS latency hides behind matrix work (masks: 0x100 DS read, 0x008 MFMA).
+    if constexpr (sizeof(T) == 2) {
+      constexpr int kReads = S::kFM + S::kFN;
+      constexpr int kMfma = S::kFM * S::kFN;
+      // next-step reads ride on the first MFMAs of a step (one each), so the
+      // last of them still has the second half of the step to land
+      constexpr int kLead = kReads < kMfma ? kReads : kMfma;
+      __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+#pragma unroll
+      for (int st = 0; st + 1 < BK / 16; ++st) {
+#pragma unroll
+        for (int t = 0; t < kLead; ++t) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        if (kReads > kLead) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kLead, 0);
+        if (kMfma > kLead) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kLead, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
     }
     if (more) {
       T* nxt = smem + ((kt + 1) & 1) * S::kStageElems;
