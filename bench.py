@@ -246,6 +246,45 @@ def cpu_baseline(shape, sample):
             "seconds": round(dt, 2)}
 
 
+def pmc_pass():
+    """Minimal dispatch sequence for hardware-counter runs: two layer forwards
+    on the 1M-token shape (random device data; traffic does not depend on the
+    values) and one plain 1 GiB device-to-device copy whose FETCH_SIZE and
+    WRITE_SIZE calibrate the counters (it must read and write 1 GiB)."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    from paper_2608_23463_amd import synth
+    B.load()
+    shape = synth.WORKLOADS[LAYER_WORKLOAD]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+    dt = torch.bfloat16
+
+    def rn(*sz, std=1.0):
+        return (torch.randn(*sz, generator=gen, device="cuda") * std).to(dt)
+
+    wsh = shape.weight_shapes()
+    w = {"compress": [(rn(*z, std=0.02), None) for z in wsh["compress"]],
+         "decompress": [(rn(*z, std=0.02), None) for z in wsh["decompress"]]}
+    for k in ("q", "k", "v", "o", "gate"):
+        w[k] = (rn(*wsh[k], std=0.02), None)
+    x = rn(shape.batch, shape.seq_len, shape.d_fine)
+    cfg = B.config_from_shape(shape)
+    ws = torch.empty(B.layer_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    x_out = torch.empty_like(x)
+    h_out = torch.empty((1, shape.n_proxies, shape.d_proxy), dtype=dt, device="cuda")
+    wst = B.layer_weights(w)
+    for _ in range(2):
+        B.layer_forward_raw(cfg, wst, x, None, x_out, h_out, None, ws)
+        torch.cuda.synchronize()
+    a = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print("pmc pass done: 2 forwards, 1 GiB copy", flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -253,7 +292,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="only the short dispatch sequence used for counter runs (prints no JSON)")
     args = ap.parse_args()
+    if args.pmc_pass:
+        pmc_pass()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build runs the hot path on a single MI355X and has no "
