@@ -13,6 +13,8 @@ Extra objects on the same line:
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
                rows each, 256 new tokens per sequence including the 4
                block-triggered appends
+  train        forward (saving activations) + backward tokens/s on the
+               factorised workload (L = 262,144, d = 2048, 16 x 128, P = 8 x 8)
   cpu_baseline the CPU oracle timed on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -31,6 +33,7 @@ if ROOT not in sys.path:
 METRIC = "ProxyFormer layer fwd tokens/sec at L=1M, P=64; proxy-KV decode tokens/sec"
 LAYER_WORKLOAD = "layer_bf16_L1M_d1024"
 DECODE_WORKLOAD = "decode_bf16_B32_n16k"
+TRAIN_WORKLOAD = "layer_bf16_L256k_d2048_f8x8"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 CPU_SAMPLE_TOKENS = 65536
@@ -229,6 +232,54 @@ def bench_decode():
     return out
 
 
+def bench_train(steps):
+    import torch
+    from paper_2608_23463_amd import binding as B
+    from paper_2608_23463_amd import synth
+    shape = synth.WORKLOADS[TRAIN_WORKLOAD]
+    log(f"generating {TRAIN_WORKLOAD} inputs")
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[TRAIN_WORKLOAD], with_dy=True)
+    x = to_dev(inp.pop("x"), shape.dtype)
+    dy = to_dev(inp.pop("dy"), shape.dtype)
+    w = dev_weights(inp["weights"], shape.dtype)
+    cfg = B.config_from_shape(shape)
+    ws_f = torch.empty(B.layer_workspace_size(cfg, False), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty(B.layer_workspace_size(cfg, True), dtype=torch.uint8, device="cuda")
+    saved = torch.empty(B.layer_saved_size(cfg), dtype=torch.uint8, device="cuda")
+    x_out = torch.empty_like(x)
+    h_out = torch.empty((1, shape.n_proxies, shape.d_proxy), dtype=x.dtype, device="cuda")
+    wst = B.layer_weights(w)
+
+    def step():
+        B.layer_forward_raw(cfg, wst, x, None, x_out, h_out, saved, ws_f)
+        B.layer_backward(cfg, w, x, None, saved, dy, workspace=ws_b)
+
+    log("train warmup")
+    step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {steps} forward+backward steps")
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    B.trace_reset()
+    B.trace_enable(True)
+    step()
+    torch.cuda.synchronize()
+    tr = B.trace_collect()
+    B.trace_enable(False)
+    out = {"metric": "layer forward+backward tokens/s", "value": round(shape.seq_len / (ms * 1e-3), 1),
+           "unit": "tokens/s", "ms_per_step": round(ms, 3), "workload": TRAIN_WORKLOAD,
+           "seq_len": shape.seq_len, "d": shape.d_fine, "levels": list(shape.factors),
+           "kernels": {k: {"launches": c, "avg_ms": round(t / c, 4)} for k, (c, t) in tr.items()}}
+    del x, dy, w, ws_f, ws_b, saved, x_out, h_out
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(shape, sample):
     import oracle
     try:
@@ -292,6 +343,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only the short dispatch sequence used for counter runs (prints no JSON)")
     args = ap.parse_args()
@@ -332,6 +384,8 @@ def main():
     }
     if not args.no_decode:
         result["decode"] = bench_decode()
+    if not args.no_train:
+        result["train"] = bench_train(max(1, min(args.steps, 5)))
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(shape, sample)
     print(json.dumps(result), flush=True)
