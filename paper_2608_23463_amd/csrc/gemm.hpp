@@ -244,6 +244,72 @@ __device__ __forceinline__ void tile_coords(const GemmParams& p, int& tm, int& t
   tn = w / gm;
 }
 
+// Epilogue through LDS, one band of kTM rows (one wave row) at a time: the
+// waves of that band park their fp32 accumulators in LDS, then every thread
+// takes 8 consecutive columns of a row and hands them to the epilogue, so
+// its global reads and writes are 16-byte and coalesced along rows.
+template <class S, int BM, int BN, int WM, class Epi>
+__device__ __forceinline__ void gemm_store(f32x16 (&acc)[S::kFM][S::kFN], float* stage, const GemmParams& p, int m0,
+                                           int n0, int wm, int wn, int lane, int tid, const Epi& epi) {
+  constexpr int kSRow = BN + 8;  // +32 bytes: the two lane halves hit disjoint banks
+  constexpr int kChunks = S::kTM * BN / 8;
+#pragma unroll 1
+  for (int band = 0; band < WM; ++band) {
+    __syncthreads();
+    if (wm == band) {
+#pragma unroll
+      for (int i = 0; i < S::kFM; ++i)
+#pragma unroll
+        for (int j = 0; j < S::kFN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            stage[(i * 32 + acc_row(r, lane)) * kSRow + wn * S::kTN + j * 32 + (lane & 31)] = acc[i][j][r];
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int c = tid; c < kChunks; c += S::kThreads) {
+      const int rl = c / (BN / 8), cl = (c % (BN / 8)) * 8;
+      const int row = m0 + band * S::kTM + rl, col = n0 + cl;
+      if (row < p.M && col < p.N) {
+        float v[8];
+        const f32x4 a = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = a[e];
+          v[e + 4] = b[e];
+        }
+        if (col + 8 <= p.N) {
+          epi.vec8(row, col, v);
+        } else {
+          for (int e = 0; col + e < p.N; ++e) epi(row, col + e, v[e]);
+        }
+      }
+    }
+  }
+}
+
+// Pins the instruction order of one BK slice: the reads of step 0, then each
+// step's MFMAs with the next step's fragment reads riding on its first
+// MFMAs (masks: 0x100 DS read, 0x008 MFMA), so LDS latency hides behind
+// matrix work.
+template <int kReads, int kMfma, int kSteps>
+__device__ __forceinline__ void pin_kstep_schedule() {
+  constexpr int kLead = kReads < kMfma ? kReads : kMfma;
+  __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+#pragma unroll
+  for (int st = 0; st + 1 < kSteps; ++st) {
+#pragma unroll
+    for (int t = 0; t < kLead; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if (kReads > kLead) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kLead, 0);
+    if (kMfma > kLead) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kLead, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+}
+
 // Occupancy: the two LDS stages of the 256x256 tile admit one workgroup per
 // CU, so the kernel declares that and lets the compiler keep the prefetched
 // fragments in registers instead of scheduling for more waves.
@@ -318,28 +384,7 @@ __global__ void __launch_bounds__(WM* WN* kWave)
 #pragma unroll
         for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[cb][i], fb[cb][j], acc[i][j]);
     }
-    // Instruction order for the block above: the reads of step 0, then each
-    // step's MFMAs interleaved with the fragment reads of the next step, so
-    // LDS latency hides behind matrix work (masks: 0x100 DS read, 0x008 MFMA).
-    if constexpr (sizeof(T) == 2) {
-      constexpr int kReads = S::kFM + S::kFN;
-      constexpr int kMfma = S::kFM * S::kFN;
-      // next-step reads ride on the first MFMAs of a step (one each), so the
-      // last of them still has the second half of the step to land
-      constexpr int kLead = kReads < kMfma ? kReads : kMfma;
-      __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
-#pragma unroll
-      for (int st = 0; st + 1 < BK / 16; ++st) {
-#pragma unroll
-        for (int t = 0; t < kLead; ++t) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-        if (kReads > kLead) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kLead, 0);
-        if (kMfma > kLead) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kLead, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
-    }
+    if constexpr (sizeof(T) == 2) pin_kstep_schedule<S::kFM + S::kFN, S::kFM * S::kFN, BK / 16>();
     if (more) {
       T* nxt = smem + ((kt + 1) & 1) * S::kStageElems;
       LdA::stash(ra, nxt, S::kStride, tid);
@@ -348,48 +393,164 @@ __global__ void __launch_bounds__(WM* WN* kWave)
     __syncthreads();
   }
 
-  // Epilogue through LDS, one band of kTM rows (one wave row) at a time: the
-  // waves of that band park their fp32 accumulators in LDS, then every thread
-  // takes 8 consecutive columns of a row and hands them to the epilogue, so
-  // its global reads and writes are 16-byte and coalesced along rows.
-  float* stage = reinterpret_cast<float*>(smem);
-  constexpr int kSRow = BN + 8;  // +32 bytes: the two lane halves hit disjoint banks
-  static_assert((size_t)S::kTM * kSRow * sizeof(float) <= S::kLdsBytes, "epilogue band must fit in LDS");
-  constexpr int kChunks = S::kTM * BN / 8;
-#pragma unroll 1
-  for (int band = 0; band < WM; ++band) {
-    __syncthreads();
-    if (wm == band) {
+  static_assert((size_t)S::kTM * (BN + 8) * sizeof(float) <= S::kLdsBytes, "epilogue band must fit in LDS");
+  gemm_store<S, BM, BN, WM>(acc, reinterpret_cast<float*>(smem), p, m0, n0, wm, wn, lane, tid, epi);
+}
+
+// Direct-to-LDS variant for operands contiguous along K (both A and B) whose
+// K concatenation point, if any, falls on a BK boundary. Each wave issues
+// buffer_load_dwordx4 ... lds: a wave instruction fills eight 128-byte tile
+// rows (64 lanes x 16 bytes), with chunk c of row r stored at c ^ (r % 8)
+// so that the 16 lanes of a fragment read hit 64 distinct banks without
+// padding. The loads for tile k+1 go out right after the single barrier of
+// step k, into the other LDS stage, and land while step k multiplies; no
+// registers hold prefetched data and no LDS stores are issued.
+template <typename T, int BM, int BN, int BK, int WM, int WN>
+struct DirectShape {
+  typedef GemmShape<T, BM, BN, BK, WM, WN> S;
+  static constexpr int kVec = S::kVec;
+  static constexpr int kCpr = BK / kVec;               // 16-byte chunks per row
+  static constexpr int kRowsPerInst = kWave / kCpr;    // rows one wave instruction fills
+  static constexpr int kWaves = WM * WN;
+  static constexpr int kNia = BM / (kRowsPerInst * kWaves);
+  static constexpr int kNib = BN / (kRowsPerInst * kWaves);
+  static constexpr int kStage = (BM + BN) * BK;          // elements per stage
+  static constexpr size_t kMainBytes = 2 * (size_t)kStage * sizeof(T);
+  static constexpr size_t kEpiBytes = (size_t)S::kTM * (BN + 8) * sizeof(float);
+  static constexpr size_t kLdsBytes = kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes;
+  static_assert(kCpr == 8, "the XOR swizzle assumes 8 chunks per tile row");
+  static_assert(kNia >= 1 && kNib >= 1 && BM % (kRowsPerInst * kWaves) == 0 && BN % (kRowsPerInst * kWaves) == 0,
+                "tile rows must split evenly over wave instructions");
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, class Epi>
+__global__ void __launch_bounds__(WM* WN* kWave)
+    __attribute__((amdgpu_waves_per_eu(1, (BM >= 256 ? 1 : 2))))
+    gemm_direct_kernel(const GemmParams p, const Epi epi) {
+  typedef DirectShape<T, BM, BN, BK, WM, WN> D;
+  typedef typename D::S S;
+  typedef Mma<T> MM;
+  __shared__ __attribute__((aligned(1024))) char smem_raw[D::kLdsBytes];
+  T* smem = reinterpret_cast<T*>(smem_raw);
+
+  int tm, tn;
+  tile_coords(p, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = blockIdx.z * p.k_slice;
+  const int kend = min(p.K, kbeg + p.k_slice);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: LDS bases go to M0
+  const int wm = wave / WN, wn = wave % WN;
+
+  // per-lane byte offsets inside a tile (rows r, swizzled chunk)
+  const int lr = lane / D::kCpr, lc = lane % D::kCpr;
+  const int64_t lda_b = p.lda * (int64_t)sizeof(T), ldb_b = p.ldb * (int64_t)sizeof(T);
+  uint32_t voa[D::kNia], vob[D::kNib];
+  int kca[D::kNia], kcb[D::kNib];
+#pragma unroll
+  for (int i = 0; i < D::kNia; ++i) {
+    const int r = (wave * D::kNia + i) * D::kRowsPerInst + lr;
+    const int gc = lc ^ (r & 7);
+    kca[i] = gc * D::kVec;
+    voa[i] = (uint32_t)(r * lda_b + gc * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < D::kNib; ++i) {
+    const int r = (wave * D::kNib + i) * D::kRowsPerInst + lr;
+    const int gc = lc ^ (r & 7);
+    kcb[i] = gc * D::kVec;
+    vob[i] = (uint32_t)(r * ldb_b + gc * 16);
+  }
+  const uint32_t a_rows = (uint32_t)(max(0, min(BM, p.M - m0)) * lda_b);
+  const uint32_t b_rows = (uint32_t)(max(0, min(BN, p.N - n0)) * ldb_b);
+  const char* a1 = reinterpret_cast<const char*>(p.a) + m0 * lda_b;
+  const char* a2 = p.a2 ? reinterpret_cast<const char*>(p.a2) + m0 * lda_b : nullptr;
+  const char* b1 = reinterpret_cast<const char*>(p.b) + n0 * ldb_b;
+  const char* b2 = p.b2 ? reinterpret_cast<const char*>(p.b2) + n0 * ldb_b : nullptr;
+
+  auto issue = [&](int k0, int stage) {
+    const bool tail = k0 + BK > kend;
+    T* st = smem + stage * D::kStage;
+    {
+      const bool second = k0 >= p.a_ksplit;
+      const int krel = second ? k0 - p.a_ksplit : k0;
+      const rsrc_t rs =
+          make_rsrc_uniform((second ? a2 : a1) + (int64_t)krel * sizeof(T), a_rows - (uint32_t)(krel * sizeof(T)));
+#pragma unroll
+      for (int i = 0; i < D::kNia; ++i)
+        buf_ld16_lds(rs, (!tail || k0 + kca[i] < kend) ? voa[i] : kOOB,
+                     st + (wave * D::kNia + i) * D::kRowsPerInst * BK);
+    }
+    {
+      const bool second = k0 >= p.b_ksplit;
+      const int krel = second ? k0 - p.b_ksplit : k0;
+      const rsrc_t rs =
+          make_rsrc_uniform((second ? b2 : b1) + (int64_t)krel * sizeof(T), b_rows - (uint32_t)(krel * sizeof(T)));
+#pragma unroll
+      for (int i = 0; i < D::kNib; ++i)
+        buf_ld16_lds(rs, (!tail || k0 + kcb[i] < kend) ? vob[i] : kOOB,
+                     st + BM * BK + (wave * D::kNib + i) * D::kRowsPerInst * BK);
+    }
+  };
+
+  f32x16 acc[S::kFM][S::kFN];
+#pragma unroll
+  for (int i = 0; i < S::kFM; ++i)
+#pragma unroll
+    for (int j = 0; j < S::kFN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  if (nk > 0) issue(kbeg, 0);
+  const int frow = lane & 31;
+  const int swz = lane & 7;  // row % 8 of every row this lane reads
+  const int g = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_vmcnt0();
+    __syncthreads();  // tile kt is in LDS for every wave; stage (kt+1)&1 is free
+    if (kt + 1 < nk) issue(kbeg + (kt + 1) * BK, (kt + 1) & 1);
+    const T* cur = smem + (kt & 1) * D::kStage;
+    const T* sa = cur + (wm * S::kTM + frow) * BK;
+    const T* sb = cur + BM * BK + (wn * S::kTN + frow) * BK;
+    auto frag = [&](const T* rowp, int st) {
+      if constexpr (sizeof(T) == 2) {
+        return MM::load(rowp + (((2 * st + g) ^ swz) * 8));
+      } else {
+        const int c0 = 4 * st + 2 * g;
+        typename MM::frag f;
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(rowp + ((c0 ^ swz) * 4));
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(rowp + (((c0 + 1) ^ swz) * 4));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[e] = lo[e];
+          f[e + 4] = hi[e];
+        }
+        return f;
+      }
+    };
+    typename MM::frag fa[2][S::kFM], fb[2][S::kFN];
+#pragma unroll
+    for (int i = 0; i < S::kFM; ++i) fa[0][i] = frag(sa + i * 32 * BK, 0);
+#pragma unroll
+    for (int j = 0; j < S::kFN; ++j) fb[0][j] = frag(sb + j * 32 * BK, 0);
+#pragma unroll
+    for (int st = 0; st < BK / 16; ++st) {
+      const int cb = st & 1, nb = cb ^ 1;
+      if (st + 1 < BK / 16) {
+#pragma unroll
+        for (int i = 0; i < S::kFM; ++i) fa[nb][i] = frag(sa + i * 32 * BK, st + 1);
+#pragma unroll
+        for (int j = 0; j < S::kFN; ++j) fb[nb][j] = frag(sb + j * 32 * BK, st + 1);
+      }
 #pragma unroll
       for (int i = 0; i < S::kFM; ++i)
 #pragma unroll
-        for (int j = 0; j < S::kFN; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            stage[(i * 32 + acc_row(r, lane)) * kSRow + wn * S::kTN + j * 32 + (lane & 31)] = acc[i][j][r];
+        for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[cb][i], fb[cb][j], acc[i][j]);
     }
-    __syncthreads();
-#pragma unroll 2
-    for (int c = tid; c < kChunks; c += S::kThreads) {
-      const int rl = c / (BN / 8), cl = (c % (BN / 8)) * 8;
-      const int row = m0 + band * S::kTM + rl, col = n0 + cl;
-      if (row < p.M && col < p.N) {
-        float v[8];
-        const f32x4 a = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl + 4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[e] = a[e];
-          v[e + 4] = b[e];
-        }
-        if (col + 8 <= p.N) {
-          epi.vec8(row, col, v);
-        } else {
-          for (int e = 0; col + e < p.N; ++e) epi(row, col + e, v[e]);
-        }
-      }
-    }
+    if constexpr (sizeof(T) == 2) pin_kstep_schedule<S::kFM + S::kFN, S::kFM * S::kFN, BK / 16>();
   }
+  gemm_store<S, BM, BN, WM>(acc, reinterpret_cast<float*>(smem), p, m0, n0, wm, wn, lane, tid, epi);
 }
 
 // Fixed-order reduction of split-K partials ws[s][M][N], then the epilogue
@@ -518,6 +679,16 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   p.tiles_n = (pr.N + BN - 1) / BN;
   p.group_m = 8;
   dim3 grid(p.tiles_m * p.tiles_n, 1, pl.splits);
+  const bool aligned_split = (pr.a_ksplit >= pr.K || pr.a_ksplit % BK == 0) &&
+                             (pr.b_ksplit >= pr.K || pr.b_ksplit % BK == 0) &&
+                             (!pr.a2 || pr.lda2 == pr.lda) && (!pr.b2 || pr.ldb2 == pr.ldb);
+  if constexpr (LA == LAYOUT_K && LB == LAYOUT_K) {
+    if (aligned_split && pl.k_slice % BK == 0) {
+      hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, WN, Epi>), grid, dim3(WM * WN * kWave), 0, stream, p,
+                         epi);
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL((gemm_kernel<T, BM, BN, BK, WM, WN, LA, LB, Epi>), grid,
                      dim3(WM * WN * kWave), 0, stream, p, epi);
   return hipGetLastError();
