@@ -59,7 +59,29 @@ __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff) {
 __device__ __forceinline__ void buf_ld16_lds(rsrc_t r, uint32_t voff, void* lds_base) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, 0, 0, 0);
 }
-__device__ __forceinline__ void wait_vmcnt0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
+// expcnt in 6:4, lgkmcnt in 11:8); a field at its maximum does not wait.
+// Issued through the builtin so the compiler's own wait insertion knows
+// about them and does not add redundant waits on younger operations.
+constexpr int waitcnt_imm(int vm, int lgkm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (lgkm << 8); }
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(N, 15));
+}
+// Workgroup barrier for LDS hand-offs: this wave's LDS reads have returned
+// before any wave passes. Unlike __syncthreads() it does not also wait for
+// every outstanding global load (in-flight direct-to-LDS stages stay in
+// flight; the caller waits for the stage it needs with wait_vmcnt first).
+// The empty asm statements keep the compiler from moving memory accesses
+// across the barrier.
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0)); }
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  wait_lgkmcnt0();
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
 // Low part of a two-term bf16 split: v = hi + lo with hi = bf16(v) and
@@ -82,6 +104,23 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
     v[i] = a[i];
     v[i + 4] = b[i];
   }
+}
+// Eight elements held as loaded (not yet widened), so the load can stay in
+// flight until raw_to_f32 first needs the values.
+template <typename T>
+struct Raw8 {
+  u32x4 w[sizeof(T) / 2];
+};
+template <typename T>
+__device__ __forceinline__ void raw_load8(const T* p, Raw8<T>& r) {
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = ld16(reinterpret_cast<const char*>(p) + 16 * i);
+}
+template <typename T>
+__device__ __forceinline__ void raw_to_f32(const Raw8<T>& r, float* v) {
+  const T* e = reinterpret_cast<const T*>(r.w);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = to_f32(e[i]);
 }
 __device__ __forceinline__ void store8(bf16* p, const float* v) {
   bf16x8 x;

@@ -25,6 +25,34 @@ struct EpiLinear {
     if (out2) out2[(int64_t)r * ldo + c] = o;
     if (out_lo) out_lo[(int64_t)r * ldo + c] = from_f32<T>(split_lo(v));
   }
+  struct Col {
+    Raw8<T> b;
+  };
+  struct Pre {
+    Raw8<T> a;
+  };
+  __device__ __forceinline__ void col(int c, Col& k) const {
+    if (bias) raw_load8(bias + c, k.b);
+  }
+  __device__ __forceinline__ void pre(int r, int c, Pre& q) const {
+    if (add) raw_load8(add + (int64_t)r * ld_add + c, q.a);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0, const Col& k, const Pre& q) const {
+    float v[8], t[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e];
+    if (bias) {
+      raw_to_f32(k.b, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    if (add) {
+      raw_to_f32(q.a, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+    finish(r, c, v);
+  }
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
     float v[8], t[8];
 #pragma unroll
@@ -39,6 +67,10 @@ struct EpiLinear {
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] += t[e];
     }
+    finish(r, c, v);
+  }
+  __device__ __forceinline__ void finish(int r, int c, const float* v) const {
+    float t[8];
     store8(out + (int64_t)r * ldo + c, v);
     if (out2) store8(out2 + (int64_t)r * ldo + c, v);
     if (out_lo) {
@@ -68,17 +100,30 @@ struct EpiHeads {
     if (out_t) out_t[(bh * dh + e) * ld_t + i] = o;
     if (out_lo) out_lo[(bh * m + i) * dh + e] = from_f32<T>(split_lo(v));
   }
-  // 8 consecutive channels stay inside one head (dh is a multiple of 8)
+  struct Col {
+    Raw8<T> b;
+  };
+  struct Pre {};
+  __device__ __forceinline__ void col(int c, Col& k) const {
+    if (bias) raw_load8(bias + c, k.b);
+  }
+  __device__ __forceinline__ void pre(int, int, Pre&) const {}
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0, const Col& k, const Pre&) const {
+    float v[8], t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (bias) raw_to_f32(k.b, t);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e] + t[e];
+    finish(r, c, v);
+  }
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
-    float v[8];
+    float v[8], t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (bias) load8(bias + c, t);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = v0[e];
-    if (bias) {
-      float t[8];
-      load8(bias + c, t);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] += t[e];
-    }
+    for (int e = 0; e < 8; ++e) v[e] = v0[e] + t[e];
+    finish(r, c, v);
+  }
+  // 8 consecutive channels stay inside one head (dh is a multiple of 8)
+  __device__ __forceinline__ void finish(int r, int c, const float* v) const {
     const int b = r / m, i = r - b * m;
     const int hd = c / dh, e0 = c - hd * dh;
     const int64_t bh = (int64_t)b * n_heads + hd;
@@ -113,16 +158,29 @@ struct EpiShift {
     else
       out[(int64_t)(r - i) * ld + c] = from_f32<T>(0.0f);
   }
+  struct Col {
+    Raw8<T> b;
+  };
+  struct Pre {};
+  __device__ __forceinline__ void col(int c, Col& k) const {
+    if (bias) raw_load8(bias + c, k.b);
+  }
+  __device__ __forceinline__ void pre(int, int, Pre&) const {}
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0, const Col& k, const Pre&) const {
+    float v[8], t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (bias) raw_to_f32(k.b, t);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v0[e] + t[e];
+    finish(r, c, v);
+  }
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
-    float v[8];
+    float v[8], t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (bias) load8(bias + c, t);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = v0[e];
-    if (bias) {
-      float t[8];
-      load8(bias + c, t);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] += t[e];
-    }
+    for (int e = 0; e < 8; ++e) v[e] = v0[e] + t[e];
+    finish(r, c, v);
+  }
+  __device__ __forceinline__ void finish(int r, int c, const float* v) const {
     const int i = r % m;
     if (i < m - 1) {
       store8(out + (int64_t)(r + 1) * ld + c, v);
@@ -150,21 +208,45 @@ struct EpiGate {
     y[i] = from_f32<T>(xv + sigmoidf(v) * dv);
     if (gsave) gsave[i] = from_f32<T>(v);
   }
+  // Two-phase form: col() reads the bias, pre() the 8 values of X and Delta.
+  struct Col {
+    Raw8<T> b;
+  };
+  struct Pre {
+    Raw8<T> x8, d8;
+  };
+  __device__ __forceinline__ void col(int c, Col& k) const {
+    if (bias) raw_load8(bias + c, k.b);
+  }
+  __device__ __forceinline__ void pre(int r, int c, Pre& q) const {
+    const int64_t i = (int64_t)r * ld + c;
+    raw_load8(x + i, q.x8);
+    raw_load8(delta + i, q.d8);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v0, const Col& k, const Pre& q) const {
+    float xv[8], dv[8], bv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    raw_to_f32(q.x8, xv);
+    raw_to_f32(q.d8, dv);
+    if (bias) raw_to_f32(k.b, bv);
+    finish(r, c, v0, xv, dv, bv);
+  }
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
-    float g[8], xv[8], dv[8], yv[8];
+    float xv[8], dv[8], bv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     const int64_t i = (int64_t)r * ld + c;
     load8(x + i, xv);
     load8(delta + i, dv);
+    if (bias) load8(bias + c, bv);
+    finish(r, c, v0, xv, dv, bv);
+  }
+  __device__ __forceinline__ void finish(int r, int c, const float* v0, const float* xv, const float* dv,
+                                         const float* bv) const {
+    float g[8], yv[8];
+    const int64_t i = (int64_t)r * ld + c;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) g[e] = v0[e];
-    if (bias) {
-      float t[8];
-      load8(bias + c, t);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) g[e] += t[e];
+    for (int e = 0; e < 8; ++e) {
+      g[e] = v0[e] + bv[e];
+      yv[e] = xv[e] + sigmoidf(g[e]) * dv[e];
     }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) yv[e] = xv[e] + sigmoidf(g[e]) * dv[e];
     store8(y + i, yv);
     if (gsave) store8(gsave + i, g);
   }

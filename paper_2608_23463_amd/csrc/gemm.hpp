@@ -244,6 +244,50 @@ __device__ __forceinline__ void tile_coords(const GemmParams& p, int& tm, int& t
   tn = w / gm;
 }
 
+// Optional two-phase epilogue protocol. An epilogue that defines the types
+// Col and Pre with methods col(c, Col&), pre(r, c, Pre&) and
+// vec8(r, c, v, const Col&, const Pre&) has its column data (a bias) read
+// once per thread and its row data (tensors it combines with) read for a
+// whole group of chunks before any result is formed or stored. Global loads
+// and stores share one in-order counter, so reads issued before the stores
+// are never held up behind them.
+struct NoData {};
+template <class Epi, class = void>
+struct EpiCol {
+  typedef NoData type;
+};
+template <class Epi>
+struct EpiCol<Epi, std::void_t<typename Epi::Col>> {
+  typedef typename Epi::Col type;
+};
+template <class Epi, class = void>
+struct EpiPre {
+  typedef NoData type;
+};
+template <class Epi>
+struct EpiPre<Epi, std::void_t<typename Epi::Pre>> {
+  typedef typename Epi::Pre type;
+};
+template <class Epi>
+constexpr bool kEpiTwoPhase = !std::is_same<typename EpiCol<Epi>::type, NoData>::value;
+template <class Epi>
+__device__ __forceinline__ void epi_col(const Epi& e, int c, typename EpiCol<Epi>::type& col) {
+  if constexpr (kEpiTwoPhase<Epi>) e.col(c, col);
+}
+template <class Epi>
+__device__ __forceinline__ void epi_pre(const Epi& e, int r, int c, typename EpiPre<Epi>::type& pre) {
+  if constexpr (kEpiTwoPhase<Epi>) e.pre(r, c, pre);
+}
+template <class Epi>
+__device__ __forceinline__ void epi_vec8(const Epi& e, int r, int c, const float* v,
+                                         const typename EpiCol<Epi>::type& col,
+                                         const typename EpiPre<Epi>::type& pre) {
+  if constexpr (kEpiTwoPhase<Epi>)
+    e.vec8(r, c, v, col, pre);
+  else
+    e.vec8(r, c, v);
+}
+
 // Epilogue through LDS, one band of kTM rows (one wave row) at a time: the
 // waves of that band park their fp32 accumulators in LDS, then every thread
 // takes 8 consecutive columns of a row and hands them to the epilogue, so
@@ -253,9 +297,13 @@ __device__ __forceinline__ void gemm_store(f32x16 (&acc)[S::kFM][S::kFN], float*
                                            int n0, int wm, int wn, int lane, int tid, const Epi& epi) {
   constexpr int kSRow = BN + 8;  // +32 bytes: the two lane halves hit disjoint banks
   constexpr int kChunks = S::kTM * BN / 8;
+  // A thread's 8 columns are the same in every chunk it takes.
+  static_assert(S::kThreads % (BN / 8) == 0, "chunk columns must be fixed per thread");
+  typename EpiCol<Epi>::type colv;
+  if (p.N >= 8) epi_col(epi, min(n0 + (tid % (BN / 8)) * 8, p.N - 8), colv);
 #pragma unroll 1
   for (int band = 0; band < WM; ++band) {
-    __syncthreads();
+    lds_barrier();  // LDS only: earlier stores may stay in flight
     if (wm == band) {
 #pragma unroll
       for (int i = 0; i < S::kFM; ++i)
@@ -265,12 +313,37 @@ __device__ __forceinline__ void gemm_store(f32x16 (&acc)[S::kFM][S::kFN], float*
           for (int r = 0; r < 16; ++r)
             stage[(i * 32 + acc_row(r, lane)) * kSRow + wn * S::kTN + j * 32 + (lane & 31)] = acc[i][j][r];
     }
-    __syncthreads();
-#pragma unroll 2
-    for (int c = tid; c < kChunks; c += S::kThreads) {
-      const int rl = c / (BN / 8), cl = (c % (BN / 8)) * 8;
-      const int row = m0 + band * S::kTM + rl, col = n0 + cl;
-      if (row < p.M && col < p.N) {
+    lds_barrier();
+    // Two phases per group of chunks: every global read the epilogue needs
+    // (Epi::pre) is issued first, then the values are combined and stored,
+    // so a thread keeps kGroup loads in flight instead of one.
+    // The reads are unconditional (coordinates clamped into the matrix; a
+    // clamped chunk's values are not used), so no branch separates a load
+    // from its use and the compiler keeps them all in flight. An epilogue
+    // with reads therefore needs N >= 8.
+    static_assert(kChunks % S::kThreads == 0, "chunks must split evenly over threads");
+    constexpr int kPerThread = kChunks / S::kThreads;
+    constexpr int kGroupMax = S::kThreads > 256 ? 2 : 4;  // 8-wave tiles have half the registers
+    constexpr int kGroup = kPerThread < kGroupMax ? kPerThread : kGroupMax;
+    static_assert(kPerThread % kGroup == 0, "chunk groups must tile the band");
+#pragma unroll 1
+    for (int c0 = 0; c0 < kPerThread; c0 += kGroup) {
+      typename EpiPre<Epi>::type pre[kGroup];
+      bool full[kGroup];
+#pragma unroll
+      for (int u = 0; u < kGroup; ++u) {
+        const int c = tid + (c0 + u) * S::kThreads;
+        const int rl = c / (BN / 8), cl = (c % (BN / 8)) * 8;
+        const int row = m0 + band * S::kTM + rl, col = n0 + cl;
+        full[u] = row < p.M && col + 8 <= p.N;
+        epi_pre(epi, min(row, p.M - 1), min(col, p.N - 8), pre[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < kGroup; ++u) {
+        const int c = tid + (c0 + u) * S::kThreads;
+        const int rl = c / (BN / 8), cl = (c % (BN / 8)) * 8;
+        const int row = m0 + band * S::kTM + rl, col = n0 + cl;
+        if (row >= p.M || col >= p.N) continue;
         float v[8];
         const f32x4 a = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl);
         const f32x4 b = *reinterpret_cast<const f32x4*>(stage + rl * kSRow + cl + 4);
@@ -279,8 +352,8 @@ __device__ __forceinline__ void gemm_store(f32x16 (&acc)[S::kFM][S::kFN], float*
           v[e] = a[e];
           v[e + 4] = b[e];
         }
-        if (col + 8 <= p.N) {
-          epi.vec8(row, col, v);
+        if (full[u]) {
+          epi_vec8(epi, row, col, v, colv, pre[u]);
         } else {
           for (int e = 0; col + e < p.N; ++e) epi(row, col + e, v[e]);
         }
@@ -289,16 +362,15 @@ __device__ __forceinline__ void gemm_store(f32x16 (&acc)[S::kFM][S::kFN], float*
   }
 }
 
-// Pins the instruction order of one BK slice: the reads of step 0, then each
-// step's MFMAs with the next step's fragment reads riding on its first
-// MFMAs (masks: 0x100 DS read, 0x008 MFMA), so LDS latency hides behind
-// matrix work.
+// Pins the instruction order of kSteps MFMA k-steps, each made of kMfma
+// MFMAs with the kReads fragment reads of the following k-step riding on
+// its first MFMAs (masks: 0x100 DS read, 0x008 MFMA), so LDS latency hides
+// behind matrix work.
 template <int kReads, int kMfma, int kSteps>
-__device__ __forceinline__ void pin_kstep_schedule() {
+__device__ __forceinline__ void pin_substeps() {
   constexpr int kLead = kReads < kMfma ? kReads : kMfma;
-  __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
 #pragma unroll
-  for (int st = 0; st + 1 < kSteps; ++st) {
+  for (int st = 0; st < kSteps; ++st) {
 #pragma unroll
     for (int t = 0; t < kLead; ++t) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -307,6 +379,14 @@ __device__ __forceinline__ void pin_kstep_schedule() {
     if (kReads > kLead) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kLead, 0);
     if (kMfma > kLead) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kLead, 0);
   }
+}
+
+// Pins the instruction order of one BK slice: the reads of step 0, then
+// pin_substeps over the remaining steps and the last step's MFMAs.
+template <int kReads, int kMfma, int kSteps>
+__device__ __forceinline__ void pin_kstep_schedule() {
+  __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+  pin_substeps<kReads, kMfma, kSteps - 1>();
   __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
 }
 
@@ -405,7 +485,7 @@ __global__ void __launch_bounds__(WM* WN* kWave)
 // padding. The loads for tile k+1 go out right after the single barrier of
 // step k, into the other LDS stage, and land while step k multiplies; no
 // registers hold prefetched data and no LDS stores are issued.
-template <typename T, int BM, int BN, int BK, int WM, int WN>
+template <typename T, int BM, int BN, int BK, int WM, int WN, int NS>
 struct DirectShape {
   typedef GemmShape<T, BM, BN, BK, WM, WN> S;
   static constexpr int kVec = S::kVec;
@@ -414,20 +494,39 @@ struct DirectShape {
   static constexpr int kWaves = WM * WN;
   static constexpr int kNia = BM / (kRowsPerInst * kWaves);
   static constexpr int kNib = BN / (kRowsPerInst * kWaves);
+  static constexpr int kLoads = kNia + kNib;           // loads per thread per stage
   static constexpr int kStage = (BM + BN) * BK;          // elements per stage
-  static constexpr size_t kMainBytes = 2 * (size_t)kStage * sizeof(T);
+  static constexpr size_t kMainBytes = (size_t)NS * kStage * sizeof(T);
   static constexpr size_t kEpiBytes = (size_t)S::kTM * (BN + 8) * sizeof(float);
   static constexpr size_t kLdsBytes = kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes;
-  static_assert(kCpr == 8, "the XOR swizzle assumes 8 chunks per tile row");
+  static_assert(kCpr == 8 || kCpr == 4, "the XOR swizzle handles 64- and 128-byte tile rows");
   static_assert(kNia >= 1 && kNib >= 1 && BM % (kRowsPerInst * kWaves) == 0 && BN % (kRowsPerInst * kWaves) == 0,
                 "tile rows must split evenly over wave instructions");
+  static_assert(NS >= 2 && kLoads * (NS - 1) < 64, "outstanding loads must fit the vmcnt counter");
+  static_assert(kLdsBytes <= 160 * 1024, "LDS budget of one workgroup");
+  // Physical chunk of logical chunk c in row r is c ^ key(r): any 8
+  // consecutive rows read at one logical chunk cover all 32 LDS banks.
+  static __device__ __forceinline__ int key(int r) { return kCpr == 8 ? (r & 7) : ((r >> 1) & 3); }
 };
 
-template <typename T, int BM, int BN, int BK, int WM, int WN, class Epi>
+// Waits until at most `pending` stages of loads (kLoads each) are in flight.
+template <int L, int NP>
+__device__ __forceinline__ void wait_stages(int pending) {
+  if constexpr (NP == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (pending >= NP)
+      wait_vmcnt<NP * L>();
+    else
+      wait_stages<L, NP - 1>(pending);
+  }
+}
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, int NS, class Epi>
 __global__ void __launch_bounds__(WM* WN* kWave)
-    __attribute__((amdgpu_waves_per_eu(1, (BM >= 256 ? 1 : 2))))
+    __attribute__((amdgpu_waves_per_eu(WM* WN / 4, (BM >= 256 ? 1 : 2) * WM * WN / 4)))
     gemm_direct_kernel(const GemmParams p, const Epi epi) {
-  typedef DirectShape<T, BM, BN, BK, WM, WN> D;
+  typedef DirectShape<T, BM, BN, BK, WM, WN, NS> D;
   typedef typename D::S S;
   typedef Mma<T> MM;
   __shared__ __attribute__((aligned(1024))) char smem_raw[D::kLdsBytes];
@@ -450,14 +549,14 @@ __global__ void __launch_bounds__(WM* WN* kWave)
 #pragma unroll
   for (int i = 0; i < D::kNia; ++i) {
     const int r = (wave * D::kNia + i) * D::kRowsPerInst + lr;
-    const int gc = lc ^ (r & 7);
+    const int gc = lc ^ D::key(r);
     kca[i] = gc * D::kVec;
     voa[i] = (uint32_t)(r * lda_b + gc * 16);
   }
 #pragma unroll
   for (int i = 0; i < D::kNib; ++i) {
     const int r = (wave * D::kNib + i) * D::kRowsPerInst + lr;
-    const int gc = lc ^ (r & 7);
+    const int gc = lc ^ D::key(r);
     kcb[i] = gc * D::kVec;
     vob[i] = (uint32_t)(r * ldb_b + gc * 16);
   }
@@ -468,30 +567,36 @@ __global__ void __launch_bounds__(WM* WN* kWave)
   const char* b1 = reinterpret_cast<const char*>(p.b) + n0 * ldb_b;
   const char* b2 = p.b2 ? reinterpret_cast<const char*>(p.b2) + n0 * ldb_b : nullptr;
 
-  auto issue = [&](int k0, int stage) {
+  // Loads [i0, i1) of one stage (A's kNia loads, then B's kNib), so a stage
+  // can be issued at once or spread over the k-steps of a tile.
+  auto issue_range = [&](int k0, int stage, int i0, int i1) {
     const bool tail = k0 + BK > kend;
     T* st = smem + stage * D::kStage;
-    {
+    if (i0 < D::kNia) {
       const bool second = k0 >= p.a_ksplit;
       const int krel = second ? k0 - p.a_ksplit : k0;
       const rsrc_t rs =
           make_rsrc_uniform((second ? a2 : a1) + (int64_t)krel * sizeof(T), a_rows - (uint32_t)(krel * sizeof(T)));
 #pragma unroll
       for (int i = 0; i < D::kNia; ++i)
-        buf_ld16_lds(rs, (!tail || k0 + kca[i] < kend) ? voa[i] : kOOB,
-                     st + (wave * D::kNia + i) * D::kRowsPerInst * BK);
+        if (i >= i0 && i < i1)
+          buf_ld16_lds(rs, (!tail || k0 + kca[i] < kend) ? voa[i] : kOOB,
+                       st + (wave * D::kNia + i) * D::kRowsPerInst * BK);
     }
-    {
+    if (i1 > D::kNia) {
       const bool second = k0 >= p.b_ksplit;
       const int krel = second ? k0 - p.b_ksplit : k0;
       const rsrc_t rs =
           make_rsrc_uniform((second ? b2 : b1) + (int64_t)krel * sizeof(T), b_rows - (uint32_t)(krel * sizeof(T)));
 #pragma unroll
       for (int i = 0; i < D::kNib; ++i)
-        buf_ld16_lds(rs, (!tail || k0 + kcb[i] < kend) ? vob[i] : kOOB,
-                     st + BM * BK + (wave * D::kNib + i) * D::kRowsPerInst * BK);
+        if (i + D::kNia >= i0 && i + D::kNia < i1)
+          buf_ld16_lds(rs, (!tail || k0 + kcb[i] < kend) ? vob[i] : kOOB,
+                       st + BM * BK + (wave * D::kNib + i) * D::kRowsPerInst * BK);
     }
   };
+  auto issue = [&](int k0, int stage) { issue_range(k0, stage, 0, D::kLoads); };
+
 
   f32x16 acc[S::kFM][S::kFN];
 #pragma unroll
@@ -502,54 +607,81 @@ __global__ void __launch_bounds__(WM* WN* kWave)
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = (kend - kbeg + BK - 1) / BK;
-  if (nk > 0) issue(kbeg, 0);
+  constexpr int kSub = BK / 16;  // MFMA k-steps per tile
+  static_assert(kSub % 2 == 0, "fragment double buffer alternates over an even number of k-steps");
   const int frow = lane & 31;
-  const int swz = lane & 7;  // row % 8 of every row this lane reads
+  const int swz = D::key(frow);  // rows this lane reads differ by multiples of 32
   const int g = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    wait_vmcnt0();
-    __syncthreads();  // tile kt is in LDS for every wave; stage (kt+1)&1 is free
-    if (kt + 1 < nk) issue(kbeg + (kt + 1) * BK, (kt + 1) & 1);
-    const T* cur = smem + (kt & 1) * D::kStage;
+  auto frag = [&](const T* rowp, int st) {
+    if constexpr (sizeof(T) == 2) {
+      return MM::load(rowp + (((2 * st + g) ^ swz) * 8));
+    } else {
+      const int c0 = 4 * st + 2 * g;
+      typename MM::frag f;
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(rowp + ((c0 ^ swz) * 4));
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(rowp + (((c0 + 1) ^ swz) * 4));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        f[e] = lo[e];
+        f[e + 4] = hi[e];
+      }
+      return f;
+    }
+  };
+  typename MM::frag fa[2][S::kFM], fb[2][S::kFN];
+  auto read_frags = [&](int tile, int st, int buf) {
+    const T* cur = smem + (tile % NS) * D::kStage;
     const T* sa = cur + (wm * S::kTM + frow) * BK;
     const T* sb = cur + BM * BK + (wn * S::kTN + frow) * BK;
-    auto frag = [&](const T* rowp, int st) {
-      if constexpr (sizeof(T) == 2) {
-        return MM::load(rowp + (((2 * st + g) ^ swz) * 8));
-      } else {
-        const int c0 = 4 * st + 2 * g;
-        typename MM::frag f;
-        const f32x4 lo = *reinterpret_cast<const f32x4*>(rowp + ((c0 ^ swz) * 4));
-        const f32x4 hi = *reinterpret_cast<const f32x4*>(rowp + (((c0 + 1) ^ swz) * 4));
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          f[e] = lo[e];
-          f[e + 4] = hi[e];
-        }
-        return f;
-      }
-    };
-    typename MM::frag fa[2][S::kFM], fb[2][S::kFN];
+    for (int i = 0; i < S::kFM; ++i) fa[buf][i] = frag(sa + i * 32 * BK, st);
 #pragma unroll
-    for (int i = 0; i < S::kFM; ++i) fa[0][i] = frag(sa + i * 32 * BK, 0);
+    for (int j = 0; j < S::kFN; ++j) fb[buf][j] = frag(sb + j * 32 * BK, st);
+  };
+  auto mfmas = [&](int buf) {
 #pragma unroll
-    for (int j = 0; j < S::kFN; ++j) fb[0][j] = frag(sb + j * 32 * BK, 0);
+    for (int i = 0; i < S::kFM; ++i)
 #pragma unroll
-    for (int st = 0; st < BK / 16; ++st) {
-      const int cb = st & 1, nb = cb ^ 1;
-      if (st + 1 < BK / 16) {
+      for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[buf][i], fb[buf][j], acc[i][j]);
+  };
+
+  // Ring of NS stages, tile t in stage t % NS. The hand-off to tile kt+1
+  // happens before the last k-step of tile kt, whose fragments are already
+  // in registers: after the barrier the first fragments of tile kt+1 are
+  // requested and the refill of stage kt % NS (tile kt+NS) is issued, and
+  // the last MFMAs of tile kt then run while both are in flight, so the
+  // matrix pipe does not drain at tile boundaries.
+  if (nk > 0) {
 #pragma unroll
-        for (int i = 0; i < S::kFM; ++i) fa[nb][i] = frag(sa + i * 32 * BK, st + 1);
-#pragma unroll
-        for (int j = 0; j < S::kFN; ++j) fb[nb][j] = frag(sb + j * 32 * BK, st + 1);
-      }
-#pragma unroll
-      for (int i = 0; i < S::kFM; ++i)
-#pragma unroll
-        for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[cb][i], fb[cb][j], acc[i][j]);
-    }
-    if constexpr (sizeof(T) == 2) pin_kstep_schedule<S::kFM + S::kFN, S::kFM * S::kFN, BK / 16>();
+    for (int s0 = 0; s0 < NS; ++s0)
+      if (s0 < nk) issue(kbeg + s0 * BK, s0);
+    wait_stages<D::kLoads, NS - 1>(min(NS - 1, nk - 1));
+    lds_barrier();
+    read_frags(0, 0, 0);
   }
+  for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+    for (int st = 0; st + 1 < kSub; ++st) {
+      read_frags(kt, st + 1, (st + 1) & 1);
+      mfmas(st & 1);
+    }
+    if constexpr (sizeof(T) == 2) pin_substeps<S::kFM + S::kFN, S::kFM * S::kFN, kSub - 1>();
+    // The last k-step's fragments are in registers on every path, so the
+    // compiler sees no reason to make its MFMAs wait for the younger reads
+    // of tile kt+1. The scheduling fence keeps the wait behind the MFMAs
+    // above.
+    __builtin_amdgcn_sched_barrier(0);
+    wait_lgkmcnt0();
+    if (kt + 1 < nk) {
+      wait_stages<D::kLoads, NS - 2>(min(NS - 2, nk - 2 - kt));
+      lds_barrier();  // tile kt+1 is in LDS; every wave is done reading tile kt
+      read_frags(kt + 1, 0, 0);
+      if (kt + NS < nk) issue(kbeg + (kt + NS) * BK, kt % NS);
+    }
+    mfmas(1);
+  }
+  // No direct load may still be writing LDS when the epilogue stages there.
+  wait_vmcnt<0>();
   gemm_store<S, BM, BN, WM>(acc, reinterpret_cast<float*>(smem), p, m0, n0, wm, wn, lane, tid, epi);
 }
 
@@ -684,8 +816,11 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
                              (!pr.a2 || pr.lda2 == pr.lda) && (!pr.b2 || pr.ldb2 == pr.ldb);
   if constexpr (LA == LAYOUT_K && LB == LAYOUT_K) {
     if (aligned_split && pl.k_slice % BK == 0) {
-      hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, WN, Epi>), grid, dim3(WM * WN * kWave), 0, stream, p,
-                         epi);
+      // 256x256 tiles run as 8 waves of 128x64: two waves per SIMD, so one
+      // wave's MFMAs cover the other's load issue and barrier waits.
+      constexpr int DWN = (BM == 256 && BN == 256) ? 4 : WN;
+      hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, DWN, 2, Epi>), grid, dim3(WM * DWN * kWave), 0,
+                         stream, p, epi);
       return hipGetLastError();
     }
   }
