@@ -5,6 +5,41 @@
 
 namespace pf {
 
+// Value of lane l ^ 32 (the other half of the wave), through the VALU.
+__device__ __forceinline__ float other_half(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_bit_cast(float, (__lane_id() < 32) ? r[1] : r[0]);
+}
+
+// P^T operand of one 16-key MFMA step taken from a 32x32 S^T accumulator
+// (keys on rows, queries on lanes). The accumulator gives a lane runs of 4
+// keys: registers 8*s2 .. 8*s2+7 hold keys 16*s2 + {0..3, 8..11} in the lower
+// lane half and 16*s2 + {4..7, 12..15} in the upper half. One
+// v_permlane32_swap per register pair exchanges keys 8..11 (lower half) with
+// keys 4..7 (upper half), so lane group g holds keys 16*s2 + 8*g .. +7 in order,
+// the operand layout whose matching V^T fragment is one contiguous 16-byte
+// read (bf16 operands).
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  // one v_cvt_pk_bf16_f32 (round to nearest even)
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+__device__ __forceinline__ bf16x8 pt_frag_bf16(const f32x16& s, int s2) {
+  const int r0 = s2 * 8;
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(s[r0 + 2 * i], s[r0 + 2 * i + 1]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const auto x = __builtin_amdgcn_permlane32_swap(w[i], w[i + 2], false, false);
+    w[i] = x[0];
+    w[i + 2] = x[1];
+  }
+  return __builtin_bit_cast(bf16x8, w);
+}
+
 // Per-head tensors of one layer call. Heads are laid out [B, h, rows, d_head]
 // ("row" tensors) or [B, h, d_head, ld_t] ("transposed" tensors, the proxy
 // index contiguous with row stride ld_t >= m, a multiple of 64 whose padding

@@ -1,69 +1,70 @@
 // Flash-style causal multi-head attention over proxies (Eq. 9), forward.
 //
 // One workgroup = 4 waves = 128 queries of one (sequence, head); each wave owns
-// 32 queries. Keys/values stream through LDS 64 at a time (double buffered).
-// A wave computes the transposed score tile S^T = K Q^T with MFMA so that each
-// lane holds one query column: the online-softmax statistics of a query live
-// in one lane pair (lane, lane ^ 32), and only the running maximum needs one
-// cross-half exchange per tile. The probabilities P^T stay in registers and
-// feed O^T += V^T P^T directly as the B operand; V arrives key-contiguous
-// (the producing GEMM writes V transposed), so the A fragments are plain LDS
-// reads. Exponentials use exp2 with log2(e)/sqrt(d_head) folded into the
-// score scale. With SPLIT, Q and K arrive as bf16 hi/lo pairs and the scores
-// are Kh Qh + Kl Qh + Kh Ql (three MFMAs into one accumulator), so a sharp
-// softmax is not moved by one bf16 rounding of its logits. Masked scores are
-// -inf and contribute exactly zero, so a query
-// never depends on later proxies (bit-exact causality).
+// 32 queries. Key and value tiles of 64 keys arrive in LDS through direct
+// (buffer -> LDS) loads into a ring of NS stages with XOR-swizzled 16-byte
+// chunks, so fragment reads are conflict-free 16-byte reads. A wave computes
+// the transposed score tile S^T = K Q^T with MFMA, so each lane holds one
+// query column: the online-softmax statistics of a query live in one lane
+// pair (lane, lane ^ 32) and the running maximum needs one cross-half
+// exchange per tile. The running maximum is only moved (and O rescaled) when
+// some score exceeds it by more than 2^8 in exp2 units; until then the stale
+// maximum is used, which leaves the result unchanged and keeps every
+// exponential below 2^8. P^T stays in registers: one v_permlane32_swap per
+// pair of packed values turns the accumulator layout (runs of 4 keys) into
+// MFMA operands of 8 consecutive keys, so V^T (key-contiguous, written
+// transposed by the producing GEMM) is read as 16-byte chunks. Exponentials
+// use exp2 with log2(e)/sqrt(d_head) folded into one FMA per score. With SPLIT,
+// Q and K arrive as bf16 hi/lo pairs and the scores are Kh Qh + Kl Qh + Kh Ql
+// (three MFMAs into one accumulator), so a sharp softmax is not moved by one
+// bf16 rounding of its logits. Masked scores are -inf and contribute exactly
+// zero, so a query never depends on later proxies (bit-exact causality).
 #include "attention.hpp"
 
 namespace pf {
 
-template <typename T, int DH, bool SPLIT>
+template <typename T, int DH, bool SPLIT, int NS>
 struct AttnFwdShape {
-  static constexpr int kVec = 16 / sizeof(T);
-  static constexpr int kKT = 64;                    // keys per tile
-  static constexpr int kKStride = DH + kVec;        // K tile row stride
-  static constexpr int kVStride = kKT + kVec;       // V^T tile row stride
-  static constexpr int kKElems = kKT * kKStride;
-  static constexpr int kKParts = SPLIT ? 2 : 1;     // K hi (and lo) tiles
-  static constexpr int kVOff = kKParts * kKElems;
-  static constexpr int kStage = kVOff + DH * kVStride;
-  static constexpr int kKLoads = kKT * DH / (256 * kVec);
-  static constexpr int kVLoads = DH * kKT / (256 * kVec);
+  static constexpr int kKT = 64;                         // keys per tile
+  static constexpr int kRowBytes = DH * (int)sizeof(T);  // K tile row: one key
+  static constexpr int kVRowBytes = kKT * (int)sizeof(T);  // V^T tile row: one channel
+  static constexpr int kKTile = kKT * kRowBytes;
+  static constexpr int kVTile = DH * kVRowBytes;
+  static constexpr int kKParts = SPLIT ? 2 : 1;
+  static constexpr int kStage = kKParts * kKTile + kVTile;  // bytes
+  static constexpr int kInsts = kStage / 1024;             // 1 KB direct loads per stage
+  static constexpr int kInstsPerWave = kInsts / 4;
+  static constexpr int kNS = NS;  // ring depth
+  static_assert(kRowBytes >= 128 && kVRowBytes >= 128, "rows of at least 8 chunks");
+  static_assert(kKTile % 1024 == 0 && kVTile % 1024 == 0 && kInsts % 4 == 0, "stage splits into wave loads");
 };
 
-template <typename T>
-struct Quad;  // four consecutive elements
-template <>
-struct Quad<bf16> {
-  typedef uint2 type;
-};
-template <>
-struct Quad<float> {
-  typedef u32x4 type;
-};
+// Physical 16-byte chunk of logical chunk c in row r.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ (r & 7); }
 
-template <typename T, int DH, bool SPLIT>
-__global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
-  typedef AttnFwdShape<T, DH, SPLIT> S;
+template <typename T, int DH, bool SPLIT, int NS, int OCC>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
+    attn_fwd_kernel(const AttnParams p) {
+  typedef AttnFwdShape<T, DH, SPLIT, NS> S;
   typedef Mma<T> MM;
-  __shared__ __attribute__((aligned(16))) T smem[2 * S::kStage];
+  __shared__ __attribute__((aligned(1024))) char smem[S::kNS * S::kStage];
 
   const int nqt = (p.m + 127) / 128;
   const int qt = nqt - 1 - (int)blockIdx.x;  // longest causal rows first
   const int bh = blockIdx.y;
   const int b = bh / p.n_heads, h = bh % p.n_heads;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, col = lane & 31;
   const int q0 = qt * 128;
   const int qw0 = q0 + wave * 32;
   const int myq = qw0 + col;
 
+  const char* kp = reinterpret_cast<const char*>(p.k) + (int64_t)bh * p.m * S::kRowBytes;
+  const char* klp = SPLIT ? reinterpret_cast<const char*>(p.k_lo) + (int64_t)bh * p.m * S::kRowBytes : nullptr;
+  const char* vtp = reinterpret_cast<const char*>(p.vt) + (int64_t)bh * DH * p.ld_t * (int64_t)sizeof(T);
   const T* qp = reinterpret_cast<const T*>(p.q) + (int64_t)bh * p.m * DH;
-  const T* kp = reinterpret_cast<const T*>(p.k) + (int64_t)bh * p.m * DH;
   const T* qlp = SPLIT ? reinterpret_cast<const T*>(p.q_lo) + (int64_t)bh * p.m * DH : nullptr;
-  const T* klp = SPLIT ? reinterpret_cast<const T*>(p.k_lo) + (int64_t)bh * p.m * DH : nullptr;
-  const T* vtp = reinterpret_cast<const T*>(p.vt) + (int64_t)bh * DH * p.ld_t;
 
   typename MM::frag qf[DH / 16], qfl[SPLIT ? DH / 16 : 1];
 #pragma unroll
@@ -83,42 +84,32 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
   const int kv_end = p.causal ? min(p.m, q0 + 128) : p.m;
   const int ntiles = (kv_end + S::kKT - 1) / S::kKT;
 
-  u32x4 rk[S::kKParts][S::kKLoads], rv[S::kVLoads];
-  auto fetch = [&](int kt0) {
-    constexpr int kc = DH / S::kVec;
+  // Direct loads of one stage: this wave's kInstsPerWave 1 KB blocks. Block
+  // i of the stage covers bytes [i KB, i+1 KB): the K tile(s), then V^T.
+  auto issue = [&](int t, int stage) {
+    const int kt0 = t * S::kKT;
+    char* st = smem + stage * S::kStage;
+    const uint32_t krows = (uint32_t)max(0, p.m - kt0) * S::kRowBytes;  // keys past m read as zero
+    const rsrc_t rk = make_rsrc_uniform(kp + (int64_t)kt0 * S::kRowBytes, krows);
+    const rsrc_t rkl = SPLIT ? make_rsrc_uniform(klp + (int64_t)kt0 * S::kRowBytes, krows) : rk;
+    const rsrc_t rv = make_rsrc_uniform(vtp + (int64_t)kt0 * sizeof(T),
+                                        (uint32_t)((int64_t)DH * p.ld_t * sizeof(T) - (int64_t)kt0 * sizeof(T)));
 #pragma unroll
-    for (int part = 0; part < S::kKParts; ++part) {
-      const T* src = part == 0 ? kp : klp;
-#pragma unroll
-      for (int i = 0; i < S::kKLoads; ++i) {
-        const int v = tid + i * 256;
-        const int key = kt0 + v / kc;
-        u32x4 val = {0u, 0u, 0u, 0u};
-        if (key < p.m) val = ld16(src + (int64_t)key * DH + (v % kc) * S::kVec);
-        rk[part][i] = val;
+    for (int j = 0; j < S::kInstsPerWave; ++j) {
+      const int i = wave * S::kInstsPerWave + j;  // wave-uniform
+      const int off = i * 1024;
+      uint32_t vo;
+      rsrc_t r;
+      if (off < S::kKParts * S::kKTile) {  // K: row = key, contiguous rows
+        r = off < S::kKTile ? rk : rkl;
+        const int row = (off % S::kKTile) / S::kRowBytes + lane / (S::kRowBytes / 16);
+        vo = (uint32_t)(row * S::kRowBytes + swz(row, lane % (S::kRowBytes / 16)) * 16);
+      } else {  // V^T: row = channel, stride ld_t
+        r = rv;
+        const int row = (off - S::kKParts * S::kKTile) / S::kVRowBytes + lane / (S::kVRowBytes / 16);
+        vo = (uint32_t)((int64_t)row * p.ld_t * sizeof(T) + swz(row, lane % (S::kVRowBytes / 16)) * 16);
       }
-    }
-    constexpr int vc = S::kKT / S::kVec;
-#pragma unroll
-    for (int i = 0; i < S::kVLoads; ++i) {
-      const int v = tid + i * 256;
-      rv[i] = ld16(vtp + (int64_t)(v / vc) * p.ld_t + kt0 + (v % vc) * S::kVec);
-    }
-  };
-  auto stash = [&](T* st) {
-    constexpr int kc = DH / S::kVec;
-#pragma unroll
-    for (int part = 0; part < S::kKParts; ++part)
-#pragma unroll
-      for (int i = 0; i < S::kKLoads; ++i) {
-        const int v = tid + i * 256;
-        st16(st + part * S::kKElems + (v / kc) * S::kKStride + (v % kc) * S::kVec, rk[part][i]);
-      }
-    constexpr int vc = S::kKT / S::kVec;
-#pragma unroll
-    for (int i = 0; i < S::kVLoads; ++i) {
-      const int v = tid + i * 256;
-      st16(st + S::kVOff + (v / vc) * S::kVStride + (v % vc) * S::kVec, rv[i]);
+      buf_ld16_lds(r, vo, st + off);
     }
   };
 
@@ -128,93 +119,141 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.0f;
   float mrun = -INFINITY, lrun = 0.0f;
+  const float sc = p.scale_log2;
+  const float thr = 8.0f / sc;  // raw-score headroom of the stale maximum (2^8)
 
-  fetch(0);
-  stash(smem);
-  __syncthreads();
+#pragma unroll
+  for (int s0 = 0; s0 < S::kNS - 1; ++s0)
+    if (s0 < ntiles) issue(s0, s0);
 
   for (int t = 0; t < ntiles; ++t) {
     const int kt0 = t * S::kKT;
-    const bool more = t + 1 < ntiles;
-    if (more) fetch(kt0 + S::kKT);
-    const T* sk = smem + (t & 1) * S::kStage;
-    const T* sv = sk + S::kVOff;
+    // tile t has landed for this wave (younger: the tiles after it), then for all
+    if constexpr (S::kNS == 3) {
+      if (t + 1 < ntiles)
+        wait_vmcnt<S::kInstsPerWave>();
+      else
+        wait_vmcnt<0>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    lds_barrier();  // also: every wave is done with tile t-1, whose stage is refilled next
+    if (t + S::kNS - 1 < ntiles) issue(t + S::kNS - 1, (t + S::kNS - 1) % S::kNS);
+    const char* sk = smem + (t % S::kNS) * S::kStage;
+    const char* sv = sk + S::kKParts * S::kKTile;
     const bool active = !p.causal || kt0 <= qw0 + 31;  // uniform across the wave
     if (active) {
+      // S^T = K Q^T for 64 keys (two 32-key blocks) x this wave's 32 queries
       f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
+        const int kr = kb * 32 + col;  // key row of this lane's A fragment
+        const char* krow = sk + kr * S::kRowBytes;
 #pragma unroll
         for (int kk = 0; kk < DH / 16; ++kk) {
-          const int off = (kb * 32 + col) * S::kKStride + kk * 16 + g * 8;
-          const typename MM::frag kh = MM::load(sk + off);
+          typename MM::frag kh, kl;
+          if constexpr (sizeof(T) == 2) {
+            const int off = swz(kr, kk * 2 + g) * 16;
+            kh = *reinterpret_cast<const typename MM::frag*>(krow + off);
+            if constexpr (SPLIT) kl = *reinterpret_cast<const typename MM::frag*>(krow + S::kKTile + off);
+          } else {
+            const int c0 = kk * 4 + g * 2;
+            const f32x4 lo = *reinterpret_cast<const f32x4*>(krow + swz(kr, c0) * 16);
+            const f32x4 hi = *reinterpret_cast<const f32x4*>(krow + swz(kr, c0 + 1) * 16);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              kh[e] = lo[e];
+              kh[e + 4] = hi[e];
+            }
+          }
           s[kb] = MM::mma(kh, qf[kk], s[kb]);
           if constexpr (SPLIT) {
-            s[kb] = MM::mma(MM::load(sk + S::kKElems + off), qf[kk], s[kb]);
+            s[kb] = MM::mma(kl, qf[kk], s[kb]);
             s[kb] = MM::mma(kh, qfl[kk], s[kb]);
           }
         }
       }
+      // online softmax on raw scores; masked entries are -inf
       const bool need_mask = (p.causal && kt0 + S::kKT - 1 > qw0) || kt0 + S::kKT > p.m;
+      if (need_mask) {  // wave-uniform; selects, no per-element branches
+        const int klim = p.causal ? min(myq, p.m - 1) : p.m - 1;  // last visible key
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kt0 + kb * 32 + acc_row(r, lane);
+            s[kb][r] = key > klim ? -INFINITY : s[kb][r];
+          }
+      }
       float mt = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float v = s[kb][r] * p.scale_log2;
-          if (need_mask) {
-            const int key = kt0 + kb * 32 + acc_row(r, lane);
-            if (key >= p.m || (p.causal && key > myq)) v = -INFINITY;
-          }
-          s[kb][r] = v;
-          mt = fmaxf(mt, v);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+      mt = fmaxf(mt, other_half(mt));
       const float mnew = fmaxf(mrun, mt);
-      const float alpha = fast_exp2(mrun - mnew);
-      mrun = mnew;
-      float ls = 0.0f;
+      if (__builtin_amdgcn_ballot_w64(mnew > mrun + thr) != 0) {
+        const float alpha = fast_exp2((mrun - mnew) * sc);  // 0 on the first tile
+        lrun *= alpha;
+#pragma unroll
+        for (int cb = 0; cb < DH / 32; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
+        mrun = mnew;
+      }
+      const float mb = mrun * sc;
+      float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // four partial sums: no serial add chain
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = fast_exp2(s[kb][r] - mnew);
+          const float e = fast_exp2(fmaf(s[kb][r], sc, -mb));
           s[kb][r] = e;
-          ls += e;
+          ls[r & 3] += e;
         }
-      lrun = lrun * alpha + ls;
-#pragma unroll
-      for (int cb = 0; cb < DH / 32; ++cb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
+      lrun += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      // O^T += V^T P^T, 16 keys per MFMA
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
-          float pv[8];
+          // bf16: after the swap lane group g holds keys 16*s2 + 8*g .. +7;
+          // fp32: no swap, slots 0-3 / 4-7 are keys 16*s2 + 4*g + {0..3} / + 8,
+          // each run one 16-byte chunk of V^T.
+          typename MM::frag pb;
+          if constexpr (sizeof(T) == 2) {
+            pb = pt_frag_bf16(s[kb], s2);
+          } else {
 #pragma unroll
-          for (int i = 0; i < 8; ++i) pv[i] = s[kb][s2 * 8 + i];
-          const typename MM::frag pb = MM::pack(pv);
+            for (int i = 0; i < 8; ++i) pb[i] = s[kb][s2 * 8 + i];
+          }
+          const int c0 = kb * 32 + s2 * 16 + g * 8;  // bf16: first key of this lane's 8
+          const int c4 = kb * 32 + s2 * 16 + g * 4;  // fp32: first key of the lane's first run
 #pragma unroll
           for (int cb = 0; cb < DH / 32; ++cb) {
-            const T* vrow = sv + (cb * 32 + col) * S::kVStride + kb * 32 + s2 * 16 + g * 4;
+            const int d = cb * 32 + col;
+            const char* vrow = sv + d * S::kVRowBytes;
             typename MM::frag va;
-            typedef typename Quad<T>::type QT;
-            const QT lo = *reinterpret_cast<const QT*>(vrow);
-            const QT hi = *reinterpret_cast<const QT*>(vrow + 8);
-            *reinterpret_cast<QT*>(&va) = lo;
-            *(reinterpret_cast<QT*>(&va) + 1) = hi;
+            if constexpr (sizeof(T) == 2) {
+              va = *reinterpret_cast<const typename MM::frag*>(vrow + swz(d, c0 / 8) * 16);
+            } else {
+              const f32x4 lo = *reinterpret_cast<const f32x4*>(vrow + swz(d, c4 / 4) * 16);
+              const f32x4 hi = *reinterpret_cast<const f32x4*>(vrow + swz(d, c4 / 4 + 2) * 16);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                va[e] = lo[e];
+                va[e + 4] = hi[e];
+              }
+            }
             oacc[cb] = MM::mma(va, pb, oacc[cb]);
           }
         }
     }
-    if (more) stash(smem + ((t + 1) & 1) * S::kStage);
-    __syncthreads();
   }
 
-  const float ltot = lrun + __shfl_xor(lrun, 32);
+  const float ltot = lrun + other_half(lrun);
   if (myq < p.m) {
     const float inv = 1.0f / ltot;
     T* orow = reinterpret_cast<T*>(p.o) + ((int64_t)b * p.m + myq) * ((int64_t)p.n_heads * DH) + h * DH;
@@ -222,27 +261,37 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const AttnParams p) {
     for (int cb = 0; cb < DH / 32; ++cb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) orow[cb * 32 + acc_row(r, lane)] = from_f32<T>(oacc[cb][r] * inv);
-    if (g == 0) p.lse[(int64_t)bh * p.m + myq] = (mrun + __log2f(ltot)) * 0.69314718055994531f;
+    if (g == 0) p.lse[(int64_t)bh * p.m + myq] = (mrun * sc + __log2f(ltot)) * 0.69314718055994531f;
   }
+}
+
+// Ring depth and the occupancy the register allocation targets (waves per
+// SIMD). Two stages and a target of 2 measured best for d_head = 64 (a
+// target of 3 caps registers at 168 and schedules worse).
+template <typename T, int DH, bool SPLIT>
+struct AttnFwdCfg {
+  static constexpr int kNS = 2;
+  static constexpr int kOcc = DH == 64 ? 2 : 1;
+};
+
+template <typename T, int DH, bool SPLIT>
+static hipError_t launch_fwd_cfg(const AttnParams& p, dim3 grid, hipStream_t stream) {
+  typedef AttnFwdCfg<T, DH, SPLIT> C;
+  hipLaunchKernelGGL((attn_fwd_kernel<T, DH, SPLIT, C::kNS, C::kOcc>), grid, dim3(256), 0, stream, p);
+  return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hipStream_t stream) {
   if (p.m <= 0) return hipSuccess;
+  // 32-bit buffer offsets: one head's transposed V must stay below 2 GiB
+  if ((int64_t)head_dim * p.ld_t * (int64_t)sizeof(T) >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   dim3 grid((p.m + 127) / 128, batch * p.n_heads);
   const bool split = sizeof(T) == 2 && p.q_lo && p.k_lo;
-  if (head_dim == 64) {
-    if (split)
-      hipLaunchKernelGGL((attn_fwd_kernel<T, 64, sizeof(T) == 2>), grid, dim3(256), 0, stream, p);
-    else
-      hipLaunchKernelGGL((attn_fwd_kernel<T, 64, false>), grid, dim3(256), 0, stream, p);
-  } else {
-    if (split)
-      hipLaunchKernelGGL((attn_fwd_kernel<T, 128, sizeof(T) == 2>), grid, dim3(256), 0, stream, p);
-    else
-      hipLaunchKernelGGL((attn_fwd_kernel<T, 128, false>), grid, dim3(256), 0, stream, p);
-  }
-  return hipGetLastError();
+  constexpr bool kSplit = sizeof(T) == 2;
+  if (head_dim == 64)
+    return split ? launch_fwd_cfg<T, 64, kSplit>(p, grid, stream) : launch_fwd_cfg<T, 64, false>(p, grid, stream);
+  return split ? launch_fwd_cfg<T, 128, kSplit>(p, grid, stream) : launch_fwd_cfg<T, 128, false>(p, grid, stream);
 }
 
 template hipError_t launch_attention_fwd<bf16>(const AttnParams&, int, int, hipStream_t);
