@@ -49,9 +49,20 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
   typedef Mma<T> MM;
   __shared__ __attribute__((aligned(1024))) char smem[S::kNS * S::kStage];
 
+  // 1-D grid over (head, query tile). Consecutive workgroups go to different
+  // XCDs (round robin over 8), so the id is remapped to give every XCD a
+  // contiguous run of tiles: the query tiles of one head share an L2 while
+  // they stream the same keys. Longest causal rows first within a head.
   const int nqt = (p.m + 127) / 128;
-  const int qt = nqt - 1 - (int)blockIdx.x;  // longest causal rows first
-  const int bh = blockIdx.y;
+  int bh, qt;
+  {
+    const int total = (int)gridDim.x;
+    const int q = total / kNumXcd, rem = total % kNumXcd;
+    const int wg = blockIdx.x, xcd = wg % kNumXcd, local = wg / kNumXcd;
+    const int t = (xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q) + local;
+    bh = t / nqt;
+    qt = nqt - 1 - t % nqt;
+  }
   const int b = bh / p.n_heads, h = bh % p.n_heads;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -286,7 +297,7 @@ hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hi
   if (p.m <= 0) return hipSuccess;
   // 32-bit buffer offsets: one head's transposed V must stay below 2 GiB
   if ((int64_t)head_dim * p.ld_t * (int64_t)sizeof(T) >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-  dim3 grid((p.m + 127) / 128, batch * p.n_heads);
+  dim3 grid(((p.m + 127) / 128) * batch * p.n_heads);
   const bool split = sizeof(T) == 2 && p.q_lo && p.k_lo;
   constexpr bool kSplit = sizeof(T) == 2;
   if (head_dim == 64)
