@@ -1,21 +1,27 @@
 // Proxy-KV-cache decode step and block-triggered append (Eq. 19-21, Sec. 3.8).
 //
-// Step (one token per sequence, the batch in lockstep):
-//  1. rmsnorm_kernel: u = RMSNorm(x) * gamma, and x is stored in block slot j.
-//  2. GEMMs of u with W_q, W_k, W_v (k, v written straight into slot j of the
-//     local block) and W_alpha (sigmoid in the epilogue).
-//  3. decode_attn_kernel: the only HBM-heavy step. Cache rows of every
+// Step (one token per sequence, the batch in lockstep), four launches:
+//  1. decode_proj_kernel: u = RMSNorm(x) * gamma formed on the fly and
+//     multiplied by W_q, W_k, W_v and W_alpha (one 32-column block of the
+//     concatenated outputs per workgroup, MFMA over 32 batch rows): q to
+//     scratch, k and v straight into slot j of the local block, alpha through
+//     a sigmoid. It also stores x into block slot j.
+//  2. decode_attn_kernel: the only HBM-heavy step. Cache rows of every
 //     (sequence, head) are cut into slices; a workgroup streams one slice of
 //     K and V with 16-byte loads (eight lanes per 64-channel row), keeps an
 //     online softmax per row slot, and writes an unnormalised partial
 //     (max, sum, weighted values). One extra slice per (sequence, head)
 //     handles the current block's slots 0..j.
-//  4. decode_combine_kernel: merges the cache slices in a fixed order (A_h),
+//  3. decode_combine_kernel: merges the cache slices in a fixed order (A_h),
 //     normalises the local part (A_x) and forms A = A_x + alpha * A_h.
-//  5. GEMM with W_o plus the residual x (y = x + A W_o^T + b_o).
+//  4. the projection kernel of step 1 in its second form:
+//     y = x + A W_o^T + b_o.
 // Append: compression GEMMs over whole blocks (the block is a zero-copy
 // [rows, P*d] view), then the K/V proxy maps write straight into cache row n.
 #include <algorithm>
+#include <mutex>
+#include <utility>
+#include <vector>
 #include <cmath>
 #include <cstring>
 
@@ -53,6 +59,8 @@ int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why) {
   d->esize = c->dtype == PF_BF16 ? 2 : 4;
   d->eps = c->rms_eps;
   if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
+  if ((int64_t)d->d * d->esize > 4096)
+    return *why = "d_model * element size must be at most 4096 bytes (32 staged rows in LDS)", PF_ERR_UNSUPPORTED;
   for (int j = 0; j <= d->M; ++j)
     if (d->dl[j] % 8 != 0) return *why = "every channel width must be a multiple of 8", PF_ERR_UNSUPPORTED;
   const int64_t lvl1_rows_per_block = d->P / d->k[0];
@@ -70,7 +78,6 @@ static DecodeWs decode_ws_layout(const DecodeDims& d) {
     return o;
   };
   const size_t es = d.esize;
-  w.u = take((size_t)d.B * d.d * es);
   w.q = take((size_t)d.B * d.d * es);
   w.alpha = take((size_t)d.B * d.nh * 4);
   w.attn = take((size_t)d.B * d.d * es);
@@ -90,28 +97,199 @@ static DecodeWs decode_ws_layout(const DecodeDims& d) {
 
 // ---- kernels ------------------------------------------------------------------
 
+// ---- small-batch projections (steps 1 and 3) ------------------------------------
+//
+// out[b, c] for 32 rows b (blockIdx.y) and one block of 32 output columns
+// (blockIdx.x) of A W^T, A = [B, d]: MFMA with the batch rows as the M side.
+// The 32 rows of A are staged once in LDS (step 1: u = RMSNorm(x) * gamma,
+// rounded to the activation type as a stored u would be), with 16-byte chunks
+// XOR-swizzled by row so fragment reads are conflict-free. Each of the four
+// waves takes a quarter of K; its weight fragments are requested eight
+// k-steps ahead, and the four partial tiles are summed in LDS in a fixed order.
+struct DecodeProjParams {
+  const void* x;        // [B, d]: the token input (RMSNorm input; the residual of step 3)
+  const void* a;        // [B, d]: step 3's A (attention output)
+  const void* gamma;    // [d] RMSNorm scale (step 1)
+  const void* w[4];     // step 1: W_q, W_k, W_v [d, d] and W_alpha [h, d]; step 3: W_o
+  const void* bias[4];  // NULL = 0
+  int width[4];         // output width of each matrix (d, d, d, h; step 3: d)
+  int B, d, nh, dh;
+  int64_t P;
+  int j;
+  float eps;
+  void* q;              // [B, d]
+  void* k_loc;          // [B, h, P, dh]
+  void* v_loc;
+  float* alpha;         // [B, h]
+  void* x_blk;          // [B, P, d]
+  void* y;              // step 3: [B, d]
+};
+
 template <typename T>
-__global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ gamma, T* u,
-                                                      T* x_blk, int d, int64_t blk_stride, int j, float eps) {
-  const int b = blockIdx.x;
-  const T* xr = x + (int64_t)b * d;
-  float ss = 0.0f;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    const float v = to_f32(xr[c]);
-    ss += v * v;
+constexpr size_t decode_small_gemm_lds(int d) {
+  return (size_t)32 * d * sizeof(T) + 4 * 32 * 33 * sizeof(float) + 32 * sizeof(float);
+}
+
+template <typename T, bool PROJ, int CPL>
+__global__ void __launch_bounds__(256) decode_small_gemm_kernel(const DecodeProjParams p) {
+  typedef Mma<T> MM;
+  constexpr int kV = 16 / sizeof(T);  // elements per 16-byte chunk
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
+  T* a_s = reinterpret_cast<T*>(dyn);                                     // [32][d], swizzled chunks
+  float* red = reinterpret_cast<float*>(dyn + (size_t)32 * p.d * sizeof(T));  // [4][32 * 33]
+  float* inv_s = red + 4 * 32 * 33;                                       // [32]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 5, l32 = lane & 31;
+  const int b0 = blockIdx.y * 32;
+  const int cpr = p.d / kV;  // chunks per row
+  // which matrix this column block belongs to (every width but the last is
+  // a multiple of 32, so a block never straddles two matrices)
+  int seg = 0, cs = blockIdx.x * 32;
+  if constexpr (PROJ) {
+    while (seg < 3 && cs >= p.width[seg]) {
+      cs -= p.width[seg];
+      ++seg;
+    }
   }
-  __shared__ float red[256];
-  red[threadIdx.x] = ss;
+  const int width = p.width[seg];
+  const T* x = reinterpret_cast<const T*>(p.x);
+  auto a_slot = [&](int r, int c) { return a_s + (int64_t)r * p.d + ((c ^ (r & 7)) * kV); };
+
+  // weight fragments of this wave's quarter of K, eight k-steps at a time
+  const int col = cs + l32;  // B column = weight row
+  const bool col_ok = col < width;
+  const T* wrow = reinterpret_cast<const T*>(p.w[seg]) + (int64_t)(col_ok ? col : 0) * p.d;
+  // stage the 32 rows of A: wave w takes rows 8w .. 8w+7 (CPL 16-byte
+  // chunks per lane and row), every load issued before any is used
+  const T* src = PROJ ? x : reinterpret_cast<const T*>(p.a);
+  u32x4 raw[8][CPL];
+#pragma unroll
+  for (int rr = 0; rr < 8; ++rr)
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int b = min(b0 + wave * 8 + rr, p.B - 1), c = min(lane + 64 * i, cpr - 1);
+      raw[rr][i] = ld16(src + (int64_t)b * p.d + c * kV);
+    }
+  // every other global read of the kernel goes out before the first use
+  u32x4 graw[CPL];  // RMSNorm scale: the same chunks for every row
+#pragma unroll
+  for (int i = 0; i < CPL; ++i)
+    graw[i] = PROJ ? ld16(reinterpret_cast<const T*>(p.gamma) + min(lane + 64 * i, cpr - 1) * kV)
+                   : u32x4{0u, 0u, 0u, 0u};
+  const int kq = p.d / 4, kbeg = wave * kq, nsteps = kq / 16;
+  constexpr int kChunk = 16;  // k-steps of weight fragments requested at once
+  typename MM::frag wf[kChunk];
+  auto fetch_w = [&](int chunk) {  // unconditional (clamped) loads stay in flight together
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i) {
+      const int st = min(chunk * kChunk + i, nsteps - 1);
+      wf[i] = MM::load(wrow + kbeg + st * 16 + g * 8);
+    }
+  };
+  fetch_w(0);
+  // the epilogue's reads (bias, residual) go out with the first requests too
+  const T* bias = reinterpret_cast<const T*>(p.bias[seg]);
+  float bv[4], xr[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int o = tid + u * 256, rr = o >> 5, cc = o & 31;
+    const int b = min(b0 + rr, p.B - 1), c = min(cs + cc, width - 1);
+    const float braw = to_f32((bias ? bias : x)[c]);  // unconditional read, no branch
+    bv[u] = bias ? braw : 0.0f;
+    xr[u] = PROJ ? 0.0f : to_f32(x[(int64_t)b * p.d + c]);
+  }
+#pragma unroll
+  for (int rr = 0; rr < 8; ++rr) {
+    const int r = wave * 8 + rr, b = b0 + r;
+    float inv = 1.0f;
+    if constexpr (PROJ) {
+      float ss = 0.0f;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        const T* v = reinterpret_cast<const T*>(&raw[rr][i]);
+        if (lane + 64 * i < cpr)
+#pragma unroll
+          for (int e = 0; e < kV; ++e) ss += to_f32(v[e]) * to_f32(v[e]);
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      inv = 1.0f / sqrtf(ss / (float)p.d + p.eps);
+    }
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int c = lane + 64 * i;
+      if (c >= cpr) continue;
+      u32x4 v = raw[rr][i];
+      if (b >= p.B) v = u32x4{0u, 0u, 0u, 0u};
+      if constexpr (PROJ) {
+        if (blockIdx.x == 0 && b < p.B)  // x into block slot j
+          st16(reinterpret_cast<T*>(p.x_blk) + ((int64_t)b * p.P + p.j) * p.d + c * kV, v);
+        const T* xv = reinterpret_cast<const T*>(&v);
+        const T* gv = reinterpret_cast<const T*>(&graw[i]);
+        T uv[kV];
+#pragma unroll
+        for (int e = 0; e < kV; ++e) uv[e] = from_f32<T>(to_f32(xv[e]) * inv * to_f32(gv[e]));
+        v = *reinterpret_cast<const u32x4*>(uv);
+      }
+      st16(a_slot(r, c), v);
+    }
+  }
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
-    __syncthreads();
+
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+  for (int chunk = 0; chunk * kChunk < nsteps; ++chunk) {
+    if (chunk > 0) fetch_w(chunk);  // d > 1024 (bf16) only
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i) {  // fully unrolled: wf stays in registers
+      const int st = chunk * kChunk + i;
+      if (st >= nsteps) continue;
+      const int k = kbeg + st * 16 + g * 8;
+      typename MM::frag af;
+      if constexpr (sizeof(T) == 2) {
+        af = *reinterpret_cast<const typename MM::frag*>(a_slot(l32, k / kV));
+      } else {
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(a_slot(l32, k / kV));
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(a_slot(l32, k / kV + 1));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          af[e] = lo[e];
+          af[e + 4] = hi[e];
+        }
+      }
+      typename MM::frag bf = wf[i];
+      if (!col_ok) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bf[e] = (T)0.0f;
+      }
+      acc = MM::mma(af, bf, acc);
+    }
   }
-  const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    const T xv = xr[c];
-    u[(int64_t)b * d + c] = from_f32<T>(to_f32(xv) * inv * to_f32(gamma[c]));
-    x_blk[(int64_t)b * blk_stride + (int64_t)j * d + c] = xv;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) red[wave * 32 * 33 + acc_row(r, lane) * 33 + l32] = acc[r];
+  __syncthreads();
+  // four outputs per thread
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int o = tid + u * 256, rr = o >> 5, cc = o & 31;
+    const int b = b0 + rr, c = cs + cc;
+    if (b >= p.B || c >= width) continue;
+    const int ri = rr * 33 + cc;
+    const float v = ((red[ri] + red[32 * 33 + ri]) + red[2 * 32 * 33 + ri]) + red[3 * 32 * 33 + ri] + bv[u];
+    if constexpr (PROJ) {
+      if (seg == 0) {
+        reinterpret_cast<T*>(p.q)[(int64_t)b * p.d + c] = from_f32<T>(v);
+      } else if (seg < 3) {
+        T* dst = reinterpret_cast<T*>(seg == 1 ? p.k_loc : p.v_loc);
+        const int hd = c / p.dh, e = c - hd * p.dh;
+        dst[(((int64_t)b * p.nh + hd) * p.P + p.j) * p.dh + e] = from_f32<T>(v);
+      } else {
+        p.alpha[(int64_t)b * p.nh + c] = sigmoidf(v);
+      }
+    } else {
+      reinterpret_cast<T*>(p.y)[(int64_t)b * p.d + c] = from_f32<T>(xr[u] + v);
+    }
   }
 }
 
@@ -124,11 +302,46 @@ struct DecodeAttnParams {
   float* part_m;       // [B*h, S+1]
   float* part_l;
   float* part_acc;     // [B*h, S+1, dh]
+  const float* alpha;  // [B, h]
+  void* attn;          // [B, d] output A
   int64_t n, n_cap, P;
   int j;               // local slots 0..j are valid
   int nh, splits, chunk;
   float scale_log2;
 };
+
+// A[b, h, c] = A_x + alpha * A_h from the partials: cache slices merged in a
+// fixed order (A_h, zero without cached rows), local slice normalised (A_x).
+// A[b, h, c] = A_x + alpha * A_h from the partials: cache slices merged in a
+// fixed order with a running maximum (A_h, zero without cached rows), local
+// slice normalised (A_x). Loads go out eight slices at a time.
+template <typename T, int DH>
+__device__ __forceinline__ void combine_partials(const DecodeAttnParams& p, int bh, int b, int h, int c) {
+  const int64_t base = (int64_t)bh * (p.splits + 1);
+  float mrun = -INFINITY, lrun = 0.0f, arun = 0.0f;
+  for (int s0 = 0; s0 < p.splits; s0 += 8) {
+    float m[8], l[8], a[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int s = min(s0 + i, p.splits - 1);
+      m[i] = p.part_m[base + s];
+      l[i] = p.part_l[base + s];
+      a[i] = p.part_acc[(base + s) * DH + c];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (s0 + i >= p.splits || m[i] == -INFINITY) continue;
+      const float mn = fmaxf(mrun, m[i]);
+      const float f0 = fast_exp2(mrun - mn), f1 = fast_exp2(m[i] - mn);
+      lrun = lrun * f0 + l[i] * f1;
+      arun = arun * f0 + a[i] * f1;
+      mrun = mn;
+    }
+  }
+  const float ah = mrun == -INFINITY ? 0.0f : arun / lrun;
+  const float ax = p.part_acc[(base + p.splits) * DH + c] / p.part_l[base + p.splits];
+  reinterpret_cast<T*>(p.attn)[(int64_t)b * p.nh * DH + h * DH + c] = from_f32<T>(ax + p.alpha[(int64_t)b * p.nh + h] * ah);
+}
 
 template <typename T, int DH>
 __global__ void __launch_bounds__(256) decode_attn_kernel(const DecodeAttnParams p) {
@@ -243,69 +456,16 @@ __global__ void __launch_bounds__(256) decode_attn_kernel(const DecodeAttnParams
   }
 }
 
+// Merge of the partials of every (sequence, head): one wave per (sequence,
+// head), DH / 64 channels per lane; see combine_partials.
 template <typename T, int DH>
-__global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restrict__ part_m,
-                                                            const float* __restrict__ part_l,
-                                                            const float* __restrict__ part_acc,
-                                                            const float* __restrict__ alpha, T* attn, int nh,
-                                                            int splits) {
-  const int bh = blockIdx.x;
-  const int b = bh / nh, h = bh % nh;
-  const int64_t base = (int64_t)bh * (splits + 1);
-  float mx = -INFINITY;
-  for (int s = 0; s < splits; ++s) mx = fmaxf(mx, part_m[base + s]);
-  const float a = alpha[(int64_t)b * nh + h];
-  for (int c = threadIdx.x; c < DH; c += 64) {
-    float ah = 0.0f;
-    if (mx != -INFINITY) {
-      float l = 0.0f, acc = 0.0f;
-      for (int s = 0; s < splits; ++s) {
-        const float f = fast_exp2(part_m[base + s] - mx);
-        l += part_l[base + s] * f;
-        acc += part_acc[(base + s) * DH + c] * f;
-      }
-      ah = acc / l;
-    }
-    const float ax = part_acc[(base + splits) * DH + c] / part_l[base + splits];
-    attn[(int64_t)b * nh * DH + h * DH + c] = from_f32<T>(ax + a * ah);
-  }
-}
-
-// k/v of the new token into slot j of the local block: out [B, h, P, dh].
-template <typename T>
-struct EpiSlot {
-  T* out;
-  const T* bias;
-  int nh, dh;
-  int64_t P;
-  int j;
-  __device__ __forceinline__ void operator()(int r, int c, float v) const {
-    if (bias) v += to_f32(bias[c]);
-    const int hd = c / dh, e = c - hd * dh;
-    out[(((int64_t)r * nh + hd) * P + j) * dh + e] = from_f32<T>(v);
-  }
-  __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
-    float v[8];
+__global__ void __launch_bounds__(256) decode_combine_kernel(const DecodeAttnParams p, int nbh) {
+  const int bh = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (bh >= nbh) return;
+  const int b = bh / p.nh, h = bh % p.nh, lane = threadIdx.x & 63;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = v0[e] + (bias ? to_f32(bias[c + e]) : 0.0f);
-    const int hd = c / dh, e0 = c - hd * dh;
-    store8(out + (((int64_t)r * nh + hd) * P + j) * dh + e0, v);
-  }
-};
-
-template <typename T>
-struct EpiSigmoidF32 {
-  float* out;
-  const T* bias;
-  int ldo;
-  __device__ __forceinline__ void operator()(int r, int c, float v) const {
-    if (bias) v += to_f32(bias[c]);
-    out[(int64_t)r * ldo + c] = sigmoidf(v);
-  }
-  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
-    for (int e = 0; e < 8; ++e) (*this)(r, c + e, v[e]);
-  }
-};
+  for (int c = lane; c < DH; c += 64) combine_partials<T, DH>(p, bh, b, h, c);
+}
 
 // Proxy K/V rows into the cache: row rr = r0 + r is (sequence rr / nblk,
 // block rr % nblk) and lands at cache row n0 + block.
@@ -390,38 +550,73 @@ static void split_plan(int64_t n, int* splits, int* chunk) {
   *splits = (int)((n + c - 1) / c);
 }
 
+// Lets a kernel use up to 160 KB of dynamic LDS, once per (kernel, device).
+static hipError_t allow_lds(const void* kernel) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static std::vector<std::pair<const void*, int>> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const auto& k : done)
+    if (k.first == kernel && k.second == dev) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e == hipSuccess && done.size() < 2 * kMaxDevices) done.emplace_back(kernel, dev);
+  return e;
+}
+
+// Chunks per lane and row of the staged A: 1, 2 or 4 (d * sizeof(T) <= 4096).
+template <typename T, bool PROJ>
+static hipError_t launch_small_gemm(dim3 grid, const DecodeProjParams& pp, hipStream_t stream) {
+  const int cpr = pp.d * (int)sizeof(T) / 16;
+  const size_t lds = decode_small_gemm_lds<T>(pp.d);
+  auto go = [&](auto kern) {
+    hipError_t e = allow_lds(reinterpret_cast<const void*>(kern));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, grid, dim3(256), lds, stream, pp);
+    return hipGetLastError();
+  };
+  if (cpr <= 64) return go(decode_small_gemm_kernel<T, PROJ, 1>);
+  if (cpr <= 128) return go(decode_small_gemm_kernel<T, PROJ, 2>);
+  return go(decode_small_gemm_kernel<T, PROJ, 4>);
+}
+
 template <typename T>
 static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
                       const void* x_t, void* y_t, char* ws) {
   const DecodeWs W = decode_ws_layout(d);
-  T* u = reinterpret_cast<T*>(ws + W.u);
   T* q = reinterpret_cast<T*>(ws + W.q);
   float* alpha = reinterpret_cast<float*>(ws + W.alpha);
   T* attn = reinterpret_cast<T*>(ws + W.attn);
-  run.launch("decode_rmsnorm", [&] {
-    hipLaunchKernelGGL((rmsnorm_kernel<T>), dim3(d.B), dim3(256), 0, run.stream, reinterpret_cast<const T*>(x_t),
-                       reinterpret_cast<const T*>(w->rms_gamma), u, reinterpret_cast<T*>(st.x_blk), d.d,
-                       (int64_t)(d.P * d.d), st.j, d.eps);
-    return hipGetLastError();
+  const int rblocks = (d.B + 31) / 32;
+
+  DecodeProjParams pp{};
+  pp.x = x_t;
+  pp.gamma = w->rms_gamma;
+  const pf_linear* lin[4] = {&w->q, &w->k, &w->v, &w->alpha};
+  for (int i = 0; i < 4; ++i) {
+    pp.w[i] = lin[i]->w;
+    pp.bias[i] = lin[i]->b;
+    pp.width[i] = i < 3 ? d.d : d.nh;
+  }
+  pp.B = d.B;
+  pp.d = d.d;
+  pp.nh = d.nh;
+  pp.dh = d.dh;
+  pp.P = d.P;
+  pp.j = st.j;
+  pp.eps = d.eps;
+  pp.q = q;
+  pp.k_loc = st.k_loc;
+  pp.v_loc = st.v_loc;
+  pp.alpha = alpha;
+  pp.x_blk = st.x_blk;
+  static_assert(decode_small_gemm_lds<T>(2048 * 2 / sizeof(T)) <= 160 * 1024, "staged rows fit the LDS");
+  run.launch("decode_proj", [&] {
+    const dim3 grid(3 * d.d / 32 + (d.nh + 31) / 32, rblocks);
+    return launch_small_gemm<T, true>(grid, pp, run.stream);
   });
-  GemmProblem pr{};
-  pr.a = u;
-  pr.lda = d.d;
-  pr.ldb = d.d;
-  pr.M = d.B;
-  pr.N = d.d;
-  pr.K = d.d;
-  pr.b = w->q.w;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>("decode_q_gemm", pr, EpiLinear<T>{q, d.d, reinterpret_cast<const T*>(w->q.b), nullptr, 0, nullptr});
-  pr.b = w->k.w;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>(
-      "decode_k_gemm", pr, EpiSlot<T>{reinterpret_cast<T*>(st.k_loc), reinterpret_cast<const T*>(w->k.b), d.nh, d.dh, d.P, st.j});
-  pr.b = w->v.w;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>(
-      "decode_v_gemm", pr, EpiSlot<T>{reinterpret_cast<T*>(st.v_loc), reinterpret_cast<const T*>(w->v.b), d.nh, d.dh, d.P, st.j});
-  pr.b = w->alpha.w;
-  pr.N = d.nh;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>("decode_alpha_gemm", pr, EpiSigmoidF32<T>{alpha, reinterpret_cast<const T*>(w->alpha.b), d.nh});
 
   int splits, chunk;
   split_plan(st.n, &splits, &chunk);
@@ -434,6 +629,8 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   ap.part_m = reinterpret_cast<float*>(ws + W.part_m);
   ap.part_l = reinterpret_cast<float*>(ws + W.part_l);
   ap.part_acc = reinterpret_cast<float*>(ws + W.part_acc);
+  ap.alpha = alpha;
+  ap.attn = attn;
   ap.n = st.n;
   ap.n_cap = st.n_cap;
   ap.P = d.P;
@@ -451,19 +648,28 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
     return hipGetLastError();
   });
   run.launch("decode_combine", [&] {
+    const int nbh = d.B * d.nh;
+    const dim3 grid((nbh + 3) / 4);
     if (d.dh == 64)
-      hipLaunchKernelGGL((decode_combine_kernel<T, 64>), dim3(d.B * d.nh), dim3(64), 0, run.stream, ap.part_m,
-                         ap.part_l, ap.part_acc, alpha, attn, d.nh, splits);
+      hipLaunchKernelGGL((decode_combine_kernel<T, 64>), grid, dim3(256), 0, run.stream, ap, nbh);
     else
-      hipLaunchKernelGGL((decode_combine_kernel<T, 128>), dim3(d.B * d.nh), dim3(64), 0, run.stream, ap.part_m,
-                         ap.part_l, ap.part_acc, alpha, attn, d.nh, splits);
+      hipLaunchKernelGGL((decode_combine_kernel<T, 128>), grid, dim3(256), 0, run.stream, ap, nbh);
     return hipGetLastError();
   });
-  pr.a = attn;
-  pr.b = w->o.w;
-  pr.N = d.d;
-  run.gemm<T, LAYOUT_K, LAYOUT_K>("decode_out_gemm", pr, EpiLinear<T>{reinterpret_cast<T*>(y_t), d.d, reinterpret_cast<const T*>(w->o.b),
-                                                   reinterpret_cast<const T*>(x_t), d.d, nullptr});
+
+  DecodeProjParams op{};
+  op.x = x_t;
+  op.a = attn;
+  op.w[0] = w->o.w;
+  op.bias[0] = w->o.b;
+  op.width[0] = d.d;
+  op.B = d.B;
+  op.d = d.d;
+  op.y = y_t;
+  run.launch("decode_out", [&] {
+    const dim3 grid(d.d / 32, rblocks);
+    return launch_small_gemm<T, false>(grid, op, run.stream);
+  });
 }
 
 // Split-K need of every GEMM a step or an append can issue (any chunk size).

@@ -25,7 +25,7 @@ constexpr int kDecodeMaxSplits = 256;   // cache-row slices per (sequence, head)
 constexpr int kDecodeRowsPerSplit = 1024;
 
 struct DecodeWs {
-  size_t u, q, alpha, attn;         // [B, d], [B, d], fp32 [B, h], [B, d]
+  size_t q, alpha, attn;            // [B, d], fp32 [B, h], [B, d]
   size_t part_m, part_l, part_acc;  // fp32 partial softmax states
   size_t z[PF_MAX_LEVELS];          // append: compression level outputs (j = 1..M)
   size_t gemm;
