@@ -37,10 +37,11 @@ TRAIN_WORKLOAD = "layer_bf16_L256k_d2048_f8x8"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 CPU_SAMPLE_TOKENS = 65536
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_bf16_L1M_d1024.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_bf16_L1M_d1024_decode_bf16_B32_n16k.txt")
 KERNEL_SOURCES = ["paper_2608_23463_amd/csrc/gemm.hpp", "paper_2608_23463_amd/csrc/epilogues.hpp",
-                  "paper_2608_23463_amd/csrc/common.hpp", "paper_2608_23463_amd/csrc/attention_fwd.hip",
-                  "paper_2608_23463_amd/csrc/layer_fwd.hip"]
+                  "paper_2608_23463_amd/csrc/common.hpp", "paper_2608_23463_amd/csrc/attention.hpp",
+                  "paper_2608_23463_amd/csrc/attention_fwd.hip", "paper_2608_23463_amd/csrc/layer_fwd.hip",
+                  "paper_2608_23463_amd/csrc/decode.hip", "paper_2608_23463_amd/csrc/decode.hpp"]
 
 
 def log(msg):
@@ -225,7 +226,12 @@ def bench_decode():
         gbs = nbytes / (avg * 1e-3) / 1e9
         out["roofline"] = {"kernel": "decode_attn", "bound": "hbm", "achieved": round(gbs, 1),
                            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                           "traffic": None, "avg_ms": round(avg, 4), "work_per_launch": nbytes}
+                           "traffic": measured_traffic("decode_attn"), "avg_ms": round(avg, 4),
+                           "work_per_launch": nbytes}
+        # the whole step (projections, merge and output map included) against HBM
+        step_gbs = nbytes / (ms / shape.steps * 1e-3) / 1e9
+        out["step_hbm"] = {"achieved": round(step_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": round(step_gbs / PEAK_HBM_GBS, 4)}
     out["kernels"] = {k: {"launches": c, "avg_ms": round(t / c, 4)} for k, (c, t) in tr.items()}
     del kc, vc, xs, ys, sess
     torch.cuda.empty_cache()
@@ -299,9 +305,10 @@ def cpu_baseline(shape, sample):
 
 def pmc_pass():
     """Minimal dispatch sequence for hardware-counter runs: two layer forwards
-    on the 1M-token shape (random device data; traffic does not depend on the
-    values) and one plain 1 GiB device-to-device copy whose FETCH_SIZE and
-    WRITE_SIZE calibrate the counters (it must read and write 1 GiB)."""
+    on the 1M-token shape and two decode steps at the decode workload's shape
+    (random device data; traffic does not depend on the values), then one
+    plain 1 GiB device-to-device copy whose FETCH_SIZE and WRITE_SIZE
+    calibrate the counters (it must read and write 1 GiB)."""
     import torch
     from paper_2608_23463_amd import binding as B
     from paper_2608_23463_amd import synth
@@ -328,12 +335,36 @@ def pmc_pass():
     for _ in range(2):
         B.layer_forward_raw(cfg, wst, x, None, x_out, h_out, None, ws)
         torch.cuda.synchronize()
+    del x, x_out, h_out, ws, w, wst
+    torch.cuda.empty_cache()
+    # two decode steps at the decode workload's shape (random device data)
+    ds = synth.WORKLOADS[DECODE_WORKLOAD]
+    dcfg = B.decode_config(ds.batch, ds.d_model, ds.n_heads, ds.head_dim, ds.factors, ds.level_dims, ds.dtype,
+                           ds.rms_eps)
+    cache_shape = (ds.batch, ds.n_heads, ds.n0 + ds.steps // ds.block + 1, ds.head_dim)
+    kc = rn(*cache_shape)
+    vc = rn(*cache_shape)
+    dw = {"rms_gamma": torch.ones(ds.d_model, dtype=dt, device="cuda")}
+    for k, (o, i) in {"q": (ds.d_model, ds.d_model), "k": (ds.d_model, ds.d_model), "v": (ds.d_model, ds.d_model),
+                      "o": (ds.d_model, ds.d_model), "alpha": (ds.n_heads, ds.d_model),
+                      "k_proxy": (ds.d_model, ds.d_model), "v_proxy": (ds.d_model, ds.d_model)}.items():
+        dw[k] = (rn(o, i, std=0.02), None)
+    dd = ds.dims()
+    dw["compress"] = [(rn(dd[j + 1], ds.factors[j] * dd[j], std=0.02), None) for j in range(len(ds.factors))]
+    sess = B.DecodeSession(dcfg, dw, kc, vc, n=ds.n0)
+    xs = rn(2, ds.batch, ds.d_model)
+    ys = torch.empty_like(xs)
+    for t in range(2):
+        sess.step(xs[t], ys[t])
+        torch.cuda.synchronize()
+    del sess, kc, vc
+    torch.cuda.empty_cache()
     a = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
     b = torch.empty_like(a)
     torch.cuda.synchronize()
     b.copy_(a)
     torch.cuda.synchronize()
-    print("pmc pass done: 2 forwards, 1 GiB copy", flush=True)
+    print("pmc pass done: 2 forwards, 2 decode steps, 1 GiB copy", flush=True)
 
 
 def main():
