@@ -764,7 +764,10 @@ inline GemmPlan plan_gemm(const GemmProblem& pr, int num_cu) {
     pl.tile = TILE_128x128;
     pl.bm = pl.bn = 128;
     pl.bk = 32;
-  } else if (mn >= (int64_t)256 * 256 * num_cu && pr.M >= 256 && pr.N >= 256) {
+  } else if (pr.M >= 256 && pr.N >= 256 &&
+             (mn >= (int64_t)256 * 256 * num_cu ||
+              // long reductions: 256x256 tiles split along K still fill the chip
+              (int64_t)pr.K * (((pr.M + 255) / 256) * ((pr.N + 255) / 256)) >= (int64_t)num_cu * 64 * 64)) {
     pl.tile = TILE_256x256;
     pl.bm = pl.bn = 256;
     pl.bk = 64;

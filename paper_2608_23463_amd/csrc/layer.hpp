@@ -67,10 +67,16 @@ struct LayerWs {
   size_t dh;                  // dH in the activation dtype [B*m, d_p]
   size_t dz[PF_MAX_LEVELS];   // dZ_j j = 1..M-1 [B*R_j, d_j]
   size_t colsum;              // bias-gradient partial column sums
+  size_t tr_a, tr_b;          // transposed GEMM operands of the large weight gradients [cols, rows]
+  size_t tr_w;                // a transposed weight [in, out] for the large data gradients
   size_t bytes;
 };
 
 constexpr int kColsumChunks = 512;
+// Weight and data gradients over at least this many rows run on transposed
+// (K-contiguous) operand copies through the direct GEMM kernel.
+constexpr int64_t kTransposeMinRows = 8192;
+inline int64_t round8(int64_t v) { return (v + 7) / 8 * 8; }
 
 // Validates cfg; on failure returns a status and writes a message.
 int layer_dims(const pf_layer_config* cfg, LayerDims* d, const char** why);

@@ -185,6 +185,61 @@ struct EpiAccum {
   }
 };
 
+// out[c, r] = in[r, c] for r < R, c < C (row strides ld_in, ld_out), through
+// 64x64 LDS tiles: 16-byte coalesced reads along c, 16-byte writes along r.
+template <typename T>
+__global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ in, int64_t ld_in, int64_t R, int C,
+                                                        T* __restrict__ out, int64_t ld_out) {
+  constexpr int kV = 16 / sizeof(T);
+  __shared__ T tile[64][64 + 2];
+  const int64_t r0 = (int64_t)blockIdx.y * 64;
+  const int c0 = blockIdx.x * 64;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < 64 * 64 / kV; i += 256) {
+    const int rr = i / (64 / kV), cc = (i % (64 / kV)) * kV;
+    const int64_t r = r0 + rr;
+    const int c = c0 + cc;
+    T v[kV];
+    if (r < R && c + kV <= C) {
+      const u32x4 raw = ld16(in + r * ld_in + c);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int k = 0; k < kV; ++k) v[k] = e[k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < kV; ++k) v[k] = (r < R && c + k < C) ? in[r * ld_in + c + k] : (T)0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < kV; ++k) tile[rr][cc + k] = v[k];
+  }
+  __syncthreads();
+  for (int i = tid; i < 64 * 64 / kV; i += 256) {
+    const int cc = i / (64 / kV), rr = (i % (64 / kV)) * kV;
+    const int c = c0 + cc;
+    const int64_t r = r0 + rr;
+    if (c >= C) continue;
+    T v[kV];
+#pragma unroll
+    for (int k = 0; k < kV; ++k) v[k] = tile[rr + k][cc];
+    if (r + kV <= R) {
+      st16(out + (int64_t)c * ld_out + r, *reinterpret_cast<const u32x4*>(v));
+    } else {
+      for (int k = 0; r + k < R; ++k) out[(int64_t)c * ld_out + r + k] = v[k];
+    }
+  }
+}
+
+template <typename T>
+static void transpose(Runner& run, const char* label, const T* in, int64_t ld_in, int64_t R, int C, T* out,
+                      int64_t ld_out) {
+  if (run.dry || R <= 0 || C <= 0) return;
+  run.launch(label, [&] {
+    hipLaunchKernelGGL((transpose_kernel<T>), dim3((C + 63) / 64, (unsigned)((R + 63) / 64)), dim3(256), 0,
+                       run.stream, in, ld_in, R, C, out, ld_out);
+    return hipGetLastError();
+  });
+}
+
 template <typename T>
 static void colsum(Runner& run, const char* label, const T* in, int64_t rows, int n, int64_t ld, float* part,
                    float* out) {
@@ -201,35 +256,57 @@ static void colsum(Runner& run, const char* label, const T* in, int64_t rows, in
 
 // dW (fp32 [M, N] with row stride ldo) = sum over rows r of A[r, m] * B[r, n]:
 // both operands are row-major [rows, *] activations, i.e. contiguous along
-// the output dimensions.
+// the output dimensions. Over many rows both are first transposed into
+// tr_a / tr_b ([M, rows] and [N, rows], rows padded to a multiple of 8) so the
+// product runs on K-contiguous operands; `a_t` passes an A already
+// transposed into tr_a by the caller.
 template <typename T>
 static void wgrad(Runner& run, const char* label, const T* a, int64_t lda, const T* b, int64_t ldb, int M, int N,
-                  int64_t rows, float* out, int64_t ldo) {
+                  int64_t rows, float* out, int64_t ldo, T* tr_a, T* tr_b, bool a_t = false) {
   if (!out) return;
   GemmProblem pr{};
+  pr.M = M;
+  pr.N = N;
+  pr.K = (int)rows;
+  if (rows >= kTransposeMinRows) {
+    const int64_t ldt = round8(rows);
+    if (!a_t) transpose<T>(run, "transpose", a, lda, rows, M, tr_a, ldt);
+    transpose<T>(run, "transpose", b, ldb, rows, N, tr_b, ldt);
+    pr.a = tr_a;
+    pr.lda = ldt;
+    pr.b = tr_b;
+    pr.ldb = ldt;
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(label, pr, EpiF32{out, ldo, 0});
+    return;
+  }
   pr.a = a;
   pr.lda = lda;
   pr.b = b;
   pr.ldb = ldb;
-  pr.M = M;
-  pr.N = N;
-  pr.K = (int)rows;
   run.gemm<T, LAYOUT_MN, LAYOUT_MN>(label, pr, EpiF32{out, ldo, 0});
 }
 
 // dA [rows, N] = G [rows, K] W [K, N] for a weight W stored [K (out), N (in)]:
-// the weight is read contiguous along N (LAYOUT_MN).
+// the weight is read contiguous along N (LAYOUT_MN), or, over many rows,
+// transposed once into tr_w ([N, K]) for the direct kernel.
 template <typename T, class Epi>
 static void dgrad(Runner& run, const char* label, const T* g, int64_t ldg, const void* w, int64_t ldw, int64_t rows,
-                  int N, int K, const Epi& epi) {
+                  int N, int K, const Epi& epi, T* tr_w) {
   GemmProblem pr{};
   pr.a = g;
   pr.lda = ldg;
-  pr.b = w;
-  pr.ldb = ldw;
   pr.M = (int)rows;
   pr.N = N;
   pr.K = K;
+  if (rows >= kTransposeMinRows) {
+    transpose<T>(run, "transpose", reinterpret_cast<const T*>(w), ldw, K, N, tr_w, K);
+    pr.b = tr_w;
+    pr.ldb = K;
+    run.gemm<T, LAYOUT_K, LAYOUT_K>(label, pr, epi);
+    return;
+  }
+  pr.b = w;
+  pr.ldb = ldw;
   run.gemm<T, LAYOUT_K, LAYOUT_MN>(label, pr, epi);
 }
 
@@ -243,6 +320,9 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   auto WT = [&](size_t off) { return reinterpret_cast<T*>(ws + off); };
   auto WF = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
   float* part = WF(W.colsum);
+  T* tra = WT(W.tr_a);
+  T* trb = WT(W.tr_b);
+  T* trw = WT(W.tr_w);
   const int64_t BL = (int64_t)d.B * d.L;
   const int64_t Bm = (int64_t)d.B * d.m;
   const int df = d.d_f, dp = d.d_p;
@@ -258,10 +338,12 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
     return hipGetLastError();
   });
   dgrad<T>(run, "gate_dgrad_gemm", WT(W.dg), df, w->gate.w, 2 * df, BL, 2 * df, df,
-           EpiGateDgrad<T>{dyp, S(A.g), WF(W.dx32), WT(W.ddelta), df});
+           EpiGateDgrad<T>{dyp, S(A.g), WF(W.dx32), WT(W.ddelta), df}, trw);
   float* dwg = reinterpret_cast<float*>(gr->gate.dw);
-  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df);
-  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, S(A.delta), df, df, df, BL, dwg ? dwg + df : nullptr, 2 * df);
+  // dG is transposed once for both halves of dW_g
+  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df, tra, trb);
+  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, S(A.delta), df, df, df, BL, dwg ? dwg + df : nullptr, 2 * df, tra,
+           trb, dwg != nullptr);
   colsum<T>(run, "bias_colsum", WT(W.dg), BL, df, df, part, reinterpret_cast<float*>(gr->gate.db));
 
   // 2. decompression levels 1..M (reverse of Eq. 17)
@@ -272,14 +354,14 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
     const int dn = d.d[j + 1];
     const T* u_in = j == d.M - 1 ? S(A.s) : S(A.u[j + 1]);
     wgrad<T>(run, "decompress_wgrad_gemm", dT, kd, u_in, dn, kd, dn, rows,
-             reinterpret_cast<float*>(gr->decompress[j].dw), dn);
+             reinterpret_cast<float*>(gr->decompress[j].dw), dn, tra, trb);
     colsum<T>(run, "bias_colsum", dT, rows, kd, kd, part, reinterpret_cast<float*>(gr->decompress[j].db));
     if (j == d.M - 1) {
       dgrad<T>(run, "decompress_dgrad_gemm", dT, kd, w->decompress[j].w, dn, rows, dn, kd,
-               EpiUnshift<T>{WT(W.dhbar), (int)d.m, dp, cfg->mask == PF_TOKEN_CAUSAL ? 1 : 0});
+               EpiUnshift<T>{WT(W.dhbar), (int)d.m, dp, cfg->mask == PF_TOKEN_CAUSAL ? 1 : 0}, trw);
     } else {
       dgrad<T>(run, "decompress_dgrad_gemm", dT, kd, w->decompress[j].w, dn, rows, dn, kd,
-               EpiLinear<T>{WT(W.du[j + 1]), dn, nullptr, nullptr, 0, nullptr});
+               EpiLinear<T>{WT(W.du[j + 1]), dn, nullptr, nullptr, 0, nullptr}, trw);
       dT = WT(W.du[j + 1]);
     }
   }
@@ -290,8 +372,9 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
     run.launch("fill_zero", [&] { return fill_zero(WT(W.dOt), tb, run.stream); });
   }
   dgrad<T>(run, "o_dgrad_gemm", WT(W.dhbar), dp, w->o.w, dp, Bm, dp, dp,
-           EpiHeads<T>{WT(W.dO), WT(W.dOt), nullptr, (int)d.m, d.dh, d.nh, d.ld_t});
-  wgrad<T>(run, "o_wgrad_gemm", WT(W.dhbar), dp, S(A.o), dp, dp, dp, Bm, reinterpret_cast<float*>(gr->o.dw), dp);
+           EpiHeads<T>{WT(W.dO), WT(W.dOt), nullptr, (int)d.m, d.dh, d.nh, d.ld_t}, trw);
+  wgrad<T>(run, "o_wgrad_gemm", WT(W.dhbar), dp, S(A.o), dp, dp, dp, Bm, reinterpret_cast<float*>(gr->o.dw), dp, tra,
+           trb);
   colsum<T>(run, "bias_colsum", WT(W.dhbar), Bm, dp, dp, part, reinterpret_cast<float*>(gr->o.db));
 
   // 4. attention (Eq. 9)
@@ -324,13 +407,14 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   const pf_linear* maps[3] = {&w->q, &w->k, &w->v};
   const pf_linear_grad* grads[3] = {&gr->q, &gr->k, &gr->v};
   for (int i = 0; i < 3; ++i) {
-    wgrad<T>(run, "qkv_wgrad_gemm", dqkv[i], dp, S(A.h), dp, dp, dp, Bm, reinterpret_cast<float*>(grads[i]->dw), dp);
+    wgrad<T>(run, "qkv_wgrad_gemm", dqkv[i], dp, S(A.h), dp, dp, dp, Bm, reinterpret_cast<float*>(grads[i]->dw), dp,
+             tra, trb);
     colsum<T>(run, "bias_colsum", dqkv[i], Bm, dp, dp, part, reinterpret_cast<float*>(grads[i]->db));
   }
   for (int i = 0; i < 3; ++i) {
     EpiAccum<T> e{WF(W.dh32), dp, reinterpret_cast<const T*>(dh_out), i == 0, i == 2 ? WT(W.dh) : nullptr,
                   i == 2 ? reinterpret_cast<T*>(dh_in) : nullptr};
-    dgrad<T>(run, "qkv_dgrad_gemm", dqkv[i], dp, maps[i]->w, dp, Bm, dp, dp, e);
+    dgrad<T>(run, "qkv_dgrad_gemm", dqkv[i], dp, maps[i]->w, dp, Bm, dp, dp, e, trw);
   }
 
   // 6. compression levels M..1 (reverse of Eq. 16)
@@ -341,14 +425,14 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
     const int dn = d.d[j + 1];
     const T* v_in = j == 0 ? xp : S(A.z[j]);
     wgrad<T>(run, "compress_wgrad_gemm", dz, dn, v_in, kd, dn, kd, rows,
-             reinterpret_cast<float*>(gr->compress[j].dw), kd);
+             reinterpret_cast<float*>(gr->compress[j].dw), kd, tra, trb);
     colsum<T>(run, "bias_colsum", dz, rows, dn, dn, part, reinterpret_cast<float*>(gr->compress[j].db));
     if (j == 0) {
       dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
-               EpiAccum<T>{WF(W.dx32), kd, nullptr, 0, reinterpret_cast<T*>(dx), nullptr});
+               EpiAccum<T>{WF(W.dx32), kd, nullptr, 0, reinterpret_cast<T*>(dx), nullptr}, trw);
     } else {
       dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
-               EpiLinear<T>{WT(W.dz[j]), kd, nullptr, nullptr, 0, nullptr});
+               EpiLinear<T>{WT(W.dz[j]), kd, nullptr, nullptr, 0, nullptr}, trw);
       dz = WT(W.dz[j]);
     }
   }

@@ -148,6 +148,26 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     int64_t widest = std::max<int64_t>(2 * d.d_f, d.d_p);
     for (int j = 0; j < d.M; ++j) widest = std::max<int64_t>(widest, (int64_t)d.k[j] * d.d[j]);
     w.colsum = take((size_t)kColsumChunks * widest * 4);
+    // transposed operands: every large gradient / activation operand is at
+    // most [B*L, d_f] elements (plus row padding to a multiple of 8)
+    size_t tr = 0, trw = 0;
+    auto op = [&](int64_t rows, int64_t cols) {
+      if (rows >= kTransposeMinRows) tr = std::max(tr, (size_t)(round8(rows) * cols) * es);
+    };
+    auto wt = [&](int64_t out, int64_t in) { trw = std::max(trw, (size_t)(out * in) * es); };
+    op((int64_t)d.B * d.L, d.d_f);
+    wt(d.d_f, 2 * (int64_t)d.d_f);
+    for (int j = 0; j < d.M; ++j) {
+      const int64_t rows = (int64_t)d.B * d.R[j + 1];
+      op(rows, (int64_t)d.k[j] * d.d[j]);
+      op(rows, d.d[j + 1]);
+      wt((int64_t)d.k[j] * d.d[j], d.d[j + 1]);
+    }
+    op((int64_t)d.B * d.m, d.d_p);
+    wt(d.d_p, d.d_p);
+    w.tr_a = take(tr);
+    w.tr_b = take(tr);
+    w.tr_w = take(trw);
   }
   w.gemm = off;
   w.bytes = off;
