@@ -362,6 +362,83 @@ __device__ __forceinline__ void gemm_store(f32x16 (&acc)[S::kFM][S::kFN], float*
   }
 }
 
+// Wave-local epilogue of the direct kernel: each wave writes its own
+// kTM x kTN tile, kRows rows per step, through a private LDS region, with
+// no workgroup barrier, so a wave that finishes its MFMAs stores while the
+// others still multiply. The epilogue's global reads (Epi::pre) run kAhead
+// steps ahead of their use; their coordinates are clamped into the matrix
+// (a clamped chunk's values are not used), which needs N >= 8.
+template <class S, int kRows, class Epi>
+__device__ __forceinline__ void gemm_store_wave(f32x16 (&acc)[S::kFM][S::kFN], float* region, const GemmParams& p,
+                                                int row0, int col0, int lane, const Epi& epi) {
+  constexpr int kTN = S::kTN;
+  constexpr int kSRow = kTN + 8;               // rows r and r + 4 land on disjoint banks
+  constexpr int kCpr = kTN / 8;                // 8-column chunks per row
+  constexpr int kRowsPerPass = kWave / kCpr;   // rows one wave instruction covers
+  constexpr int kPer = kRows / kRowsPerPass;   // chunks per lane per step
+  constexpr int kHalves = 32 / kRows;          // steps per 32-row MFMA block
+  constexpr int kSteps = S::kFM * kHalves;
+  constexpr int kAhead = 2;
+  static_assert((kRows == 16 || kRows == 8) && kCpr <= kWave && kRows % kRowsPerPass == 0, "wave tile width");
+  const int cl = (lane % kCpr) * 8;
+  const int rl0 = lane / kCpr;
+  const int col = col0 + cl;
+  typename EpiCol<Epi>::type colv;
+  if (p.N >= 8) epi_col(epi, min(col, p.N - 8), colv);
+  typename EpiPre<Epi>::type pre[kAhead + 1][kPer];
+  auto issue = [&](int step, typename EpiPre<Epi>::type (&q)[kPer]) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int row = row0 + step * kRows + rl0 + u * kRowsPerPass;
+      epi_pre(epi, min(row, p.M - 1), min(col, p.N - 8), q[u]);
+    }
+  };
+#pragma unroll
+  for (int a = 0; a < kAhead; ++a)
+    if (a < kSteps && p.N >= 8) issue(a, pre[a]);
+#pragma unroll
+  for (int step = 0; step < kSteps; ++step) {
+    const int i = step / kHalves, h = step % kHalves;
+    if (step + kAhead < kSteps && p.N >= 8) issue(step + kAhead, pre[(step + kAhead) % (kAhead + 1)]);
+    // Block i holds rows 8 (r / 4) + 4 (lane / 32) + r % 4 in register r, so
+    // registers [h kRows / 2, (h + 1) kRows / 2) are rows [h kRows, (h + 1) kRows).
+#pragma unroll
+    for (int j = 0; j < S::kFN; ++j)
+#pragma unroll
+      for (int r = h * kRows / 2; r < (h + 1) * kRows / 2; ++r)
+        region[(acc_row(r, lane) - h * kRows) * kSRow + j * 32 + (lane & 31)] = acc[i][j][r];
+    // The region is private to the wave: LDS completion is the only ordering needed.
+    asm volatile("" ::: "memory");
+    wait_lgkmcnt0();
+    asm volatile("" ::: "memory");
+    float v[kPer][8];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const float* src = region + (rl0 + u * kRowsPerPass) * kSRow + cl;
+      const f32x4 a = *reinterpret_cast<const f32x4*>(src);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(src + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[u][e] = a[e];
+        v[u][e + 4] = b[e];
+      }
+    }
+    asm volatile("" ::: "memory");
+    wait_lgkmcnt0();
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int row = row0 + step * kRows + rl0 + u * kRowsPerPass;
+      if (row >= p.M || col >= p.N) continue;
+      if (col + 8 <= p.N) {
+        epi_vec8(epi, row, col, v[u], colv, pre[step % (kAhead + 1)][u]);
+      } else {
+        for (int e = 0; col + e < p.N; ++e) epi(row, col + e, v[u][e]);
+      }
+    }
+  }
+}
+
 // Pins the instruction order of kSteps MFMA k-steps, each made of kMfma
 // MFMAs with the kReads fragment reads of the following k-step riding on
 // its first MFMAs (masks: 0x100 DS read, 0x008 MFMA), so LDS latency hides
@@ -497,8 +574,9 @@ struct DirectShape {
   static constexpr int kLoads = kNia + kNib;           // loads per thread per stage
   static constexpr int kStage = (BM + BN) * BK;          // elements per stage
   static constexpr size_t kMainBytes = (size_t)NS * kStage * sizeof(T);
-  static constexpr size_t kEpiBytes = (size_t)S::kTM * (BN + 8) * sizeof(float);
-  static constexpr size_t kLdsBytes = kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes;
+  // fp32 staging of 16 rows of every wave's tile (the wave-local epilogue)
+  static constexpr size_t kEpiRegion16 = (size_t)kWaves * 16 * (S::kTN + 8) * sizeof(float);
+  static constexpr size_t kLdsBytes = kMainBytes;
   static_assert(kCpr == 8 || kCpr == 4, "the XOR swizzle handles 64- and 128-byte tile rows");
   static_assert(kNia >= 1 && kNib >= 1 && BM % (kRowsPerInst * kWaves) == 0 && BN % (kRowsPerInst * kWaves) == 0,
                 "tile rows must split evenly over wave instructions");
@@ -680,9 +758,15 @@ __global__ void __launch_bounds__(WM* WN* kWave)
     }
     mfmas(1);
   }
-  // No direct load may still be writing LDS when the epilogue stages there.
-  wait_vmcnt<0>();
-  gemm_store<S, BM, BN, WM>(acc, reinterpret_cast<float*>(smem), p, m0, n0, wm, wn, lane, tid, epi);
+  // Every direct load has landed (the last wait_stages drained them all).
+  // The stage that held tile nk-2 is free on every wave: nothing reads it
+  // after the barrier that handed over tile nk-1 and no load refills it;
+  // with fewer tiles an unused stage is free.
+  const int free_stage = nk >= 2 ? (nk - 2) % NS : (nk == 1 ? 1 : 0);
+  constexpr int kRows = D::kEpiRegion16 <= D::kStage * sizeof(T) ? 16 : 8;
+  static_assert(D::kEpiRegion16 / (16 / kRows) <= D::kStage * sizeof(T), "wave epilogue regions must fit one stage");
+  float* region = reinterpret_cast<float*>(smem + free_stage * D::kStage) + wave * kRows * (S::kTN + 8);
+  gemm_store_wave<S, kRows>(acc, region, p, m0 + wm * S::kTM, n0 + wn * S::kTN, lane, epi);
 }
 
 // Fixed-order reduction of split-K partials ws[s][M][N], then the epilogue
