@@ -67,6 +67,7 @@ struct LayerWs {
   size_t dh;                  // dH in the activation dtype [B*m, d_p]
   size_t dz[PF_MAX_LEVELS];   // dZ_j j = 1..M-1 [B*R_j, d_j]
   size_t colsum;              // bias-gradient partial column sums
+  size_t colsum2;             // second-stage partials (64 groups)
   size_t tr_a, tr_b;          // transposed GEMM operands of the large weight gradients [cols, rows]
   size_t tr_w;                // a transposed weight [in, out] for the large data gradients
   size_t bytes;

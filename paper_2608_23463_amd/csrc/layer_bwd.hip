@@ -87,6 +87,35 @@ struct EpiGateDgrad {
       ddelta[i] = from_f32<T>(to_f32(dy[i]) * sigmoidf(to_f32(g[i])) + v);
     }
   }
+  // Two-phase form (the direct kernel's epilogue reads ahead): pre() loads
+  // dY, and G for the dDelta half.
+  struct Col {};
+  struct Pre {
+    Raw8<T> a, z;
+  };
+  __device__ __forceinline__ void col(int, Col&) const {}
+  __device__ __forceinline__ void pre(int r, int c, Pre& q) const {
+    const int64_t i = (int64_t)r * d + (c < d ? c : c - d);
+    raw_load8(dy + i, q.a);
+    if (c >= d) raw_load8(g + i, q.z);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v, const Col&, const Pre& q) const {
+    float a[8], o[8];
+    raw_to_f32(q.a, a);
+    if (c < d) {
+      const int64_t i = (int64_t)r * d + c;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = a[e] + v[e];
+      store8(dx32 + i, o);
+    } else {
+      const int64_t i = (int64_t)r * d + (c - d);
+      float z[8];
+      raw_to_f32(q.z, z);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = a[e] * sigmoidf(z[e]) + v[e];
+      store8(ddelta + i, o);
+    }
+  }
   __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
     float a[8], o[8];
     if (c < d) {  // d is a multiple of 8, so a chunk never straddles the halves
@@ -161,6 +190,39 @@ struct EpiAccum {
       acc[i] = t;
     }
   }
+  // Two-phase form: pre() loads the addend (`add` or the accumulator).
+  struct Col {};
+  struct Pre {
+    Raw8<T> a;
+    Raw8<float> f;
+  };
+  __device__ __forceinline__ void col(int, Col&) const {}
+  __device__ __forceinline__ void pre(int r, int c, Pre& q) const {
+    const int64_t i = (int64_t)r * ld + c;
+    if (!first)
+      raw_load8(acc + i, q.f);
+    else if (add)
+      raw_load8(add + i, q.a);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v, const Col&, const Pre& q) const {
+    float b[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (!first)
+      raw_to_f32(q.f, b);
+    else if (add)
+      raw_to_f32(q.a, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b[e] += v[e];
+    finish(r, c, b);
+  }
+  __device__ __forceinline__ void finish(int r, int c, const float* t) const {
+    const int64_t i = (int64_t)r * ld + c;
+    if (out) {
+      store8(out + i, t);
+      if (out2) store8(out2 + i, t);
+    } else {
+      store8(acc + i, t);
+    }
+  }
   __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
     const int64_t i = (int64_t)r * ld + c;
     float t[8], b[8];
@@ -187,10 +249,14 @@ struct EpiAccum {
 
 // out[c, r] = in[r, c] for r < R, c < C (row strides ld_in, ld_out), through
 // 64x64 LDS tiles: 16-byte coalesced reads along c, 16-byte writes along r.
+// With `part`, the tile also leaves the column sums of its 64 rows in
+// part[blockIdx.y][c] (fixed order: a thread's 16-byte run, then a butterfly
+// over the runs of one column), the first stage of a bias gradient.
 template <typename T>
 __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ in, int64_t ld_in, int64_t R, int C,
-                                                        T* __restrict__ out, int64_t ld_out) {
+                                                        T* __restrict__ out, int64_t ld_out, float* __restrict__ part) {
   constexpr int kV = 16 / sizeof(T);
+  constexpr int kRuns = 64 / kV;  // runs per column; consecutive threads
   __shared__ T tile[64][64 + 2];
   const int64_t r0 = (int64_t)blockIdx.y * 64;
   const int c0 = blockIdx.x * 64;
@@ -214,13 +280,21 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ in
   }
   __syncthreads();
   for (int i = tid; i < 64 * 64 / kV; i += 256) {
-    const int cc = i / (64 / kV), rr = (i % (64 / kV)) * kV;
+    const int cc = i / kRuns, rr = (i % kRuns) * kV;
     const int c = c0 + cc;
     const int64_t r = r0 + rr;
-    if (c >= C) continue;
     T v[kV];
 #pragma unroll
     for (int k = 0; k < kV; ++k) v[k] = tile[rr + k][cc];
+    if (part) {  // block-uniform; rows past R and columns past C hold zeros
+      float sum = 0.0f;
+#pragma unroll
+      for (int k = 0; k < kV; ++k) sum += to_f32(v[k]);
+#pragma unroll
+      for (int off = 1; off < kRuns; off <<= 1) sum += __shfl_xor(sum, off);
+      if (rr == 0 && c < C) part[(int64_t)blockIdx.y * C + c] = sum;
+    }
+    if (c >= C) continue;
     if (r + kV <= R) {
       st16(out + (int64_t)c * ld_out + r, *reinterpret_cast<const u32x4*>(v));
     } else {
@@ -231,11 +305,11 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ in
 
 template <typename T>
 static void transpose(Runner& run, const char* label, const T* in, int64_t ld_in, int64_t R, int C, T* out,
-                      int64_t ld_out) {
+                      int64_t ld_out, float* part = nullptr) {
   if (run.dry || R <= 0 || C <= 0) return;
   run.launch(label, [&] {
     hipLaunchKernelGGL((transpose_kernel<T>), dim3((C + 63) / 64, (unsigned)((R + 63) / 64)), dim3(256), 0,
-                       run.stream, in, ld_in, R, C, out, ld_out);
+                       run.stream, in, ld_in, R, C, out, ld_out, part);
     return hipGetLastError();
   });
 }
@@ -254,23 +328,47 @@ static void colsum(Runner& run, const char* label, const T* in, int64_t rows, in
   });
 }
 
+// Remaining stages of a bias gradient whose per-64-row partial sums a
+// transpose left in `part` (ceil(rows / 64) chunks): the chunks are summed
+// in groups of consecutive chunks into part2, then the groups in order.
+static void colsum_final(Runner& run, const char* label, int64_t rows, int n, const float* part, float* part2,
+                         float* out) {
+  if (!out || run.dry) return;
+  const int chunks = (int)((rows + 63) / 64);
+  const int groups = std::min(chunks, 64);
+  const int64_t per = (chunks + groups - 1) / groups;
+  run.launch(label, [&] {
+    hipLaunchKernelGGL((colsum_partial_kernel<float>), dim3((n + 255) / 256, groups), dim3(256), 0, run.stream, part,
+                       (int64_t)chunks, n, (int64_t)n, per, part2);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((n + 255) / 256), dim3(256), 0, run.stream, part2, groups, n, out);
+    return hipGetLastError();
+  });
+}
+
 // dW (fp32 [M, N] with row stride ldo) = sum over rows r of A[r, m] * B[r, n]:
 // both operands are row-major [rows, *] activations, i.e. contiguous along
 // the output dimensions. Over many rows both are first transposed into
 // tr_a / tr_b ([M, rows] and [N, rows], rows padded to a multiple of 8) so the
 // product runs on K-contiguous operands; `a_t` passes an A already
-// transposed into tr_a by the caller.
+// transposed into tr_a by the caller. With `db`, the column sums of A (a
+// bias gradient) are formed too, from the transpose's tiles when there is one.
 template <typename T>
 static void wgrad(Runner& run, const char* label, const T* a, int64_t lda, const T* b, int64_t ldb, int M, int N,
-                  int64_t rows, float* out, int64_t ldo, T* tr_a, T* tr_b, bool a_t = false) {
-  if (!out) return;
+                  int64_t rows, float* out, int64_t ldo, T* tr_a, T* tr_b, bool a_t = false, float* db = nullptr,
+                  float* part = nullptr, float* part2 = nullptr) {
   GemmProblem pr{};
   pr.M = M;
   pr.N = N;
   pr.K = (int)rows;
+  if (out && rows >= kTransposeMinRows && !a_t) {
+    transpose<T>(run, "transpose", a, lda, rows, M, tr_a, round8(rows), db ? part : nullptr);
+    if (db) colsum_final(run, "bias_colsum", rows, M, part, part2, db);
+  } else if (db) {
+    colsum<T>(run, "bias_colsum", a, rows, M, lda, part, db);
+  }
+  if (!out) return;
   if (rows >= kTransposeMinRows) {
     const int64_t ldt = round8(rows);
-    if (!a_t) transpose<T>(run, "transpose", a, lda, rows, M, tr_a, ldt);
     transpose<T>(run, "transpose", b, ldb, rows, N, tr_b, ldt);
     pr.a = tr_a;
     pr.lda = ldt;
@@ -320,6 +418,7 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   auto WT = [&](size_t off) { return reinterpret_cast<T*>(ws + off); };
   auto WF = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
   float* part = WF(W.colsum);
+  float* part2 = WF(W.colsum2);
   T* tra = WT(W.tr_a);
   T* trb = WT(W.tr_b);
   T* trw = WT(W.tr_w);
@@ -341,10 +440,10 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
            EpiGateDgrad<T>{dyp, S(A.g), WF(W.dx32), WT(W.ddelta), df}, trw);
   float* dwg = reinterpret_cast<float*>(gr->gate.dw);
   // dG is transposed once for both halves of dW_g
-  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df, tra, trb);
+  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df, tra, trb, false,
+           reinterpret_cast<float*>(gr->gate.db), part, part2);
   wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, S(A.delta), df, df, df, BL, dwg ? dwg + df : nullptr, 2 * df, tra,
            trb, dwg != nullptr);
-  colsum<T>(run, "bias_colsum", WT(W.dg), BL, df, df, part, reinterpret_cast<float*>(gr->gate.db));
 
   // 2. decompression levels 1..M (reverse of Eq. 17)
   const T* dT = WT(W.ddelta);  // dU_0 = dDelta
@@ -354,8 +453,8 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
     const int dn = d.d[j + 1];
     const T* u_in = j == d.M - 1 ? S(A.s) : S(A.u[j + 1]);
     wgrad<T>(run, "decompress_wgrad_gemm", dT, kd, u_in, dn, kd, dn, rows,
-             reinterpret_cast<float*>(gr->decompress[j].dw), dn, tra, trb);
-    colsum<T>(run, "bias_colsum", dT, rows, kd, kd, part, reinterpret_cast<float*>(gr->decompress[j].db));
+             reinterpret_cast<float*>(gr->decompress[j].dw), dn, tra, trb, false,
+             reinterpret_cast<float*>(gr->decompress[j].db), part, part2);
     if (j == d.M - 1) {
       dgrad<T>(run, "decompress_dgrad_gemm", dT, kd, w->decompress[j].w, dn, rows, dn, kd,
                EpiUnshift<T>{WT(W.dhbar), (int)d.m, dp, cfg->mask == PF_TOKEN_CAUSAL ? 1 : 0}, trw);
@@ -374,8 +473,7 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   dgrad<T>(run, "o_dgrad_gemm", WT(W.dhbar), dp, w->o.w, dp, Bm, dp, dp,
            EpiHeads<T>{WT(W.dO), WT(W.dOt), nullptr, (int)d.m, d.dh, d.nh, d.ld_t}, trw);
   wgrad<T>(run, "o_wgrad_gemm", WT(W.dhbar), dp, S(A.o), dp, dp, dp, Bm, reinterpret_cast<float*>(gr->o.dw), dp, tra,
-           trb);
-  colsum<T>(run, "bias_colsum", WT(W.dhbar), Bm, dp, dp, part, reinterpret_cast<float*>(gr->o.db));
+           trb, false, reinterpret_cast<float*>(gr->o.db), part, part2);
 
   // 4. attention (Eq. 9)
   AttnBwdParams ap{};
@@ -408,8 +506,7 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   const pf_linear_grad* grads[3] = {&gr->q, &gr->k, &gr->v};
   for (int i = 0; i < 3; ++i) {
     wgrad<T>(run, "qkv_wgrad_gemm", dqkv[i], dp, S(A.h), dp, dp, dp, Bm, reinterpret_cast<float*>(grads[i]->dw), dp,
-             tra, trb);
-    colsum<T>(run, "bias_colsum", dqkv[i], Bm, dp, dp, part, reinterpret_cast<float*>(grads[i]->db));
+             tra, trb, false, reinterpret_cast<float*>(grads[i]->db), part, part2);
   }
   for (int i = 0; i < 3; ++i) {
     EpiAccum<T> e{WF(W.dh32), dp, reinterpret_cast<const T*>(dh_out), i == 0, i == 2 ? WT(W.dh) : nullptr,
@@ -425,8 +522,8 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
     const int dn = d.d[j + 1];
     const T* v_in = j == 0 ? xp : S(A.z[j]);
     wgrad<T>(run, "compress_wgrad_gemm", dz, dn, v_in, kd, dn, kd, rows,
-             reinterpret_cast<float*>(gr->compress[j].dw), kd, tra, trb);
-    colsum<T>(run, "bias_colsum", dz, rows, dn, dn, part, reinterpret_cast<float*>(gr->compress[j].db));
+             reinterpret_cast<float*>(gr->compress[j].dw), kd, tra, trb, false,
+             reinterpret_cast<float*>(gr->compress[j].db), part, part2);
     if (j == 0) {
       dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
                EpiAccum<T>{WF(W.dx32), kd, nullptr, 0, reinterpret_cast<T*>(dx), nullptr}, trw);

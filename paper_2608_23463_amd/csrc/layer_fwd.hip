@@ -147,7 +147,20 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     // widest bias: max over every linear map's output width
     int64_t widest = std::max<int64_t>(2 * d.d_f, d.d_p);
     for (int j = 0; j < d.M; ++j) widest = std::max<int64_t>(widest, (int64_t)d.k[j] * d.d[j]);
-    w.colsum = take((size_t)kColsumChunks * widest * 4);
+    // bias-gradient partials: kColsumChunks row chunks, or one per 64 rows
+    // when the column sums come out of a transpose
+    size_t part = (size_t)kColsumChunks * widest;
+    auto tp = [&](int64_t rows, int64_t cols) {
+      if (rows >= kTransposeMinRows) part = std::max(part, (size_t)((rows + 63) / 64 * cols));
+    };
+    tp((int64_t)d.B * d.L, d.d_f);
+    for (int j = 0; j < d.M; ++j) {
+      tp((int64_t)d.B * d.R[j + 1], (int64_t)d.k[j] * d.d[j]);
+      tp((int64_t)d.B * d.R[j + 1], d.d[j + 1]);
+    }
+    tp((int64_t)d.B * d.m, d.d_p);
+    w.colsum = take(part * 4);
+    w.colsum2 = take((size_t)64 * widest * 4);
     // transposed operands: every large gradient / activation operand is at
     // most [B*L, d_f] elements (plus row padding to a multiple of 8)
     size_t tr = 0, trw = 0;
