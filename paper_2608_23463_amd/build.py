@@ -28,9 +28,11 @@ HIPCC_FLAGS = [
 
 # Per-file additions. The attention kernels read and rescale their MFMA
 # results with ordinary VALU code; keeping MFMA destinations in VGPRs avoids a
-# v_accvgpr move for every score.
+# v_accvgpr move for every score (and, in the backward, copies of the
+# gradient accumulators between register files on every tile).
 FILE_FLAGS = {
     "attention_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "attention_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 
