@@ -36,7 +36,7 @@ DECODE_WORKLOAD = "decode_bf16_B32_n16k"
 TRAIN_WORKLOAD = "layer_bf16_L256k_d2048_f8x8"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
-CPU_SAMPLE_TOKENS = 65536
+CPU_SAMPLE_TOKENS = 393216
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_bf16_L1M_d1024_decode_bf16_B32_n16k.txt")
 KERNEL_SOURCES = ["paper_2608_23463_amd/csrc/gemm.hpp", "paper_2608_23463_amd/csrc/epilogues.hpp",
                   "paper_2608_23463_amd/csrc/common.hpp", "paper_2608_23463_amd/csrc/attention.hpp",
