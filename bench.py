@@ -15,6 +15,9 @@ Extra objects on the same line:
                block-triggered appends
   train        forward (saving activations) + backward tokens/s on the
                factorised workload (L = 262,144, d = 2048, 16 x 128, P = 8 x 8)
+  lm           the paper's language-model shape: layer forward tokens/s at
+               L = 1M with a 64-wide local stream and a 512-wide proxy stream
+               (8 x 64, P = 64), and decode tokens/s at d_model = 512
   cpu_baseline the CPU oracle timed on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -34,6 +37,8 @@ METRIC = "ProxyFormer layer fwd tokens/sec at L=1M, P=64; proxy-KV decode tokens
 LAYER_WORKLOAD = "layer_bf16_L1M_d1024"
 DECODE_WORKLOAD = "decode_bf16_B32_n16k"
 TRAIN_WORKLOAD = "layer_bf16_L256k_d2048_f8x8"
+LM_LAYER_WORKLOAD = "layer_bf16_L1M_lm_df64_dp512"
+LM_DECODE_WORKLOAD = "decode_bf16_B32_n16k_lm_d512"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 CPU_SAMPLE_TOKENS = 393216
@@ -112,14 +117,16 @@ def dev_weights(w, dt):
     return out
 
 
-def bench_layer(steps, warmup):
+def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     import torch
     from paper_2608_23463_amd import binding as B
     from paper_2608_23463_amd import synth
-    shape = synth.WORKLOADS[LAYER_WORKLOAD]
-    log(f"generating {LAYER_WORKLOAD} inputs")
-    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[LAYER_WORKLOAD])
-    sample = {"x": inp["x"][:, :CPU_SAMPLE_TOKENS].copy(), "weights": inp["weights"]}
+    shape = synth.WORKLOADS[workload]
+    log(f"generating {workload} inputs")
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[workload])
+    sample = None
+    if workload == LAYER_WORKLOAD:
+        sample = {"x": inp["x"][:, :CPU_SAMPLE_TOKENS].copy(), "weights": inp["weights"]}
     x = to_dev(inp["x"], shape.dtype)
     del inp["x"]
     w = dev_weights(inp["weights"], shape.dtype)
@@ -166,7 +173,8 @@ def bench_layer(steps, warmup):
     dom = max((k for k in tr if k in flops), key=lambda k: tr[k][1])
     dom_ms = tr[dom][1] / tr[dom][0]
     achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
-    traffic = measured_traffic(dom)
+    # the committed counter summary covers the headline workload only
+    traffic = measured_traffic(dom) if workload == LAYER_WORKLOAD else None
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
@@ -175,14 +183,14 @@ def bench_layer(steps, warmup):
     return shape, ms, kernels, roof, sample
 
 
-def bench_decode():
+def bench_decode(workload=DECODE_WORKLOAD):
     import numpy as np
     import torch
     from paper_2608_23463_amd import binding as B
     from paper_2608_23463_amd import synth
-    shape = synth.WORKLOADS[DECODE_WORKLOAD]
-    log(f"generating {DECODE_WORKLOAD} inputs")
-    inp = synth.decode_inputs(shape, synth.WORKLOAD_SEEDS[DECODE_WORKLOAD])
+    shape = synth.WORKLOADS[workload]
+    log(f"generating {workload} inputs")
+    inp = synth.decode_inputs(shape, synth.WORKLOAD_SEEDS[workload])
     cfg = B.decode_config(shape.batch, shape.d_model, shape.n_heads, shape.head_dim, shape.factors,
                           shape.level_dims, shape.dtype, shape.rms_eps)
     kc = to_dev(inp.pop("k_cache"), shape.dtype)
@@ -216,7 +224,7 @@ def bench_decode():
     attn = tr.get("decode_attn")
     out = {"metric": "proxy-KV decode tokens/s", "value": round(shape.batch * shape.steps / (ms * 1e-3), 1),
            "unit": "tokens/s", "ms_total": round(ms, 3), "ms_per_step": round(ms / shape.steps, 4),
-           "workload": DECODE_WORKLOAD, "batch": shape.batch, "cached_rows": shape.n0, "steps": shape.steps,
+           "workload": workload, "batch": shape.batch, "cached_rows": shape.n0, "steps": shape.steps,
            "appends": shape.steps // shape.block}
     if attn:
         avg = attn[1] / attn[0]
@@ -226,7 +234,8 @@ def bench_decode():
         gbs = nbytes / (avg * 1e-3) / 1e9
         out["roofline"] = {"kernel": "decode_attn", "bound": "hbm", "achieved": round(gbs, 1),
                            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                           "traffic": measured_traffic("decode_attn"), "avg_ms": round(avg, 4),
+                           "traffic": measured_traffic("decode_attn") if workload == DECODE_WORKLOAD else None,
+                           "avg_ms": round(avg, 4),
                            "work_per_launch": nbytes}
         # the whole step (projections, merge and output map included) against HBM
         step_gbs = nbytes / (ms / shape.steps * 1e-3) / 1e9
@@ -375,6 +384,7 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-train", action="store_true")
+    ap.add_argument("--no-lm", action="store_true")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only the short dispatch sequence used for counter runs (prints no JSON)")
     args = ap.parse_args()
@@ -417,6 +427,15 @@ def main():
         result["decode"] = bench_decode()
     if not args.no_train:
         result["train"] = bench_train(max(1, min(args.steps, 5)))
+    if not args.no_lm:
+        lshape, lms, lkernels, lroof, _ = bench_layer(args.steps, args.warmup, LM_LAYER_WORKLOAD)
+        result["lm"] = {"metric": "layer fwd tokens/s (language-model shape)",
+                        "value": round(lshape.seq_len * lshape.batch / (lms * 1e-3), 1), "unit": "tokens/s",
+                        "ms_per_step": round(lms, 4), "workload": LM_LAYER_WORKLOAD, "d_fine": lshape.d_fine,
+                        "d_proxy": lshape.d_proxy, "n_heads": lshape.n_heads, "roofline": lroof,
+                        "kernels": lkernels}
+        if not args.no_decode:
+            result["lm"]["decode"] = bench_decode(LM_DECODE_WORKLOAD)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(shape, sample)
     print(json.dumps(result), flush=True)

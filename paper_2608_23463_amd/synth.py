@@ -118,14 +118,20 @@ class DecodeShape:
         return [self.d_model] + lv
 
 
-# The five workloads: a small fp32 correctness layer, two bf16 layers at
-# 64K and 1M tokens, a factorised forward+backward layer and the decode run.
+# The workloads: a small fp32 correctness layer, two bf16 layers at 64K and
+# 1M tokens, a factorised forward+backward layer, the decode run, and the
+# language-model shape (layer and decode).
 WORKLOADS = {
     "layer_fp32_L4k_d256": LayerShape(1, 4096, 256, 256, 4, 64, (64,), dtype="fp32"),
     "layer_bf16_L64k_d1024": LayerShape(1, 65536, 1024, 1024, 16, 64, (64,)),
     "layer_bf16_L1M_d1024": LayerShape(1, 1 << 20, 1024, 1024, 16, 64, (64,)),
     "layer_bf16_L256k_d2048_f8x8": LayerShape(1, 1 << 18, 2048, 2048, 16, 128, (8, 8)),
     "decode_bf16_B32_n16k": DecodeShape(32, 1024, 16, 64, (64,), n0=16384, steps=256),
+    # The paper's language-model shape (Sec. 3.2, Sec. 5.1): a 64-wide history
+    # stream compressed into a 512-wide proxy stream (8 heads x 64, P = 64),
+    # and the generation side decoding 512-wide tokens against that cache.
+    "layer_bf16_L1M_lm_df64_dp512": LayerShape(1, 1 << 20, 64, 512, 8, 64, (64,)),
+    "decode_bf16_B32_n16k_lm_d512": DecodeShape(32, 512, 8, 64, (64,), n0=16384, steps=256),
 }
 WORKLOAD_SEEDS = {name: 20260000 + i + 1 for i, name in enumerate(WORKLOADS)}
 

@@ -78,6 +78,9 @@ CASES = {
     "bf16_tc_ragged": (LayerShape(2, 16 * 37, 192, 192, 3, 64, (16,)), True),
     "bf16_tc_factorised": (LayerShape(1, 64 * 70, 128, 256, 2, 128, (8, 8), level_dims=(160,)), True),
     "bf16_bi": (LayerShape(1, 16 * 130, 128, 256, 4, 64, (16,), mask=synth.BIDIRECTIONAL), False),
+    # the language-model shape (64-wide local stream, 512-wide proxies, 8 x 64, P = 64) over
+    # 10,240 tokens: 160 proxies, and enough token rows for the transposed weight-gradient path
+    "bf16_lm_shape": (LayerShape(1, 64 * 160, 64, 512, 8, 64, (64,)), True),
 }
 
 

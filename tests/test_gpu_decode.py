@@ -65,6 +65,7 @@ CASES = {
     "bf16_empty_cache": DecodeShape(2, 128, 2, 64, (8,), n0=0, steps=20),
     "bf16_dh128_factorised": DecodeShape(2, 256, 2, 128, (2, 4), level_dims=(192,), n0=3000, steps=17),
     "bf16_many_splits": DecodeShape(4, 512, 8, 64, (16,), n0=5000, steps=33),
+    "bf16_lm_shape": DecodeShape(3, 512, 8, 64, (64,), n0=1100, steps=70),
 }
 
 
@@ -76,8 +77,8 @@ def test_decode_parity_small(gpu, name):
     run_and_compare(shape, inp, label=name)
 
 
-def test_decode_parity_full_workload_sampled(gpu):
-    name = "decode_bf16_B32_n16k"
+@pytest.mark.parametrize("name", ["decode_bf16_B32_n16k", "decode_bf16_B32_n16k_lm_d512"])
+def test_decode_parity_full_workload_sampled(gpu, name):
     shape = synth.WORKLOADS[name]
     print(f"[workload {name}] generating inputs", flush=True)
     inp = synth.decode_inputs(shape, synth.WORKLOAD_SEEDS[name])

@@ -70,9 +70,9 @@ def test_forward_parity_workload(gpu, name):
     assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
 
 
-def test_forward_parity_L1M_sampled(gpu):
-    """Full-size 1M-token layer: every proxy, and 64 sampled blocks of X_out."""
-    name = "layer_bf16_L1M_d1024"
+@pytest.mark.parametrize("name", ["layer_bf16_L1M_d1024", "layer_bf16_L1M_lm_df64_dp512"])
+def test_forward_parity_L1M_sampled(gpu, name):
+    """Full-size 1M-token layers: every proxy, and 64 sampled blocks of X_out."""
     shape = synth.WORKLOADS[name]
     print(f"[workload {name}] generating inputs", flush=True)
     inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
