@@ -56,6 +56,12 @@ enum pf_dtype { PF_FP32 = 0, PF_BF16 = 1 };
  * PF_BIDIRECTIONAL: block i receives proxy i, mask M = 0 in Eq. 9. */
 enum pf_mask { PF_TOKEN_CAUSAL = 0, PF_BLOCK_CAUSAL = 1, PF_BIDIRECTIONAL = 2 };
 
+/* Local fusion of the decompressed proxy Delta into the local stream (Sec. 3.4):
+ * PF_INJECT_GATED: Y = X + sigmoid([X, Delta] W_g^T + b_g) * Delta (Eq. 12);
+ * PF_INJECT_ADD:   Y = X + Delta (Eq. 11); the gate weights are not read and
+ *   its gradients are not written. */
+enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1 };
+
 typedef struct {
   const void* w; /* [out, in] */
   const void* b; /* [out] or NULL */
@@ -70,7 +76,7 @@ typedef struct {
  *  level_dims[j] = d_{j+1} for j < M-1 (0 -> d_proxy); level_dims[M-1] is
  *            ignored (d_M = d_proxy).
  *  head_dim  64 or 128.
- *  dtype     pf_dtype; mask pf_mask. */
+ *  dtype     pf_dtype; mask pf_mask; injection pf_injection. */
 typedef struct {
   int32_t batch;
   int64_t seq_len;
@@ -79,12 +85,14 @@ typedef struct {
   int32_t factors[PF_MAX_LEVELS];
   int32_t level_dims[PF_MAX_LEVELS];
   int32_t dtype, mask;
+  int32_t injection;
 } pf_layer_config;
 
 /* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)
  * q, k, v, o : W [d_proxy, d_proxy]     (Eq. 9 and its output map)
  * decompress[j]: W [k_{j+1} d_j, d_{j+1}] (Eq. 10, Eq. 17)
- * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12) */
+ * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12); unused
+ *              with PF_INJECT_ADD (may be NULL) */
 typedef struct {
   pf_linear compress[PF_MAX_LEVELS];
   pf_linear q, k, v, o;

@@ -18,7 +18,7 @@ Every function states the passage it follows. Readings of points the paper
 leaves open are listed in the module docstrings where they apply.
 """
 from .layer import (  # noqa: F401
-    TOKEN_CAUSAL, BLOCK_CAUSAL, BIDIRECTIONAL,
+    TOKEN_CAUSAL, BLOCK_CAUSAL, BIDIRECTIONAL, INJECT_GATED, INJECT_ADD,
     sigmoid, compress, layer_forward, layer_backward, attention_rows,
     proxies_and_attention_inputs,
 )

@@ -40,6 +40,10 @@ TOKEN_CAUSAL = 0
 BLOCK_CAUSAL = 1
 BIDIRECTIONAL = 2
 
+# local fusion of Delta into X (Sec. 3.4)
+INJECT_GATED = 0  # Eq. 12
+INJECT_ADD = 1    # Eq. 11
+
 _ROW_CHUNK = 512  # query rows per chunk; rows are independent (Eq. 9)
 
 
@@ -170,14 +174,15 @@ def proxies_and_attention_inputs(x, weights, factors, h_in=None):
 def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
                   mask: int = TOKEN_CAUSAL, h_in=None,
                   sample_blocks: Optional[Sequence[int]] = None,
-                  keep: bool = False) -> Dict[str, object]:
+                  keep: bool = False, injection: int = INJECT_GATED) -> Dict[str, object]:
     """One ProxyFormer layer (Algorithm 1) on x [B, L, d_fine].
 
     Steps: partition and compress every block (Eq. 2, 7, 15-16); residual
     proxy update H = H_in + c (Eq. 8); causal multi-head attention over the
     m proxies (Eq. 9) followed by the output map W_o; decompress the proxy
     each block receives (Eq. 10, 17); gated injection
-    Y = X + sigmoid(G) * Delta with G = [X, Delta] W_g^T + b_g (Eq. 12).
+    Y = X + sigmoid(G) * Delta with G = [X, Delta] W_g^T + b_g (Eq. 12),
+    or with INJECT_ADD the residual addition Y = X + Delta (Eq. 11).
 
     Returns x_out [B, L, d_fine] and h_out = H [B, m, d_proxy]. With
     ``sample_blocks`` only those blocks are decompressed and injected
@@ -219,9 +224,13 @@ def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
         s[src >= 0] = hbar_need[pos]
         delta, dinputs = decompress(s, factors, weights["decompress"])
         xb = x[b].reshape(m, p_blk, d_f)[blocks].reshape(-1, d_f)
-        wg, bg = _f64(weights["gate"][0]), _f64(weights["gate"][1])
-        g = xb @ wg[:, :d_f].T + delta @ wg[:, d_f:].T + bg
-        y = xb + sigmoid(g) * delta
+        if injection == INJECT_ADD:
+            g = None
+            y = xb + delta
+        else:
+            wg, bg = _f64(weights["gate"][0]), _f64(weights["gate"][1])
+            g = xb @ wg[:, :d_f].T + delta @ wg[:, d_f:].T + bg
+            y = xb + sigmoid(g) * delta
         if sample_blocks is None:
             x_out[b] = y
             lse_full = np.zeros((n_heads, m))
@@ -276,7 +285,8 @@ def _attention_backward(q, k, v, o, do, n_heads, mask):
 
 
 def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
-                   mask: int = TOKEN_CAUSAL, h_in=None, dh_out=None) -> Dict[str, object]:
+                   mask: int = TOKEN_CAUSAL, h_in=None, dh_out=None,
+                   injection: int = INJECT_GATED) -> Dict[str, object]:
     """Gradients of the layer forward (chain rule of Eq. 7-17 as read above).
 
     Given dY = dL/dX_out [B, L, d_fine] and optionally dH_out [B, m, d_proxy],
@@ -284,7 +294,7 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
     summed over the batch in the layout of the weights, and the gradients of
     the projections Q, K, V per proxy ("proj_grads", [B, m, d_proxy] each).
     """
-    fwd = layer_forward(x, weights, factors, n_heads, mask, h_in, keep=True)
+    fwd = layer_forward(x, weights, factors, n_heads, mask, h_in, keep=True, injection=injection)
     dy = _f64(dy)
     bsz, seq, d_f = dy.shape
     p_blk = int(np.prod(factors))
@@ -299,22 +309,27 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
           "q": zgrad(weights["q"]), "k": zgrad(weights["k"]), "v": zgrad(weights["v"]),
           "o": zgrad(weights["o"]),
           "decompress": [zgrad(w) for w in weights["decompress"]],
-          "gate": zgrad(weights["gate"])}
+          "gate": zgrad(weights["gate"]) if injection == INJECT_GATED else None}
     dx = np.zeros_like(dy)
     d_p = weights["q"][0].shape[0]
     dh_in = None if h_in is None else np.zeros((bsz, m, d_p))
     proj_grads = {name: np.zeros((bsz, m, d_p)) for name in ("q", "k", "v")}
-    wg = _f64(weights["gate"][0])
     for b in range(bsz):
         kp = fwd["kept"][b]
         xb, delta, g = kp["x"], kp["delta"], kp["g"]
-        sg = sigmoid(g)
-        # Eq. 12: Y = X + sigmoid(G) * Delta, G = X W_gx^T + Delta W_gd^T + b_g
-        dg = dy[b] * delta * sg * (1.0 - sg)
-        ddelta = dy[b] * sg + dg @ wg[:, d_f:]
-        dxb = dy[b] + dg @ wg[:, :d_f]
-        gr["gate"][0] += dg.T @ np.concatenate([xb, delta], axis=1)
-        gr["gate"][1] += dg.sum(axis=0)
+        if injection == INJECT_ADD:
+            # Eq. 11: Y = X + Delta
+            ddelta = dy[b]
+            dxb = dy[b]
+        else:
+            wg = _f64(weights["gate"][0])
+            sg = sigmoid(g)
+            # Eq. 12: Y = X + sigmoid(G) * Delta, G = X W_gx^T + Delta W_gd^T + b_g
+            dg = dy[b] * delta * sg * (1.0 - sg)
+            ddelta = dy[b] * sg + dg @ wg[:, d_f:]
+            dxb = dy[b] + dg @ wg[:, :d_f]
+            gr["gate"][0] += dg.T @ np.concatenate([xb, delta], axis=1)
+            gr["gate"][1] += dg.sum(axis=0)
         # Eq. 17 in reverse: level j = 1..M (the forward ran M..1)
         du = ddelta
         for j in range(nlev):

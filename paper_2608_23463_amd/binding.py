@@ -22,6 +22,8 @@ PF_ERR_WORKSPACE = -4
 PF_ERR_HIP = -5
 PF_FP32 = 0
 PF_BF16 = 1
+PF_INJECT_GATED = 0
+PF_INJECT_ADD = 1
 
 EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
@@ -44,7 +46,7 @@ class PfLayerConfig(ctypes.Structure):
     _fields_ = [("batch", c_int32), ("seq_len", c_int64), ("d_fine", c_int32), ("d_proxy", c_int32),
                 ("n_heads", c_int32), ("head_dim", c_int32), ("n_levels", c_int32),
                 ("factors", c_int32 * MAX_LEVELS), ("level_dims", c_int32 * MAX_LEVELS),
-                ("dtype", c_int32), ("mask", c_int32)]
+                ("dtype", c_int32), ("mask", c_int32), ("injection", c_int32)]
 
 
 class PfLayerWeights(ctypes.Structure):
@@ -181,7 +183,7 @@ def _stream(stream) -> Optional[int]:
 
 def layer_config(batch: int, seq_len: int, d_fine: int, d_proxy: int, n_heads: int, head_dim: int,
                  factors: Sequence[int], level_dims: Sequence[int] = (), dtype: str = "bf16",
-                 mask: int = 0) -> PfLayerConfig:
+                 mask: int = 0, injection: int = 0) -> PfLayerConfig:
     c = PfLayerConfig()
     c.batch = batch
     c.seq_len = seq_len
@@ -196,6 +198,7 @@ def layer_config(batch: int, seq_len: int, d_fine: int, d_proxy: int, n_heads: i
         c.level_dims[i] = v
     c.dtype = PF_BF16 if dtype == "bf16" else PF_FP32
     c.mask = mask
+    c.injection = injection
     return c
 
 
@@ -203,10 +206,13 @@ def config_from_shape(shape) -> PfLayerConfig:
     """PfLayerConfig of a synth.LayerShape."""
     dims = list(shape.level_dims) if shape.level_dims else []
     return layer_config(shape.batch, shape.seq_len, shape.d_fine, shape.d_proxy, shape.n_heads,
-                        shape.head_dim, shape.factors, dims, shape.dtype, shape.mask)
+                        shape.head_dim, shape.factors, dims, shape.dtype, shape.mask,
+                        getattr(shape, "injection", 0))
 
 
 def _lin(pair) -> PfLinear:
+    if pair is None:
+        return PfLinear(None, None)
     w, b = pair
     return PfLinear(_ptr(w), _ptr(b))
 
@@ -219,7 +225,7 @@ def layer_weights(w: Dict[str, object]) -> PfLayerWeights:
     for i, pair in enumerate(w["decompress"]):
         s.decompress[i] = _lin(pair)
     for name in ("q", "k", "v", "o", "gate"):
-        setattr(s, name, _lin(w[name]))
+        setattr(s, name, _lin(w.get(name)))
     return s
 
 
@@ -269,6 +275,8 @@ def layer_grads(g: Dict[str, object]) -> PfLayerGrads:
     s = PfLayerGrads()
 
     def lg(pair):
+        if pair is None:
+            return PfLinearGrad(None, None)
         dw, db = pair
         return PfLinearGrad(_ptr(dw), _ptr(db))
 
@@ -277,7 +285,7 @@ def layer_grads(g: Dict[str, object]) -> PfLayerGrads:
     for i, pair in enumerate(g["decompress"]):
         s.decompress[i] = lg(pair)
     for name in ("q", "k", "v", "o", "gate"):
-        setattr(s, name, lg(g[name]))
+        setattr(s, name, lg(g.get(name)))
     return s
 
 
@@ -296,8 +304,10 @@ def layer_backward(cfg: PfLayerConfig, weights: Dict[str, object], x, h_in, save
 
     grads = {"compress": [g_like(p) for p in weights["compress"]],
              "decompress": [g_like(p) for p in weights["decompress"]]}
-    for name in ("q", "k", "v", "o", "gate"):
+    for name in ("q", "k", "v", "o"):
         grads[name] = g_like(weights[name])
+    # the gate is only read (and differentiated) by gated injection
+    grads["gate"] = g_like(weights["gate"]) if cfg.injection == PF_INJECT_GATED else None
     if workspace is None:
         workspace = _bytes(layer_workspace_size(cfg, True), dev)
     _check(load().proxy_layer_backward(ctypes.byref(cfg), ctypes.byref(layer_weights(weights)), _ptr(x),

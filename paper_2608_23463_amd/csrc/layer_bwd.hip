@@ -4,6 +4,7 @@
 //  1. gate: dG = dY * Delta * s(1 - s) with s = sigmoid(G) (elementwise), then
 //     one GEMM [dG W_gx | dG W_gd] whose epilogue forms dX = dY + dG W_gx (fp32
 //     accumulator) and dDelta = s * dY + dG W_gd; dW_g = dG^T [X, Delta].
+//     With residual-add injection (Eq. 11) dDelta = dY and dX starts at dY.
 //  2. decompression levels 1..M (reverse of Eq. 17): dW_dj = dT^T U_j,
 //     dU_j = dT W_dj; the top level's epilogue undoes the token-causal shift.
 //  3. output map: dO = dHbar W_o (written per head in both layouts for the
@@ -428,25 +429,28 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   const T* dyp = reinterpret_cast<const T*>(dy);
   const T* xp = reinterpret_cast<const T*>(x);
 
-  // 1. gate (Eq. 12)
-  run.launch("gate_bwd_prep", [&] {
-    const int64_t n8 = BL * df / 8;
-    const int blocks = (int)std::min<int64_t>((n8 + 255) / 256, 16384);
-    hipLaunchKernelGGL((gate_bwd_prep_kernel<T>), dim3(blocks), dim3(256), 0, run.stream, dyp, S(A.delta), S(A.g),
-                       WT(W.dg), n8);
-    return hipGetLastError();
-  });
-  dgrad<T>(run, "gate_dgrad_gemm", WT(W.dg), df, w->gate.w, 2 * df, BL, 2 * df, df,
-           EpiGateDgrad<T>{dyp, S(A.g), WF(W.dx32), WT(W.ddelta), df}, trw);
-  float* dwg = reinterpret_cast<float*>(gr->gate.dw);
-  // dG is transposed once for both halves of dW_g
-  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df, tra, trb, false,
-           reinterpret_cast<float*>(gr->gate.db), part, part2);
-  wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, S(A.delta), df, df, df, BL, dwg ? dwg + df : nullptr, 2 * df, tra,
-           trb, dwg != nullptr);
+  // 1. injection: gated (Eq. 12) or residual add (Eq. 11: dDelta = dX = dY)
+  const bool add_inject = cfg->injection == PF_INJECT_ADD;
+  if (!add_inject) {
+    run.launch("gate_bwd_prep", [&] {
+      const int64_t n8 = BL * df / 8;
+      const int blocks = (int)std::min<int64_t>((n8 + 255) / 256, 16384);
+      hipLaunchKernelGGL((gate_bwd_prep_kernel<T>), dim3(blocks), dim3(256), 0, run.stream, dyp, S(A.delta), S(A.g),
+                         WT(W.dg), n8);
+      return hipGetLastError();
+    });
+    dgrad<T>(run, "gate_dgrad_gemm", WT(W.dg), df, w->gate.w, 2 * df, BL, 2 * df, df,
+             EpiGateDgrad<T>{dyp, S(A.g), WF(W.dx32), WT(W.ddelta), df}, trw);
+    float* dwg = reinterpret_cast<float*>(gr->gate.dw);
+    // dG is transposed once for both halves of dW_g
+    wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, xp, df, df, df, BL, dwg, 2 * df, tra, trb, false,
+             reinterpret_cast<float*>(gr->gate.db), part, part2);
+    wgrad<T>(run, "gate_wgrad_gemm", WT(W.dg), df, S(A.delta), df, df, df, BL, dwg ? dwg + df : nullptr, 2 * df, tra,
+             trb, dwg != nullptr);
+  }
 
   // 2. decompression levels 1..M (reverse of Eq. 17)
-  const T* dT = WT(W.ddelta);  // dU_0 = dDelta
+  const T* dT = add_inject ? dyp : WT(W.ddelta);  // dU_0 = dDelta
   for (int j = 0; j < d.M; ++j) {
     const int64_t rows = (int64_t)d.B * d.R[j + 1];
     const int kd = d.k[j] * d.d[j];
@@ -525,8 +529,10 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
              reinterpret_cast<float*>(gr->compress[j].dw), kd, tra, trb, false,
              reinterpret_cast<float*>(gr->compress[j].db), part, part2);
     if (j == 0) {
-      dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
-               EpiAccum<T>{WF(W.dx32), kd, nullptr, 0, reinterpret_cast<T*>(dx), nullptr}, trw);
+      // dX = (dY + dG W_gx, in dx32) or dY, plus this level's data gradient
+      EpiAccum<T> e = add_inject ? EpiAccum<T>{WF(W.dx32), kd, dyp, 1, reinterpret_cast<T*>(dx), nullptr}
+                                 : EpiAccum<T>{WF(W.dx32), kd, nullptr, 0, reinterpret_cast<T*>(dx), nullptr};
+      dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn, e, trw);
     } else {
       dgrad<T>(run, "compress_dgrad_gemm", dz, dn, w->compress[j].w, kd, rows, kd, dn,
                EpiLinear<T>{WT(W.dz[j]), kd, nullptr, nullptr, 0, nullptr}, trw);

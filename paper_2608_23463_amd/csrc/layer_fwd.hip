@@ -42,6 +42,8 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
   if (c->dtype != PF_FP32 && c->dtype != PF_BF16) return *why = "dtype must be PF_FP32 or PF_BF16", PF_ERR_INVALID_ARG;
   if (c->mask < PF_TOKEN_CAUSAL || c->mask > PF_BIDIRECTIONAL) return *why = "unknown mask mode", PF_ERR_INVALID_ARG;
+  if (c->injection != PF_INJECT_GATED && c->injection != PF_INJECT_ADD)
+    return *why = "unknown injection mode", PF_ERR_INVALID_ARG;
   if (c->batch < 1 || c->seq_len < 1) return *why = "batch and seq_len must be >= 1", PF_ERR_INVALID_ARG;
   if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
   if (c->d_fine < 1 || c->d_proxy < 1 || c->n_heads < 1 || c->head_dim < 1)
@@ -318,7 +320,10 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     }
   }
 
-  // 5. decompression, level M down to 1 (Eq. 10, 17)
+  // 5. decompression, level M down to 1 (Eq. 10, 17). With residual-add
+  // injection (Eq. 11) the last level's epilogue adds X and writes Y itself:
+  // its [B R_1, k_1 d_fine] output is X_out byte for byte.
+  const bool add_inject = cfg->injection == PF_INJECT_ADD;
   for (int j = d.M - 1; j >= 0; --j) {
     GemmProblem pr{};
     pr.a = j == d.M - 1 ? P(A.s) : P(A.u[j + 1]);
@@ -328,13 +333,19 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.M = (int)(d.B * d.R[j + 1]);
     pr.N = d.k[j] * d.d[j];
     pr.K = d.d[j + 1];
+    const T* bias = reinterpret_cast<const T*>(w->decompress[j].b);
+    if (j == 0 && add_inject) {
+      EpiLinear<T> e{reinterpret_cast<T*>(x_out), pr.N, bias, reinterpret_cast<const T*>(x), pr.N, nullptr};
+      run.gemm<T, LAYOUT_K, LAYOUT_K>("decompress_gemm", pr, e);
+      continue;
+    }
     T* out = j == 0 ? P(A.delta) : P(A.u[j]);
-    EpiLinear<T> e{out, pr.N, reinterpret_cast<const T*>(w->decompress[j].b), nullptr, 0, nullptr};
+    EpiLinear<T> e{out, pr.N, bias, nullptr, 0, nullptr};
     run.gemm<T, LAYOUT_K, LAYOUT_K>("decompress_gemm", pr, e);
   }
 
   // 6. gated injection (Eq. 12)
-  {
+  if (!add_inject) {
     GemmProblem pr{};
     pr.a = x;
     pr.lda = d.d_f;

@@ -29,6 +29,9 @@ TOKEN_CAUSAL = 0
 BLOCK_CAUSAL = 1
 BIDIRECTIONAL = 2
 
+INJECT_GATED = 0  # Eq. 12
+INJECT_ADD = 1    # Eq. 11
+
 WEIGHT_STD = 0.02
 
 
@@ -46,6 +49,7 @@ class LayerShape:
     level_dims: Tuple[int, ...] = ()  # d_1..d_{M-1}; missing or 0 -> d_proxy
     dtype: str = "bf16"               # "bf16" or "fp32"
     mask: int = TOKEN_CAUSAL
+    injection: int = INJECT_GATED
 
     @property
     def block(self) -> int:

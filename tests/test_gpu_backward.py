@@ -57,6 +57,9 @@ def compare(shape, inp, res, ref, label):
         chk(host(dh_in), ref["dh_in"], "dh_in")
     rg = ref["grads"]
     for name in ("q", "k", "v", "o", "gate"):
+        if rg[name] is None:  # no gate with residual-add injection
+            assert grads[name] is None
+            continue
         chk(host(grads[name][0]), rg[name][0], f"dW_{name}")
         if name == "k":
             scale = float(np.max(np.sum(np.abs(ref["proj_grads"]["k"]), axis=(0, 1))))
@@ -81,6 +84,11 @@ CASES = {
     # the language-model shape (64-wide local stream, 512-wide proxies, 8 x 64, P = 64) over
     # 10,240 tokens: 160 proxies, and enough token rows for the transposed weight-gradient path
     "bf16_lm_shape": (LayerShape(1, 64 * 160, 64, 512, 8, 64, (64,)), True),
+    # residual-add injection (Eq. 11); level 1 groups pairs of 16,384 tokens, so its weight
+    # gradients (8,192 rows) take the transposed path with column sums from the transpose
+    "bf16_inject_add": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_ADD), True),
+    "fp32_inject_add_factorised": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
+                                              injection=synth.INJECT_ADD), False),
 }
 
 
@@ -101,7 +109,7 @@ def test_backward_parity_small(gpu, name):
             dh_out = synth.bf16_round(dh_out)
     res = run_gpu_backward(shape, inp, dh_out)
     ref = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask,
-                                inp["h_in"], dh_out)
+                                inp["h_in"], dh_out, injection=shape.injection)
     compare(shape, inp, res, ref, name)
 
 

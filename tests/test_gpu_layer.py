@@ -28,6 +28,10 @@ SMALL = {
     "bf16_dfine_ne_dproxy": (LayerShape(1, 64 * 300, 64, 512, 8, 64, (64,)), False),
     "bf16_single_block": (LayerShape(1, 64, 128, 128, 2, 64, (64,)), False),
     "bf16_block1": (LayerShape(1, 200, 64, 128, 2, 64, (1,)), False),
+    # residual-add injection (Eq. 11): the decompression epilogue writes Y = X + Delta
+    "bf16_inject_add": (LayerShape(2, 37 * 16, 192, 192, 3, 64, (16,), injection=synth.INJECT_ADD), True),
+    "fp32_inject_add_factorised": (LayerShape(1, 8 * 40, 64, 128, 1, 128, (2, 4), level_dims=(48,), dtype="fp32",
+                                              injection=synth.INJECT_ADD), False),
 }
 
 
@@ -54,7 +58,8 @@ def test_forward_parity_small(gpu, name):
         wq, bq = inp["weights"][key]
         inp["weights"][key] = (synth.bf16_round(wq * 4) if shape.dtype == "bf16" else wq * 4, bq)
     x_out, h_out = run_gpu(shape, inp)
-    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask, inp["h_in"])
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask, inp["h_in"],
+                               injection=shape.injection)
     assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
     assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
 

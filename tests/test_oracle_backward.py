@@ -12,8 +12,8 @@ import oracle
 from test_oracle_layer import rand_weights
 
 
-def _loss(x, w, factors, nh, mask, h_in, dy, dh):
-    r = oracle.layer_forward(x, w, factors, nh, mask, h_in)
+def _loss(x, w, factors, nh, mask, h_in, dy, dh, injection=oracle.INJECT_GATED):
+    r = oracle.layer_forward(x, w, factors, nh, mask, h_in, injection=injection)
     val = float(np.sum(r["x_out"] * dy))
     if dh is not None:
         val += float(np.sum(r["h_out"] * dh))
@@ -23,6 +23,8 @@ def _loss(x, w, factors, nh, mask, h_in, dy, dh):
 def _param_paths(w):
     paths = []
     for name in ("q", "k", "v", "o", "gate"):
+        if name not in w:
+            continue
         paths += [((name, 0),), ((name, 1),)]
     for lvl in range(len(w["compress"])):
         paths += [("compress", (lvl, 0)), ("compress", (lvl, 1))]
@@ -98,6 +100,42 @@ def test_backward_finite_differences(mask, factors):
         v = rng.standard_normal(p0.shape)
         num = fd(_loss(x, _set(w, path, p0 + eps * v), factors, nh, mask, h_in, dy, dh),
                  _loss(x, _set(w, path, p0 - eps * v), factors, nh, mask, h_in, dy, dh))
+        ana = float(np.sum(_grad_of(res["grads"], path) * v))
+        assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (path, num, ana)
+
+
+@pytest.mark.parametrize("factors", [(4,), (2, 4)])
+def test_backward_finite_differences_residual_add(factors):
+    """Eq. 11 injection: every gradient against central differences (no gate)."""
+    rng = np.random.default_rng(31)
+    d_f, d_p, nh, L, B = 4, 6, 2, 16, 2
+    dims = [d_f] + [5] * (len(factors) - 1) + [d_p]
+    w = rand_weights(rng, d_f, d_p, factors, dims=dims, std=0.4)
+    w.pop("gate")
+    x = rng.standard_normal((B, L, d_f))
+    m = L // int(np.prod(factors))
+    h_in = rng.standard_normal((B, m, d_p))
+    dy = rng.standard_normal((B, L, d_f))
+    dh = rng.standard_normal((B, m, d_p))
+    inj = oracle.INJECT_ADD
+    res = oracle.layer_backward(x, w, factors, nh, dy, oracle.TOKEN_CAUSAL, h_in, dh, injection=inj)
+    assert res["grads"]["gate"] is None
+    eps = 1e-5
+    vx = rng.standard_normal(x.shape)
+    num = (_loss(x + eps * vx, w, factors, nh, 0, h_in, dy, dh, inj) -
+           _loss(x - eps * vx, w, factors, nh, 0, h_in, dy, dh, inj)) / (2 * eps)
+    ana = float(np.sum(res["dx"] * vx))
+    assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (num, ana)
+    vh = rng.standard_normal(h_in.shape)
+    num = (_loss(x, w, factors, nh, 0, h_in + eps * vh, dy, dh, inj) -
+           _loss(x, w, factors, nh, 0, h_in - eps * vh, dy, dh, inj)) / (2 * eps)
+    ana = float(np.sum(res["dh_in"] * vh))
+    assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (num, ana)
+    for path in _param_paths(w):
+        p0 = _get(w, path)
+        v = rng.standard_normal(p0.shape)
+        num = (_loss(x, _set(w, path, p0 + eps * v), factors, nh, 0, h_in, dy, dh, inj) -
+               _loss(x, _set(w, path, p0 - eps * v), factors, nh, 0, h_in, dy, dh, inj)) / (2 * eps)
         ana = float(np.sum(_grad_of(res["grads"], path) * v))
         assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (path, num, ana)
 

@@ -275,6 +275,27 @@ def test_gate_closed_forms_constant_proxy(mask):
                                x[0] + delta / (1 + np.exp(-beta * delta)), rtol=1e-13, atol=1e-13)
 
 
+@pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BLOCK_CAUSAL])
+def test_residual_add_injection_closed_form(mask):
+    """Eq. 11: Y = X + Delta exactly, whatever the gate weights hold."""
+    rng = np.random.default_rng(19)
+    d_f, d_p, P, L = 3, 4, 4, 12
+    s0 = rng.standard_normal(d_p)
+    w = _constant_proxy_weights(rng, d_f, d_p, P, s0)
+    wd, bd = w["decompress"][0]
+    delta_full = (wd @ s0 + bd).reshape(P, d_f)
+    delta_zero = bd.reshape(P, d_f)
+    deltas = [delta_zero if (mask == oracle.TOKEN_CAUSAL and i == 0) else delta_full
+              for i in range(L // P)]
+    x = rng.standard_normal((1, L, d_f))
+    w["gate"] = (rng.standard_normal((d_f, 2 * d_f)), rng.standard_normal(d_f))
+    y = oracle.layer_forward(x, w, (P,), 2, mask, injection=oracle.INJECT_ADD)["x_out"][0]
+    np.testing.assert_allclose(y, x[0] + np.concatenate(deltas, axis=0), rtol=1e-13, atol=1e-13)
+    w.pop("gate")  # the gate is not read in this mode
+    y2 = oracle.layer_forward(x, w, (P,), 2, mask, injection=oracle.INJECT_ADD)["x_out"][0]
+    assert np.array_equal(y, y2)
+
+
 def test_factorised_decompression_constant_proxy():
     """Two-level D of a constant proxy: reverse reshape order of Eq. 17."""
     rng = np.random.default_rng(10)
