@@ -9,6 +9,7 @@ torch.cuda.synchronize() and HIP events on the launch stream.
 Extra objects on the same line:
   kernels      per-kernel average duration from the library's event tracing
                (a second pass over K calls) and achieved TFLOP/s or GB/s
+  variants     the same forward with residual-add injection (Eq. 11)
   roofline     the dominant kernel against the MI355X peak of its bound
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
                rows each, 256 new tokens per sequence including the 4
@@ -175,12 +176,29 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
     # the committed counter summary covers the headline workload only
     traffic = measured_traffic(dom) if workload == LAYER_WORKLOAD else None
+    variants = {}
+    if workload == LAYER_WORKLOAD:
+        # the same inputs with residual-add injection (Eq. 11): no gate GEMM
+        cfg_add = B.config_from_shape(shape)
+        cfg_add.injection = B.PF_INJECT_ADD
+        for _ in range(warmup):
+            B.layer_forward_raw(cfg_add, wst, x, None, x_out, h_out, None, ws)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            B.layer_forward_raw(cfg_add, wst, x, None, x_out, h_out, None, ws)
+        stop.record()
+        torch.cuda.synchronize()
+        ms_add = start.elapsed_time(stop) / steps
+        variants["inject_add"] = {"ms_per_step": round(ms_add, 4),
+                                  "value": round(shape.seq_len * shape.batch / (ms_add * 1e-3), 1),
+                                  "unit": "tokens/s"}
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
     del x, x_out, h_out, ws, w
     torch.cuda.empty_cache()
-    return shape, ms, kernels, roof, sample
+    return shape, ms, kernels, roof, sample, variants
 
 
 def bench_decode(workload=DECODE_WORKLOAD):
@@ -402,7 +420,7 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     B.load()
-    shape, ms, kernels, roof, sample = bench_layer(args.steps, args.warmup)
+    shape, ms, kernels, roof, sample, variants = bench_layer(args.steps, args.warmup)
     result = {
         "metric": METRIC,
         "value": round(shape.seq_len * shape.batch / (ms * 1e-3), 1),
@@ -422,13 +440,14 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": roof,
         "kernels": kernels,
+        "variants": variants,
     }
     if not args.no_decode:
         result["decode"] = bench_decode()
     if not args.no_train:
         result["train"] = bench_train(max(1, min(args.steps, 5)))
     if not args.no_lm:
-        lshape, lms, lkernels, lroof, _ = bench_layer(args.steps, args.warmup, LM_LAYER_WORKLOAD)
+        lshape, lms, lkernels, lroof, _, _ = bench_layer(args.steps, args.warmup, LM_LAYER_WORKLOAD)
         result["lm"] = {"metric": "layer fwd tokens/s (language-model shape)",
                         "value": round(lshape.seq_len * lshape.batch / (lms * 1e-3), 1), "unit": "tokens/s",
                         "ms_per_step": round(lms, 4), "workload": LM_LAYER_WORKLOAD, "d_fine": lshape.d_fine,

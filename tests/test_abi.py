@@ -80,6 +80,7 @@ def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 
     (dict(seq_len=4000), B.PF_ERR_INVALID_ARG),
     (dict(n_heads=8), B.PF_ERR_INVALID_ARG),
     (dict(mask=5), B.PF_ERR_INVALID_ARG),
+    (dict(injection=2), B.PF_ERR_INVALID_ARG),
     (dict(head_dim=32, n_heads=8), B.PF_ERR_UNSUPPORTED),
     (dict(d_fine=100), B.PF_ERR_UNSUPPORTED),
 ])
@@ -99,6 +100,16 @@ def test_forward_rejects_bad_pointers(lib):
     assert _fwd(lib, cfg, _weights_struct(), x=(2 << 32) + 8) == B.PF_ERR_INVALID_ARG  # misaligned
     assert _fwd(lib, cfg, _weights_struct(), ws_bytes=1024) == B.PF_ERR_WORKSPACE
     assert _fwd(lib, cfg, _weights_struct(), ws=None) == B.PF_ERR_WORKSPACE
+
+
+def test_gate_weights_only_required_by_gated_injection(lib):
+    w = _weights_struct(null="gate")
+    assert _fwd(lib, _cfg(), w) == B.PF_ERR_INVALID_ARG
+    assert "gate" in B.last_error()
+    # with residual-add injection a NULL gate passes validation; the call then
+    # stops at the next check (a NULL x), so nothing is launched
+    assert _fwd(lib, _cfg(injection=B.PF_INJECT_ADD), w, x=None) == B.PF_ERR_INVALID_ARG
+    assert "gate" not in B.last_error()
 
 
 def test_backward_rejects_bad_arguments(lib):
