@@ -154,7 +154,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
     const char* sv = sk + S::kKParts * S::kKTile;
     const bool active = !p.causal || kt0 <= qw0 + 31;  // uniform across the wave
     if (active) {
-      // S^T = K Q^T for 64 keys (two 32-key blocks) x this wave's 32 queries
+      // S^T = K Q^T for 64 keys (two 32-key blocks) x this wave's 32 queries.
+      // The matrix phases run at raised wave priority, so the SIMD's other
+      // wave (in its softmax phase) fills the issue slots between MFMAs.
+      __builtin_amdgcn_s_setprio(1);
       f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -186,6 +189,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
           }
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       // online softmax on raw scores; masked entries are -inf
       const bool need_mask = (p.causal && kt0 + S::kKT - 1 > qw0) || kt0 + S::kKT > p.m;
       if (need_mask) {  // wave-uniform; selects, no per-element branches
@@ -225,6 +229,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
           ls[r & 3] += e;
         }
       lrun += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      __builtin_amdgcn_s_setprio(1);
       // O^T += V^T P^T, 16 keys per MFMA
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -264,6 +269,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
     }
   }
 
+  __builtin_amdgcn_s_setprio(0);
   const float ltot = lrun + other_half(lrun);
   if (myq < p.m) {
     const float inv = 1.0f / ltot;
