@@ -10,6 +10,7 @@ Extra objects on the same line:
   kernels      per-kernel average duration from the library's event tracing
                (a second pass over K calls) and achieved TFLOP/s or GB/s
   variants     the same forward with residual-add injection (Eq. 11)
+  ceilings     a 1 GiB device copy (achievable HBM rate) beside the vendor peaks
   roofline     the dominant kernel against the MI355X peak of its bound
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
                rows each, 256 new tokens per sequence including the 4
@@ -170,6 +171,9 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
         ent = {"launches_per_step": per_call, "avg_ms": round(avg, 4)}
         if label in flops:
             ent["tflops"] = round(flops[label] / (avg * 1e-3) / 1e12, 1)
+        hbm = measured_traffic(label) if workload == LAYER_WORKLOAD else None
+        if hbm:  # measured HBM bytes per launch over this run's duration
+            ent["hbm_gbs"] = round(hbm / (avg * 1e-3) / 1e9, 1)
         kernels[label] = ent
     dom = max((k for k in tr if k in flops), key=lambda k: tr[k][1])
     dom_ms = tr[dom][1] / tr[dom][0]
@@ -199,6 +203,29 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     del x, x_out, h_out, ws, w
     torch.cuda.empty_cache()
     return shape, ms, kernels, roof, sample, variants
+
+
+def hbm_copy_ceiling():
+    """Achievable HBM rate on this device: a 1 GiB device-to-device copy
+    (reads and writes 1 GiB), best of five."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(5):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        b.copy_(a)
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop)
+        best = ms if best is None else min(best, ms)
+    del a, b
+    torch.cuda.empty_cache()
+    return round(2 * n / (best * 1e-3) / 1e9, 1)
 
 
 def bench_decode(workload=DECODE_WORKLOAD):
@@ -441,6 +468,8 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "variants": variants,
+        "ceilings": {"hbm_copy_gbs": hbm_copy_ceiling(), "hbm_peak_gbs": PEAK_HBM_GBS,
+                     "mfma_bf16_peak_tflops": PEAK_BF16_TFLOPS},
     }
     if not args.no_decode:
         result["decode"] = bench_decode()

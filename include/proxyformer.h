@@ -174,7 +174,14 @@ typedef struct {
  *  k_cache, v_cache [B, n_heads, n_cap, head_dim]: rows 0..n-1 valid.
  *  x_blk [B, P, d]: inputs of the current block; k_loc, v_loc
  *  [B, n_heads, P, head_dim]: its keys/values; slots 0..j-1 valid.
- * The batch moves in lockstep (one n and one j for all sequences). */
+ * With n_seq = j_seq = NULL the batch moves in lockstep (one n and one j for
+ * all sequences). With both set (host arrays of B entries, batch <= 64) every
+ * sequence keeps its own position: sequence b has n_seq[b] cached rows and
+ * j_seq[b] filled slots, the scalar n and j are ignored, a step advances each
+ * sequence by one token and appends the blocks that complete in it (Sec. 3.8
+ * streams every sequence on its own; ragged batches serve sequences that
+ * started at different times). */
+#define PF_MAX_RAGGED_BATCH 64
 typedef struct {
   void* k_cache;
   void* v_cache;
@@ -183,6 +190,8 @@ typedef struct {
   void* k_loc;
   void* v_loc;
   int32_t j;
+  int64_t* n_seq;  /* host [B] or NULL */
+  int32_t* j_seq;  /* host [B] or NULL */
 } pf_decode_state;
 
 size_t proxy_decode_workspace_size(const pf_decode_config* cfg);
@@ -194,7 +203,8 @@ size_t proxy_decode_workspace_size(const pf_decode_config* cfg);
  * Writes x/k/v of the token into slot j; on success j += 1, and when j
  * reaches P the block is appended (as proxy_cache_append) in the same call,
  * n += 1 and j = 0. A full cache (n == n_cap when the block completes)
- * returns PF_ERR_CAPACITY before any launch. */
+ * returns PF_ERR_CAPACITY before any launch. With per-sequence positions
+ * (n_seq, j_seq) the same holds per sequence. */
 int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w,
                       pf_decode_state* st, const void* x_t, void* y_t,
                       void* workspace, size_t ws_bytes, void* stream);
@@ -202,7 +212,8 @@ int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w,
 /* Append nblk whole blocks to the cache (prefill path and the streaming
  * update of Sec. 3.8): for each block h = C(x_block) (Eq. 7 / 16), then
  * K_p[n] = h W_kp^T + b, V_p[n] = h W_vp^T + b, n += 1 (Eq. 21).
- *  x_blocks [B, nblk * P, d]. PF_ERR_CAPACITY if n + nblk > n_cap. */
+ *  x_blocks [B, nblk * P, d]. PF_ERR_CAPACITY if n + nblk > n_cap. With
+ *  per-sequence positions every sequence b appends at row n_seq[b]. */
 int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w,
                        pf_decode_state* st, const void* x_blocks, int64_t nblk,
                        void* workspace, size_t ws_bytes, void* stream);

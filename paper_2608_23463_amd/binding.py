@@ -78,7 +78,8 @@ class PfDecodeWeights(ctypes.Structure):
 
 class PfDecodeState(ctypes.Structure):
     _fields_ = [("k_cache", c_void_p), ("v_cache", c_void_p), ("n_cap", c_int64), ("n", c_int64),
-                ("x_blk", c_void_p), ("k_loc", c_void_p), ("v_loc", c_void_p), ("j", c_int32)]
+                ("x_blk", c_void_p), ("k_loc", c_void_p), ("v_loc", c_void_p), ("j", c_int32),
+                ("n_seq", ctypes.POINTER(c_int64)), ("j_seq", ctypes.POINTER(c_int32))]
 
 
 _lib = None
@@ -347,10 +348,13 @@ def decode_weights(w: Dict[str, object]) -> PfDecodeWeights:
 
 
 class DecodeSession:
-    """Caller-owned decode state on the device plus the host counters n, j."""
+    """Caller-owned decode state on the device plus the host counters n, j.
+
+    With ``ragged=True`` every sequence keeps its own position: ``n_seq`` and
+    ``j_seq`` (host int64 / int32 arrays of batch entries) replace n and j."""
 
     def __init__(self, cfg: PfDecodeConfig, weights: Dict[str, object], k_cache, v_cache, n: int = 0,
-                 device="cuda"):
+                 device="cuda", ragged: bool = False, n_seq=None, j_seq=None):
         import torch
         self.cfg = cfg
         self.weights = weights            # keeps the device tensors alive
@@ -364,6 +368,14 @@ class DecodeSession:
         self.v_loc = torch.zeros_like(self.k_loc)
         self.state = PfDecodeState(k_cache.data_ptr(), v_cache.data_ptr(), k_cache.shape[2], n,
                                    self.x_blk.data_ptr(), self.k_loc.data_ptr(), self.v_loc.data_ptr(), 0)
+        self.n_seq = self.j_seq = None
+        if ragged:
+            import numpy as np
+            # own copies: the library advances these counters in place
+            self.n_seq = np.array(np.full(cfg.batch, n) if n_seq is None else n_seq, dtype=np.int64, copy=True)
+            self.j_seq = np.array(np.zeros(cfg.batch) if j_seq is None else j_seq, dtype=np.int32, copy=True)
+            self.state.n_seq = self.n_seq.ctypes.data_as(ctypes.POINTER(c_int64))
+            self.state.j_seq = self.j_seq.ctypes.data_as(ctypes.POINTER(c_int32))
         self.workspace = _bytes(int(load().proxy_decode_workspace_size(ctypes.byref(cfg))), device)
 
     @property

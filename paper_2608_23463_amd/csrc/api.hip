@@ -172,9 +172,22 @@ static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weig
   }
   if (!st->k_cache || !st->v_cache || !st->x_blk || !st->k_loc || !st->v_loc)
     return fail(PF_ERR_INVALID_ARG, "a decode state buffer is NULL");
-  if (st->n < 0 || st->n_cap < 0 || st->n > st->n_cap) return fail(PF_ERR_INVALID_ARG, "state n must be in 0..n_cap");
+  if (st->n_cap < 0) return fail(PF_ERR_INVALID_ARG, "state n_cap must be >= 0");
   if (st->n_cap > INT32_MAX) return fail(PF_ERR_UNSUPPORTED, "n_cap above 2^31 - 1");
-  if (st->j < 0 || st->j >= d->P) return fail(PF_ERR_INVALID_ARG, "state j must be in 0..P-1");
+  if ((st->n_seq == nullptr) != (st->j_seq == nullptr))
+    return fail(PF_ERR_INVALID_ARG, "n_seq and j_seq must be both set or both NULL");
+  if (st->n_seq) {
+    if (d->B > PF_MAX_RAGGED_BATCH)
+      return fail(PF_ERR_UNSUPPORTED, "per-sequence positions need batch <= %d", PF_MAX_RAGGED_BATCH);
+    for (int b = 0; b < d->B; ++b) {
+      if (st->n_seq[b] < 0 || st->n_seq[b] > st->n_cap)
+        return fail(PF_ERR_INVALID_ARG, "n_seq[%d] must be in 0..n_cap", b);
+      if (st->j_seq[b] < 0 || st->j_seq[b] >= d->P) return fail(PF_ERR_INVALID_ARG, "j_seq[%d] must be in 0..P-1", b);
+    }
+  } else {
+    if (st->n < 0 || st->n > st->n_cap) return fail(PF_ERR_INVALID_ARG, "state n must be in 0..n_cap");
+    if (st->j < 0 || st->j >= d->P) return fail(PF_ERR_INVALID_ARG, "state j must be in 0..P-1");
+  }
   const DecodeWs W = decode_ws(*d);
   if (!workspace || ws_bytes < W.bytes)
     return fail(PF_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", W.bytes, workspace ? ws_bytes : 0);
@@ -190,16 +203,51 @@ int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, p
   if (!aligned16(x_t) || !aligned16(y_t)) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be 16-byte aligned");
   if (overlaps(x_t, (size_t)d.B * d.d * d.esize, y_t, (size_t)d.B * d.d * d.esize))
     return fail(PF_ERR_INVALID_ARG, "y_t must not alias x_t");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  char* ws = reinterpret_cast<char*>(workspace);
+  DecodePos pos{};
+  if (st->n_seq) {
+    // per-sequence positions: the blocks that complete in this step are
+    // appended together (one pass over the compression weights), each at
+    // its own sequence's row
+    pos.ragged = 1;
+    for (int b = 0; b < d.B; ++b) {
+      pos.n[b] = (int32_t)st->n_seq[b];
+      pos.j[b] = st->j_seq[b];
+      if (st->j_seq[b] + 1 == d.P) {
+        if (st->n_seq[b] + 1 > st->n_cap)
+          return fail(PF_ERR_CAPACITY, "proxy cache of sequence %d full: n = %lld, n_cap = %lld", b,
+                      (long long)st->n_seq[b], (long long)st->n_cap);
+        pos.write |= (uint64_t)1 << b;
+      }
+    }
+    hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, w, *st, pos, x_t, y_t, ws, hs)
+                                : decode_step_run<float>(d, w, *st, pos, x_t, y_t, ws, hs);
+    if (e != hipSuccess) return hip_status(e, "proxy_decode_step launch");
+    if (pos.write) {
+      e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, pos, st->x_blk, 1, ws, hs)
+                       : cache_append_run<float>(d, w, *st, pos, st->x_blk, 1, ws, hs);
+      if (e != hipSuccess) return hip_status(e, "proxy_decode_step append launch");
+    }
+    for (int b = 0; b < d.B; ++b) {
+      if ((pos.write >> b) & 1) {
+        st->n_seq[b] += 1;
+        st->j_seq[b] = 0;
+      } else {
+        st->j_seq[b] += 1;
+      }
+    }
+    return PF_OK;
+  }
   const bool completes = st->j + 1 == d.P;
   if (completes && st->n + 1 > st->n_cap)
     return fail(PF_ERR_CAPACITY, "proxy cache full: n = %lld, n_cap = %lld", (long long)st->n, (long long)st->n_cap);
-  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, w, *st, x_t, y_t, reinterpret_cast<char*>(workspace), hs)
-                              : decode_step_run<float>(d, w, *st, x_t, y_t, reinterpret_cast<char*>(workspace), hs);
+  hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, w, *st, pos, x_t, y_t, ws, hs)
+                              : decode_step_run<float>(d, w, *st, pos, x_t, y_t, ws, hs);
   if (e != hipSuccess) return hip_status(e, "proxy_decode_step launch");
   if (completes) {
-    e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, st->x_blk, 1, reinterpret_cast<char*>(workspace), hs)
-                     : cache_append_run<float>(d, w, *st, st->x_blk, 1, reinterpret_cast<char*>(workspace), hs);
+    e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, pos, st->x_blk, 1, ws, hs)
+                     : cache_append_run<float>(d, w, *st, pos, st->x_blk, 1, ws, hs);
     if (e != hipSuccess) return hip_status(e, "proxy_decode_step append launch");
     st->n += 1;
     st->j = 0;
@@ -218,14 +266,30 @@ int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w, 
   if (nblk == 0) return PF_OK;
   if (!x_blocks) return fail(PF_ERR_INVALID_ARG, "x_blocks is NULL");
   if (!aligned16(x_blocks)) return fail(PF_ERR_INVALID_ARG, "x_blocks must be 16-byte aligned");
-  if (st->n + nblk > st->n_cap)
+  DecodePos pos{};
+  if (st->n_seq) {
+    pos.ragged = 1;
+    for (int b = 0; b < d.B; ++b) {
+      if (st->n_seq[b] + nblk > st->n_cap)
+        return fail(PF_ERR_CAPACITY, "append of %lld blocks overflows the cache of sequence %d (n = %lld, n_cap = %lld)",
+                    (long long)nblk, b, (long long)st->n_seq[b], (long long)st->n_cap);
+      pos.n[b] = (int32_t)st->n_seq[b];
+      pos.write |= (uint64_t)1 << b;
+    }
+  } else if (st->n + nblk > st->n_cap) {
     return fail(PF_ERR_CAPACITY, "append of %lld blocks overflows the cache (n = %lld, n_cap = %lld)",
                 (long long)nblk, (long long)st->n, (long long)st->n_cap);
+  }
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, x_blocks, nblk, reinterpret_cast<char*>(workspace), hs)
-                              : cache_append_run<float>(d, w, *st, x_blocks, nblk, reinterpret_cast<char*>(workspace), hs);
+  char* ws = reinterpret_cast<char*>(workspace);
+  hipError_t e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, pos, x_blocks, nblk, ws, hs)
+                              : cache_append_run<float>(d, w, *st, pos, x_blocks, nblk, ws, hs);
   if (e != hipSuccess) return hip_status(e, "proxy_cache_append launch");
-  st->n += nblk;
+  if (st->n_seq) {
+    for (int b = 0; b < d.B; ++b) st->n_seq[b] += nblk;
+  } else {
+    st->n += nblk;
+  }
   return PF_OK;
 }
 

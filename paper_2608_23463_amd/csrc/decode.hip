@@ -115,7 +115,7 @@ struct DecodeProjParams {
   int width[4];         // output width of each matrix (d, d, d, h; step 3: d)
   int B, d, nh, dh;
   int64_t P;
-  int j;
+  int j;                // local slot of the new token (lockstep)
   float eps;
   void* q;              // [B, d]
   void* k_loc;          // [B, h, P, dh]
@@ -123,6 +123,8 @@ struct DecodeProjParams {
   float* alpha;         // [B, h]
   void* x_blk;          // [B, P, d]
   void* y;              // step 3: [B, d]
+  DecodePos pos;        // per-sequence slots when pos.ragged
+  __device__ __forceinline__ int slot(int b) const { return pos.ragged ? pos.j[b] : j; }
 };
 
 template <typename T>
@@ -223,7 +225,7 @@ __global__ void __launch_bounds__(256) decode_small_gemm_kernel(const DecodeProj
       if (b >= p.B) v = u32x4{0u, 0u, 0u, 0u};
       if constexpr (PROJ) {
         if (blockIdx.x == 0 && b < p.B)  // x into block slot j
-          st16(reinterpret_cast<T*>(p.x_blk) + ((int64_t)b * p.P + p.j) * p.d + c * kV, v);
+          st16(reinterpret_cast<T*>(p.x_blk) + ((int64_t)b * p.P + p.slot(b)) * p.d + c * kV, v);
         const T* xv = reinterpret_cast<const T*>(&v);
         const T* gv = reinterpret_cast<const T*>(&graw[i]);
         T uv[kV];
@@ -283,7 +285,7 @@ __global__ void __launch_bounds__(256) decode_small_gemm_kernel(const DecodeProj
       } else if (seg < 3) {
         T* dst = reinterpret_cast<T*>(seg == 1 ? p.k_loc : p.v_loc);
         const int hd = c / p.dh, e = c - hd * p.dh;
-        dst[(((int64_t)b * p.nh + hd) * p.P + p.j) * p.dh + e] = from_f32<T>(v);
+        dst[(((int64_t)b * p.nh + hd) * p.P + p.slot(b)) * p.dh + e] = from_f32<T>(v);
       } else {
         p.alpha[(int64_t)b * p.nh + c] = sigmoidf(v);
       }
@@ -308,6 +310,7 @@ struct DecodeAttnParams {
   int j;               // local slots 0..j are valid
   int nh, splits, chunk;
   float scale_log2;
+  DecodePos pos;       // per-sequence n and j when pos.ragged
 };
 
 // A[b, h, c] = A_x + alpha * A_h from the partials: cache slices merged in a
@@ -362,12 +365,12 @@ __global__ void __launch_bounds__(256) decode_attn_kernel(const DecodeAttnParams
     base_k = reinterpret_cast<const T*>(p.kc) + (int64_t)bh * p.n_cap * DH;
     base_v = reinterpret_cast<const T*>(p.vc) + (int64_t)bh * p.n_cap * DH;
     r0 = (int64_t)s * p.chunk;
-    r1 = std::min<int64_t>(p.n, r0 + p.chunk);
+    r1 = std::min<int64_t>(p.pos.ragged ? p.pos.n[b] : p.n, r0 + p.chunk);  // empty slices leave m = -inf
   } else {
     base_k = reinterpret_cast<const T*>(p.kl) + (int64_t)bh * p.P * DH;
     base_v = reinterpret_cast<const T*>(p.vl) + (int64_t)bh * p.P * DH;
     r0 = 0;
-    r1 = p.j + 1;
+    r1 = (p.pos.ragged ? p.pos.j[b] : p.j) + 1;
   }
 
   float qv[kVec];
@@ -468,19 +471,28 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(const DecodeAttnPar
 }
 
 // Proxy K/V rows into the cache: row rr = r0 + r is (sequence rr / nblk,
-// block rr % nblk) and lands at cache row n0 + block.
+// block rr % nblk) and lands at cache row n0 + block (per-sequence n and a
+// write mask with ragged positions).
 template <typename T>
 struct EpiCache {
   T* cache;
   const T* bias;
   int64_t n_cap, n0, nblk, r0;
   int nh, dh;
+  DecodePos pos;
+  // cache row of (sequence b, block i), or -1 when the sequence is not written
+  __device__ __forceinline__ int64_t row_of(int64_t b, int64_t i) const {
+    if (!pos.ragged) return n0 + i;
+    return ((pos.write >> b) & 1) ? pos.n[b] + i : -1;
+  }
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     if (bias) v += to_f32(bias[c]);
     const int64_t rr = r0 + r;
     const int64_t b = rr / nblk, i = rr - b * nblk;
+    const int64_t row = row_of(b, i);
+    if (row < 0) return;
     const int hd = c / dh, e = c - hd * dh;
-    cache[(((int64_t)b * nh + hd) * n_cap + n0 + i) * dh + e] = from_f32<T>(v);
+    cache[(((int64_t)b * nh + hd) * n_cap + row) * dh + e] = from_f32<T>(v);
   }
   __device__ __forceinline__ void vec8(int r, int c, const float* v0) const {
     float v[8];
@@ -488,8 +500,10 @@ struct EpiCache {
     for (int e = 0; e < 8; ++e) v[e] = v0[e] + (bias ? to_f32(bias[c + e]) : 0.0f);
     const int64_t rr = r0 + r;
     const int64_t b = rr / nblk, i = rr - b * nblk;
+    const int64_t row = row_of(b, i);
+    if (row < 0) return;
     const int hd = c / dh, e0 = c - hd * dh;
-    store8(cache + (((int64_t)b * nh + hd) * n_cap + n0 + i) * dh + e0, v);
+    store8(cache + (((int64_t)b * nh + hd) * n_cap + row) * dh + e0, v);
   }
 };
 
@@ -497,7 +511,7 @@ struct EpiCache {
 
 template <typename T>
 static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                        const void* x_blocks, int64_t nblk, char* ws) {
+                        const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws) {
   const DecodeWs W = decode_ws_layout(d);
   const int64_t total = (int64_t)d.B * nblk;   // (sequence, block) rows of the [B*nblk, P*d] view
   const int64_t row_elems = d.P * d.d;
@@ -532,7 +546,7 @@ static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weight
       pr.N = d.d;
       pr.K = d.d;
       EpiCache<T> e{reinterpret_cast<T*>(caches[i]), reinterpret_cast<const T*>(maps[i]->b), st.n_cap, st.n, nblk, r0,
-                    d.nh, d.dh};
+                    d.nh, d.dh, pos};
       run.gemm<T, LAYOUT_K, LAYOUT_K>("append_kv_gemm", pr, e);
     }
   }
@@ -584,7 +598,7 @@ static hipError_t launch_small_gemm(dim3 grid, const DecodeProjParams& pp, hipSt
 
 template <typename T>
 static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                      const void* x_t, void* y_t, char* ws) {
+                      const DecodePos& pos, const void* x_t, void* y_t, char* ws) {
   const DecodeWs W = decode_ws_layout(d);
   T* q = reinterpret_cast<T*>(ws + W.q);
   float* alpha = reinterpret_cast<float*>(ws + W.alpha);
@@ -612,14 +626,20 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   pp.v_loc = st.v_loc;
   pp.alpha = alpha;
   pp.x_blk = st.x_blk;
+  pp.pos = pos;
   static_assert(decode_small_gemm_lds<T>(2048 * 2 / sizeof(T)) <= 160 * 1024, "staged rows fit the LDS");
   run.launch("decode_proj", [&] {
     const dim3 grid(3 * d.d / 32 + (d.nh + 31) / 32, rblocks);
     return launch_small_gemm<T, true>(grid, pp, run.stream);
   });
 
+  int64_t n_max = st.n;  // slices cover the longest cache of the batch
+  if (pos.ragged) {
+    n_max = 0;
+    for (int b = 0; b < d.B; ++b) n_max = std::max<int64_t>(n_max, pos.n[b]);
+  }
   int splits, chunk;
-  split_plan(st.n, &splits, &chunk);
+  split_plan(n_max, &splits, &chunk);
   DecodeAttnParams ap{};
   ap.q = q;
   ap.kc = st.k_cache;
@@ -639,6 +659,7 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
   ap.splits = splits;
   ap.chunk = chunk;
   ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  ap.pos = pos;
   run.launch("decode_attn", [&] {
     const dim3 grid(splits + 1, d.B * d.nh);
     if (d.dh == 64)
@@ -678,19 +699,20 @@ static size_t decode_gemm_need(const DecodeDims& d) {
   pf_decode_weights nw{};
   pf_decode_state ns{};
   ns.n_cap = 1;
+  const DecodePos np{};
   for (int rows = 1; rows <= d.append_rows; ++rows) {
     // one append of `rows` blocks of a single sequence exercises every chunk size
     DecodeDims d1 = d;
     d1.B = 1;
     if (d.esize == 2)
-      append_impl<bf16>(dry, d1, &nw, ns, nullptr, rows, nullptr);
+      append_impl<bf16>(dry, d1, &nw, ns, np, nullptr, rows, nullptr);
     else
-      append_impl<float>(dry, d1, &nw, ns, nullptr, rows, nullptr);
+      append_impl<float>(dry, d1, &nw, ns, np, nullptr, rows, nullptr);
   }
   if (d.esize == 2)
-    step_impl<bf16>(dry, d, &nw, ns, nullptr, nullptr, nullptr);
+    step_impl<bf16>(dry, d, &nw, ns, np, nullptr, nullptr, nullptr);
   else
-    step_impl<float>(dry, d, &nw, ns, nullptr, nullptr, nullptr);
+    step_impl<float>(dry, d, &nw, ns, np, nullptr, nullptr, nullptr);
   return dry.gemm_need;
 }
 
@@ -715,29 +737,29 @@ DecodeWs decode_ws(const DecodeDims& d) {
 
 template <typename T>
 hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                           const void* x_t, void* y_t, char* ws, hipStream_t stream) {
+                           const DecodePos& pos, const void* x_t, void* y_t, char* ws, hipStream_t stream) {
   const DecodeWs W = decode_ws_layout(d);
   Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
-  step_impl<T>(run, d, w, st, x_t, y_t, ws);
+  step_impl<T>(run, d, w, st, pos, x_t, y_t, ws);
   return run.err;
 }
 
 template <typename T>
 hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                            const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream) {
+                            const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream) {
   const DecodeWs W = decode_ws_layout(d);
   Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
-  append_impl<T>(run, d, w, st, x_blocks, nblk, ws);
+  append_impl<T>(run, d, w, st, pos, x_blocks, nblk, ws);
   return run.err;
 }
 
 template hipError_t decode_step_run<bf16>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                          const void*, void*, char*, hipStream_t);
+                                          const DecodePos&, const void*, void*, char*, hipStream_t);
 template hipError_t decode_step_run<float>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                           const void*, void*, char*, hipStream_t);
+                                           const DecodePos&, const void*, void*, char*, hipStream_t);
 template hipError_t cache_append_run<bf16>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                           const void*, int64_t, char*, hipStream_t);
+                                           const DecodePos&, const void*, int64_t, char*, hipStream_t);
 template hipError_t cache_append_run<float>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                            const void*, int64_t, char*, hipStream_t);
+                                            const DecodePos&, const void*, int64_t, char*, hipStream_t);
 
 }  // namespace pf

@@ -21,6 +21,17 @@ struct DecodeDims {
   int append_rows;            // rows (sequence, block) compressed per append GEMM chunk
 };
 
+// Per-sequence positions, passed by value in kernel arguments: sequence b
+// has n[b] cached rows and j[b] filled local slots; `write` marks the
+// sequences whose rows a cache write stores (bit b). With ragged = 0 every
+// sequence uses the scalar n and j.
+struct DecodePos {
+  int32_t n[PF_MAX_RAGGED_BATCH];
+  int32_t j[PF_MAX_RAGGED_BATCH];
+  uint64_t write;
+  int32_t ragged;
+};
+
 constexpr int kDecodeMaxSplits = 256;   // cache-row slices per (sequence, head)
 constexpr int kDecodeRowsPerSplit = 1024;
 
@@ -35,12 +46,13 @@ struct DecodeWs {
 int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why);
 DecodeWs decode_ws(const DecodeDims& d);
 
+// `pos` carries the per-sequence positions when st.n_seq / st.j_seq are set.
 template <typename T>
 hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                           const void* x_t, void* y_t, char* ws, hipStream_t stream);
+                           const DecodePos& pos, const void* x_t, void* y_t, char* ws, hipStream_t stream);
 
 template <typename T>
 hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                            const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream);
+                            const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream);
 
 }  // namespace pf

@@ -120,3 +120,64 @@ def test_snapshot_restore_bitwise(gpu):
         yb = b.step(dev(inp["x"][t], shape.dtype))
         torch.cuda.synchronize()
         assert torch.equal(ya, yb)
+
+
+def test_ragged_positions_match_per_sequence_oracle(gpu):
+    """Per-sequence positions: four sequences with different cache lengths and
+    different fill of their current block decode together; each must match the
+    oracle run on that sequence alone (blocks complete at different steps)."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    shape = DecodeShape(4, 128, 2, 64, (8,), n0=0, steps=21, n_cap=24)
+    P, h, dh, d = shape.block, shape.n_heads, shape.head_dim, shape.d_model
+    inp = synth.decode_inputs(shape, 77)
+    rng = np.random.default_rng(78)
+    n0 = np.array([0, 5, 13, 2], dtype=np.int64)
+    j0 = np.array([0, 3, 7, 5], dtype=np.int32)
+    bf = synth.bf16_round
+    kc = bf(rng.standard_normal((4, h, shape.capacity, dh)).astype(np.float32))
+    vc = bf(rng.standard_normal((4, h, shape.capacity, dh)).astype(np.float32))
+    x_blk = bf(rng.standard_normal((4, P, d)).astype(np.float32))
+    k_loc = bf(rng.standard_normal((4, h, P, dh)).astype(np.float32))
+    v_loc = bf(rng.standard_normal((4, h, P, dh)).astype(np.float32))
+    cfg = B.decode_config(4, d, h, dh, shape.factors, (), "bf16", shape.rms_eps)
+    sess = B.DecodeSession(cfg, dev_weights(inp["weights"], "bf16"), dev(kc, "bf16"), dev(vc, "bf16"),
+                           ragged=True, n_seq=n0, j_seq=j0)
+    sess.x_blk.copy_(dev(x_blk, "bf16"))
+    sess.k_loc.copy_(dev(k_loc, "bf16"))
+    sess.v_loc.copy_(dev(v_loc, "bf16"))
+    ys = [host(sess.step(dev(inp["x"][t], "bf16"))) for t in range(shape.steps)]
+    torch.cuda.synchronize()
+    got = np.stack(ys)
+    for b in range(4):
+        st = oracle.DecodeState(kc[b:b + 1].astype(np.float64), vc[b:b + 1].astype(np.float64), int(n0[b]),
+                                x_blk[b:b + 1].astype(np.float64), k_loc[b:b + 1].astype(np.float64),
+                                v_loc[b:b + 1].astype(np.float64), int(j0[b]))
+        ref = np.stack([oracle.decode_step(st, inp["weights"], shape.factors, inp["x"][t][b:b + 1], shape.rms_eps)
+                        for t in range(shape.steps)])
+        assert_close(got[:, b:b + 1], ref, "bf16", f"ragged sequence {b} y")
+        assert sess.n_seq[b] == st.n and sess.j_seq[b] == st.j, (b, sess.n_seq[b], sess.j_seq[b], st.n, st.j)
+        new = slice(int(n0[b]), st.n)
+        assert_close(host(sess.k_cache)[b:b + 1, :, new], st.k_cache[:, :, new], "bf16", f"ragged {b} K rows")
+        assert_close(host(sess.v_cache)[b:b + 1, :, new], st.v_cache[:, :, new], "bf16", f"ragged {b} V rows")
+        # rows past the sequence's own length are untouched
+        assert np.array_equal(host(sess.k_cache)[b, :, st.n:], kc[b, :, st.n:])
+
+
+def test_ragged_mode_with_equal_positions_is_lockstep_bitwise(gpu):
+    import torch
+    shape = CASES["bf16_small"]
+    inp = synth.decode_inputs(shape, 5)
+    a = make_session(shape, inp)
+    from paper_2608_23463_amd import binding as B
+    cfg = B.decode_config(shape.batch, shape.d_model, shape.n_heads, shape.head_dim, shape.factors,
+                          shape.level_dims, shape.dtype, shape.rms_eps)
+    b = B.DecodeSession(cfg, dev_weights(inp["weights"], shape.dtype), dev(inp["k_cache"], shape.dtype),
+                        dev(inp["v_cache"], shape.dtype), n=inp["n0"], ragged=True)
+    for t in range(shape.steps):
+        ya = a.step(dev(inp["x"][t], shape.dtype))
+        yb = b.step(dev(inp["x"][t], shape.dtype))
+        torch.cuda.synchronize()
+        assert torch.equal(ya, yb), t
+    assert all(b.n_seq == a.n) and all(b.j_seq == a.j)
+    assert torch.equal(a.k_cache, b.k_cache) and torch.equal(a.v_cache, b.v_cache)
