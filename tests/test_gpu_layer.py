@@ -126,3 +126,31 @@ def test_run_twice_bitwise(gpu):
     a = run_gpu(shape, inp)
     b = run_gpu(shape, inp)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_layer_stack_with_cross_layer_proxies_and_dynamic_p(gpu):
+    """Three stacked layers (Sec. 3.1, Sec. 3.6): layer 2 takes layer 1's proxy
+    stream as H_in (Eq. 8); layer 3 uses another block size, so its proxy
+    state is re-extracted from the local stream (H_in absent). The chain of
+    HIP calls matches the chained oracle."""
+    from paper_2608_23463_amd import binding as B
+    L, d = 64 * 24, 256
+    shapes = [LayerShape(1, L, d, d, 4, 64, (16,)), LayerShape(1, L, d, d, 4, 64, (16,)),
+              LayerShape(1, L, d, d, 4, 64, (8, 8))]
+    ws = [synth.layer_inputs(s, 40 + i)["weights"] for i, s in enumerate(shapes)]
+    x0 = synth.layer_inputs(shapes[0], 39)["x"]
+    # GPU chain
+    x = dev(x0, "bf16")
+    h = None
+    for i, s in enumerate(shapes):
+        h_in = h if i == 1 else None
+        x, h, _ = B.layer_forward(B.config_from_shape(s), dev_weights(ws[i], "bf16"), x, h_in)
+    import torch
+    torch.cuda.synchronize()
+    # oracle chain on the same (bf16-valued) inputs; intermediate activations stay fp64
+    rx, rh = x0, None
+    for i, s in enumerate(shapes):
+        r = oracle.layer_forward(rx, ws[i], s.factors, s.n_heads, s.mask, rh if i == 1 else None)
+        rx, rh = r["x_out"], r["h_out"]
+    assert_close(host(h), rh, "bf16", "stack layer 3 h_out")
+    assert_close(host(x), rx, "bf16", "stack layer 3 x_out")
