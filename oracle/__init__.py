@@ -22,5 +22,5 @@ from .layer import (  # noqa: F401
     sigmoid, compress, layer_forward, layer_backward, attention_rows,
     proxies_and_attention_inputs,
 )
-from .decode import DecodeState, decode_step, cache_append, rms_norm  # noqa: F401
+from .decode import DecodeState, decode_step, cache_append, prefill, rms_norm  # noqa: F401
 from .metrics import max_rel_err  # noqa: F401

@@ -5,7 +5,9 @@ generation block of the language model (Eq. 19-20) decoding one token per
 sequence against the frozen proxy cache of Eq. 21, with the streaming
 update of Sec. 3.8: once P new tokens have been decoded the block is
 compressed, appended to the cache as one new proxy row and its local
-features are dropped.
+features are dropped. `prefill` is the parallel form of the same block over
+a whole chunk of tokens (every output at once, the chunk's complete blocks
+appended), equal to that many streaming steps.
 
 Readings of points the paper leaves open:
 * The block is pre-norm: u = RMSNorm(x) (eps = 1e-6, learnable gain gamma)
@@ -136,4 +138,70 @@ def decode_step(state: DecodeState, weights, factors: Sequence[int], x_t, rms_ep
         state.x_blk[:] = 0
         state.k_loc[:] = 0
         state.v_loc[:] = 0
+    return y
+
+
+def prefill(state: DecodeState, weights, factors: Sequence[int], xs, rms_eps=1e-6, tokens=None):
+    """Parallel form of the generation block over a chunk of tokens (Eq. 19-20).
+
+    xs: [B, T, d], the next T tokens of every sequence, starting at a block
+    boundary (state.j == 0). Token t of the chunk belongs to block t // P; it
+    attends to the tokens of its own block up to itself (A_x) and to the
+    cached proxies of every block completed before its own (A_h): the n0
+    rows already in the cache plus one row per earlier block of the chunk
+    (Eq. 21). The T // P complete blocks are appended to the cache; the
+    tokens of an unfinished last block stay in the local slots, so decoding
+    continues at j = T % P. The result equals T streaming decode steps.
+
+    tokens: optional list of chunk positions; outputs are computed only
+    there (the state update is always complete). Returns y [B, T, d], or
+    [B, len(tokens), d] when tokens is given.
+    """
+    if state.j != 0:
+        raise ValueError("prefill starts at a block boundary")
+    xs = _f64(xs)
+    bsz, T, d = xs.shape
+    n_heads = state.k_loc.shape[1]
+    dh = state.k_loc.shape[3]
+    p_blk = state.x_blk.shape[1]
+    scale = 1.0 / np.sqrt(dh)
+    n0 = state.n
+    nblk = T // p_blk
+    if nblk:
+        cache_append(state, weights, factors, xs[:, :nblk * p_blk])
+    toks = list(range(T)) if tokens is None else list(tokens)
+    rem = T - nblk * p_blk
+    # keys and values are needed for every token some output attends to,
+    # and for the unfinished block that stays in the local slots
+    need = sorted({s for t in toks for s in range((t // p_blk) * p_blk, t + 1)} | set(range(nblk * p_blk, T)))
+    at = {s: i for i, s in enumerate(need)}
+    u_need = rms_norm(xs[:, need], weights["rms_gamma"], rms_eps)                  # [B, |need|, d]
+    k = linear(u_need, *weights["k"]).reshape(bsz, len(need), n_heads, dh)
+    v = linear(u_need, *weights["v"]).reshape(bsz, len(need), n_heads, dh)
+    y = np.zeros((bsz, len(toks), d))
+    for i, t in enumerate(toks):
+        blk = t // p_blk
+        local = [at[s] for s in range(blk * p_blk, t + 1)]
+        n_vis = n0 + blk                  # proxies of the blocks before this one
+        u = rms_norm(xs[:, t], weights["rms_gamma"], rms_eps)                       # [B, d]
+        q = linear(u, *weights["q"]).reshape(bsz, n_heads, dh)
+        alpha = sigmoid(linear(u, *weights["alpha"]))                              # [B, n_heads]
+        attn = np.zeros((bsz, n_heads, dh))
+        for b in range(bsz):
+            for h in range(n_heads):
+                a_x = _softmax_attend(q[b, h], k[b, local, h], v[b, local, h], scale)
+                if n_vis > 0:
+                    a_h = _softmax_attend(q[b, h], state.k_cache[b, h, :n_vis], state.v_cache[b, h, :n_vis], scale)
+                else:
+                    a_h = np.zeros(dh)
+                attn[b, h] = a_x + alpha[b, h] * a_h
+        y[:, i] = xs[:, t] + linear(attn.reshape(bsz, d), *weights["o"])
+    state.x_blk[:] = 0
+    state.k_loc[:] = 0
+    state.v_loc[:] = 0
+    for s in range(rem):
+        state.x_blk[:, s] = xs[:, nblk * p_blk + s]
+        state.k_loc[:, :, s] = k[:, at[nblk * p_blk + s]]
+        state.v_loc[:, :, s] = v[:, at[nblk * p_blk + s]]
+    state.j = rem
     return y

@@ -175,3 +175,81 @@ def test_cache_is_one_over_p_of_full_kv():
     st = DecodeState.empty(bsz, nh, d, P, 8, d)
     oracle.cache_append(st, w, (2, 4), rng.standard_normal((bsz, L, d)))
     assert st.n * P == L
+
+
+def _stream_state(bsz, nh, dh, P, cap, d, n0, rng):
+    st = DecodeState.empty(bsz, nh, dh, P, cap, d)
+    st.k_cache[:, :, :n0] = rng.standard_normal((bsz, nh, n0, dh))
+    st.v_cache[:, :, :n0] = rng.standard_normal((bsz, nh, n0, dh))
+    st.n = n0
+    return st
+
+
+def _copy_state(st):
+    return DecodeState(st.k_cache.copy(), st.v_cache.copy(), st.n, st.x_blk.copy(), st.k_loc.copy(),
+                       st.v_loc.copy(), st.j)
+
+
+@pytest.mark.parametrize("n0,T,factors", [(0, 11, (4,)), (5, 12, (4,)), (3, 3, (4,)), (2, 17, (2, 2)),
+                                          (0, 1, (4,))])
+def test_prefill_equals_streaming_steps(n0, T, factors):
+    """The parallel form over a chunk gives every output and the whole state
+    that T streaming decode steps give (Eq. 19-21, Sec. 3.8)."""
+    rng = np.random.default_rng(70 + n0 + T)
+    bsz, d, nh = 2, 8, 2
+    dh = d // nh
+    P = int(np.prod(factors))
+    w = decode_weights(rng, d, nh, factors)
+    cap = n0 + T // P + 1
+    a = _stream_state(bsz, nh, dh, P, cap, d, n0, rng)
+    b = _copy_state(a)
+    xs = rng.standard_normal((bsz, T, d))
+    y_par = oracle.prefill(a, w, factors, xs)
+    y_seq = np.stack([oracle.decode_step(b, w, factors, xs[:, t]) for t in range(T)], axis=1)
+    np.testing.assert_allclose(y_par, y_seq, rtol=1e-12, atol=1e-12)
+    assert (a.n, a.j) == (b.n, b.j) == (n0 + T // P, T % P)
+    for name in ("k_cache", "v_cache", "x_blk", "k_loc", "v_loc"):
+        np.testing.assert_allclose(getattr(a, name), getattr(b, name), rtol=1e-12, atol=1e-12, err_msg=name)
+    # decoding continues from the prefilled state exactly as from the streamed one
+    x_next = rng.standard_normal((bsz, d))
+    np.testing.assert_allclose(oracle.decode_step(a, w, factors, x_next), oracle.decode_step(b, w, factors, x_next),
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_prefill_equals_independent_parallel_form():
+    rng = np.random.default_rng(81)
+    bsz, d, nh, P, n0, T = 2, 8, 2, 4, 3, 14
+    dh = d // nh
+    w = decode_weights(rng, d, nh, (P,))
+    st = _stream_state(bsz, nh, dh, P, n0 + T // P + 1, d, n0, rng)
+    k0 = st.k_cache[:, :, :n0].copy()
+    v0 = st.v_cache[:, :, :n0].copy()
+    xs = rng.standard_normal((bsz, T, d))
+    y = oracle.prefill(st, w, (P,), xs)
+    ref = _parallel_form(xs.transpose(1, 0, 2), w, nh, P, k0, v0, 0, np.zeros((bsz, 0, d)), 1e-6)
+    np.testing.assert_allclose(y, ref.transpose(1, 0, 2), rtol=1e-12, atol=1e-12)
+
+
+def test_prefill_token_subset_matches_full():
+    rng = np.random.default_rng(82)
+    bsz, d, nh, P, n0, T = 2, 8, 2, 4, 2, 13
+    dh = d // nh
+    w = decode_weights(rng, d, nh, (P,))
+    a = _stream_state(bsz, nh, dh, P, n0 + T // P + 1, d, n0, rng)
+    b = _copy_state(a)
+    xs = rng.standard_normal((bsz, T, d))
+    toks = [0, 5, 7, 12]
+    full = oracle.prefill(a, w, (P,), xs)
+    part = oracle.prefill(b, w, (P,), xs, tokens=toks)
+    np.testing.assert_allclose(part, full[:, toks], rtol=1e-12, atol=1e-12)
+    for name in ("k_cache", "v_cache", "x_blk", "k_loc", "v_loc"):
+        np.testing.assert_array_equal(getattr(a, name), getattr(b, name), err_msg=name)
+
+
+def test_prefill_requires_block_boundary():
+    rng = np.random.default_rng(83)
+    w = decode_weights(rng, 8, 2, (4,))
+    st = _stream_state(1, 2, 4, 4, 4, 8, 0, rng)
+    oracle.decode_step(st, w, (4,), rng.standard_normal((1, 8)))
+    with pytest.raises(ValueError):
+        oracle.prefill(st, w, (4,), rng.standard_normal((1, 3, 8)))
