@@ -218,6 +218,30 @@ int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w,
                        pf_decode_state* st, const void* x_blocks, int64_t nblk,
                        void* workspace, size_t ws_bytes, void* stream);
 
+/* Prefill: the parallel (training-time) form of the generation block of
+ * Eq. 19-20 over the next n_tokens tokens of every sequence, with the cache
+ * update of Eq. 21 for the chunk's complete blocks; the result equals
+ * n_tokens calls of proxy_decode_step (up to rounding order).
+ * Token t of the chunk lies in block t / P. Its output is
+ * y_t = x_t + (A_x + alpha_t * A_h) W_o^T + b_o, where A_x attends over the
+ * tokens of its own block up to t and A_h over the n cached proxies plus the
+ * t / P blocks of the chunk before its own (appended first, each compressed
+ * as proxy_cache_append does). The tokens of an unfinished last block stay
+ * in the local slots.
+ *  x [B, n_tokens, d]: layer inputs; y [B, n_tokens, d]: outputs (must not
+ *  overlap x). Positions must be lockstep (n_seq = j_seq = NULL) with
+ *  j == 0, else PF_ERR_UNSUPPORTED; PF_ERR_CAPACITY if n + n_tokens / P >
+ *  n_cap. On success n += n_tokens / P and j = n_tokens % P; n_tokens = 0
+ *  does nothing.
+ *  workspace: proxy_prefill_workspace_size(cfg, n_tokens, st->n_cap) bytes
+ *  (0 for an invalid config or sizes beyond the limits: batch * n_tokens
+ *  below 2^31, head_dim * n_tokens and head_dim * n_cap elements per head
+ *  below 2 GiB). */
+size_t proxy_prefill_workspace_size(const pf_decode_config* cfg, int64_t n_tokens, int64_t n_cap);
+int proxy_decode_prefill(const pf_decode_config* cfg, const pf_decode_weights* w,
+                         pf_decode_state* st, const void* x, int64_t n_tokens, void* y,
+                         void* workspace, size_t ws_bytes, void* stream);
+
 /* Launch tracing (profiling aid). While enabled, every kernel launch of the
  * library is bracketed by two HIP events recorded on its stream and
  * attributed to a label (e.g. "gate_gemm", "attention_fwd", "decode_attn").

@@ -28,7 +28,8 @@ PF_INJECT_ADD = 1
 EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
     "proxy_layer_backward", "proxy_decode_workspace_size", "proxy_decode_step",
-    "proxy_cache_append", "proxy_last_error", "proxy_version",
+    "proxy_cache_append", "proxy_prefill_workspace_size", "proxy_decode_prefill",
+    "proxy_last_error", "proxy_version",
     "proxy_trace_enable", "proxy_trace_collect", "proxy_trace_get", "proxy_trace_reset",
 )
 
@@ -119,6 +120,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.proxy_cache_append.argtypes = [P(PfDecodeConfig), P(PfDecodeWeights), P(PfDecodeState), c_void_p,
                                        c_int64, c_void_p, c_size_t, c_void_p]
     lib.proxy_cache_append.restype = c_int32
+    lib.proxy_prefill_workspace_size.argtypes = [P(PfDecodeConfig), c_int64, c_int64]
+    lib.proxy_prefill_workspace_size.restype = c_size_t
+    lib.proxy_decode_prefill.argtypes = [P(PfDecodeConfig), P(PfDecodeWeights), P(PfDecodeState), c_void_p,
+                                         c_int64, c_void_p, c_void_p, c_size_t, c_void_p]
+    lib.proxy_decode_prefill.restype = c_int32
     lib.proxy_last_error.argtypes = []
     lib.proxy_last_error.restype = ctypes.c_char_p
     lib.proxy_version.argtypes = []
@@ -394,6 +400,24 @@ class DecodeSession:
                                         ctypes.byref(self.state), _ptr(x_t), _ptr(y_t),
                                         _ptr(self.workspace), self.workspace.numel(), _stream(stream)))
         return y_t
+
+    def prefill(self, x, y=None, stream=None):
+        """Parallel form of the generation block over x [B, T, d] (the next T
+        tokens of every sequence, from a block boundary); returns y [B, T, d].
+        The prefill workspace is allocated on first use and grown as needed."""
+        import torch
+        if y is None:
+            y = torch.empty_like(x)
+        lib = load()
+        need = int(lib.proxy_prefill_workspace_size(ctypes.byref(self.cfg), x.shape[1], self.state.n_cap))
+        if need == 0:
+            raise ProxyFormerError(-2, "prefill sizes beyond the library's limits")
+        if getattr(self, "prefill_ws", None) is None or self.prefill_ws.numel() < need:
+            self.prefill_ws = _bytes(need, x.device)
+        _check(lib.proxy_decode_prefill(ctypes.byref(self.cfg), ctypes.byref(self.wstruct), ctypes.byref(self.state),
+                                        _ptr(x), x.shape[1], _ptr(y), _ptr(self.prefill_ws),
+                                        self.prefill_ws.numel(), _stream(stream)))
+        return y
 
     def append(self, x_blocks, nblk: int, stream=None):
         _check(load().proxy_cache_append(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),

@@ -33,6 +33,7 @@ HIPCC_FLAGS = [
 FILE_FLAGS = {
     "attention_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "attention_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "decode_prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 

@@ -151,8 +151,9 @@ size_t proxy_decode_workspace_size(const pf_decode_config* cfg) {
   return decode_ws(d).bytes;
 }
 
+// prefill_tokens >= 0: the workspace is checked against a prefill of that many tokens
 static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weights* w, const pf_decode_state* st,
-                               DecodeDims* d, void* workspace, size_t ws_bytes) {
+                               DecodeDims* d, void* workspace, size_t ws_bytes, int64_t prefill_tokens = -1) {
   const char* why;
   int s = decode_dims(cfg, d, &why);
   if (s != PF_OK) return fail(s, "invalid decode config: %s", why);
@@ -188,9 +189,16 @@ static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weig
     if (st->n < 0 || st->n > st->n_cap) return fail(PF_ERR_INVALID_ARG, "state n must be in 0..n_cap");
     if (st->j < 0 || st->j >= d->P) return fail(PF_ERR_INVALID_ARG, "state j must be in 0..P-1");
   }
-  const DecodeWs W = decode_ws(*d);
-  if (!workspace || ws_bytes < W.bytes)
-    return fail(PF_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", W.bytes, workspace ? ws_bytes : 0);
+  size_t need;
+  if (prefill_tokens >= 0) {
+    if (const char* lim = prefill_limits(*d, prefill_tokens, st->n_cap))
+      return fail(PF_ERR_UNSUPPORTED, "prefill: %s", lim);
+    need = prefill_ws(*d, prefill_tokens, st->n_cap).bytes;
+  } else {
+    need = decode_ws(*d).bytes;
+  }
+  if (!workspace || ws_bytes < need)
+    return fail(PF_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", need, workspace ? ws_bytes : 0);
   return PF_OK;
 }
 
@@ -254,6 +262,41 @@ int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, p
   } else {
     st->j += 1;
   }
+  return PF_OK;
+}
+
+size_t proxy_prefill_workspace_size(const pf_decode_config* cfg, int64_t n_tokens, int64_t n_cap) {
+  DecodeDims d;
+  const char* why;
+  if (decode_dims(cfg, &d, &why) != PF_OK) return 0;
+  if (prefill_limits(d, n_tokens, n_cap)) return 0;
+  return prefill_ws(d, n_tokens, n_cap).bytes;
+}
+
+int proxy_decode_prefill(const pf_decode_config* cfg, const pf_decode_weights* w, pf_decode_state* st, const void* x,
+                         int64_t n_tokens, void* y, void* workspace, size_t ws_bytes, void* stream) {
+  if (n_tokens < 0) return fail(PF_ERR_INVALID_ARG, "n_tokens must be >= 0");
+  DecodeDims d;
+  int s = check_decode_common(cfg, w, st, &d, workspace, ws_bytes, n_tokens);
+  if (s != PF_OK) return s;
+  if (st->n_seq) return fail(PF_ERR_UNSUPPORTED, "prefill needs lockstep positions (n_seq = j_seq = NULL)");
+  if (st->j != 0) return fail(PF_ERR_UNSUPPORTED, "prefill starts at a block boundary (j = 0), got j = %d", st->j);
+  if (n_tokens == 0) return PF_OK;
+  if (!x || !y) return fail(PF_ERR_INVALID_ARG, "x and y must be non-NULL");
+  if (!aligned16(x) || !aligned16(y)) return fail(PF_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
+  const size_t bytes = (size_t)d.B * n_tokens * d.d * d.esize;
+  if (overlaps(x, bytes, y, bytes)) return fail(PF_ERR_INVALID_ARG, "y must not alias x");
+  const int64_t nblk = n_tokens / d.P;
+  if (st->n + nblk > st->n_cap)
+    return fail(PF_ERR_CAPACITY, "prefill of %lld blocks overflows the cache (n = %lld, n_cap = %lld)",
+                (long long)nblk, (long long)st->n, (long long)st->n_cap);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  char* ws = reinterpret_cast<char*>(workspace);
+  hipError_t e = d.esize == 2 ? prefill_run<bf16>(d, w, *st, x, n_tokens, y, ws, hs)
+                              : prefill_run<float>(d, w, *st, x, n_tokens, y, ws, hs);
+  if (e != hipSuccess) return hip_status(e, "proxy_decode_prefill launch");
+  st->n += nblk;
+  st->j = (int32_t)(n_tokens - nblk * d.P);
   return PF_OK;
 }
 

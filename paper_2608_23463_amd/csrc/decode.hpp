@@ -51,6 +51,28 @@ template <typename T>
 hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
                            const DecodePos& pos, const void* x_t, void* y_t, char* ws, hipStream_t stream);
 
+// Prefill (parallel form of the generation block over a chunk of T tokens):
+// buffers placed after the decode workspace, which the chunk's append uses.
+struct PrefillWs {
+  size_t u;      // [B*T, d] RMSNorm output, later the attention output A
+  size_t q, k;   // [B, h, T, dh]
+  size_t vt;     // [B, h, dh, ld_t] values of the chunk, token-contiguous
+  size_t alpha;  // fp32 [B*T, h]
+  size_t vct;    // [B, h, dh, ld_c] cached values, row-contiguous
+  size_t xc;     // [B, T/P*P, d] complete blocks, gathered when T % P != 0
+  size_t gemm;   // split-K partials of the chunk's GEMMs
+  size_t bytes;
+  int64_t ld_t, ld_c;
+};
+
+// Limits of a prefill of T tokens with cache capacity n_cap (NULL: fits).
+const char* prefill_limits(const DecodeDims& d, int64_t T, int64_t n_cap);
+PrefillWs prefill_ws(const DecodeDims& d, int64_t T, int64_t n_cap);
+
+template <typename T>
+hipError_t prefill_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st, const void* x,
+                       int64_t n_tok, void* y, char* ws, hipStream_t stream);
+
 template <typename T>
 hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
                             const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream);

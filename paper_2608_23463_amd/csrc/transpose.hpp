@@ -12,10 +12,12 @@ namespace pf {
 // part[blockIdx.y][c] (fixed order: a thread's 16-byte run, then a butterfly
 // over the runs of one column), the first stage of a bias gradient.
 // blockIdx.z selects a batch entry: in/out advance by in_bs/out_bs elements.
+// With R_out > R the output columns R .. R_out-1 are written as zeros (the
+// grid then covers R_out rows).
 template <typename T>
 __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ in, int64_t ld_in, int64_t R, int C,
                                                         T* __restrict__ out, int64_t ld_out, float* __restrict__ part,
-                                                        int64_t in_bs = 0, int64_t out_bs = 0) {
+                                                        int64_t in_bs = 0, int64_t out_bs = 0, int64_t R_out = 0) {
   constexpr int kV = 16 / sizeof(T);
   constexpr int kRuns = 64 / kV;  // runs per column; consecutive threads
   __shared__ T tile[64][64 + 2];
@@ -58,10 +60,11 @@ __global__ void __launch_bounds__(256) transpose_kernel(const T* __restrict__ in
       if (rr == 0 && c < C) part[(int64_t)blockIdx.y * C + c] = sum;
     }
     if (c >= C) continue;
-    if (r + kV <= R) {
+    const int64_t rw = R_out > R ? R_out : R;  // rows read past R are zeros
+    if (r + kV <= rw) {
       st16(out + (int64_t)c * ld_out + r, *reinterpret_cast<const u32x4*>(v));
     } else {
-      for (int k = 0; r + k < R; ++k) out[(int64_t)c * ld_out + r + k] = v[k];
+      for (int k = 0; r + k < rw; ++k) out[(int64_t)c * ld_out + r + k] = v[k];
     }
   }
 }

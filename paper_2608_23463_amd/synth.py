@@ -123,8 +123,8 @@ class DecodeShape:
 
 
 # The workloads: a small fp32 correctness layer, two bf16 layers at 64K and
-# 1M tokens, a factorised forward+backward layer, the decode run, and the
-# language-model shape (layer and decode).
+# 1M tokens, a factorised forward+backward layer, the decode run, the
+# language-model shape (layer and decode) and a chunked prefill.
 WORKLOADS = {
     "layer_fp32_L4k_d256": LayerShape(1, 4096, 256, 256, 4, 64, (64,), dtype="fp32"),
     "layer_bf16_L64k_d1024": LayerShape(1, 65536, 1024, 1024, 16, 64, (64,)),
@@ -136,6 +136,10 @@ WORKLOADS = {
     # and the generation side decoding 512-wide tokens against that cache.
     "layer_bf16_L1M_lm_df64_dp512": LayerShape(1, 1 << 20, 64, 512, 8, 64, (64,)),
     "decode_bf16_B32_n16k_lm_d512": DecodeShape(32, 512, 8, 64, (64,), n0=16384, steps=256),
+    # Chunked prefill (parallel form of the generation block, Eq. 19-20): the
+    # next 4,096 tokens of 32 sequences against a 16,384-proxy cache, the
+    # chunk's 64 blocks per sequence appended (Eq. 21). `steps` is the chunk.
+    "prefill_bf16_B32_T4096_n16k": DecodeShape(32, 1024, 16, 64, (64,), n0=16384, steps=4096),
 }
 WORKLOAD_SEEDS = {name: 20260000 + i + 1 for i, name in enumerate(WORKLOADS)}
 

@@ -174,3 +174,41 @@ def test_decode_validation(lib):
     assert lib.proxy_decode_step(ctypes.byref(bad), ctypes.byref(w), ctypes.byref(_dstate()), 0x70000, 0x80000,
                                  0x90000, ws, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_decode_workspace_size(ctypes.byref(bad)) == 0
+
+
+def test_prefill_validation(lib):
+    cfg = _dcfg()
+    pws = int(lib.proxy_prefill_workspace_size(ctypes.byref(cfg), 10, 4))
+    assert pws > int(lib.proxy_decode_workspace_size(ctypes.byref(cfg))) and pws % 256 == 0
+    assert lib.proxy_prefill_workspace_size(ctypes.byref(cfg), -1, 4) == 0
+    assert lib.proxy_prefill_workspace_size(ctypes.byref(_dcfg(n_heads=3)), 10, 4) == 0
+    w = _dweights()
+
+    def call(st, x=0x70000, n_tok=10, y=0x80000, ws=0x90000, nbytes=pws):
+        return lib.proxy_decode_prefill(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), x, n_tok, y, ws,
+                                        nbytes, None)
+
+    # not at a block boundary
+    st = _dstate(j=1)
+    assert call(st) == B.PF_ERR_UNSUPPORTED
+    # per-sequence positions
+    import numpy as np
+    st = _dstate()
+    n_seq = np.zeros(2, np.int64)
+    j_seq = np.zeros(2, np.int32)
+    st.n_seq = n_seq.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+    st.j_seq = j_seq.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    assert call(st) == B.PF_ERR_UNSUPPORTED
+    # 10 tokens = 2 complete blocks of 4 into a cache with room for 1
+    st = _dstate(n=3, n_cap=4)
+    assert call(st) == B.PF_ERR_CAPACITY
+    assert st.n == 3 and st.j == 0
+    # workspace too small, negative count, aliasing, NULL input
+    assert call(_dstate(), nbytes=pws - 256) == B.PF_ERR_WORKSPACE
+    assert call(_dstate(), n_tok=-1) == B.PF_ERR_INVALID_ARG
+    assert call(_dstate(), y=0x70000 + 256) == B.PF_ERR_INVALID_ARG
+    assert call(_dstate(), x=None) == B.PF_ERR_INVALID_ARG
+    # nothing to prefill is a no-op
+    st = _dstate(n=1)
+    assert call(st, n_tok=0, x=None, y=None) == B.PF_OK
+    assert st.n == 1 and st.j == 0
