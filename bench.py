@@ -20,6 +20,9 @@ Extra objects on the same line:
   lm           the paper's language-model shape: layer forward tokens/s at
                L = 1M with a 64-wide local stream and a 512-wide proxy stream
                (8 x 64, P = 64), and decode tokens/s at d_model = 512
+  prefill      parallel form of the generation block: the next 4,096 tokens
+               of 32 sequences against 16,384 cached proxies (d = 1024,
+               16 x 64, P = 64), the chunk's 64 blocks per sequence appended
   cpu_baseline the CPU oracle timed on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -41,6 +44,7 @@ DECODE_WORKLOAD = "decode_bf16_B32_n16k"
 TRAIN_WORKLOAD = "layer_bf16_L256k_d2048_f8x8"
 LM_LAYER_WORKLOAD = "layer_bf16_L1M_lm_df64_dp512"
 LM_DECODE_WORKLOAD = "decode_bf16_B32_n16k_lm_d512"
+PREFILL_WORKLOAD = "prefill_bf16_B32_T4096_n16k"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 CPU_SAMPLE_TOKENS = 393216
@@ -292,6 +296,74 @@ def bench_decode(workload=DECODE_WORKLOAD):
     return out
 
 
+def prefill_attn_flops(shape):
+    """Algorithmic MFMA flops of the prefill attention: 4 * d_head per visible
+    (token, key) pair and head; token t sees t % P + 1 tokens of its block and
+    n0 + t // P cached proxies."""
+    P, T = shape.block, shape.steps
+    pairs = 0
+    for t in range(T):
+        pairs += t % P + 1 + shape.n0 + t // P
+    return 4.0 * shape.head_dim * shape.batch * shape.n_heads * pairs
+
+
+def bench_prefill(workload=PREFILL_WORKLOAD, calls=3):
+    import numpy as np
+    import torch
+    from paper_2608_23463_amd import binding as B
+    from paper_2608_23463_amd import synth
+    shape = synth.WORKLOADS[workload]
+    log(f"generating {workload} inputs")
+    inp = synth.decode_inputs(shape, synth.WORKLOAD_SEEDS[workload])
+    cfg = B.decode_config(shape.batch, shape.d_model, shape.n_heads, shape.head_dim, shape.factors,
+                          shape.level_dims, shape.dtype, shape.rms_eps)
+    kc = to_dev(inp.pop("k_cache"), shape.dtype)
+    vc = to_dev(inp.pop("v_cache"), shape.dtype)
+    x = to_dev(np.ascontiguousarray(inp.pop("x").transpose(1, 0, 2)), shape.dtype)   # [B, T, d]
+    sess = B.DecodeSession(cfg, dev_weights(inp["weights"], shape.dtype), kc, vc, n=shape.n0)
+    y = torch.empty_like(x)
+
+    def one():
+        sess.state.n = shape.n0   # every call prefills the same chunk onto the same cache
+        sess.state.j = 0
+        sess.prefill(x, y)
+
+    log("prefill warmup")
+    one()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {calls} prefill calls")
+    start.record()
+    for _ in range(calls):
+        one()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / calls
+    B.trace_reset()
+    B.trace_enable(True)
+    for _ in range(calls):
+        one()
+    torch.cuda.synchronize()
+    tr = B.trace_collect()
+    B.trace_enable(False)
+    toks = shape.batch * shape.steps
+    out = {"metric": "prefill tokens/s (parallel generation block)", "value": round(toks / (ms * 1e-3), 1),
+           "unit": "tokens/s", "ms_per_call": round(ms, 3), "workload": workload, "batch": shape.batch,
+           "chunk_tokens": shape.steps, "cached_rows": shape.n0, "appended_blocks": shape.steps // shape.block}
+    attn = tr.get("prefill_attn")
+    if attn:
+        avg = attn[1] / attn[0]
+        fl = prefill_attn_flops(shape)
+        tf = fl / (avg * 1e-3) / 1e12
+        out["roofline"] = {"kernel": "prefill_attn", "bound": "mfma", "achieved": round(tf, 1),
+                           "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                           "traffic": None, "avg_ms": round(avg, 4), "work_per_launch": fl}
+    out["kernels"] = {k: {"launches": c, "avg_ms": round(t / c, 4)} for k, (c, t) in tr.items()}
+    del kc, vc, x, y, sess
+    torch.cuda.empty_cache()
+    return out
+
+
 def bench_train(steps):
     import torch
     from paper_2608_23463_amd import binding as B
@@ -430,6 +502,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--no-lm", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only the short dispatch sequence used for counter runs (prints no JSON)")
     args = ap.parse_args()
@@ -475,6 +548,8 @@ def main():
         result["decode"] = bench_decode()
     if not args.no_train:
         result["train"] = bench_train(max(1, min(args.steps, 5)))
+    if not args.no_prefill:
+        result["prefill"] = bench_prefill()
     if not args.no_lm:
         lshape, lms, lkernels, lroof, _, _ = bench_layer(args.steps, args.warmup, LM_LAYER_WORKLOAD)
         result["lm"] = {"metric": "layer fwd tokens/s (language-model shape)",

@@ -99,6 +99,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with paper_2608_23463_amd.build.build()")
+    # torch first: the library then binds to the HIP runtime torch has loaded
+    # (its buffers and streams are torch's). Loaded before torch, the library
+    # would map the system runtime and torch its own, two runtimes in one
+    # process, and the library's launches fail.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P = ctypes.POINTER
     lib.proxy_layer_workspace_size.argtypes = [P(PfLayerConfig), c_int32]
