@@ -5,6 +5,18 @@
 
 namespace pf {
 
+// Physical 16-byte chunk of logical chunk c in row r of an LDS tile whose
+// rows hold C chunks (C a power of two). A 16-byte read serves 16 lanes per
+// pass over 64 banks, i.e. 16 chunk slots of 256 bytes, and the fragment
+// reads put 16 consecutive rows (same logical chunk) in one pass: the XOR
+// term walks through all C chunks as r steps over the 16 / C rows that share
+// a 256-byte span, so the 16 rows land on 16 different slots.
+template <int C>
+__device__ __forceinline__ int lds_swz(int r, int c) {
+  static_assert(C >= 4 && (C & (C - 1)) == 0, "rows of 4, 8, 16, ... chunks");
+  return C >= 16 ? c ^ (r & 15) : c ^ ((r / (16 / C)) & (C - 1));
+}
+
 // Value of lane l ^ 32 (the other half of the wave), through the VALU.
 __device__ __forceinline__ float other_half(float x) {
   const uint32_t u = __builtin_bit_cast(uint32_t, x);

@@ -60,13 +60,6 @@ struct BwdShape {
   static_assert(kRowB >= 128 && kTRowB >= 64, "rows of at least 4 chunks");
 };
 
-// Physical 16-byte chunk of logical chunk c in row r of a tile whose rows
-// hold C chunks: rows of 8+ chunks XOR with r mod 8, rows of 4 chunks with
-// (r / 2) mod 4.
-template <int C>
-__device__ __forceinline__ int bswz(int r, int c) {
-  return c ^ (C >= 8 ? (r & 7) : ((r >> 1) & 3));
-}
 
 // A-operand fragment of a row-layout tile: row r, k-step kk (bf16: logical
 // chunk 2 kk + g; fp32: chunks 4 kk + 2 g and the next).
@@ -75,10 +68,10 @@ __device__ __forceinline__ typename Mma<T>::frag row_frag(const char* tile, int 
   constexpr int C = kRowB / 16;
   const char* row = tile + r * kRowB;
   if constexpr (sizeof(T) == 2) {
-    return *reinterpret_cast<const bf16x8*>(row + bswz<C>(r, kk * 2 + g) * 16);
+    return *reinterpret_cast<const bf16x8*>(row + lds_swz<C>(r, kk * 2 + g) * 16);
   } else {
-    const f32x4 lo = *reinterpret_cast<const f32x4*>(row + bswz<C>(r, kk * 4 + g * 2) * 16);
-    const f32x4 hi = *reinterpret_cast<const f32x4*>(row + bswz<C>(r, kk * 4 + g * 2 + 1) * 16);
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(row + lds_swz<C>(r, kk * 4 + g * 2) * 16);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(row + lds_swz<C>(r, kk * 4 + g * 2 + 1) * 16);
     typename Mma<T>::frag f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -110,10 +103,10 @@ __device__ __forceinline__ typename Mma<T>::frag t_frag(const char* tile, int d,
   constexpr int C = kTRowB / 16;
   const char* row = tile + d * kTRowB;
   if constexpr (sizeof(T) == 2) {
-    return *reinterpret_cast<const bf16x8*>(row + bswz<C>(d, s2 * 2 + g) * 16);
+    return *reinterpret_cast<const bf16x8*>(row + lds_swz<C>(d, s2 * 2 + g) * 16);
   } else {
-    const f32x4 lo = *reinterpret_cast<const f32x4*>(row + bswz<C>(d, s2 * 4 + g) * 16);
-    const f32x4 hi = *reinterpret_cast<const f32x4*>(row + bswz<C>(d, s2 * 4 + g + 2) * 16);
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(row + lds_swz<C>(d, s2 * 4 + g) * 16);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(row + lds_swz<C>(d, s2 * 4 + g + 2) * 16);
     typename Mma<T>::frag f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -131,13 +124,13 @@ template <int kRowB>
 __device__ __forceinline__ uint32_t row_voff(int blk, int lane) {
   constexpr int C = kRowB / 16;
   const int r = blk * (1024 / kRowB) + lane / C, pc = lane % C;
-  return (uint32_t)(r * kRowB + bswz<C>(r, pc) * 16);
+  return (uint32_t)(r * kRowB + lds_swz<C>(r, pc) * 16);
 }
 template <int kTRowB>
 __device__ __forceinline__ uint32_t t_voff(int blk, int lane, int64_t ld_bytes) {
   constexpr int C = kTRowB / 16;
   const int r = blk * (1024 / kTRowB) + lane / C, pc = lane % C;
-  return (uint32_t)(r * ld_bytes + bswz<C>(r, pc) * 16);
+  return (uint32_t)(r * ld_bytes + lds_swz<C>(r, pc) * 16);
 }
 
 // Stages of kInsts 1 KB loads are dealt to the four waves in contiguous

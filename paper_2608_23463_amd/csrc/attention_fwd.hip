@@ -39,8 +39,6 @@ struct AttnFwdShape {
   static_assert(kKTile % 1024 == 0 && kVTile % 1024 == 0 && kInsts % 4 == 0, "stage splits into wave loads");
 };
 
-// Physical 16-byte chunk of logical chunk c in row r.
-__device__ __forceinline__ int swz(int r, int c) { return c ^ (r & 7); }
 
 template <typename T, int DH, bool SPLIT, int NS, int OCC>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
@@ -114,11 +112,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
       if (off < S::kKParts * S::kKTile) {  // K: row = key, contiguous rows
         r = off < S::kKTile ? rk : rkl;
         const int row = (off % S::kKTile) / S::kRowBytes + lane / (S::kRowBytes / 16);
-        vo = (uint32_t)(row * S::kRowBytes + swz(row, lane % (S::kRowBytes / 16)) * 16);
+        vo = (uint32_t)(row * S::kRowBytes + lds_swz<S::kRowBytes / 16>(row, lane % (S::kRowBytes / 16)) * 16);
       } else {  // V^T: row = channel, stride ld_t
         r = rv;
         const int row = (off - S::kKParts * S::kKTile) / S::kVRowBytes + lane / (S::kVRowBytes / 16);
-        vo = (uint32_t)((int64_t)row * p.ld_t * sizeof(T) + swz(row, lane % (S::kVRowBytes / 16)) * 16);
+        vo = (uint32_t)((int64_t)row * p.ld_t * sizeof(T) + lds_swz<S::kVRowBytes / 16>(row, lane % (S::kVRowBytes / 16)) * 16);
       }
       buf_ld16_lds(r, vo, st + off);
     }
@@ -169,13 +167,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
         for (int kk = 0; kk < DH / 16; ++kk) {
           typename MM::frag kh, kl;
           if constexpr (sizeof(T) == 2) {
-            const int off = swz(kr, kk * 2 + g) * 16;
+            const int off = lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16;
             kh = *reinterpret_cast<const typename MM::frag*>(krow + off);
             if constexpr (SPLIT) kl = *reinterpret_cast<const typename MM::frag*>(krow + S::kKTile + off);
           } else {
             const int c0 = kk * 4 + g * 2;
-            const f32x4 lo = *reinterpret_cast<const f32x4*>(krow + swz(kr, c0) * 16);
-            const f32x4 hi = *reinterpret_cast<const f32x4*>(krow + swz(kr, c0 + 1) * 16);
+            const f32x4 lo = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0) * 16);
+            const f32x4 hi = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0 + 1) * 16);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               kh[e] = lo[e];
@@ -253,10 +251,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
             const char* vrow = sv + d * S::kVRowBytes;
             typename MM::frag va;
             if constexpr (sizeof(T) == 2) {
-              va = *reinterpret_cast<const typename MM::frag*>(vrow + swz(d, c0 / 8) * 16);
+              va = *reinterpret_cast<const typename MM::frag*>(vrow + lds_swz<S::kVRowBytes / 16>(d, c0 / 8) * 16);
             } else {
-              const f32x4 lo = *reinterpret_cast<const f32x4*>(vrow + swz(d, c4 / 4) * 16);
-              const f32x4 hi = *reinterpret_cast<const f32x4*>(vrow + swz(d, c4 / 4 + 2) * 16);
+              const f32x4 lo = *reinterpret_cast<const f32x4*>(vrow + lds_swz<S::kVRowBytes / 16>(d, c4 / 4) * 16);
+              const f32x4 hi = *reinterpret_cast<const f32x4*>(vrow + lds_swz<S::kVRowBytes / 16>(d, c4 / 4 + 2) * 16);
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 va[e] = lo[e];

@@ -118,17 +118,6 @@ struct GenShape {
   static_assert(kKTile % 1024 == 0 && kVTile % 1024 == 0 && (kStage / 1024) % 4 == 0, "stage splits into wave loads");
 };
 
-// Physical 16-byte chunk of logical chunk c in row r of a tile with NC
-// chunks per row. A 16-byte LDS read serves 16 lanes per pass across 64
-// banks (16 chunk slots of 256 bytes); the fragment reads put 16 consecutive
-// rows in one pass, so those rows must land on 16 different slots: with
-// 128-byte rows (NC = 8) row parity picks the half and (r / 2) % 8 the
-// chunk, with 256 bytes or more r % 16 picks the chunk.
-template <int NC>
-__device__ __forceinline__ int gswz(int r, int c) {
-  static_assert(NC == 8 || NC >= 16, "rows of 128 bytes or of 256 bytes and more");
-  return NC == 8 ? c ^ ((r >> 1) & 7) : c ^ (r & 15);
-}
 
 // One softmax over the keys lo .. hi (inclusive, per lane; hi < lo: none) of
 // the 64-key tiles t_first .. t_last. Keys come from kp (rows of DH, nkeys
@@ -171,11 +160,11 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
       if (off < S::kKTile) {  // K: row = key
         r = rk;
         const int row = off / S::kRowBytes + lane / (S::kRowBytes / 16);
-        vo = (uint32_t)(row * S::kRowBytes + gswz<S::kRowBytes / 16>(row, lane % (S::kRowBytes / 16)) * 16);
+        vo = (uint32_t)(row * S::kRowBytes + lds_swz<S::kRowBytes / 16>(row, lane % (S::kRowBytes / 16)) * 16);
       } else {  // V^T: row = channel, stride ld_v
         r = rv;
         const int row = (off - S::kKTile) / S::kVRowBytes + lane / (S::kVRowBytes / 16);
-        vo = (uint32_t)((int64_t)row * ld_v * sizeof(T) + gswz<S::kVRowBytes / 16>(row, lane % (S::kVRowBytes / 16)) * 16);
+        vo = (uint32_t)((int64_t)row * ld_v * sizeof(T) + lds_swz<S::kVRowBytes / 16>(row, lane % (S::kVRowBytes / 16)) * 16);
       }
       buf_ld16_lds(r, vo, st + off);
     }
@@ -204,11 +193,11 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
       for (int kk = 0; kk < DH / 16; ++kk) {
         typename MM::frag kh;
         if constexpr (sizeof(T) == 2) {
-          kh = *reinterpret_cast<const typename MM::frag*>(krow + gswz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16);
+          kh = *reinterpret_cast<const typename MM::frag*>(krow + lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16);
         } else {
           const int c0 = kk * 4 + g * 2;
-          const f32x4 a = *reinterpret_cast<const f32x4*>(krow + gswz<S::kRowBytes / 16>(kr, c0) * 16);
-          const f32x4 b = *reinterpret_cast<const f32x4*>(krow + gswz<S::kRowBytes / 16>(kr, c0 + 1) * 16);
+          const f32x4 a = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0) * 16);
+          const f32x4 b = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0 + 1) * 16);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             kh[e] = a[e];
@@ -278,10 +267,10 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
           const char* vrow = sv + dd * S::kVRowBytes;
           typename MM::frag va;
           if constexpr (sizeof(T) == 2) {
-            va = *reinterpret_cast<const typename MM::frag*>(vrow + gswz<S::kVRowBytes / 16>(dd, c0 / 8) * 16);
+            va = *reinterpret_cast<const typename MM::frag*>(vrow + lds_swz<S::kVRowBytes / 16>(dd, c0 / 8) * 16);
           } else {
-            const f32x4 a = *reinterpret_cast<const f32x4*>(vrow + gswz<S::kVRowBytes / 16>(dd, c4 / 4) * 16);
-            const f32x4 b = *reinterpret_cast<const f32x4*>(vrow + gswz<S::kVRowBytes / 16>(dd, c4 / 4 + 2) * 16);
+            const f32x4 a = *reinterpret_cast<const f32x4*>(vrow + lds_swz<S::kVRowBytes / 16>(dd, c4 / 4) * 16);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(vrow + lds_swz<S::kVRowBytes / 16>(dd, c4 / 4 + 2) * 16);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               va[e] = a[e];
