@@ -29,6 +29,9 @@ the C-ABI):
   [X, Delta]: G = X W_gx^T + Delta W_gd^T + b_g with W_g = [W_gx | W_gd].
 * Intermediate level widths d_j default to d_proxy; there is no
   non-linearity between levels (the cascade is reshape -> project).
+* A length L that is not a multiple of P gives m = ceil(L/P) blocks
+  (Sec. 3.1); the partial last block is zero-padded to P tokens, the
+  padding's outputs are dropped and it receives no gradient.
 """
 from __future__ import annotations
 
@@ -195,7 +198,14 @@ def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
     p_blk = int(np.prod(factors))
     m = seq // p_blk
     if m * p_blk != seq:
-        raise ValueError("seq_len must be a multiple of the block size P")
+        # m = ceil(L/P) blocks (Sec. 3.1): the partial last block is read as
+        # zero-padded to P tokens; outputs of the padding are dropped
+        # (sampled blocks keep the padded rows of the last block)
+        xp = np.concatenate([x, np.zeros((bsz, (m + 1) * p_blk - seq, d_f))], axis=1)
+        res = layer_forward(xp, weights, factors, n_heads, mask, h_in, sample_blocks, keep, injection)
+        if sample_blocks is None:
+            res["x_out"] = res["x_out"][:, :seq]
+        return res
     d_p = weights["q"][0].shape[0]
     h_out = np.zeros((bsz, m, d_p))
     if sample_blocks is None:
@@ -294,11 +304,20 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
     summed over the batch in the layout of the weights, and the gradients of
     the projections Q, K, V per proxy ("proj_grads", [B, m, d_proxy] each).
     """
-    fwd = layer_forward(x, weights, factors, n_heads, mask, h_in, keep=True, injection=injection)
     dy = _f64(dy)
     bsz, seq, d_f = dy.shape
     p_blk = int(np.prod(factors))
     m = seq // p_blk
+    if m * p_blk != seq:
+        # zero-padded last block (Sec. 3.1): the padding receives no gradient
+        # (dY = 0 there) and its dX is dropped
+        pad = (m + 1) * p_blk - seq
+        xp = np.concatenate([_f64(x), np.zeros((bsz, pad, d_f))], axis=1)
+        dyp = np.concatenate([dy, np.zeros((bsz, pad, d_f))], axis=1)
+        res = layer_backward(xp, weights, factors, n_heads, dyp, mask, h_in, dh_out, injection)
+        res["dx"] = res["dx"][:, :seq]
+        return res
+    fwd = layer_forward(x, weights, factors, n_heads, mask, h_in, keep=True, injection=injection)
     nlev = len(factors)
 
     def zgrad(w):

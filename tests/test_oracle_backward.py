@@ -185,3 +185,36 @@ def test_key_bias_gradient_vanishes():
         assert scale > 1e-3
         assert np.max(np.abs(res["grads"]["k"][1])) < 1e-12 * scale
         np.testing.assert_allclose(res["grads"]["k"][1], res["proj_grads"]["k"].sum(axis=(0, 1)), atol=1e-14)
+
+
+@pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BIDIRECTIONAL])
+def test_backward_finite_differences_partial_last_block(mask):
+    """L % P != 0: the zero-padded last block (Sec. 3.1) in the backward."""
+    rng = np.random.default_rng(95 + mask)
+    factors = (2, 2)
+    d_f, d_p, nh, L, B = 4, 6, 2, 14, 2
+    w = rand_weights(rng, d_f, d_p, factors, std=0.4)
+    x = rng.standard_normal((B, L, d_f))
+    m = -(-L // 4)
+    h_in = rng.standard_normal((B, m, d_p))
+    dy = rng.standard_normal((B, L, d_f))
+    dh = rng.standard_normal((B, m, d_p))
+    res = oracle.layer_backward(x, w, factors, nh, dy, mask, h_in, dh)
+    assert res["dx"].shape == x.shape
+    eps = 1e-5
+    for idx in [(0, 0, 1), (1, 12, 2), (0, 13, 0), (1, 13, 3)]:   # incl. the partial block's tokens
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += eps
+        xm[idx] -= eps
+        fd = (_loss(xp, w, factors, nh, mask, h_in, dy, dh) - _loss(xm, w, factors, nh, mask, h_in, dy, dh)) / (2 * eps)
+        assert abs(fd - res["dx"][idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, res["dx"][idx])
+    for path in _param_paths(w):
+        wt = _get(w, path)
+        flat = np.unravel_index(rng.integers(wt.size), wt.shape)
+        wp, wm = wt.copy(), wt.copy()
+        wp[flat] += eps
+        wm[flat] -= eps
+        fd = (_loss(x, _set(w, path, wp), factors, nh, mask, h_in, dy, dh)
+              - _loss(x, _set(w, path, wm), factors, nh, mask, h_in, dy, dh)) / (2 * eps)
+        g = _grad_of(res["grads"], path)[flat]
+        assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)

@@ -364,3 +364,47 @@ def test_sampled_forward_matches_full():
         ref = full["x_out"].reshape(2, 8, 4, d_f)[:, blocks]
         np.testing.assert_allclose(s["x_out"], ref, rtol=1e-13, atol=1e-13)
         np.testing.assert_array_equal(s["h_out"], full["h_out"])
+
+
+# ------------------------------------------------------ partial last block
+
+@pytest.mark.parametrize("factors", [(4,), (2, 2)])
+def test_partial_last_block_prefix_and_last_proxy(factors):
+    """m = ceil(L / P) blocks (Sec. 3.1), the last one partial: with token
+    causality the complete blocks' outputs and proxies equal those of the
+    layer run on the complete blocks alone, and the last proxy is the
+    compression of the partial block with zero padding, i.e. its weight
+    columns for the missing tokens drop out."""
+    rng = np.random.default_rng(90 + len(factors))
+    d_f, d_p, nh, B = 4, 6, 2, 2
+    P = int(np.prod(factors))
+    full, rem = 3, 3                      # three complete blocks and 3 tokens
+    L = full * P + rem
+    w = rand_weights(rng, d_f, d_p, factors)
+    x = rng.standard_normal((B, L, d_f))
+    res = oracle.layer_forward(x, w, factors, nh, oracle.TOKEN_CAUSAL)
+    assert res["x_out"].shape == (B, L, d_f) and res["h_out"].shape == (B, full + 1, d_p)
+    head = oracle.layer_forward(x[:, :full * P], w, factors, nh, oracle.TOKEN_CAUSAL)
+    np.testing.assert_array_equal(res["x_out"][:, :full * P], head["x_out"])
+    np.testing.assert_array_equal(res["h_out"][:, :full], head["h_out"])
+    if len(factors) == 1:
+        wc, bc = w["compress"][0]
+        for b in range(B):
+            tail = x[b, full * P:].reshape(-1)
+            np.testing.assert_allclose(res["h_out"][b, -1], wc[:, :rem * d_f] @ tail + bc, rtol=1e-12, atol=1e-12)
+
+
+def test_partial_last_block_outputs_ignore_padding_content():
+    """Under token causality the partial block receives the proxy of the block
+    before it, so its outputs do not depend on what fills the missing tokens;
+    under block causality they do (its own proxy includes the padding)."""
+    rng = np.random.default_rng(93)
+    d_f, d_p, nh, B, P = 4, 6, 2, 1, 4
+    L = 2 * P + 1
+    w = rand_weights(rng, d_f, d_p, (P,))
+    x = rng.standard_normal((B, L, d_f))
+    junk = np.concatenate([x, rng.standard_normal((B, 3 * P - L, d_f))], axis=1)
+    for mask, same in ((oracle.TOKEN_CAUSAL, True), (oracle.BLOCK_CAUSAL, False)):
+        a = oracle.layer_forward(x, w, (P,), nh, mask)["x_out"]
+        b = oracle.layer_forward(junk, w, (P,), nh, mask)["x_out"][:, :L]
+        assert np.array_equal(a, b) == same, mask
