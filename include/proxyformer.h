@@ -69,7 +69,12 @@ typedef struct {
 
 /* One layer call (Algorithm 1 inputs; factorisation of Eq. 15).
  *  batch     B >= 1 sequences, processed independently.
- *  seq_len   L tokens per sequence; must be a multiple of P.
+ *  seq_len   L >= 1 tokens per sequence. There are m = ceil(L / P) blocks
+ *            (Sec. 3.1); when P does not divide L the last block is
+ *            zero-padded to P tokens inside the library (its proxy sees the
+ *            padding as zeros; the padding produces no output and receives
+ *            no gradient). The workspace then also holds padded copies of
+ *            the token tensors.
  *  d_fine    local-stream width d_0.
  *  d_proxy   proxy width d_M = n_heads * head_dim.
  *  n_levels  M in 1..4; factors[0..M-1] = k_1..k_M, P = prod k_j.

@@ -266,7 +266,7 @@ def layer_forward(cfg: PfLayerConfig, weights: Dict[str, object], x, h_in=None, 
                   workspace=None, stream=None):
     """Allocate outputs (and workspace), run the forward; returns (x_out, h_out, saved)."""
     import torch
-    m = cfg.seq_len // _block(cfg)
+    m = -(-cfg.seq_len // _block(cfg))  # ceil(L / P): a partial last block has a proxy
     x_out = torch.empty_like(x)
     h_out = torch.empty((cfg.batch, m, cfg.d_proxy), dtype=x.dtype, device=x.device)
     saved = _bytes(layer_saved_size(cfg), x.device) if save else None

@@ -95,7 +95,7 @@ int proxy_layer_forward(const pf_layer_config* cfg, const pf_layer_weights* w, c
   if (!aligned16(x) || !aligned16(x_out) || !aligned16(h_out) || (h_in && !aligned16(h_in)) ||
       (saved && !aligned16(saved)))
     return fail(PF_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-  const size_t tok_bytes = (size_t)d.B * d.L * d.d_f * d.esize;
+  const size_t tok_bytes = (size_t)d.B * d.L_in * d.d_f * d.esize;
   const size_t prox_bytes = (size_t)d.B * d.m * d.d_p * d.esize;
   if (overlaps(x, tok_bytes, x_out, tok_bytes)) return fail(PF_ERR_INVALID_ARG, "x_out must not alias x");
   if (overlaps(h_out, prox_bytes, x_out, tok_bytes) || overlaps(h_out, prox_bytes, x, tok_bytes))
@@ -106,9 +106,20 @@ int proxy_layer_forward(const pf_layer_config* cfg, const pf_layer_weights* w, c
   char* ws = reinterpret_cast<char*>(workspace);
   char* acts = saved ? reinterpret_cast<char*>(saved) : ws + W.acts;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = cfg->dtype == PF_BF16
-                     ? layer_forward_run<bf16>(d, cfg, w, x, h_in, x_out, h_out, acts, saved != nullptr, ws, s)
-                     : layer_forward_run<float>(d, cfg, w, x, h_in, x_out, h_out, acts, saved != nullptr, ws, s);
+  const bool padded = d.L_in != d.L;  // partial last block: run on a zero-padded copy
+  const int64_t row_bytes = (int64_t)d.d_f * d.esize;
+  const void* xk = x;
+  void* yk = x_out;
+  hipError_t e = hipSuccess;
+  if (padded) {
+    xk = ws + W.x_pad;
+    yk = ws + W.y_pad;
+    e = pad_rows(x, ws + W.x_pad, d.B, d.L_in, d.L, row_bytes, s);
+    if (e != hipSuccess) return hip_status(e, "proxy_layer_forward padding");
+  }
+  e = cfg->dtype == PF_BF16 ? layer_forward_run<bf16>(d, cfg, w, xk, h_in, yk, h_out, acts, saved != nullptr, ws, s)
+                            : layer_forward_run<float>(d, cfg, w, xk, h_in, yk, h_out, acts, saved != nullptr, ws, s);
+  if (e == hipSuccess && padded) e = unpad_rows(yk, x_out, d.B, d.L_in, d.L, row_bytes, s);
   return hip_status(e, "proxy_layer_forward launch");
 }
 
@@ -127,7 +138,7 @@ int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w, 
   if (!aligned16(x) || !aligned16(saved) || !aligned16(dy) || !aligned16(dx) || (dh_out && !aligned16(dh_out)) ||
       (dh_in && !aligned16(dh_in)) || (h_in && !aligned16(h_in)))
     return fail(PF_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-  const size_t tok_bytes = (size_t)d.B * d.L * d.d_f * d.esize;
+  const size_t tok_bytes = (size_t)d.B * d.L_in * d.d_f * d.esize;
   if (overlaps(dx, tok_bytes, dy, tok_bytes)) return fail(PF_ERR_INVALID_ARG, "dx must not alias dy");
   const LayerWs W = layer_ws(d, true);
   if (W.bytes && (!workspace || ws_bytes < W.bytes))
@@ -135,10 +146,26 @@ int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w, 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const char* sv = reinterpret_cast<const char*>(saved);
   char* ws = reinterpret_cast<char*>(workspace);
-  hipError_t e = cfg->dtype == PF_BF16
-                     ? layer_backward_run<bf16>(d, cfg, w, x, h_in, sv, dy, dh_out, dx, dh_in, grads, ws, s)
-                     : layer_backward_run<float>(d, cfg, w, x, h_in, sv, dy, dh_out, dx, dh_in, grads, ws, s);
+  // partial last block: the padding has dY = 0 and its dX is dropped
+  const bool padded = d.L_in != d.L;
+  const int64_t row_bytes = (int64_t)d.d_f * d.esize;
+  const void* xk = x;
+  const void* dyk = dy;
+  void* dxk = dx;
+  hipError_t e = hipSuccess;
+  if (padded) {
+    xk = ws + W.x_pad;
+    dyk = ws + W.dy_pad;
+    dxk = ws + W.y_pad;
+    e = pad_rows(x, ws + W.x_pad, d.B, d.L_in, d.L, row_bytes, s);
+    if (e == hipSuccess) e = pad_rows(dy, ws + W.dy_pad, d.B, d.L_in, d.L, row_bytes, s);
+    if (e != hipSuccess) return hip_status(e, "proxy_layer_backward padding");
+  }
+  e = cfg->dtype == PF_BF16
+          ? layer_backward_run<bf16>(d, cfg, w, xk, h_in, sv, dyk, dh_out, dxk, dh_in, grads, ws, s)
+          : layer_backward_run<float>(d, cfg, w, xk, h_in, sv, dyk, dh_out, dxk, dh_in, grads, ws, s);
   if (e == hipErrorNotSupported) return fail(PF_ERR_UNSUPPORTED, "backward not available for this config");
+  if (e == hipSuccess && padded) e = unpad_rows(dxk, dx, d.B, d.L_in, d.L, row_bytes, s);
   return hip_status(e, "proxy_layer_backward launch");
 }
 

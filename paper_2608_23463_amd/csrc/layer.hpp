@@ -17,7 +17,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct LayerDims {
   int B;
-  int64_t L;
+  int64_t L;        // tokens per sequence the kernels see: m * P (the last block zero-padded)
+  int64_t L_in;     // tokens per sequence of the caller's tensors (<= L)
   int d_f, d_p, nh, dh;
   int M;            // levels
   int k[PF_MAX_LEVELS];
@@ -70,6 +71,10 @@ struct LayerWs {
   size_t colsum2;             // second-stage partials (64 groups)
   size_t tr_a, tr_b;          // transposed GEMM operands of the large weight gradients [cols, rows]
   size_t tr_w;                // a transposed weight [in, out] for the large data gradients
+  // L_in < L: the caller's token tensors padded to L tokens per sequence
+  size_t x_pad;               // X with zero padding [B*L, d_f]
+  size_t y_pad;               // forward: X_out; backward: dX [B*L, d_f]
+  size_t dy_pad;              // backward: dY with zero padding [B*L, d_f]
   size_t bytes;
 };
 
@@ -78,6 +83,14 @@ constexpr int kColsumChunks = 512;
 // (K-contiguous) operand copies through the direct GEMM kernel.
 constexpr int64_t kTransposeMinRows = 8192;
 inline int64_t round8(int64_t v) { return (v + 7) / 8 * 8; }
+
+// dst[b, t] = t < L_in ? src[b, t] : 0 for t < L_pad, rows of row_bytes (a
+// multiple of 16) with per-sequence strides L_in and L_pad rows.
+hipError_t pad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L_pad, int64_t row_bytes,
+                    hipStream_t stream);
+// dst[b, t] = src[b, t] for t < L_in (the first L_in of L_pad rows per sequence).
+hipError_t unpad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L_pad, int64_t row_bytes,
+                      hipStream_t stream);
 
 // Validates cfg; on failure returns a status and writes a message.
 int layer_dims(const pf_layer_config* cfg, LayerDims* d, const char** why);

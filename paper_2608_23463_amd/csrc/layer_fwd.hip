@@ -37,6 +37,32 @@ hipError_t fill_zero(void* p, size_t bytes, hipStream_t stream) {
   return hipGetLastError();
 }
 
+__global__ void pad_rows_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst, int64_t L_in,
+                                int64_t L_pad, int64_t row16, int64_t total) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const int64_t c = i % row16, r = i / row16;
+    const int64_t b = r / L_pad, t = r - b * L_pad;
+    dst[i] = t < L_in ? src[(b * L_in + t) * row16 + c] : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+hipError_t pad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L_pad, int64_t row_bytes,
+                    hipStream_t stream) {
+  const int64_t row16 = row_bytes / 16, total = (int64_t)B * L_pad * row16;
+  if (total == 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(pad_rows_kernel, dim3(blocks), dim3(256), 0, stream, reinterpret_cast<const u32x4*>(src),
+                     reinterpret_cast<u32x4*>(dst), L_in, L_pad, row16, total);
+  return hipGetLastError();
+}
+
+hipError_t unpad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L_pad, int64_t row_bytes,
+                      hipStream_t stream) {
+  return hipMemcpy2DAsync(dst, (size_t)(L_in * row_bytes), src, (size_t)(L_pad * row_bytes),
+                          (size_t)(L_in * row_bytes), (size_t)B, hipMemcpyDeviceToDevice, stream);
+}
+
 int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   *why = nullptr;
   if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
@@ -50,7 +76,7 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
     return *why = "widths and head counts must be >= 1", PF_ERR_INVALID_ARG;
   if ((int64_t)c->n_heads * c->head_dim != c->d_proxy) return *why = "n_heads * head_dim must equal d_proxy", PF_ERR_INVALID_ARG;
   d->B = c->batch;
-  d->L = c->seq_len;
+  d->L_in = c->seq_len;
   d->d_f = c->d_fine;
   d->d_p = c->d_proxy;
   d->nh = c->n_heads;
@@ -63,7 +89,8 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
     d->P *= c->factors[j];
     if (d->P > (1 << 20)) return *why = "block size P too large", PF_ERR_INVALID_ARG;
   }
-  if (d->L % d->P != 0) return *why = "seq_len must be a multiple of P = prod(factors)", PF_ERR_INVALID_ARG;
+  // m = ceil(L / P) blocks (Sec. 3.1); a partial last block is zero-padded
+  d->L = (d->L_in + d->P - 1) / d->P * d->P;
   d->d[0] = d->d_f;
   for (int j = 1; j < d->M; ++j) d->d[j] = c->level_dims[j - 1] > 0 ? c->level_dims[j - 1] : d->d_p;
   d->d[d->M] = d->d_p;
@@ -183,6 +210,11 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     w.tr_a = take(tr);
     w.tr_b = take(tr);
     w.tr_w = take(trw);
+  }
+  if (d.L_in != d.L) {
+    w.x_pad = take(tok);
+    w.y_pad = take(tok);
+    w.dy_pad = bwd ? take(tok) : 0;
   }
   w.gemm = off;
   w.bytes = off;

@@ -60,7 +60,8 @@ class LayerShape:
 
     @property
     def n_proxies(self) -> int:
-        return self.seq_len // self.block
+        # m = ceil(L / P) (Sec. 3.1): a partial last block still has a proxy
+        return -(-self.seq_len // self.block)
 
     def dims(self) -> List[int]:
         """d_0..d_M: d_0 = d_fine, d_j = level_dims[j-1] (0 or absent -> d_proxy), d_M = d_proxy."""

@@ -50,7 +50,7 @@ def test_size_queries(lib):
     # saved activations include at least Delta and G for every token
     assert saved >= 2 * 4096 * 256 * 2
     assert B.layer_workspace_size(cfg, True) > 0
-    for bad in (dict(seq_len=4000), dict(n_heads=3), dict(factors=()), dict(head_dim=32, n_heads=8),
+    for bad in (dict(seq_len=0), dict(n_heads=3), dict(factors=()), dict(head_dim=32, n_heads=8),
                 dict(d_fine=100), dict(batch=0), dict(dtype="fp16")):
         c = _cfg(**bad) if "dtype" not in bad else _cfg()
         if "dtype" in bad:
@@ -77,7 +77,7 @@ def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 
 
 
 @pytest.mark.parametrize("bad,status", [
-    (dict(seq_len=4000), B.PF_ERR_INVALID_ARG),
+    (dict(seq_len=0), B.PF_ERR_INVALID_ARG),
     (dict(n_heads=8), B.PF_ERR_INVALID_ARG),
     (dict(mask=5), B.PF_ERR_INVALID_ARG),
     (dict(injection=2), B.PF_ERR_INVALID_ARG),
@@ -88,6 +88,17 @@ def test_forward_rejects_bad_config(lib, bad, status):
     cfg = _cfg(**bad)
     assert _fwd(lib, cfg, _weights_struct()) == status
     assert B.last_error()
+
+
+def test_partial_last_block_sizes(lib):
+    # L = 4000 with P = 64: m = 63 blocks, the last zero-padded (Sec. 3.1)
+    ragged, whole = _cfg(seq_len=4000), _cfg(seq_len=63 * 64)
+    assert B.layer_saved_size(ragged) == B.layer_saved_size(whole)
+    tok = 4000 * 256 * 2
+    pad = 63 * 64 * 256 * 2
+    assert B.layer_workspace_size(ragged) >= B.layer_workspace_size(whole) + 2 * pad
+    assert B.layer_workspace_size(ragged, True) >= B.layer_workspace_size(whole, True) + 3 * pad
+    assert tok < pad
 
 
 def test_forward_rejects_bad_pointers(lib):

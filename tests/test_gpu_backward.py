@@ -89,6 +89,10 @@ CASES = {
     "bf16_inject_add": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_ADD), True),
     "fp32_inject_add_factorised": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
                                               injection=synth.INJECT_ADD), False),
+    # partial last block (L % P != 0): zero-padded inside the library, dY = 0 on the padding
+    "bf16_tc_partial_block": (LayerShape(2, 16 * 37 + 9, 192, 192, 3, 64, (16,)), True),
+    "fp32_bi_partial_block_factorised": (LayerShape(1, 8 * 37 + 5, 64, 128, 2, 64, (2, 4), level_dims=(96,),
+                                                    dtype="fp32", mask=synth.BIDIRECTIONAL), True),
 }
 
 
