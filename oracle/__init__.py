@@ -20,7 +20,7 @@ leaves open are listed in the module docstrings where they apply.
 from .layer import (  # noqa: F401
     TOKEN_CAUSAL, BLOCK_CAUSAL, BIDIRECTIONAL, INJECT_GATED, INJECT_ADD,
     sigmoid, compress, layer_forward, layer_backward, attention_rows,
-    proxies_and_attention_inputs,
+    proxies_and_attention_inputs, patch_order, layer_forward_2d, layer_backward_2d,
 )
 from .decode import DecodeState, decode_step, cache_append, prefill, rms_norm  # noqa: F401
 from .metrics import max_rel_err  # noqa: F401

@@ -29,6 +29,10 @@ the C-ABI):
   [X, Delta]: G = X W_gx^T + Delta W_gd^T + b_g with W_g = [W_gx | W_gd].
 * Intermediate level widths d_j default to d_proxy; there is no
   non-linearity between levels (the cascade is reshape -> project).
+* The 2-D partition of the vision instantiation (Sec. 3.9) groups each
+  p x p patch of a raster-order image into one block (P = p^2, one level),
+  tokens row by row inside the patch, patches in raster order of the patch
+  grid; the layer is otherwise unchanged (layer_forward_2d).
 * A length L that is not a multiple of P gives m = ceil(L/P) blocks
   (Sec. 3.1); the partial last block is zero-padded to P tokens, the
   padding's outputs are dropped and it receives no gradient.
@@ -385,3 +389,59 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             dz = ungroup_rows(dz @ _f64(weights["compress"][j][0]), factors[j])
         dx[b] = dxb + dz
     return {"dx": dx, "dh_in": dh_in, "grads": gr, "proj_grads": proj_grads}
+
+
+def patch_order(height: int, width: int, p: int):
+    """Token order of the 2-D partition (Sec. 3.9): blocks are the p x p
+    patches of a height x width raster-order image, taken in raster order
+    of the patch grid; inside a patch the tokens go row by row. Returns
+    order[j] = raster index of the j-th token of the partitioned sequence."""
+    if height % p or width % p:
+        raise ValueError("image sides must be multiples of the patch side")
+    order = []
+    for py in range(height // p):
+        for px in range(width // p):
+            for i in range(p):
+                for j in range(p):
+                    order.append((py * p + i) * width + px * p + j)
+    return np.asarray(order, dtype=np.int64)
+
+
+def _patch_side(factors: Sequence[int]) -> int:
+    if len(factors) != 1:
+        raise ValueError("the 2-D partition is single-level (P = p * p)")
+    p = int(round(np.sqrt(factors[0])))
+    if p * p != factors[0]:
+        raise ValueError("the 2-D partition needs P = p * p")
+    return p
+
+
+def layer_forward_2d(x, weights, factors: Sequence[int], n_heads: int, image_width: int,
+                     mask: int = BIDIRECTIONAL, h_in=None, injection: int = INJECT_GATED):
+    """The layer on an image (Sec. 3.9): x [B, height * width, d_fine] in
+    raster order, a block = one p x p patch (P = p^2), proxies in raster order
+    of the patch grid. The tokens are gathered into patch order, the layer of
+    Algorithm 1 runs on that sequence, and the output returns to raster
+    order. Returns x_out (raster order) and h_out [B, (height/p)(width/p), d_proxy]."""
+    x = _f64(x)
+    p = _patch_side(factors)
+    order = patch_order(x.shape[1] // image_width, image_width, p)
+    res = layer_forward(x[:, order], weights, factors, n_heads, mask, h_in, injection=injection)
+    y = np.zeros_like(x)
+    y[:, order] = res["x_out"]
+    return {"x_out": y, "h_out": res["h_out"]}
+
+
+def layer_backward_2d(x, weights, factors: Sequence[int], n_heads: int, image_width: int, dy,
+                      mask: int = BIDIRECTIONAL, h_in=None, dh_out=None, injection: int = INJECT_GATED):
+    """Gradients of layer_forward_2d: the gather is a permutation, so dY is
+    gathered the same way and dX scattered back to raster order."""
+    x = _f64(x)
+    p = _patch_side(factors)
+    order = patch_order(x.shape[1] // image_width, image_width, p)
+    res = layer_backward(x[:, order], weights, factors, n_heads, _f64(dy)[:, order], mask, h_in, dh_out,
+                         injection)
+    dx = np.zeros_like(x)
+    dx[:, order] = res["dx"]
+    res["dx"] = dx
+    return res

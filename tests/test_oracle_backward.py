@@ -218,3 +218,32 @@ def test_backward_finite_differences_partial_last_block(mask):
               - _loss(x, _set(w, path, wm), factors, nh, mask, h_in, dy, dh)) / (2 * eps)
         g = _grad_of(res["grads"], path)[flat]
         assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)
+
+
+def test_backward_finite_differences_2d_partition():
+    rng = np.random.default_rng(104)
+    d_f, d_p, nh, B, p, hgt, wid = 3, 4, 2, 1, 2, 4, 4
+    w = rand_weights(rng, d_f, d_p, (p * p,), std=0.4)
+    x = rng.standard_normal((B, hgt * wid, d_f))
+    dy = rng.standard_normal((B, hgt * wid, d_f))
+    res = oracle.layer_backward_2d(x, w, (p * p,), nh, wid, dy)
+
+    def loss(xx, ww):
+        return float(np.sum(oracle.layer_forward_2d(xx, ww, (p * p,), nh, wid)["x_out"] * dy))
+
+    eps = 1e-5
+    for idx in [(0, 0, 0), (0, 5, 1), (0, 10, 2), (0, 15, 0)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += eps
+        xm[idx] -= eps
+        fd = (loss(xp, w) - loss(xm, w)) / (2 * eps)
+        assert abs(fd - res["dx"][idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, res["dx"][idx])
+    for path in _param_paths(w):
+        wt = _get(w, path)
+        flat = np.unravel_index(rng.integers(wt.size), wt.shape)
+        wp, wm = wt.copy(), wt.copy()
+        wp[flat] += eps
+        wm[flat] -= eps
+        fd = (loss(x, _set(w, path, wp)) - loss(x, _set(w, path, wm))) / (2 * eps)
+        g = _grad_of(res["grads"], path)[flat]
+        assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)

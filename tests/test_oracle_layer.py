@@ -408,3 +408,54 @@ def test_partial_last_block_outputs_ignore_padding_content():
         a = oracle.layer_forward(x, w, (P,), nh, mask)["x_out"]
         b = oracle.layer_forward(junk, w, (P,), nh, mask)["x_out"][:, :L]
         assert np.array_equal(a, b) == same, mask
+
+
+# ------------------------------------------------------------ 2-D partition
+
+def test_patch_proxies_closed_form():
+    """Sec. 3.9: a block is a p x p patch. Without H_in each proxy is the
+    compression of its patch's pixels (row by row), patches in raster order."""
+    rng = np.random.default_rng(101)
+    d_f, d_p, nh, B, p, hgt, wid = 3, 4, 2, 2, 2, 4, 6
+    w = rand_weights(rng, d_f, d_p, (p * p,))
+    x = rng.standard_normal((B, hgt * wid, d_f))
+    res = oracle.layer_forward_2d(x, w, (p * p,), nh, wid)
+    wc, bc = w["compress"][0]
+    img = x.reshape(B, hgt, wid, d_f)
+    for b in range(B):
+        k = 0
+        for py in range(hgt // p):
+            for px in range(wid // p):
+                patch = img[b, py * p:(py + 1) * p, px * p:(px + 1) * p].reshape(-1)
+                np.testing.assert_allclose(res["h_out"][b, k], wc @ patch + bc, rtol=1e-12, atol=1e-12)
+                k += 1
+
+
+def test_patch_order_is_a_permutation_and_one_column_is_1d():
+    order = oracle.patch_order(6, 4, 2)
+    assert sorted(order.tolist()) == list(range(24))
+    # a single column of patches: patch order = raster order, same layer as 1-D
+    rng = np.random.default_rng(102)
+    w = rand_weights(rng, 3, 4, (4,))
+    x = rng.standard_normal((1, 8 * 2, 3))
+    np.testing.assert_array_equal(oracle.patch_order(8, 2, 2), np.arange(16))
+    a = oracle.layer_forward_2d(x, w, (4,), 2, 2, mask=oracle.BLOCK_CAUSAL)
+    b = oracle.layer_forward(x, w, (4,), 2, oracle.BLOCK_CAUSAL)
+    np.testing.assert_array_equal(a["x_out"], b["x_out"])
+
+
+def test_patch_block_causality():
+    """Block-causal over the patch grid: changing one pixel changes the outputs
+    of its own patch and of later patches only (raster order of patches)."""
+    rng = np.random.default_rng(103)
+    d_f, d_p, nh, p, hgt, wid = 3, 4, 2, 2, 4, 4
+    w = rand_weights(rng, d_f, d_p, (p * p,))
+    x = rng.standard_normal((1, hgt * wid, d_f))
+    y0 = oracle.layer_forward_2d(x, w, (p * p,), nh, wid, mask=oracle.BLOCK_CAUSAL)["x_out"]
+    x2 = x.copy()
+    x2[0, 2 * wid + 1] += 1.0            # pixel (2, 1): patch (1, 0), the third patch
+    y1 = oracle.layer_forward_2d(x2, w, (p * p,), nh, wid, mask=oracle.BLOCK_CAUSAL)["x_out"]
+    patch_of = lambda t: (t // wid // p) * (wid // p) + (t % wid) // p
+    for t in range(hgt * wid):
+        changed = not np.array_equal(y0[0, t], y1[0, t])
+        assert changed == (patch_of(t) >= 2), t
