@@ -81,7 +81,15 @@ typedef struct {
  *  level_dims[j] = d_{j+1} for j < M-1 (0 -> d_proxy); level_dims[M-1] is
  *            ignored (d_M = d_proxy).
  *  head_dim  64 or 128.
- *  dtype     pf_dtype; mask pf_mask; injection pf_injection. */
+ *  dtype     pf_dtype; mask pf_mask; injection pf_injection.
+ *  image_width  0: the tokens are a sequence and a block is P consecutive
+ *            tokens. > 0: 2-D partition of the vision instantiation
+ *            (Sec. 3.9): the tokens are a raster-order image of this width
+ *            and height seq_len / image_width, a block is one p x p patch
+ *            (P = p * p, n_levels = 1, both sides multiples of p), tokens
+ *            row by row inside a patch, blocks and proxies in raster order
+ *            of the patch grid. x, x_out, dy and dx stay in raster order;
+ *            the workspace then also holds patch-ordered copies of them. */
 typedef struct {
   int32_t batch;
   int64_t seq_len;
@@ -91,6 +99,7 @@ typedef struct {
   int32_t level_dims[PF_MAX_LEVELS];
   int32_t dtype, mask;
   int32_t injection;
+  int32_t image_width;
 } pf_layer_config;
 
 /* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)

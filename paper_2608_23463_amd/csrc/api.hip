@@ -106,20 +106,24 @@ int proxy_layer_forward(const pf_layer_config* cfg, const pf_layer_weights* w, c
   char* ws = reinterpret_cast<char*>(workspace);
   char* acts = saved ? reinterpret_cast<char*>(saved) : ws + W.acts;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const bool padded = d.L_in != d.L;  // partial last block: run on a zero-padded copy
+  // partial last block: run on a zero-padded copy; 2-D partition: on a
+  // patch-ordered copy
   const int64_t row_bytes = (int64_t)d.d_f * d.esize;
   const void* xk = x;
   void* yk = x_out;
   hipError_t e = hipSuccess;
-  if (padded) {
+  if (d.staged()) {
     xk = ws + W.x_pad;
     yk = ws + W.y_pad;
-    e = pad_rows(x, ws + W.x_pad, d.B, d.L_in, d.L, row_bytes, s);
-    if (e != hipSuccess) return hip_status(e, "proxy_layer_forward padding");
+    e = d.img_w ? permute_patches(x, ws + W.x_pad, d.B, d.L, d.img_w, d.patch, row_bytes, false, s)
+                : pad_rows(x, ws + W.x_pad, d.B, d.L_in, d.L, row_bytes, s);
+    if (e != hipSuccess) return hip_status(e, "proxy_layer_forward staging");
   }
   e = cfg->dtype == PF_BF16 ? layer_forward_run<bf16>(d, cfg, w, xk, h_in, yk, h_out, acts, saved != nullptr, ws, s)
                             : layer_forward_run<float>(d, cfg, w, xk, h_in, yk, h_out, acts, saved != nullptr, ws, s);
-  if (e == hipSuccess && padded) e = unpad_rows(yk, x_out, d.B, d.L_in, d.L, row_bytes, s);
+  if (e == hipSuccess && d.staged())
+    e = d.img_w ? permute_patches(yk, x_out, d.B, d.L, d.img_w, d.patch, row_bytes, true, s)
+                : unpad_rows(yk, x_out, d.B, d.L_in, d.L, row_bytes, s);
   return hip_status(e, "proxy_layer_forward launch");
 }
 
@@ -146,26 +150,33 @@ int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w, 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const char* sv = reinterpret_cast<const char*>(saved);
   char* ws = reinterpret_cast<char*>(workspace);
-  // partial last block: the padding has dY = 0 and its dX is dropped
-  const bool padded = d.L_in != d.L;
+  // partial last block: the padding has dY = 0 and its dX is dropped;
+  // 2-D partition: X and dY gathered into patch order, dX scattered back
   const int64_t row_bytes = (int64_t)d.d_f * d.esize;
   const void* xk = x;
   const void* dyk = dy;
   void* dxk = dx;
   hipError_t e = hipSuccess;
-  if (padded) {
+  if (d.staged()) {
     xk = ws + W.x_pad;
     dyk = ws + W.dy_pad;
     dxk = ws + W.y_pad;
-    e = pad_rows(x, ws + W.x_pad, d.B, d.L_in, d.L, row_bytes, s);
-    if (e == hipSuccess) e = pad_rows(dy, ws + W.dy_pad, d.B, d.L_in, d.L, row_bytes, s);
-    if (e != hipSuccess) return hip_status(e, "proxy_layer_backward padding");
+    if (d.img_w) {
+      e = permute_patches(x, ws + W.x_pad, d.B, d.L, d.img_w, d.patch, row_bytes, false, s);
+      if (e == hipSuccess) e = permute_patches(dy, ws + W.dy_pad, d.B, d.L, d.img_w, d.patch, row_bytes, false, s);
+    } else {
+      e = pad_rows(x, ws + W.x_pad, d.B, d.L_in, d.L, row_bytes, s);
+      if (e == hipSuccess) e = pad_rows(dy, ws + W.dy_pad, d.B, d.L_in, d.L, row_bytes, s);
+    }
+    if (e != hipSuccess) return hip_status(e, "proxy_layer_backward staging");
   }
   e = cfg->dtype == PF_BF16
           ? layer_backward_run<bf16>(d, cfg, w, xk, h_in, sv, dyk, dh_out, dxk, dh_in, grads, ws, s)
           : layer_backward_run<float>(d, cfg, w, xk, h_in, sv, dyk, dh_out, dxk, dh_in, grads, ws, s);
   if (e == hipErrorNotSupported) return fail(PF_ERR_UNSUPPORTED, "backward not available for this config");
-  if (e == hipSuccess && padded) e = unpad_rows(dxk, dx, d.B, d.L_in, d.L, row_bytes, s);
+  if (e == hipSuccess && d.staged())
+    e = d.img_w ? permute_patches(dxk, dx, d.B, d.L, d.img_w, d.patch, row_bytes, true, s)
+                : unpad_rows(dxk, dx, d.B, d.L_in, d.L, row_bytes, s);
   return hip_status(e, "proxy_layer_backward launch");
 }
 

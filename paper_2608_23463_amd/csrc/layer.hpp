@@ -27,6 +27,9 @@ struct LayerDims {
   int64_t P, m;
   int ld_t;         // row stride of transposed per-head tensors (m rounded up to 64)
   int esize;        // bytes per activation element
+  int img_w, patch; // 2-D partition: image width and patch side (0 for sequences)
+  // the caller's token tensors go through workspace copies (padded or patch-ordered)
+  bool staged() const { return L_in != L || img_w > 0; }
 };
 
 // Byte offsets of every activation inside the region that holds them
@@ -71,7 +74,8 @@ struct LayerWs {
   size_t colsum2;             // second-stage partials (64 groups)
   size_t tr_a, tr_b;          // transposed GEMM operands of the large weight gradients [cols, rows]
   size_t tr_w;                // a transposed weight [in, out] for the large data gradients
-  // L_in < L: the caller's token tensors padded to L tokens per sequence
+  // staged token tensors (L_in < L: zero-padded to L tokens; 2-D partition:
+  // in patch order)
   size_t x_pad;               // X with zero padding [B*L, d_f]
   size_t y_pad;               // forward: X_out; backward: dX [B*L, d_f]
   size_t dy_pad;              // backward: dY with zero padding [B*L, d_f]
@@ -91,6 +95,12 @@ hipError_t pad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L_p
 // dst[b, t] = src[b, t] for t < L_in (the first L_in of L_pad rows per sequence).
 hipError_t unpad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L_pad, int64_t row_bytes,
                       hipStream_t stream);
+
+// 2-D partition: position j of the patch-ordered sequence holds raster
+// token perm(j) of an image of width w with p x p patches. Gather:
+// dst[b, j] = src[b, perm(j)]; scatter: dst[b, perm(j)] = src[b, j].
+hipError_t permute_patches(const void* src, void* dst, int B, int64_t L, int w, int p, int64_t row_bytes,
+                           bool scatter, hipStream_t stream);
 
 // Validates cfg; on failure returns a status and writes a message.
 int layer_dims(const pf_layer_config* cfg, LayerDims* d, const char** why);

@@ -63,6 +63,32 @@ hipError_t unpad_rows(const void* src, void* dst, int B, int64_t L_in, int64_t L
                           (size_t)(L_in * row_bytes), (size_t)B, hipMemcpyDeviceToDevice, stream);
 }
 
+__global__ void permute_patches_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst, int64_t L, int w,
+                                       int p, int64_t row16, int64_t total, int scatter) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t P = (int64_t)p * p, pw = w / p;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const int64_t c = i % row16, r = i / row16;
+    const int64_t b = r / L, j = r - b * L;
+    const int64_t blk = j / P, u = j - blk * P;
+    const int64_t t = ((blk / pw) * p + u / p) * w + (blk % pw) * p + u % p;  // raster index
+    if (scatter)
+      dst[(b * L + t) * row16 + c] = src[i];
+    else
+      dst[i] = src[(b * L + t) * row16 + c];
+  }
+}
+
+hipError_t permute_patches(const void* src, void* dst, int B, int64_t L, int w, int p, int64_t row_bytes,
+                           bool scatter, hipStream_t stream) {
+  const int64_t row16 = row_bytes / 16, total = (int64_t)B * L * row16;
+  if (total == 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(permute_patches_kernel, dim3(blocks), dim3(256), 0, stream, reinterpret_cast<const u32x4*>(src),
+                     reinterpret_cast<u32x4*>(dst), L, w, p, row16, total, scatter ? 1 : 0);
+  return hipGetLastError();
+}
+
 int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   *why = nullptr;
   if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
@@ -91,6 +117,21 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   }
   // m = ceil(L / P) blocks (Sec. 3.1); a partial last block is zero-padded
   d->L = (d->L_in + d->P - 1) / d->P * d->P;
+  d->img_w = 0;
+  d->patch = 0;
+  if (c->image_width < 0) return *why = "image_width must be >= 0", PF_ERR_INVALID_ARG;
+  if (c->image_width > 0) {  // 2-D partition (Sec. 3.9)
+    if (d->M != 1) return *why = "the 2-D partition takes one level (P = p * p)", PF_ERR_UNSUPPORTED;
+    int p = 1;
+    while ((int64_t)(p + 1) * (p + 1) <= d->P) ++p;
+    if ((int64_t)p * p != d->P) return *why = "the 2-D partition needs P = p * p", PF_ERR_INVALID_ARG;
+    if (d->L_in % c->image_width != 0) return *why = "seq_len must be image_width * height", PF_ERR_INVALID_ARG;
+    const int64_t h = d->L_in / c->image_width;
+    if (c->image_width % p != 0 || h % p != 0)
+      return *why = "image width and height must be multiples of the patch side", PF_ERR_INVALID_ARG;
+    d->img_w = c->image_width;
+    d->patch = p;
+  }
   d->d[0] = d->d_f;
   for (int j = 1; j < d->M; ++j) d->d[j] = c->level_dims[j - 1] > 0 ? c->level_dims[j - 1] : d->d_p;
   d->d[d->M] = d->d_p;
@@ -211,7 +252,7 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     w.tr_b = take(tr);
     w.tr_w = take(trw);
   }
-  if (d.L_in != d.L) {
+  if (d.staged()) {
     w.x_pad = take(tok);
     w.y_pad = take(tok);
     w.dy_pad = bwd ? take(tok) : 0;

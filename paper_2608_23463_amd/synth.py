@@ -50,6 +50,7 @@ class LayerShape:
     dtype: str = "bf16"               # "bf16" or "fp32"
     mask: int = TOKEN_CAUSAL
     injection: int = INJECT_GATED
+    image_width: int = 0              # > 0: raster-order image, blocks are p x p patches (Sec. 3.9)
 
     @property
     def block(self) -> int:

@@ -223,3 +223,18 @@ def test_prefill_validation(lib):
     st = _dstate(n=1)
     assert call(st, n_tok=0, x=None, y=None) == B.PF_OK
     assert st.n == 1 and st.j == 0
+
+
+def test_2d_partition_validation(lib):
+    ok = _cfg(seq_len=64 * 64, factors=(64,))
+    ok.image_width = 64
+    assert B.layer_workspace_size(ok) > B.layer_workspace_size(_cfg(seq_len=64 * 64, factors=(64,)))
+    for bad_w, fac, status in ((60, (64,), B.PF_ERR_INVALID_ARG),    # width not a multiple of p = 8
+                               (48, (64,), B.PF_ERR_INVALID_ARG),    # 4096 / 48 is not whole
+                               (64, (32,), B.PF_ERR_INVALID_ARG),    # P not a square
+                               (64, (4, 16), B.PF_ERR_UNSUPPORTED),  # one level only
+                               (-1, (64,), B.PF_ERR_INVALID_ARG)):
+        c = _cfg(seq_len=64 * 64, factors=fac)
+        c.image_width = bad_w
+        assert _fwd(lib, c, _weights_struct(nlev=len(fac))) == status, (bad_w, fac)
+        assert B.layer_workspace_size(c) == 0

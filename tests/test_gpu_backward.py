@@ -154,3 +154,25 @@ def test_backward_run_twice_bitwise(gpu):
     for name in ("q", "k", "v", "o", "gate"):
         assert torch.equal(a[2][name][0], b[2][name][0]) and torch.equal(a[2][name][1], b[2][name][1])
     assert torch.equal(a[2]["compress"][0][0], b[2]["compress"][0][0])
+
+
+@pytest.mark.parametrize("name,shape", [
+    ("bf16_image_32x32_p4_bi", LayerShape(1, 32 * 32, 128, 256, 4, 64, (16,), mask=synth.BIDIRECTIONAL,
+                                          image_width=32)),
+    ("fp32_image_16x24_p4_bc", LayerShape(1, 16 * 24, 64, 128, 2, 64, (16,), dtype="fp32",
+                                          mask=synth.BLOCK_CAUSAL, image_width=24)),
+])
+def test_backward_parity_2d_partition(gpu, name, shape):
+    print(f"[case {name}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, zlib.crc32(name.encode()) % 1000, with_dy=True, with_h_in=True)
+    for key in ("q", "k"):
+        wq, bq = inp["weights"][key]
+        inp["weights"][key] = (synth.bf16_round(wq * 4) if shape.dtype == "bf16" else wq * 4, bq)
+    rng = np.random.default_rng(4)
+    dh_out = rng.standard_normal((shape.batch, shape.n_proxies, shape.d_proxy)).astype(np.float32)
+    if shape.dtype == "bf16":
+        dh_out = synth.bf16_round(dh_out)
+    res = run_gpu_backward(shape, inp, dh_out)
+    ref = oracle.layer_backward_2d(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.image_width,
+                                   inp["dy"], shape.mask, inp["h_in"], dh_out)
+    compare(shape, inp, res, ref, name)

@@ -159,3 +159,27 @@ def test_layer_stack_with_cross_layer_proxies_and_dynamic_p(gpu):
         rx, rh = r["x_out"], r["h_out"]
     assert_close(host(h), rh, "bf16", "stack layer 3 h_out")
     assert_close(host(x), rx, "bf16", "stack layer 3 x_out")
+
+
+IMAGES = {
+    # 2-D partition (Sec. 3.9): a 32 x 48 image in 4 x 4 patches (P = 16), and 16 x 16 in 8 x 8 patches
+    "bf16_image_32x48_p4_bi": LayerShape(2, 32 * 48, 192, 192, 3, 64, (16,), mask=synth.BIDIRECTIONAL,
+                                         image_width=48),
+    "fp32_image_16x16_p8_bc": LayerShape(1, 16 * 16, 64, 128, 2, 64, (64,), dtype="fp32",
+                                         mask=synth.BLOCK_CAUSAL, image_width=16),
+}
+
+
+@pytest.mark.parametrize("name", list(IMAGES))
+def test_forward_parity_2d_partition(gpu, name):
+    shape = IMAGES[name]
+    print(f"[case {name}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, seed=zlib.crc32(name.encode()) % 1000, with_h_in=True)
+    for key in ("q", "k"):
+        wq, bq = inp["weights"][key]
+        inp["weights"][key] = (synth.bf16_round(wq * 4) if shape.dtype == "bf16" else wq * 4, bq)
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward_2d(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.image_width,
+                                  shape.mask, inp["h_in"])
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
