@@ -33,6 +33,11 @@ the C-ABI):
   p x p patch of a raster-order image into one block (P = p^2, one level),
   tokens row by row inside the patch, patches in raster order of the patch
   grid; the layer is otherwise unchanged (layer_forward_2d).
+* The affine modulation of Eq. 13 leaves s, t and Norm open: s and t are
+  one linear map of Delta per token, [s | t] = Delta W_a^T + b_a with W_a
+  [2 d_fine, d_fine]; Norm is an RMSNorm over the d_fine channels without
+  a gain (eps = 1e-6; a gain would duplicate 1 + s). As written, X is
+  replaced, not added to.
 * A length L that is not a multiple of P gives m = ceil(L/P) blocks
   (Sec. 3.1); the partial last block is zero-padded to P tokens, the
   padding's outputs are dropped and it receives no gradient.
@@ -50,6 +55,14 @@ BIDIRECTIONAL = 2
 # local fusion of Delta into X (Sec. 3.4)
 INJECT_GATED = 0  # Eq. 12
 INJECT_ADD = 1    # Eq. 11
+INJECT_AFFINE = 2  # Eq. 13
+
+AFFINE_EPS = 1e-6  # RMSNorm epsilon of the affine modulation
+
+
+def rms_normalise(x):
+    """Norm of Eq. 13 (reading): x / sqrt(mean(x^2) + eps) per token, no gain."""
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + AFFINE_EPS)
 
 _ROW_CHUNK = 512  # query rows per chunk; rows are independent (Eq. 9)
 
@@ -189,7 +202,9 @@ def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
     m proxies (Eq. 9) followed by the output map W_o; decompress the proxy
     each block receives (Eq. 10, 17); gated injection
     Y = X + sigmoid(G) * Delta with G = [X, Delta] W_g^T + b_g (Eq. 12),
-    or with INJECT_ADD the residual addition Y = X + Delta (Eq. 11).
+    with INJECT_ADD the residual addition Y = X + Delta (Eq. 11), with
+    INJECT_AFFINE the modulation Y = (1 + s(Delta)) * Norm(X) + t(Delta)
+    (Eq. 13; [s | t] = Delta W_a^T + b_a, Norm an RMSNorm without gain).
 
     Returns x_out [B, L, d_fine] and h_out = H [B, m, d_proxy]. With
     ``sample_blocks`` only those blocks are decompressed and injected
@@ -241,6 +256,11 @@ def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
         if injection == INJECT_ADD:
             g = None
             y = xb + delta
+        elif injection == INJECT_AFFINE:
+            # Eq. 13: Y = (1 + s(Delta)) * Norm(X) + t(Delta), [s | t] = Delta W_a^T + b_a
+            st = linear(delta, *weights["affine"])
+            g = st[:, :d_f]                      # s, kept for the backward
+            y = (1.0 + g) * rms_normalise(xb) + st[:, d_f:]
         else:
             wg, bg = _f64(weights["gate"][0]), _f64(weights["gate"][1])
             g = xb @ wg[:, :d_f].T + delta @ wg[:, d_f:].T + bg
@@ -332,7 +352,8 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
           "q": zgrad(weights["q"]), "k": zgrad(weights["k"]), "v": zgrad(weights["v"]),
           "o": zgrad(weights["o"]),
           "decompress": [zgrad(w) for w in weights["decompress"]],
-          "gate": zgrad(weights["gate"]) if injection == INJECT_GATED else None}
+          "gate": zgrad(weights["gate"]) if injection == INJECT_GATED else None,
+          "affine": zgrad(weights["affine"]) if injection == INJECT_AFFINE else None}
     dx = np.zeros_like(dy)
     d_p = weights["q"][0].shape[0]
     dh_in = None if h_in is None else np.zeros((bsz, m, d_p))
@@ -344,6 +365,17 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             # Eq. 11: Y = X + Delta
             ddelta = dy[b]
             dxb = dy[b]
+        elif injection == INJECT_AFFINE:
+            # Eq. 13: Y = (1 + s) * N + t, N = X r, r = (mean(X^2) + eps)^(-1/2)
+            wa = _f64(weights["affine"][0])
+            r = 1.0 / np.sqrt(np.mean(xb * xb, axis=1, keepdims=True) + AFFINE_EPS)
+            nx = xb * r
+            dst = np.concatenate([dy[b] * nx, dy[b]], axis=1)          # [dS | dT]
+            dn = dy[b] * (1.0 + g)
+            dxb = r * (dn - nx * np.mean(dn * nx, axis=1, keepdims=True))
+            ddelta = dst @ wa
+            gr["affine"][0] += dst.T @ delta
+            gr["affine"][1] += dst.sum(axis=0)
         else:
             wg = _f64(weights["gate"][0])
             sg = sigmoid(g)

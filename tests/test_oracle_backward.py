@@ -247,3 +247,38 @@ def test_backward_finite_differences_2d_partition():
         fd = (loss(x, _set(w, path, wp)) - loss(x, _set(w, path, wm))) / (2 * eps)
         g = _grad_of(res["grads"], path)[flat]
         assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)
+
+
+@pytest.mark.parametrize("mask,factors", [(oracle.TOKEN_CAUSAL, (4,)), (oracle.BIDIRECTIONAL, (2, 2))])
+def test_backward_finite_differences_affine_modulation(mask, factors):
+    """Eq. 13 injection: dX through the RMSNorm, dDelta and dW_a / db_a."""
+    rng = np.random.default_rng(97 + mask)
+    d_f, d_p, nh, L, B = 4, 6, 2, 16, 2
+    w = rand_weights(rng, d_f, d_p, factors, std=0.4)
+    del w["gate"]
+    w["affine"] = (rng.standard_normal((2 * d_f, d_f)) * 0.4, rng.standard_normal(2 * d_f) * 0.1)
+    x = rng.standard_normal((B, L, d_f))
+    m = L // int(np.prod(factors))
+    h_in = rng.standard_normal((B, m, d_p))
+    dy = rng.standard_normal((B, L, d_f))
+    dh = rng.standard_normal((B, m, d_p))
+    inj = oracle.INJECT_AFFINE
+    res = oracle.layer_backward(x, w, factors, nh, dy, mask, h_in, dh, injection=inj)
+    assert res["grads"]["gate"] is None
+    eps = 1e-5
+    for idx in [(0, 0, 0), (1, 7, 2), (0, 15, 3)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += eps
+        xm[idx] -= eps
+        fd = (_loss(xp, w, factors, nh, mask, h_in, dy, dh, inj) - _loss(xm, w, factors, nh, mask, h_in, dy, dh, inj)) / (2 * eps)
+        assert abs(fd - res["dx"][idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, res["dx"][idx])
+    for path in _param_paths(w) + [(("affine", 0),), (("affine", 1),)]:
+        wt = _get(w, path)
+        flat = np.unravel_index(rng.integers(wt.size), wt.shape)
+        wp, wm = wt.copy(), wt.copy()
+        wp[flat] += eps
+        wm[flat] -= eps
+        fd = (_loss(x, _set(w, path, wp), factors, nh, mask, h_in, dy, dh, inj)
+              - _loss(x, _set(w, path, wm), factors, nh, mask, h_in, dy, dh, inj)) / (2 * eps)
+        g = _grad_of(res["grads"], path)[flat]
+        assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)

@@ -459,3 +459,50 @@ def test_patch_block_causality():
     for t in range(hgt * wid):
         changed = not np.array_equal(y0[0, t], y1[0, t])
         assert changed == (patch_of(t) >= 2), t
+
+
+# ------------------------------------------------------- affine modulation
+
+def _affine_weights(rng, d_f, scale=0.3):
+    return (rng.standard_normal((2 * d_f, d_f)) * scale, rng.standard_normal(2 * d_f) * 0.1)
+
+
+@pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BIDIRECTIONAL])
+def test_affine_modulation_constant_terms(mask):
+    """Eq. 13 with s and t independent of Delta (W_a = 0): every output row
+    minus t, divided by 1 + s, is a positive multiple of its input row with
+    mean square mean(x^2) / (mean(x^2) + eps) (the RMSNorm reading)."""
+    rng = np.random.default_rng(111)
+    d_f, d_p, nh, B, P, L = 4, 6, 2, 2, 4, 12
+    w = rand_weights(rng, d_f, d_p, (P,))
+    s0 = rng.uniform(-0.5, 0.5, d_f)
+    t0 = rng.standard_normal(d_f)
+    w["affine"] = (np.zeros((2 * d_f, d_f)), np.concatenate([s0, t0]))
+    x = rng.standard_normal((B, L, d_f))
+    y = oracle.layer_forward(x, w, (P,), nh, mask, injection=oracle.INJECT_AFFINE)["x_out"]
+    n = (y - t0) / (1.0 + s0)
+    ratio = n / x
+    np.testing.assert_allclose(ratio, ratio[..., :1] * np.ones_like(ratio), rtol=1e-12)
+    assert np.all(ratio > 0)
+    ms = np.mean(x * x, axis=-1)
+    np.testing.assert_allclose(np.mean(n * n, axis=-1), ms / (ms + oracle.layer.AFFINE_EPS), rtol=1e-12)
+
+
+def test_affine_modulation_is_affine_in_the_decompressed_signal():
+    """With X fixed, Y depends on Delta through one linear map per token: Y is
+    affine in the decompression biases (doubling their offset from the
+    baseline doubles Y's change), unlike the gate of Eq. 12."""
+    rng = np.random.default_rng(112)
+    d_f, d_p, nh, B, P, L = 4, 6, 2, 1, 4, 8
+    w = rand_weights(rng, d_f, d_p, (P,))
+    w["affine"] = _affine_weights(rng, d_f)
+    x = rng.standard_normal((B, L, d_f))
+    wd, bd = w["decompress"][0]
+    outs = []
+    for k in (0.0, 1.0, 2.0):
+        w2 = dict(w)
+        w2["decompress"] = [(wd, bd + k * 0.7)]
+        outs.append(oracle.layer_forward(x, w2, (P,), nh, oracle.BIDIRECTIONAL,
+                                         injection=oracle.INJECT_AFFINE)["x_out"])
+    np.testing.assert_allclose(outs[2] - outs[0], 2 * (outs[1] - outs[0]), rtol=1e-10, atol=1e-12)
+    assert np.max(np.abs(outs[1] - outs[0])) > 1e-3
