@@ -59,8 +59,11 @@ enum pf_mask { PF_TOKEN_CAUSAL = 0, PF_BLOCK_CAUSAL = 1, PF_BIDIRECTIONAL = 2 };
 /* Local fusion of the decompressed proxy Delta into the local stream (Sec. 3.4):
  * PF_INJECT_GATED: Y = X + sigmoid([X, Delta] W_g^T + b_g) * Delta (Eq. 12);
  * PF_INJECT_ADD:   Y = X + Delta (Eq. 11); the gate weights are not read and
- *   its gradients are not written. */
-enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1 };
+ *   its gradients are not written.
+ * PF_INJECT_AFFINE: Y = (1 + s) * Norm(X) + t with [s | t] = Delta W_a^T + b_a
+ *   per token (Eq. 13; Norm = x / sqrt(mean(x^2) + 1e-6) over d_fine, no
+ *   gain); reads the affine weights instead of the gate's. */
+enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1, PF_INJECT_AFFINE = 2 };
 
 typedef struct {
   const void* w; /* [out, in] */
@@ -105,13 +108,17 @@ typedef struct {
 /* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)
  * q, k, v, o : W [d_proxy, d_proxy]     (Eq. 9 and its output map)
  * decompress[j]: W [k_{j+1} d_j, d_{j+1}] (Eq. 10, Eq. 17)
- * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12); unused
- *              with PF_INJECT_ADD (may be NULL) */
+ * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12); read
+ *              only with PF_INJECT_GATED (may be NULL otherwise)
+ * affine     : W [2 d_fine, d_fine] acting on Delta, rows 0..d_fine-1 give
+ *              s and the next d_fine rows t (Eq. 13); read only with
+ *              PF_INJECT_AFFINE (may be NULL otherwise) */
 typedef struct {
   pf_linear compress[PF_MAX_LEVELS];
   pf_linear q, k, v, o;
   pf_linear decompress[PF_MAX_LEVELS];
   pf_linear gate;
+  pf_linear affine;
 } pf_layer_weights;
 
 typedef struct {
@@ -124,6 +131,7 @@ typedef struct {
   pf_linear_grad q, k, v, o;
   pf_linear_grad decompress[PF_MAX_LEVELS];
   pf_linear_grad gate;
+  pf_linear_grad affine; /* with PF_INJECT_AFFINE */
 } pf_layer_grads;
 
 /* Bytes of scratch the forward (for_backward = 0) or backward

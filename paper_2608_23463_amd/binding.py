@@ -24,6 +24,7 @@ PF_FP32 = 0
 PF_BF16 = 1
 PF_INJECT_GATED = 0
 PF_INJECT_ADD = 1
+PF_INJECT_AFFINE = 2
 
 EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
@@ -52,7 +53,7 @@ class PfLayerConfig(ctypes.Structure):
 
 class PfLayerWeights(ctypes.Structure):
     _fields_ = [("compress", PfLinear * MAX_LEVELS), ("q", PfLinear), ("k", PfLinear), ("v", PfLinear),
-                ("o", PfLinear), ("decompress", PfLinear * MAX_LEVELS), ("gate", PfLinear)]
+                ("o", PfLinear), ("decompress", PfLinear * MAX_LEVELS), ("gate", PfLinear), ("affine", PfLinear)]
 
 
 class PfLinearGrad(ctypes.Structure):
@@ -62,7 +63,7 @@ class PfLinearGrad(ctypes.Structure):
 class PfLayerGrads(ctypes.Structure):
     _fields_ = [("compress", PfLinearGrad * MAX_LEVELS), ("q", PfLinearGrad), ("k", PfLinearGrad),
                 ("v", PfLinearGrad), ("o", PfLinearGrad), ("decompress", PfLinearGrad * MAX_LEVELS),
-                ("gate", PfLinearGrad)]
+                ("gate", PfLinearGrad), ("affine", PfLinearGrad)]
 
 
 class PfDecodeConfig(ctypes.Structure):
@@ -237,7 +238,7 @@ def layer_weights(w: Dict[str, object]) -> PfLayerWeights:
         s.compress[i] = _lin(pair)
     for i, pair in enumerate(w["decompress"]):
         s.decompress[i] = _lin(pair)
-    for name in ("q", "k", "v", "o", "gate"):
+    for name in ("q", "k", "v", "o", "gate", "affine"):
         setattr(s, name, _lin(w.get(name)))
     return s
 
@@ -297,7 +298,7 @@ def layer_grads(g: Dict[str, object]) -> PfLayerGrads:
         s.compress[i] = lg(pair)
     for i, pair in enumerate(g["decompress"]):
         s.decompress[i] = lg(pair)
-    for name in ("q", "k", "v", "o", "gate"):
+    for name in ("q", "k", "v", "o", "gate", "affine"):
         setattr(s, name, lg(g.get(name)))
     return s
 
@@ -321,6 +322,7 @@ def layer_backward(cfg: PfLayerConfig, weights: Dict[str, object], x, h_in, save
         grads[name] = g_like(weights[name])
     # the gate is only read (and differentiated) by gated injection
     grads["gate"] = g_like(weights["gate"]) if cfg.injection == PF_INJECT_GATED else None
+    grads["affine"] = g_like(weights["affine"]) if cfg.injection == PF_INJECT_AFFINE else None
     if workspace is None:
         workspace = _bytes(layer_workspace_size(cfg, True), dev)
     _check(load().proxy_layer_backward(ctypes.byref(cfg), ctypes.byref(layer_weights(weights)), _ptr(x),

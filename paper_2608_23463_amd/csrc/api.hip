@@ -65,7 +65,8 @@ size_t proxy_layer_saved_size(const pf_layer_config* cfg) {
   return layer_acts(d, true).bytes;
 }
 
-static int check_weights(const LayerDims& d, const pf_layer_weights* w, bool gated) {
+static int check_weights(const LayerDims& d, const pf_layer_weights* w, int injection) {
+  const bool gated = injection == PF_INJECT_GATED;
   if (!w) return fail(PF_ERR_INVALID_ARG, "weights struct is NULL");
   for (int j = 0; j < d.M; ++j) {
     if (!w->compress[j].w) return fail(PF_ERR_INVALID_ARG, "compress[%d].w is NULL", j);
@@ -81,6 +82,11 @@ static int check_weights(const LayerDims& d, const pf_layer_weights* w, bool gat
     if (!aligned16(maps[i]->w) || !aligned16(maps[i]->b))
       return fail(PF_ERR_INVALID_ARG, "%s weights and bias must be 16-byte aligned", names[i]);
   }
+  if (injection == PF_INJECT_AFFINE) {
+    if (!w->affine.w) return fail(PF_ERR_INVALID_ARG, "affine.w is NULL");
+    if (!aligned16(w->affine.w) || !aligned16(w->affine.b))
+      return fail(PF_ERR_INVALID_ARG, "affine weights and bias must be 16-byte aligned");
+  }
   return PF_OK;
 }
 
@@ -90,7 +96,7 @@ int proxy_layer_forward(const pf_layer_config* cfg, const pf_layer_weights* w, c
   const char* why;
   int st = layer_dims(cfg, &d, &why);
   if (st != PF_OK) return fail(st, "invalid layer config: %s", why);
-  if ((st = check_weights(d, w, cfg->injection == PF_INJECT_GATED)) != PF_OK) return st;
+  if ((st = check_weights(d, w, cfg->injection)) != PF_OK) return st;
   if (!x || !x_out || !h_out) return fail(PF_ERR_INVALID_ARG, "x, x_out and h_out must be non-NULL");
   if (!aligned16(x) || !aligned16(x_out) || !aligned16(h_out) || (h_in && !aligned16(h_in)) ||
       (saved && !aligned16(saved)))
@@ -134,7 +140,7 @@ int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w, 
   const char* why;
   int st = layer_dims(cfg, &d, &why);
   if (st != PF_OK) return fail(st, "invalid layer config: %s", why);
-  if ((st = check_weights(d, w, cfg->injection == PF_INJECT_GATED)) != PF_OK) return st;
+  if ((st = check_weights(d, w, cfg->injection)) != PF_OK) return st;
   if (!x || !saved || !dy || !dx || !grads)
     return fail(PF_ERR_INVALID_ARG, "x, saved, dy, dx and grads must be non-NULL");
   if ((h_in == nullptr) != (dh_in == nullptr))

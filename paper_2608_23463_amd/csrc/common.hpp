@@ -139,6 +139,31 @@ __device__ __forceinline__ void store8(float* p, const float* v) {
   *reinterpret_cast<f32x4*>(p + 4) = b;
 }
 
+// Four consecutive elements <-> fp32 (8-byte aligned for bf16, 16 for fp32).
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void load4(const bf16* p, float* v) {
+  const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (float)x[i];
+}
+__device__ __forceinline__ void load4(const float* p, float* v) {
+  const f32x4 x = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = x[i];
+}
+__device__ __forceinline__ void store4(bf16* p, const float* v) {
+  bf16x4 x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = (bf16)v[i];
+  *reinterpret_cast<bf16x4*>(p) = x;
+}
+__device__ __forceinline__ void store4(float* p, const float* v) {
+  f32x4 x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = v[i];
+  *reinterpret_cast<f32x4*>(p) = x;
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Logistic function on the hardware base-2 exponential and reciprocal (each

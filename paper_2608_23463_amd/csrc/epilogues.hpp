@@ -252,6 +252,40 @@ struct EpiGate {
   }
 };
 
+constexpr float kAffineEps = 1e-6f;  // RMSNorm epsilon of Eq. 13
+
+// Affine modulation (Eq. 13) on the GEMM [S | T] = Delta W_a^T + b_a with s
+// and t interleaved per channel (columns 2c, 2c+1): y[r, c] = (1 + s) *
+// x[r, c] * rstd[r] + t; optionally s is kept for the backward. The GEMM's
+// N = 2 d_fine is a multiple of 16 (d_fine % 8 == 0), so every store goes
+// through vec8 and covers 4 whole channels; the scalar form is never called.
+template <typename T>
+struct EpiAffine {
+  const T* x;
+  const float* rstd;
+  const T* bias;  // interleaved [2 d_fine]
+  T* y;
+  T* ssave;       // [rows, d_fine] or NULL
+  int d;
+  __device__ __forceinline__ void operator()(int, int, float) const {}
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    const int ch = c >> 1;
+    const int64_t i = (int64_t)r * d + ch;
+    float b[8], xv[4], yv[4], sv[4];
+    load8(bias + c, b);
+    load4(x + i, xv);
+    const float rs = rstd[r];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float s = v[2 * e] + b[2 * e], t = v[2 * e + 1] + b[2 * e + 1];
+      sv[e] = s;
+      yv[e] = fmaf(1.0f + s, xv[e] * rs, t);
+    }
+    store4(y + i, yv);
+    if (ssave) store4(ssave + i, sv);
+  }
+};
+
 // fp32 store with optional accumulation into what is there (fixed order:
 // one writer per element per launch, launches ordered on the stream).
 struct EpiF32 {

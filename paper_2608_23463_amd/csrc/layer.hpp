@@ -28,6 +28,7 @@ struct LayerDims {
   int ld_t;         // row stride of transposed per-head tensors (m rounded up to 64)
   int esize;        // bytes per activation element
   int img_w, patch; // 2-D partition: image width and patch side (0 for sequences)
+  int inject;       // pf_injection
   // the caller's token tensors go through workspace copies (padded or patch-ordered)
   bool staged() const { return L_in != L || img_w > 0; }
 };
@@ -52,7 +53,9 @@ struct LayerActs {
   size_t s;                   // S [B*m, d_p]: the contextualised proxy each block receives
   size_t u[PF_MAX_LEVELS];    // U_j, j = 1..M-1: decompression level outputs [B*R_j, d_j]
   size_t delta;               // [B*L, d_f]
-  size_t g;                   // gate pre-activation G [B*L, d_f]
+  size_t g;                   // gate pre-activation G, or s of Eq. 13 [B*L, d_f]
+  size_t rstd;                // Eq. 13: 1 / RMS of every X row, fp32 [B*L]
+  size_t aff_w, aff_b;        // Eq. 13: W_a, b_a with s and t rows interleaved [2 d_f, d_f], [2 d_f]
   size_t bytes;
 };
 
@@ -79,6 +82,7 @@ struct LayerWs {
   size_t x_pad;               // X with zero padding [B*L, d_f]
   size_t y_pad;               // forward: X_out; backward: dX [B*L, d_f]
   size_t dy_pad;              // backward: dY with zero padding [B*L, d_f]
+  size_t dst;                 // Eq. 13 backward: [dS | dT] [B*L, 2 d_f]
   size_t bytes;
 };
 

@@ -47,6 +47,50 @@ __global__ void __launch_bounds__(256) gate_bwd_prep_kernel(const T* __restrict_
   }
 }
 
+// Eq. 13 backward, one wave per row: N = X rstd, dS = dY N, dT = dY,
+// dN = dY (1 + S) and the RMSNorm's dX = rstd (dN - N mean(dN N)).
+// [dS | dT] go to dst [rows, 2d], dX to dx32 (fp32; the compression's data
+// gradient is added to it later). The row mean takes a first pass (per-lane
+// runs of 8, then a butterfly), the outputs a second.
+template <typename T>
+__global__ void __launch_bounds__(256) affine_bwd_prep_kernel(const T* __restrict__ dy, const T* __restrict__ x,
+                                                              const T* __restrict__ s, const float* __restrict__ rstd,
+                                                              T* __restrict__ dst, float* __restrict__ dx32,
+                                                              int64_t rows, int d) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int64_t base = row * d;
+  const float rs = rstd[row];
+  float acc = 0.0f;
+  for (int c = lane * 8; c < d; c += 64 * 8) {
+    float g[8], xv[8], sv[8];
+    load8(dy + base + c, g);
+    load8(x + base + c, xv);
+    load8(s + base + c, sv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fmaf(g[e] * (1.0f + sv[e]), xv[e] * rs, acc);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  const float mean = acc / (float)d;
+  for (int c = lane * 8; c < d; c += 64 * 8) {
+    float g[8], xv[8], sv[8], ds[8], dx[8];
+    load8(dy + base + c, g);
+    load8(x + base + c, xv);
+    load8(s + base + c, sv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float n = xv[e] * rs;
+      ds[e] = g[e] * n;
+      dx[e] = rs * (g[e] * (1.0f + sv[e]) - n * mean);
+    }
+    store8(dst + row * 2 * d + c, ds);
+    store8(dst + row * 2 * d + d + c, g);
+    store8(dx32 + base + c, dx);
+  }
+}
+
 // Column sums in two fixed-order stages: partial sums over row chunks, then
 // the sum of the partials in chunk order.
 template <typename T>
@@ -374,9 +418,26 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   const T* dyp = reinterpret_cast<const T*>(dy);
   const T* xp = reinterpret_cast<const T*>(x);
 
-  // 1. injection: gated (Eq. 12) or residual add (Eq. 11: dDelta = dX = dY)
+  // 1. injection: gated (Eq. 12), affine (Eq. 13) or residual add (Eq. 11:
+  //    dDelta = dX = dY)
   const bool add_inject = cfg->injection == PF_INJECT_ADD;
-  if (!add_inject) {
+  if (cfg->injection == PF_INJECT_AFFINE) {
+    run.launch("affine_bwd_prep", [&] {
+      hipLaunchKernelGGL((affine_bwd_prep_kernel<T>), dim3((unsigned)((BL + 3) / 4)), dim3(256), 0, run.stream, dyp,
+                         xp, S(A.g), reinterpret_cast<const float*>(saved + A.rstd), WT(W.dst), WF(W.dx32), BL, df);
+      return hipGetLastError();
+    });
+    // dDelta = [dS | dT] W_a
+    dgrad<T>(run, "affine_dgrad_gemm", WT(W.dst), 2 * df, w->affine.w, df, BL, df, 2 * df,
+             EpiLinear<T>{WT(W.ddelta), df, nullptr, nullptr, 0, nullptr}, trw);
+    // dW_a = [dS | dT]^T Delta, one half (and its bias columns) at a time
+    float* dwa = reinterpret_cast<float*>(gr->affine.dw);
+    float* dba = reinterpret_cast<float*>(gr->affine.db);
+    for (int half = 0; half < 2; ++half)
+      wgrad<T>(run, "affine_wgrad_gemm", WT(W.dst) + half * df, 2 * df, S(A.delta), df, df, df, BL,
+               dwa ? dwa + (int64_t)half * df * df : nullptr, df, tra, trb, false, dba ? dba + half * df : nullptr,
+               part, part2);
+  } else if (!add_inject) {
     run.launch("gate_bwd_prep", [&] {
       const int64_t n8 = BL * df / 8;
       const int blocks = (int)std::min<int64_t>((n8 + 255) / 256, 16384);
@@ -499,12 +560,13 @@ hipError_t layer_backward_run(const LayerDims& d, const pf_layer_config* cfg, co
 size_t layer_backward_gemm_ws(const LayerDims& d) {
   pf_layer_config cfg{};
   cfg.mask = PF_TOKEN_CAUSAL;
+  cfg.injection = d.inject;
   pf_layer_weights w{};
   // every weight gradient requested, so every GEMM is planned
   static float dummy;
   pf_layer_grads gr{};
   for (int j = 0; j < PF_MAX_LEVELS; ++j) gr.compress[j].dw = gr.decompress[j].dw = &dummy;
-  gr.q.dw = gr.k.dw = gr.v.dw = gr.o.dw = gr.gate.dw = &dummy;
+  gr.q.dw = gr.k.dw = gr.v.dw = gr.o.dw = gr.gate.dw = gr.affine.dw = &dummy;
   Runner run(true);
   if (d.esize == 2)
     backward_impl<bf16>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, &gr, nullptr);

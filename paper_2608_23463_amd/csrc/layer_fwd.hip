@@ -89,12 +89,47 @@ hipError_t permute_patches(const void* src, void* dst, int B, int64_t L, int w, 
   return hipGetLastError();
 }
 
+// Eq. 13: rstd[r] = 1 / sqrt(mean(x[r]^2) + eps), one wave per row (fp32
+// sum of squares: per-lane runs of 8, then a butterfly over the wave).
+template <typename T>
+__global__ void __launch_bounds__(256) rstd_rows_kernel(const T* __restrict__ x, float* __restrict__ rstd,
+                                                        int64_t rows, int d, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const T* xr = x + row * d;
+  float ss = 0.0f;
+  for (int c = lane * 8; c < d; c += 64 * 8) {
+    float v[8];
+    load8(xr + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(v[e], v[e], ss);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if (lane == 0) rstd[row] = 1.0f / sqrtf(ss / (float)d + eps);
+}
+
+// W_a [2d, d] (s rows, then t rows) -> rows interleaved s_0, t_0, s_1, t_1,
+// ..., so the affine GEMM's columns 2c and 2c+1 are s and t of channel c.
+template <typename T>
+__global__ void __launch_bounds__(256) affine_interleave_kernel(const T* __restrict__ w, const T* __restrict__ b,
+                                                                T* __restrict__ w_il, T* __restrict__ b_il, int d) {
+  const int64_t total = (int64_t)2 * d * d;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int rr = (int)(i / d), cc = (int)(i % d);
+    const int src = (rr & 1) ? d + (rr >> 1) : (rr >> 1);
+    w_il[i] = w[(int64_t)src * d + cc];
+    if (cc == 0) b_il[rr] = b ? b[src] : (T)0.0f;
+  }
+}
+
 int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   *why = nullptr;
   if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
   if (c->dtype != PF_FP32 && c->dtype != PF_BF16) return *why = "dtype must be PF_FP32 or PF_BF16", PF_ERR_INVALID_ARG;
   if (c->mask < PF_TOKEN_CAUSAL || c->mask > PF_BIDIRECTIONAL) return *why = "unknown mask mode", PF_ERR_INVALID_ARG;
-  if (c->injection != PF_INJECT_GATED && c->injection != PF_INJECT_ADD)
+  if (c->injection != PF_INJECT_GATED && c->injection != PF_INJECT_ADD && c->injection != PF_INJECT_AFFINE)
     return *why = "unknown injection mode", PF_ERR_INVALID_ARG;
   if (c->batch < 1 || c->seq_len < 1) return *why = "batch and seq_len must be >= 1", PF_ERR_INVALID_ARG;
   if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
@@ -102,6 +137,7 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
     return *why = "widths and head counts must be >= 1", PF_ERR_INVALID_ARG;
   if ((int64_t)c->n_heads * c->head_dim != c->d_proxy) return *why = "n_heads * head_dim must equal d_proxy", PF_ERR_INVALID_ARG;
   d->B = c->batch;
+  d->inject = c->injection;
   d->L_in = c->seq_len;
   d->d_f = c->d_fine;
   d->d_p = c->d_proxy;
@@ -180,7 +216,11 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   a.s = take(prox);
   for (int j = 1; j < d.M; ++j) a.u[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
   a.delta = take((size_t)d.B * d.L * d.d_f * es);
-  a.g = bwd ? take((size_t)d.B * d.L * d.d_f * es) : 0;
+  a.g = bwd && d.inject != PF_INJECT_ADD ? take((size_t)d.B * d.L * d.d_f * es) : 0;
+  const bool affine = d.inject == PF_INJECT_AFFINE;
+  a.rstd = take(affine ? (size_t)d.B * d.L * 4 : 0);
+  a.aff_w = take(affine ? (size_t)2 * d.d_f * d.d_f * es : 0);
+  a.aff_b = take(affine ? (size_t)2 * d.d_f * es : 0);
   a.bytes = off;
   return a;
 }
@@ -252,6 +292,7 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     w.tr_b = take(tr);
     w.tr_w = take(trw);
   }
+  if (bwd && d.inject == PF_INJECT_AFFINE) w.dst = take(2 * tok);
   if (d.staged()) {
     w.x_pad = take(tok);
     w.y_pad = take(tok);
@@ -417,6 +458,37 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     run.gemm<T, LAYOUT_K, LAYOUT_K>("decompress_gemm", pr, e);
   }
 
+  // 6. affine modulation (Eq. 13): [S | T] = Delta W_a^T + b_a with s and t
+  //    interleaved per channel, Y = (1 + S) * X * rstd + T in the epilogue
+  if (cfg->injection == PF_INJECT_AFFINE) {
+    const int64_t rows = (int64_t)d.B * d.L;
+    float* rstd = reinterpret_cast<float*>(act + A.rstd);
+    run.launch("affine_rstd", [&] {
+      hipLaunchKernelGGL((rstd_rows_kernel<T>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, run.stream,
+                         reinterpret_cast<const T*>(x), rstd, rows, d.d_f, kAffineEps);
+      return hipGetLastError();
+    });
+    run.launch("affine_interleave", [&] {
+      const int64_t total = (int64_t)2 * d.d_f * d.d_f;
+      hipLaunchKernelGGL((affine_interleave_kernel<T>), dim3((unsigned)std::min<int64_t>((total + 255) / 256, 4096)),
+                         dim3(256), 0, run.stream, reinterpret_cast<const T*>(w->affine.w),
+                         reinterpret_cast<const T*>(w->affine.b), P(A.aff_w), P(A.aff_b), d.d_f);
+      return hipGetLastError();
+    });
+    GemmProblem pr{};
+    pr.a = P(A.delta);
+    pr.lda = d.d_f;
+    pr.b = P(A.aff_w);
+    pr.ldb = d.d_f;
+    pr.M = (int)rows;
+    pr.N = 2 * d.d_f;
+    pr.K = d.d_f;
+    EpiAffine<T> e{reinterpret_cast<const T*>(x), rstd, P(A.aff_b), reinterpret_cast<T*>(x_out),
+                   saving ? P(A.g) : nullptr, d.d_f};
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("affine_gemm", pr, e);
+    return;
+  }
+
   // 6. gated injection (Eq. 12)
   if (!add_inject) {
     GemmProblem pr{};
@@ -449,6 +521,7 @@ hipError_t layer_forward_run(const LayerDims& d, const pf_layer_config* cfg, con
 size_t layer_forward_gemm_ws(const LayerDims& d) {
   pf_layer_config cfg{};
   cfg.mask = PF_TOKEN_CAUSAL;
+  cfg.injection = d.inject;
   pf_layer_weights w{};
   Runner run(true);
   if (d.esize == 2)

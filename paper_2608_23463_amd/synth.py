@@ -31,6 +31,7 @@ BIDIRECTIONAL = 2
 
 INJECT_GATED = 0  # Eq. 12
 INJECT_ADD = 1    # Eq. 11
+INJECT_AFFINE = 2  # Eq. 13
 
 WEIGHT_STD = 0.02
 
@@ -189,6 +190,8 @@ def layer_inputs(shape: LayerShape, seed: int, with_dy: bool = False,
         w[name] = lin(*ws[name])
     w["decompress"] = [lin(*s) for s in ws["decompress"]]
     w["gate"] = lin(*ws["gate"])
+    if shape.injection == INJECT_AFFINE:   # [s | t] = Delta W_a^T + b_a (Eq. 13)
+        w["affine"] = lin(2 * shape.d_fine, shape.d_fine)
     out["weights"] = w
     if with_dy:
         out["dy"] = _normal(rng, (shape.batch, shape.seq_len, shape.d_fine), 1.0, dt)

@@ -80,7 +80,7 @@ def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 
     (dict(seq_len=0), B.PF_ERR_INVALID_ARG),
     (dict(n_heads=8), B.PF_ERR_INVALID_ARG),
     (dict(mask=5), B.PF_ERR_INVALID_ARG),
-    (dict(injection=2), B.PF_ERR_INVALID_ARG),
+    (dict(injection=3), B.PF_ERR_INVALID_ARG),
     (dict(head_dim=32, n_heads=8), B.PF_ERR_UNSUPPORTED),
     (dict(d_fine=100), B.PF_ERR_UNSUPPORTED),
 ])
@@ -238,3 +238,12 @@ def test_2d_partition_validation(lib):
         c.image_width = bad_w
         assert _fwd(lib, c, _weights_struct(nlev=len(fac))) == status, (bad_w, fac)
         assert B.layer_workspace_size(c) == 0
+
+
+def test_affine_weights_required_by_affine_injection(lib):
+    cfg = _cfg(injection=2)
+    assert B.layer_workspace_size(cfg) > 0 and B.layer_saved_size(cfg) > B.layer_saved_size(_cfg())
+    w = _weights_struct(null="gate")   # the gate is not read with Eq. 13
+    assert _fwd(lib, cfg, w) == B.PF_ERR_INVALID_ARG and "affine" in B.last_error()
+    w.affine = B.PfLinear(0x10000, 0x10008)  # misaligned bias
+    assert _fwd(lib, cfg, w) == B.PF_ERR_INVALID_ARG

@@ -56,9 +56,9 @@ def compare(shape, inp, res, ref, label):
     if ref["dh_in"] is not None:
         chk(host(dh_in), ref["dh_in"], "dh_in")
     rg = ref["grads"]
-    for name in ("q", "k", "v", "o", "gate"):
-        if rg[name] is None:  # no gate with residual-add injection
-            assert grads[name] is None
+    for name in ("q", "k", "v", "o", "gate", "affine"):
+        if rg.get(name) is None:  # the gate (or the affine map) only with its injection mode
+            assert grads.get(name) is None
             continue
         chk(host(grads[name][0]), rg[name][0], f"dW_{name}")
         if name == "k":
@@ -89,6 +89,10 @@ CASES = {
     "bf16_inject_add": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_ADD), True),
     "fp32_inject_add_factorised": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
                                               injection=synth.INJECT_ADD), False),
+    # affine modulation (Eq. 13); 16,384 token rows take the transposed weight-gradient path
+    "bf16_inject_affine": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_AFFINE), True),
+    "fp32_inject_affine": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
+                                      injection=synth.INJECT_AFFINE), False),
     # partial last block (L % P != 0): zero-padded inside the library, dY = 0 on the padding
     "bf16_tc_partial_block": (LayerShape(2, 16 * 37 + 9, 192, 192, 3, 64, (16,)), True),
     "fp32_bi_partial_block_factorised": (LayerShape(1, 8 * 37 + 5, 64, 128, 2, 64, (2, 4), level_dims=(96,),

@@ -32,6 +32,11 @@ SMALL = {
     "bf16_inject_add": (LayerShape(2, 37 * 16, 192, 192, 3, 64, (16,), injection=synth.INJECT_ADD), True),
     "fp32_inject_add_factorised": (LayerShape(1, 8 * 40, 64, 128, 1, 128, (2, 4), level_dims=(48,), dtype="fp32",
                                               injection=synth.INJECT_ADD), False),
+    # affine modulation (Eq. 13): [S | T] from Delta, Y = (1 + S) Norm(X) + T in the GEMM epilogue
+    "bf16_inject_affine": (LayerShape(2, 37 * 16, 192, 192, 3, 64, (16,), injection=synth.INJECT_AFFINE), True),
+    "fp32_inject_affine_factorised_bi": (LayerShape(1, 8 * 40, 64, 128, 1, 128, (2, 4), level_dims=(48,),
+                                                    dtype="fp32", mask=synth.BIDIRECTIONAL,
+                                                    injection=synth.INJECT_AFFINE), False),
     # partial last block (L % P != 0, m = ceil(L / P), zero-padded, Sec. 3.1)
     "bf16_partial_block_tc": (LayerShape(2, 37 * 16 + 5, 192, 192, 3, 64, (16,)), True),
     "fp32_partial_block_factorised_bi": (LayerShape(1, 8 * 40 + 3, 64, 128, 1, 128, (2, 4), level_dims=(48,),
