@@ -9,7 +9,8 @@ torch.cuda.synchronize() and HIP events on the launch stream.
 Extra objects on the same line:
   kernels      per-kernel average duration from the library's event tracing
                (a second pass over K calls) and achieved TFLOP/s or GB/s
-  variants     the same forward with residual-add injection (Eq. 11)
+  variants     the same forward with residual-add injection (Eq. 11) and with
+               affine modulation (Eq. 13)
   ceilings     a 1 GiB device copy (achievable HBM rate) beside the vendor peaks
   roofline     the dominant kernel against the MI355X peak of its bound
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
@@ -201,6 +202,29 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
         variants["inject_add"] = {"ms_per_step": round(ms_add, 4),
                                   "value": round(shape.seq_len * shape.batch / (ms_add * 1e-3), 1),
                                   "unit": "tokens/s"}
+        # affine modulation (Eq. 13): [S | T] GEMM (N = 2 d_fine, K = d_fine) instead of the gate
+        cfg_aff = B.config_from_shape(shape)
+        cfg_aff.injection = B.PF_INJECT_AFFINE
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(13)
+        w_aff = dict(w)
+        w_aff["affine"] = ((torch.randn(2 * shape.d_fine, shape.d_fine, generator=gen, device="cuda") * 0.02)
+                           .to(x.dtype), torch.zeros(2 * shape.d_fine, dtype=x.dtype, device="cuda"))
+        wst_aff = B.layer_weights(w_aff)
+        ws_aff = torch.empty(B.layer_workspace_size(cfg_aff), dtype=torch.uint8, device="cuda")
+        for _ in range(warmup):
+            B.layer_forward_raw(cfg_aff, wst_aff, x, None, x_out, h_out, None, ws_aff)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            B.layer_forward_raw(cfg_aff, wst_aff, x, None, x_out, h_out, None, ws_aff)
+        stop.record()
+        torch.cuda.synchronize()
+        ms_aff = start.elapsed_time(stop) / steps
+        variants["inject_affine"] = {"ms_per_step": round(ms_aff, 4),
+                                     "value": round(shape.seq_len * shape.batch / (ms_aff * 1e-3), 1),
+                                     "unit": "tokens/s"}
+        del ws_aff, w_aff, wst_aff
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
