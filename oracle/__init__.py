@@ -18,7 +18,7 @@ Every function states the passage it follows. Readings of points the paper
 leaves open are listed in the module docstrings where they apply.
 """
 from .layer import (  # noqa: F401
-    TOKEN_CAUSAL, BLOCK_CAUSAL, BIDIRECTIONAL, INJECT_GATED, INJECT_ADD, INJECT_AFFINE, rms_normalise,
+    TOKEN_CAUSAL, BLOCK_CAUSAL, BIDIRECTIONAL, INJECT_GATED, INJECT_ADD, INJECT_AFFINE, INJECT_GATED_HEAD, rms_normalise, head_of_channel,
     sigmoid, compress, layer_forward, layer_backward, attention_rows,
     proxies_and_attention_inputs, patch_order, layer_forward_2d, layer_backward_2d,
 )

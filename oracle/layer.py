@@ -33,6 +33,9 @@ the C-ABI):
   p x p patch of a raster-order image into one block (P = p^2, one level),
   tokens row by row inside the patch, patches in raster order of the patch
   grid; the layer is otherwise unchanged (layer_forward_2d).
+* The per-head gate (INJECT_GATED_HEAD) is Eq. 12 with the per-head
+  weighting of Eq. 20: G = [X, Delta] W_g^T + b_g with W_g [n_heads,
+  2 d_fine], and channel c takes the gate of head c // (d_fine / n_heads).
 * The affine modulation of Eq. 13 leaves s, t and Norm open: s and t are
   one linear map of Delta per token, [s | t] = Delta W_a^T + b_a with W_a
   [2 d_fine, d_fine]; Norm is an RMSNorm over the d_fine channels without
@@ -56,6 +59,14 @@ BIDIRECTIONAL = 2
 INJECT_GATED = 0  # Eq. 12
 INJECT_ADD = 1    # Eq. 11
 INJECT_AFFINE = 2  # Eq. 13
+INJECT_GATED_HEAD = 3  # Eq. 12 with one gate per head (the per-head weighting of Eq. 20)
+
+
+def head_of_channel(d_f: int, n_heads: int):
+    """Channel c of the local stream belongs to head c // (d_f / n_heads)."""
+    if d_f % n_heads:
+        raise ValueError("the per-head gate needs n_heads | d_fine")
+    return np.arange(d_f) // (d_f // n_heads)
 
 AFFINE_EPS = 1e-6  # RMSNorm epsilon of the affine modulation
 
@@ -256,6 +267,11 @@ def layer_forward(x, weights, factors: Sequence[int], n_heads: int,
         if injection == INJECT_ADD:
             g = None
             y = xb + delta
+        elif injection == INJECT_GATED_HEAD:
+            # Eq. 12 with one gate per head: G = [X, Delta] W_g^T + b_g, W_g [n_heads, 2 d_fine]
+            wg, bg = _f64(weights["gate"][0]), _f64(weights["gate"][1])
+            g = xb @ wg[:, :d_f].T + delta @ wg[:, d_f:].T + bg
+            y = xb + sigmoid(g)[:, head_of_channel(d_f, n_heads)] * delta
         elif injection == INJECT_AFFINE:
             # Eq. 13: Y = (1 + s(Delta)) * Norm(X) + t(Delta), [s | t] = Delta W_a^T + b_a
             st = linear(delta, *weights["affine"])
@@ -352,7 +368,7 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
           "q": zgrad(weights["q"]), "k": zgrad(weights["k"]), "v": zgrad(weights["v"]),
           "o": zgrad(weights["o"]),
           "decompress": [zgrad(w) for w in weights["decompress"]],
-          "gate": zgrad(weights["gate"]) if injection == INJECT_GATED else None,
+          "gate": zgrad(weights["gate"]) if injection in (INJECT_GATED, INJECT_GATED_HEAD) else None,
           "affine": zgrad(weights["affine"]) if injection == INJECT_AFFINE else None}
     dx = np.zeros_like(dy)
     d_p = weights["q"][0].shape[0]
@@ -365,6 +381,17 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             # Eq. 11: Y = X + Delta
             ddelta = dy[b]
             dxb = dy[b]
+        elif injection == INJECT_GATED_HEAD:
+            wg = _f64(weights["gate"][0])
+            sg = sigmoid(g)                                   # [rows, n_heads]
+            hc = head_of_channel(d_f, n_heads)
+            gsz = d_f // n_heads
+            # dG_h = sum over the head's channels of dY * Delta, times sigmoid'
+            dg = (dy[b] * delta).reshape(-1, n_heads, gsz).sum(axis=2) * sg * (1.0 - sg)
+            ddelta = dy[b] * sg[:, hc] + dg @ wg[:, d_f:]
+            dxb = dy[b] + dg @ wg[:, :d_f]
+            gr["gate"][0] += dg.T @ np.concatenate([xb, delta], axis=1)
+            gr["gate"][1] += dg.sum(axis=0)
         elif injection == INJECT_AFFINE:
             # Eq. 13: Y = (1 + s) * N + t, N = X r, r = (mean(X^2) + eps)^(-1/2)
             wa = _f64(weights["affine"][0])

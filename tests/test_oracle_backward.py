@@ -282,3 +282,36 @@ def test_backward_finite_differences_affine_modulation(mask, factors):
               - _loss(x, _set(w, path, wm), factors, nh, mask, h_in, dy, dh, inj)) / (2 * eps)
         g = _grad_of(res["grads"], path)[flat]
         assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)
+
+
+@pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BLOCK_CAUSAL])
+def test_backward_finite_differences_per_head_gate(mask):
+    rng = np.random.default_rng(131 + mask)
+    factors = (2, 2)
+    d_f, d_p, nh, L, B = 6, 6, 3, 16, 2
+    w = rand_weights(rng, d_f, d_p, factors, std=0.4)
+    w["gate"] = (rng.standard_normal((nh, 2 * d_f)) * 0.4, rng.standard_normal(nh) * 0.1)
+    x = rng.standard_normal((B, L, d_f))
+    m = L // 4
+    h_in = rng.standard_normal((B, m, d_p))
+    dy = rng.standard_normal((B, L, d_f))
+    dh = rng.standard_normal((B, m, d_p))
+    inj = oracle.INJECT_GATED_HEAD
+    res = oracle.layer_backward(x, w, factors, nh, dy, mask, h_in, dh, injection=inj)
+    eps = 1e-5
+    for idx in [(0, 0, 0), (1, 9, 4), (0, 15, 5)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += eps
+        xm[idx] -= eps
+        fd = (_loss(xp, w, factors, nh, mask, h_in, dy, dh, inj) - _loss(xm, w, factors, nh, mask, h_in, dy, dh, inj)) / (2 * eps)
+        assert abs(fd - res["dx"][idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, res["dx"][idx])
+    for path in _param_paths(w):
+        wt = _get(w, path)
+        flat = np.unravel_index(rng.integers(wt.size), wt.shape)
+        wp, wm = wt.copy(), wt.copy()
+        wp[flat] += eps
+        wm[flat] -= eps
+        fd = (_loss(x, _set(w, path, wp), factors, nh, mask, h_in, dy, dh, inj)
+              - _loss(x, _set(w, path, wm), factors, nh, mask, h_in, dy, dh, inj)) / (2 * eps)
+        g = _grad_of(res["grads"], path)[flat]
+        assert abs(fd - g) <= 1e-6 * max(1.0, abs(fd)), (path, flat, fd, g)

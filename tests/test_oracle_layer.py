@@ -506,3 +506,25 @@ def test_affine_modulation_is_affine_in_the_decompressed_signal():
                                          injection=oracle.INJECT_AFFINE)["x_out"])
     np.testing.assert_allclose(outs[2] - outs[0], 2 * (outs[1] - outs[0]), rtol=1e-10, atol=1e-12)
     assert np.max(np.abs(outs[1] - outs[0])) > 1e-3
+
+
+# ----------------------------------------------------------- per-head gate
+
+@pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BIDIRECTIONAL])
+def test_per_head_gate_equals_channel_gate_with_tied_rows(mask):
+    """The per-head gate is the channel gate of Eq. 12 whose rows (and biases)
+    are tied within each head's channel group."""
+    rng = np.random.default_rng(121)
+    d_f, d_p, nh, B, P, L = 6, 6, 3, 2, 4, 12
+    w = rand_weights(rng, d_f, d_p, (P,))
+    wh = (rng.standard_normal((nh, 2 * d_f)) * 0.3, rng.standard_normal(nh) * 0.2)
+    x = rng.standard_normal((B, L, d_f))
+    w_head = dict(w)
+    w_head["gate"] = wh
+    hc = oracle.head_of_channel(d_f, nh)
+    np.testing.assert_array_equal(hc, [0, 0, 1, 1, 2, 2])
+    w_chan = dict(w)
+    w_chan["gate"] = (wh[0][hc], wh[1][hc])
+    a = oracle.layer_forward(x, w_head, (P,), nh, mask, injection=oracle.INJECT_GATED_HEAD)["x_out"]
+    b = oracle.layer_forward(x, w_chan, (P,), nh, mask, injection=oracle.INJECT_GATED)["x_out"]
+    np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-13)
