@@ -62,8 +62,12 @@ enum pf_mask { PF_TOKEN_CAUSAL = 0, PF_BLOCK_CAUSAL = 1, PF_BIDIRECTIONAL = 2 };
  *   its gradients are not written.
  * PF_INJECT_AFFINE: Y = (1 + s) * Norm(X) + t with [s | t] = Delta W_a^T + b_a
  *   per token (Eq. 13; Norm = x / sqrt(mean(x^2) + 1e-6) over d_fine, no
- *   gain); reads the affine weights instead of the gate's. */
-enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1, PF_INJECT_AFFINE = 2 };
+ *   gain); reads the affine weights instead of the gate's.
+ * PF_INJECT_GATED_HEAD: Eq. 12 with one gate per head (the per-head
+ *   weighting of Eq. 20): G = [X, Delta] W_g^T + b_g with the gate weight
+ *   W_g [n_heads, 2 d_fine], and channel c takes the gate of head
+ *   c / (d_fine / n_heads); d_fine / n_heads must be a multiple of 8. */
+enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1, PF_INJECT_AFFINE = 2, PF_INJECT_GATED_HEAD = 3 };
 
 typedef struct {
   const void* w; /* [out, in] */
@@ -108,8 +112,9 @@ typedef struct {
 /* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)
  * q, k, v, o : W [d_proxy, d_proxy]     (Eq. 9 and its output map)
  * decompress[j]: W [k_{j+1} d_j, d_{j+1}] (Eq. 10, Eq. 17)
- * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12); read
- *              only with PF_INJECT_GATED (may be NULL otherwise)
+ * gate       : W [d_fine, 2 d_fine] acting on [X, Delta] (Eq. 12), or
+ *              W [n_heads, 2 d_fine] with PF_INJECT_GATED_HEAD; not read by
+ *              the other injections (may be NULL there)
  * affine     : W [2 d_fine, d_fine] acting on Delta, rows 0..d_fine-1 give
  *              s and the next d_fine rows t (Eq. 13); read only with
  *              PF_INJECT_AFFINE (may be NULL otherwise) */

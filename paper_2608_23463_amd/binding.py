@@ -25,6 +25,7 @@ PF_BF16 = 1
 PF_INJECT_GATED = 0
 PF_INJECT_ADD = 1
 PF_INJECT_AFFINE = 2
+PF_INJECT_GATED_HEAD = 3
 
 EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
@@ -321,7 +322,7 @@ def layer_backward(cfg: PfLayerConfig, weights: Dict[str, object], x, h_in, save
     for name in ("q", "k", "v", "o"):
         grads[name] = g_like(weights[name])
     # the gate is only read (and differentiated) by gated injection
-    grads["gate"] = g_like(weights["gate"]) if cfg.injection == PF_INJECT_GATED else None
+    grads["gate"] = g_like(weights["gate"]) if cfg.injection in (PF_INJECT_GATED, PF_INJECT_GATED_HEAD) else None
     grads["affine"] = g_like(weights["affine"]) if cfg.injection == PF_INJECT_AFFINE else None
     if workspace is None:
         workspace = _bytes(layer_workspace_size(cfg, True), dev)

@@ -66,7 +66,7 @@ size_t proxy_layer_saved_size(const pf_layer_config* cfg) {
 }
 
 static int check_weights(const LayerDims& d, const pf_layer_weights* w, int injection) {
-  const bool gated = injection == PF_INJECT_GATED;
+  const bool gated = injection == PF_INJECT_GATED || injection == PF_INJECT_GATED_HEAD;
   if (!w) return fail(PF_ERR_INVALID_ARG, "weights struct is NULL");
   for (int j = 0; j < d.M; ++j) {
     if (!w->compress[j].w) return fail(PF_ERR_INVALID_ARG, "compress[%d].w is NULL", j);

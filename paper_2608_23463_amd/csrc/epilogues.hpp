@@ -252,6 +252,21 @@ struct EpiGate {
   }
 };
 
+// fp32 out[r, c] = acc + bias[c] (bias in the activation type, optional).
+template <typename T>
+struct EpiBiasF32 {
+  float* out;
+  int ldo;
+  const T* bias;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    out[(int64_t)r * ldo + c] = v + (bias ? to_f32(bias[c]) : 0.0f);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) (*this)(r, c + e, v[e]);
+  }
+};
+
 constexpr float kAffineEps = 1e-6f;  // RMSNorm epsilon of Eq. 13
 
 // Affine modulation (Eq. 13) on the GEMM [S | T] = Delta W_a^T + b_a with s

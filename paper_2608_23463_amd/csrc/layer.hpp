@@ -55,6 +55,7 @@ struct LayerActs {
   size_t delta;               // [B*L, d_f]
   size_t g;                   // gate pre-activation G, or s of Eq. 13 [B*L, d_f]
   size_t rstd;                // Eq. 13: 1 / RMS of every X row, fp32 [B*L]
+  size_t gh;                  // per-head gate pre-activation, fp32 [B*L, n_heads]
   size_t aff_w, aff_b;        // Eq. 13: W_a, b_a with s and t rows interleaved [2 d_f, d_f], [2 d_f]
   size_t bytes;
 };
@@ -83,6 +84,7 @@ struct LayerWs {
   size_t y_pad;               // forward: X_out; backward: dX [B*L, d_f]
   size_t dy_pad;              // backward: dY with zero padding [B*L, d_f]
   size_t dst;                 // Eq. 13 backward: [dS | dT] [B*L, 2 d_f]
+  size_t dgh;                 // per-head gate backward: dG [B*L, round8(n_heads)]
   size_t bytes;
 };
 

@@ -91,6 +91,76 @@ __global__ void __launch_bounds__(256) affine_bwd_prep_kernel(const T* __restric
   }
 }
 
+// Per-head gate backward, one wave per row (4 rows per workgroup): the
+// head sums dG_h = sum over the head's channels of dY * Delta, times
+// sigmoid'(G_h) (partials per run of 8 channels through LDS, summed in run
+// order), then dDelta = dY sigmoid(G_h(c)) + dG W_gd and the fp32 dX = dY +
+// dG W_gx, with dG in fp32 and the gate rows read per run; dG in the
+// activation type (row stride ldg) for the weight gradient.
+// d <= 4096, nh <= 64, d / nh a multiple of 8.
+template <typename T>
+__global__ void __launch_bounds__(256) head_gate_bwd_kernel(const T* __restrict__ dy, const T* __restrict__ delta,
+                                                            const float* __restrict__ gh, const T* __restrict__ wg,
+                                                            T* __restrict__ ddelta, float* __restrict__ dx32,
+                                                            T* __restrict__ dgh, int64_t rows, int d, int nh,
+                                                            int ldg) {
+  __shared__ float part[4][512];
+  __shared__ float dgs[4][64];
+  __shared__ float sgs[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  const bool live = row < rows;  // every wave reaches the barriers
+  const int runs = d / 8, rph = d / nh / 8;  // runs per row, runs per head
+  const int64_t base = row * d;
+  if (live) {
+    for (int run = lane; run < runs; run += 64) {
+      float a[8], b[8];
+      load8(dy + base + run * 8, a);
+      load8(delta + base + run * 8, b);
+      float p = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) p = fmaf(a[e], b[e], p);
+      part[w][run] = p;
+    }
+  }
+  __syncthreads();
+  if (live && lane < nh) {
+    float acc = 0.0f;
+    for (int k = 0; k < rph; ++k) acc += part[w][lane * rph + k];
+    const float sg = sigmoidf(gh[row * nh + lane]);
+    const float dg = acc * sg * (1.0f - sg);
+    dgs[w][lane] = dg;
+    sgs[w][lane] = sg;
+    dgh[row * ldg + lane] = from_f32<T>(dg);
+  }
+  __syncthreads();
+  if (!live) return;
+  for (int run = lane; run < runs; run += 64) {
+    const int c0 = run * 8, h = run / rph;
+    float a[8], dd[8], dx[8];
+    load8(dy + base + c0, a);
+    const float sg = sgs[w][h];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      dd[e] = a[e] * sg;
+      dx[e] = a[e];
+    }
+    for (int k = 0; k < nh; ++k) {
+      const float g = dgs[w][k];
+      float wx[8], wd[8];
+      load8(wg + (int64_t)k * 2 * d + c0, wx);
+      load8(wg + (int64_t)k * 2 * d + d + c0, wd);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        dx[e] = fmaf(g, wx[e], dx[e]);
+        dd[e] = fmaf(g, wd[e], dd[e]);
+      }
+    }
+    store8(ddelta + base + c0, dd);
+    store8(dx32 + base + c0, dx);
+  }
+}
+
 // Column sums in two fixed-order stages: partial sums over row chunks, then
 // the sum of the partials in chunk order.
 template <typename T>
@@ -437,6 +507,21 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
       wgrad<T>(run, "affine_wgrad_gemm", WT(W.dst) + half * df, 2 * df, S(A.delta), df, df, df, BL,
                dwa ? dwa + (int64_t)half * df * df : nullptr, df, tra, trb, false, dba ? dba + half * df : nullptr,
                part, part2);
+  } else if (cfg->injection == PF_INJECT_GATED_HEAD) {
+    const int ldg = (int)round8(d.nh);
+    run.launch("head_gate_bwd", [&] {
+      hipLaunchKernelGGL((head_gate_bwd_kernel<T>), dim3((unsigned)((BL + 3) / 4)), dim3(256), 0, run.stream, dyp,
+                         S(A.delta), reinterpret_cast<const float*>(saved + A.gh),
+                         reinterpret_cast<const T*>(w->gate.w), WT(W.ddelta), WF(W.dx32), WT(W.dgh), BL, df, d.nh,
+                         ldg);
+      return hipGetLastError();
+    });
+    // dW_g = dG^T [X | Delta]: dG is transposed once for both halves
+    float* dwg = reinterpret_cast<float*>(gr->gate.dw);
+    wgrad<T>(run, "head_gate_wgrad_gemm", WT(W.dgh), ldg, xp, df, d.nh, df, BL, dwg, 2 * df, tra, trb, false,
+             reinterpret_cast<float*>(gr->gate.db), part, part2);
+    wgrad<T>(run, "head_gate_wgrad_gemm", WT(W.dgh), ldg, S(A.delta), df, d.nh, df, BL, dwg ? dwg + df : nullptr,
+             2 * df, tra, trb, dwg != nullptr);
   } else if (!add_inject) {
     run.launch("gate_bwd_prep", [&] {
       const int64_t n8 = BL * df / 8;

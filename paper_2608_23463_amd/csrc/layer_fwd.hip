@@ -110,6 +110,28 @@ __global__ void __launch_bounds__(256) rstd_rows_kernel(const T* __restrict__ x,
   if (lane == 0) rstd[row] = 1.0f / sqrtf(ss / (float)d + eps);
 }
 
+// Per-head gate (Eq. 12 with one gate per head): y = x + sigmoid(G[r, h(c)])
+// * delta for runs of 8 channels (d / n_heads is a multiple of 8, so a run
+// stays inside one head).
+template <typename T>
+__global__ void __launch_bounds__(256) head_gate_combine_kernel(const T* __restrict__ x, const T* __restrict__ delta,
+                                                                const float* __restrict__ gh, T* __restrict__ y,
+                                                                int64_t rows, int d, int nh) {
+  const int64_t n8 = rows * d / 8;
+  const int gs = d / nh;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (int64_t)gridDim.x * 256) {
+    const int64_t e0 = i * 8, r = e0 / d;
+    const int c = (int)(e0 - r * d);
+    const float s = sigmoidf(gh[r * nh + c / gs]);
+    float a[8], b[8], o[8];
+    load8(x + e0, a);
+    load8(delta + e0, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = fmaf(s, b[e], a[e]);
+    store8(y + e0, o);
+  }
+}
+
 // W_a [2d, d] (s rows, then t rows) -> rows interleaved s_0, t_0, s_1, t_1,
 // ..., so the affine GEMM's columns 2c and 2c+1 are s and t of channel c.
 template <typename T>
@@ -129,7 +151,7 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   if (!c) return *why = "config is NULL", PF_ERR_INVALID_ARG;
   if (c->dtype != PF_FP32 && c->dtype != PF_BF16) return *why = "dtype must be PF_FP32 or PF_BF16", PF_ERR_INVALID_ARG;
   if (c->mask < PF_TOKEN_CAUSAL || c->mask > PF_BIDIRECTIONAL) return *why = "unknown mask mode", PF_ERR_INVALID_ARG;
-  if (c->injection != PF_INJECT_GATED && c->injection != PF_INJECT_ADD && c->injection != PF_INJECT_AFFINE)
+  if (c->injection < PF_INJECT_GATED || c->injection > PF_INJECT_GATED_HEAD)
     return *why = "unknown injection mode", PF_ERR_INVALID_ARG;
   if (c->batch < 1 || c->seq_len < 1) return *why = "batch and seq_len must be >= 1", PF_ERR_INVALID_ARG;
   if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
@@ -182,6 +204,10 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   for (int j = 0; j < d->M; ++j)
     if ((int64_t)d->k[j] * d->d[j] > INT32_MAX / 2) return *why = "k_j * d_j too large", PF_ERR_UNSUPPORTED;
   if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
+  if (c->injection == PF_INJECT_GATED_HEAD && (d->d_f % d->nh != 0 || (d->d_f / d->nh) % 8 != 0))
+    return *why = "the per-head gate needs d_fine / n_heads to be a multiple of 8", PF_ERR_UNSUPPORTED;
+  if (c->injection == PF_INJECT_GATED_HEAD && (d->d_f > 4096 || d->nh > 64))
+    return *why = "the per-head gate takes d_fine <= 4096 and n_heads <= 64", PF_ERR_UNSUPPORTED;
   return PF_OK;
 }
 
@@ -216,9 +242,11 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   a.s = take(prox);
   for (int j = 1; j < d.M; ++j) a.u[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
   a.delta = take((size_t)d.B * d.L * d.d_f * es);
-  a.g = bwd && d.inject != PF_INJECT_ADD ? take((size_t)d.B * d.L * d.d_f * es) : 0;
+  a.g = bwd && (d.inject == PF_INJECT_GATED || d.inject == PF_INJECT_AFFINE) ? take((size_t)d.B * d.L * d.d_f * es)
+                                                                               : 0;
   const bool affine = d.inject == PF_INJECT_AFFINE;
   a.rstd = take(affine ? (size_t)d.B * d.L * 4 : 0);
+  a.gh = take(d.inject == PF_INJECT_GATED_HEAD ? (size_t)d.B * d.L * d.nh * 4 : 0);
   a.aff_w = take(affine ? (size_t)2 * d.d_f * d.d_f * es : 0);
   a.aff_b = take(affine ? (size_t)2 * d.d_f * es : 0);
   a.bytes = off;
@@ -293,6 +321,7 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     w.tr_w = take(trw);
   }
   if (bwd && d.inject == PF_INJECT_AFFINE) w.dst = take(2 * tok);
+  if (bwd && d.inject == PF_INJECT_GATED_HEAD) w.dgh = take((size_t)d.B * d.L * round8(d.nh) * es);
   if (d.staged()) {
     w.x_pad = take(tok);
     w.y_pad = take(tok);
@@ -486,6 +515,33 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     EpiAffine<T> e{reinterpret_cast<const T*>(x), rstd, P(A.aff_b), reinterpret_cast<T*>(x_out),
                    saving ? P(A.g) : nullptr, d.d_f};
     run.gemm<T, LAYOUT_K, LAYOUT_K>("affine_gemm", pr, e);
+    return;
+  }
+
+  // 6. per-head gate: G = [X, Delta] W_g^T + b_g (N = n_heads, fp32), then
+  //    Y = X + sigmoid(G[head]) * Delta
+  if (cfg->injection == PF_INJECT_GATED_HEAD) {
+    const int64_t rows = (int64_t)d.B * d.L;
+    float* gh = reinterpret_cast<float*>(act + A.gh);
+    GemmProblem pr{};
+    pr.a = x;
+    pr.lda = d.d_f;
+    pr.a2 = P(A.delta);
+    pr.lda2 = d.d_f;
+    pr.a_ksplit = d.d_f;
+    pr.b = w->gate.w;
+    pr.ldb = 2 * d.d_f;
+    pr.M = (int)rows;
+    pr.N = d.nh;
+    pr.K = 2 * d.d_f;
+    run.gemm<T, LAYOUT_K, LAYOUT_K>("head_gate_gemm", pr, EpiBiasF32<T>{gh, d.nh, reinterpret_cast<const T*>(w->gate.b)});
+    run.launch("head_gate_combine", [&] {
+      const int64_t n8 = rows * d.d_f / 8;
+      hipLaunchKernelGGL((head_gate_combine_kernel<T>), dim3((unsigned)std::min<int64_t>((n8 + 255) / 256, 16384)),
+                         dim3(256), 0, run.stream, reinterpret_cast<const T*>(x), P(A.delta), gh,
+                         reinterpret_cast<T*>(x_out), rows, d.d_f, d.nh);
+      return hipGetLastError();
+    });
     return;
   }
 

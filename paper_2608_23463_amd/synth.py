@@ -32,6 +32,7 @@ BIDIRECTIONAL = 2
 INJECT_GATED = 0  # Eq. 12
 INJECT_ADD = 1    # Eq. 11
 INJECT_AFFINE = 2  # Eq. 13
+INJECT_GATED_HEAD = 3  # Eq. 12 with one gate per head (Eq. 20's per-head weighting)
 
 WEIGHT_STD = 0.02
 
@@ -84,7 +85,7 @@ class LayerShape:
             "compress": comp,
             "q": (dp, dp), "k": (dp, dp), "v": (dp, dp), "o": (dp, dp),
             "decompress": dec,
-            "gate": (self.d_fine, 2 * self.d_fine),
+            "gate": (self.n_heads if self.injection == INJECT_GATED_HEAD else self.d_fine, 2 * self.d_fine),
         }
 
 

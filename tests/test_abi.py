@@ -80,7 +80,7 @@ def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 
     (dict(seq_len=0), B.PF_ERR_INVALID_ARG),
     (dict(n_heads=8), B.PF_ERR_INVALID_ARG),
     (dict(mask=5), B.PF_ERR_INVALID_ARG),
-    (dict(injection=3), B.PF_ERR_INVALID_ARG),
+    (dict(injection=4), B.PF_ERR_INVALID_ARG),
     (dict(head_dim=32, n_heads=8), B.PF_ERR_UNSUPPORTED),
     (dict(d_fine=100), B.PF_ERR_UNSUPPORTED),
 ])
@@ -247,3 +247,14 @@ def test_affine_weights_required_by_affine_injection(lib):
     assert _fwd(lib, cfg, w) == B.PF_ERR_INVALID_ARG and "affine" in B.last_error()
     w.affine = B.PfLinear(0x10000, 0x10008)  # misaligned bias
     assert _fwd(lib, cfg, w) == B.PF_ERR_INVALID_ARG
+
+
+def test_per_head_gate_shape_limits(lib):
+    # d_fine = 256, 4 heads: 64 channels per head
+    assert B.layer_workspace_size(_cfg(injection=3)) > 0
+    # 256 / 8 heads = 32 channels: fine; d_fine = 24 over 4 heads = 6 channels: not a multiple of 8
+    for kw, status in ((dict(d_fine=24), B.PF_ERR_UNSUPPORTED),
+                       (dict(d_fine=4096 + 256, injection=3), B.PF_ERR_UNSUPPORTED)):
+        c = _cfg(**kw)
+        c.injection = 3
+        assert _fwd(lib, c, _weights_struct()) == status, kw

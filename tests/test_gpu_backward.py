@@ -93,6 +93,11 @@ CASES = {
     "bf16_inject_affine": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_AFFINE), True),
     "fp32_inject_affine": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
                                       injection=synth.INJECT_AFFINE), False),
+    # per-head gate; 16,384 token rows take the transposed weight-gradient path
+    "bf16_inject_gated_head": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_GATED_HEAD),
+                               True),
+    "fp32_inject_gated_head": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
+                                          injection=synth.INJECT_GATED_HEAD), False),
     # partial last block (L % P != 0): zero-padded inside the library, dY = 0 on the padding
     "bf16_tc_partial_block": (LayerShape(2, 16 * 37 + 9, 192, 192, 3, 64, (16,)), True),
     "fp32_bi_partial_block_factorised": (LayerShape(1, 8 * 37 + 5, 64, 128, 2, 64, (2, 4), level_dims=(96,),

@@ -37,6 +37,13 @@ SMALL = {
     "fp32_inject_affine_factorised_bi": (LayerShape(1, 8 * 40, 64, 128, 1, 128, (2, 4), level_dims=(48,),
                                                     dtype="fp32", mask=synth.BIDIRECTIONAL,
                                                     injection=synth.INJECT_AFFINE), False),
+    # per-head gate (Eq. 12 with the per-head weighting of Eq. 20): N = n_heads gate GEMM + combine
+    "bf16_inject_gated_head": (LayerShape(2, 37 * 16, 192, 192, 3, 64, (16,), injection=synth.INJECT_GATED_HEAD),
+                               True),
+    "fp32_gated_head_factorised": (LayerShape(1, 8 * 40, 64, 128, 2, 64, (2, 4), level_dims=(48,), dtype="fp32",
+                                              injection=synth.INJECT_GATED_HEAD), False),
+    "bf16_gated_head_lm_shape": (LayerShape(1, 64 * 300, 64, 512, 8, 64, (64,), injection=synth.INJECT_GATED_HEAD),
+                                 False),
     # partial last block (L % P != 0, m = ceil(L / P), zero-padded, Sec. 3.1)
     "bf16_partial_block_tc": (LayerShape(2, 37 * 16 + 5, 192, 192, 3, 64, (16,)), True),
     "fp32_partial_block_factorised_bi": (LayerShape(1, 8 * 40 + 3, 64, 128, 1, 128, (2, 4), level_dims=(48,),
