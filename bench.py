@@ -9,8 +9,8 @@ torch.cuda.synchronize() and HIP events on the launch stream.
 Extra objects on the same line:
   kernels      per-kernel average duration from the library's event tracing
                (a second pass over K calls) and achieved TFLOP/s or GB/s
-  variants     the same forward with residual-add injection (Eq. 11) and with
-               affine modulation (Eq. 13)
+  variants     the same forward with residual-add injection (Eq. 11), affine
+               modulation (Eq. 13) and the per-head gate
   ceilings     a 1 GiB device copy (achievable HBM rate) beside the vendor peaks
   roofline     the dominant kernel against the MI355X peak of its bound
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
@@ -225,6 +225,27 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
                                      "value": round(shape.seq_len * shape.batch / (ms_aff * 1e-3), 1),
                                      "unit": "tokens/s"}
         del ws_aff, w_aff, wst_aff
+        # per-head gate (Eq. 12 with one gate per head): N = n_heads gate GEMM and a combine pass
+        cfg_gh = B.config_from_shape(shape)
+        cfg_gh.injection = B.PF_INJECT_GATED_HEAD
+        w_gh = dict(w)
+        w_gh["gate"] = ((torch.randn(shape.n_heads, 2 * shape.d_fine, generator=gen, device="cuda") * 0.02)
+                        .to(x.dtype), torch.zeros(shape.n_heads, dtype=x.dtype, device="cuda"))
+        wst_gh = B.layer_weights(w_gh)
+        ws_gh = torch.empty(B.layer_workspace_size(cfg_gh), dtype=torch.uint8, device="cuda")
+        for _ in range(warmup):
+            B.layer_forward_raw(cfg_gh, wst_gh, x, None, x_out, h_out, None, ws_gh)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            B.layer_forward_raw(cfg_gh, wst_gh, x, None, x_out, h_out, None, ws_gh)
+        stop.record()
+        torch.cuda.synchronize()
+        ms_gh = start.elapsed_time(stop) / steps
+        variants["inject_gated_head"] = {"ms_per_step": round(ms_gh, 4),
+                                         "value": round(shape.seq_len * shape.batch / (ms_gh * 1e-3), 1),
+                                         "unit": "tokens/s"}
+        del ws_gh, w_gh, wst_gh
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
