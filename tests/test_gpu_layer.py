@@ -195,3 +195,32 @@ def test_forward_parity_2d_partition(gpu, name):
                                   shape.mask, inp["h_in"])
     assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
     assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+
+
+@pytest.mark.parametrize("name,shape", [
+    ("bf16_affine_L16k_d1024", LayerShape(1, 16384, 1024, 1024, 16, 64, (64,), injection=synth.INJECT_AFFINE)),
+    ("bf16_gated_head_L16k_d1024", LayerShape(1, 16384, 1024, 1024, 16, 64, (64,),
+                                              injection=synth.INJECT_GATED_HEAD)),
+    ("bf16_partial_block_L16k_d1024", LayerShape(1, 16384 - 23, 1024, 1024, 16, 64, (64,))),
+])
+def test_forward_parity_variants_at_width_1024(gpu, name, shape):
+    """Injection variants and a partial last block at the workloads' width
+    (d = 1024, 16 heads, P = 64) over 16K tokens: every output compared."""
+    print(f"[case {name}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, zlib.crc32(name.encode()) % 1000)
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask,
+                               injection=shape.injection)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+
+
+def test_forward_parity_2d_partition_image_128x128(gpu):
+    """A 128 x 128 image in 8 x 8 patches (P = 64, 256 proxies) at d = 1024."""
+    shape = LayerShape(1, 128 * 128, 1024, 1024, 16, 64, (64,), mask=synth.BIDIRECTIONAL, image_width=128)
+    inp = synth.layer_inputs(shape, 77)
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward_2d(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.image_width,
+                                  shape.mask)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, "image 128x128 h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, "image 128x128 x_out")
