@@ -554,38 +554,67 @@ __global__ void __launch_bounds__(WM* WN* kWave)
   gemm_store<S, BM, BN, WM>(acc, reinterpret_cast<float*>(smem), p, m0, n0, wm, wn, lane, tid, epi);
 }
 
-// Direct-to-LDS variant for operands contiguous along K (both A and B) whose
-// K concatenation point, if any, falls on a BK boundary. Each wave issues
-// buffer_load_dwordx4 ... lds: a wave instruction fills eight 128-byte tile
-// rows (64 lanes x 16 bytes), with chunk c of row r stored at c ^ (r % 8)
-// so that the 16 lanes of a fragment read hit 64 distinct banks without
-// padding. The loads for tile k+1 go out right after the single barrier of
-// step k, into the other LDS stage, and land while step k multiplies; no
-// registers hold prefetched data and no LDS stores are issued.
-template <typename T, int BM, int BN, int BK, int WM, int WN, int NS>
+// Direct-to-LDS GEMM. Each wave issues buffer_load_dwordx4 ... lds: a wave
+// instruction fills 1 KB of a tile (64 lanes x 16 bytes) and no registers
+// hold prefetched data. An operand contiguous along K (LAYOUT_K) lands as
+// ROWS rows of BK elements; one contiguous along M or N (LAYOUT_MN, bf16) as
+// BK rows of ROWS elements, and its MFMA fragments (8 consecutive k of one
+// row or column) come from two LDS transpose reads (ds_read_b64_tr_b16),
+// so weight and data gradients need no transposed copies in HBM. 16-byte
+// chunks are XOR-swizzled by row so every fragment read pass hits 64
+// distinct banks without padding. The loads for tile k+1 go out right after
+// the single barrier of step k, into the other LDS stage, and land while
+// step k multiplies. The K concatenation point, if any, falls on a BK
+// boundary.
+template <typename T, int ROWS, int BK, int LAYOUT, int WAVES>
+struct DirectOp {
+  static constexpr bool kMN = LAYOUT == LAYOUT_MN;
+  static constexpr int kRowElems = kMN ? ROWS : BK;
+  static constexpr int kTileRows = kMN ? BK : ROWS;
+  static constexpr int kRowBytes = kRowElems * (int)sizeof(T);
+  static constexpr int kCpr = kRowBytes / 16;            // 16-byte chunks per row
+  static constexpr int kRowsPerInst = kWave / kCpr;      // rows one wave instruction fills
+  static constexpr int kInsts = kTileRows / (kRowsPerInst * WAVES);  // loads per thread per stage
+  static constexpr int kElems = kTileRows * kRowElems;
+  static_assert(!kMN || sizeof(T) == 2, "transpose reads take 16-bit elements");
+  static_assert(kMN ? kCpr >= 16 : (kCpr == 8 || kCpr == 4), "swizzle covers these row widths");
+  static_assert(kInsts >= 1 && kTileRows % (kRowsPerInst * WAVES) == 0, "tile rows split evenly over waves");
+  // Physical chunk of logical chunk c in row r is c ^ key(r). K-major: any 8
+  // consecutive rows read at one logical chunk cover all 32 LDS banks.
+  // M/N-major: a transpose-read pass touches 4 consecutive rows (k) at 4
+  // consecutive chunks; the key moves each row by 64 bytes.
+  static __device__ __forceinline__ int key(int r) {
+    if constexpr (kMN) return (r & 3) * 4;
+    return kCpr == 8 ? (r & 7) : ((r >> 1) & 3);
+  }
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, int NS, int LA = LAYOUT_K, int LB = LAYOUT_K>
 struct DirectShape {
   typedef GemmShape<T, BM, BN, BK, WM, WN> S;
-  static constexpr int kVec = S::kVec;
-  static constexpr int kCpr = BK / kVec;               // 16-byte chunks per row
-  static constexpr int kRowsPerInst = kWave / kCpr;    // rows one wave instruction fills
   static constexpr int kWaves = WM * WN;
-  static constexpr int kNia = BM / (kRowsPerInst * kWaves);
-  static constexpr int kNib = BN / (kRowsPerInst * kWaves);
+  typedef DirectOp<T, BM, BK, LA, WM * WN> OA;
+  typedef DirectOp<T, BN, BK, LB, WM * WN> OB;
+  static constexpr int kNia = OA::kInsts;
+  static constexpr int kNib = OB::kInsts;
   static constexpr int kLoads = kNia + kNib;           // loads per thread per stage
-  static constexpr int kStage = (BM + BN) * BK;          // elements per stage
+  static constexpr int kStage = OA::kElems + OB::kElems;  // elements per stage
   static constexpr size_t kMainBytes = (size_t)NS * kStage * sizeof(T);
   // fp32 staging of 16 rows of every wave's tile (the wave-local epilogue)
   static constexpr size_t kEpiRegion16 = (size_t)kWaves * 16 * (S::kTN + 8) * sizeof(float);
   static constexpr size_t kLdsBytes = kMainBytes;
-  static_assert(kCpr == 8 || kCpr == 4, "the XOR swizzle handles 64- and 128-byte tile rows");
-  static_assert(kNia >= 1 && kNib >= 1 && BM % (kRowsPerInst * kWaves) == 0 && BN % (kRowsPerInst * kWaves) == 0,
-                "tile rows must split evenly over wave instructions");
   static_assert(NS >= 2 && kLoads * (NS - 1) < 64, "outstanding loads must fit the vmcnt counter");
   static_assert(kLdsBytes <= 160 * 1024, "LDS budget of one workgroup");
-  // Physical chunk of logical chunk c in row r is c ^ key(r): any 8
-  // consecutive rows read at one logical chunk cover all 32 LDS banks.
-  static __device__ __forceinline__ int key(int r) { return kCpr == 8 ? (r & 7) : ((r >> 1) & 3); }
 };
+
+typedef short pf_v4i16 __attribute__((ext_vector_type(4)));
+// LDS transpose read: within each 16-lane group, lane i supplies the address
+// of 4 consecutive 16-bit elements and lane l receives element l % 4 of the
+// lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4, in that order.
+__device__ __forceinline__ pf_v4i16 lds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) pf_v4i16*)(const_cast<void*>(p)));
+}
 
 // Waits until at most `pending` stages of loads (kLoads each) are in flight.
 template <int L, int NP>
@@ -600,13 +629,17 @@ __device__ __forceinline__ void wait_stages(int pending) {
   }
 }
 
-template <typename T, int BM, int BN, int BK, int WM, int WN, int NS, class Epi>
+template <typename T, int BM, int BN, int BK, int WM, int WN, int NS, class Epi, int LA = LAYOUT_K,
+          int LB = LAYOUT_K>
 __global__ void __launch_bounds__(WM* WN* kWave)
     __attribute__((amdgpu_waves_per_eu(WM* WN / 4, (BM >= 256 ? 1 : 2) * WM * WN / 4)))
     gemm_direct_kernel(const GemmParams p, const Epi epi) {
-  typedef DirectShape<T, BM, BN, BK, WM, WN, NS> D;
+  typedef DirectShape<T, BM, BN, BK, WM, WN, NS, LA, LB> D;
   typedef typename D::S S;
+  typedef typename D::OA OA;
+  typedef typename D::OB OB;
   typedef Mma<T> MM;
+  constexpr int kVec = 16 / (int)sizeof(T);  // elements per chunk
   __shared__ __attribute__((aligned(1024))) char smem_raw[D::kLdsBytes];
   T* smem = reinterpret_cast<T*>(smem_raw);
 
@@ -619,62 +652,85 @@ __global__ void __launch_bounds__(WM* WN* kWave)
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: LDS bases go to M0
   const int wm = wave / WN, wn = wave % WN;
 
-  // per-lane byte offsets inside a tile (rows r, swizzled chunk)
-  const int lr = lane / D::kCpr, lc = lane % D::kCpr;
   const int64_t lda_b = p.lda * (int64_t)sizeof(T), ldb_b = p.ldb * (int64_t)sizeof(T);
-  uint32_t voa[D::kNia], vob[D::kNib];
-  int kca[D::kNia], kcb[D::kNib];
+  // per-lane byte offsets inside a tile (rows r, swizzled chunk)
+  uint32_t voa[OA::kInsts], vob[OB::kInsts];
+  int kca[OA::kInsts], kcb[OB::kInsts];
+  {
+    const int lr_a = lane / OA::kCpr, lc_a = lane % OA::kCpr;
 #pragma unroll
-  for (int i = 0; i < D::kNia; ++i) {
-    const int r = (wave * D::kNia + i) * D::kRowsPerInst + lr;
-    const int gc = lc ^ D::key(r);
-    kca[i] = gc * D::kVec;
-    voa[i] = (uint32_t)(r * lda_b + gc * 16);
-  }
+    for (int i = 0; i < OA::kInsts; ++i) {
+      const int r = (wave * OA::kInsts + i) * OA::kRowsPerInst + lr_a;
+      const int gc = lc_a ^ OA::key(r);
+      kca[i] = gc * kVec;
+      voa[i] = (uint32_t)(r * lda_b + gc * 16);
+    }
+    const int lr_b = lane / OB::kCpr, lc_b = lane % OB::kCpr;
 #pragma unroll
-  for (int i = 0; i < D::kNib; ++i) {
-    const int r = (wave * D::kNib + i) * D::kRowsPerInst + lr;
-    const int gc = lc ^ D::key(r);
-    kcb[i] = gc * D::kVec;
-    vob[i] = (uint32_t)(r * ldb_b + gc * 16);
+    for (int i = 0; i < OB::kInsts; ++i) {
+      const int r = (wave * OB::kInsts + i) * OB::kRowsPerInst + lr_b;
+      const int gc = lc_b ^ OB::key(r);
+      kcb[i] = gc * kVec;
+      vob[i] = (uint32_t)(r * ldb_b + gc * 16);
+    }
   }
+  // K-major: the tile is BM (BN) rows from m0 (n0), a stage advances along
+  // each row. M/N-major: the tile is BK rows of the operand starting at row
+  // k0, each read from column m0 (n0); only the rows below kend and the
+  // columns below M (N) of the last row are in range.
+  const char* a1 = reinterpret_cast<const char*>(p.a) + (OA::kMN ? m0 * (int64_t)sizeof(T) : m0 * lda_b);
+  const char* a2 = p.a2 ? reinterpret_cast<const char*>(p.a2) + (OA::kMN ? m0 * (int64_t)sizeof(T) : m0 * lda_b)
+                        : nullptr;
+  const char* b1 = reinterpret_cast<const char*>(p.b) + (OB::kMN ? n0 * (int64_t)sizeof(T) : n0 * ldb_b);
+  const char* b2 = p.b2 ? reinterpret_cast<const char*>(p.b2) + (OB::kMN ? n0 * (int64_t)sizeof(T) : n0 * ldb_b)
+                        : nullptr;
   const uint32_t a_rows = (uint32_t)(max(0, min(BM, p.M - m0)) * lda_b);
   const uint32_t b_rows = (uint32_t)(max(0, min(BN, p.N - n0)) * ldb_b);
-  const char* a1 = reinterpret_cast<const char*>(p.a) + m0 * lda_b;
-  const char* a2 = p.a2 ? reinterpret_cast<const char*>(p.a2) + m0 * lda_b : nullptr;
-  const char* b1 = reinterpret_cast<const char*>(p.b) + n0 * ldb_b;
-  const char* b2 = p.b2 ? reinterpret_cast<const char*>(p.b2) + n0 * ldb_b : nullptr;
+  const int a_cols = max(0, min(BM, p.M - m0)), b_cols = max(0, min(BN, p.N - n0));
 
-  // Loads [i0, i1) of one stage (A's kNia loads, then B's kNib), so a stage
-  // can be issued at once or spread over the k-steps of a tile.
+  // Loads [i0, i1) of one stage (A's loads, then B's), so a stage can be
+  // issued at once or spread over the k-steps of a tile.
   auto issue_range = [&](int k0, int stage, int i0, int i1) {
     const bool tail = k0 + BK > kend;
     T* st = smem + stage * D::kStage;
-    if (i0 < D::kNia) {
+    if (i0 < OA::kInsts) {
       const bool second = k0 >= p.a_ksplit;
       const int krel = second ? k0 - p.a_ksplit : k0;
-      const rsrc_t rs =
-          make_rsrc_uniform((second ? a2 : a1) + (int64_t)krel * sizeof(T), a_rows - (uint32_t)(krel * sizeof(T)));
+      rsrc_t rs;
+      if constexpr (OA::kMN) {
+        const int rows = min(BK, kend - k0);
+        rs = make_rsrc_uniform((second ? a2 : a1) + (int64_t)krel * lda_b,
+                               (uint32_t)((int64_t)(rows - 1) * lda_b + a_cols * (int64_t)sizeof(T)));
+      } else {
+        rs = make_rsrc_uniform((second ? a2 : a1) + (int64_t)krel * sizeof(T), a_rows - (uint32_t)(krel * sizeof(T)));
+      }
 #pragma unroll
-      for (int i = 0; i < D::kNia; ++i)
-        if (i >= i0 && i < i1)
-          buf_ld16_lds(rs, (!tail || k0 + kca[i] < kend) ? voa[i] : kOOB,
-                       st + (wave * D::kNia + i) * D::kRowsPerInst * BK);
+      for (int i = 0; i < OA::kInsts; ++i)
+        if (i >= i0 && i < i1) {
+          const bool oob = !OA::kMN && tail && k0 + kca[i] >= kend;
+          buf_ld16_lds(rs, oob ? kOOB : voa[i], st + (wave * OA::kInsts + i) * 1024 / (int)sizeof(T));
+        }
     }
-    if (i1 > D::kNia) {
+    if (i1 > OA::kInsts) {
       const bool second = k0 >= p.b_ksplit;
       const int krel = second ? k0 - p.b_ksplit : k0;
-      const rsrc_t rs =
-          make_rsrc_uniform((second ? b2 : b1) + (int64_t)krel * sizeof(T), b_rows - (uint32_t)(krel * sizeof(T)));
+      rsrc_t rs;
+      if constexpr (OB::kMN) {
+        const int rows = min(BK, kend - k0);
+        rs = make_rsrc_uniform((second ? b2 : b1) + (int64_t)krel * ldb_b,
+                               (uint32_t)((int64_t)(rows - 1) * ldb_b + b_cols * (int64_t)sizeof(T)));
+      } else {
+        rs = make_rsrc_uniform((second ? b2 : b1) + (int64_t)krel * sizeof(T), b_rows - (uint32_t)(krel * sizeof(T)));
+      }
 #pragma unroll
-      for (int i = 0; i < D::kNib; ++i)
-        if (i + D::kNia >= i0 && i + D::kNia < i1)
-          buf_ld16_lds(rs, (!tail || k0 + kcb[i] < kend) ? vob[i] : kOOB,
-                       st + BM * BK + (wave * D::kNib + i) * D::kRowsPerInst * BK);
+      for (int i = 0; i < OB::kInsts; ++i)
+        if (i + OA::kInsts >= i0 && i + OA::kInsts < i1) {
+          const bool oob = !OB::kMN && tail && k0 + kcb[i] >= kend;
+          buf_ld16_lds(rs, oob ? kOOB : vob[i], st + OA::kElems + (wave * OB::kInsts + i) * 1024 / (int)sizeof(T));
+        }
     }
   };
   auto issue = [&](int k0, int stage) { issue_range(k0, stage, 0, D::kLoads); };
-
 
   f32x16 acc[S::kFM][S::kFN];
 #pragma unroll
@@ -688,9 +744,9 @@ __global__ void __launch_bounds__(WM* WN* kWave)
   constexpr int kSub = BK / 16;  // MFMA k-steps per tile
   static_assert(kSub % 2 == 0, "fragment double buffer alternates over an even number of k-steps");
   const int frow = lane & 31;
-  const int swz = D::key(frow);  // rows this lane reads differ by multiples of 32
   const int g = lane >> 5;
-  auto frag = [&](const T* rowp, int st) {
+  // K-major fragment: row frow of the 32-row block at rowp, k-step st
+  auto frag_k = [&](const T* rowp, int swz, int st) {
     if constexpr (sizeof(T) == 2) {
       return MM::load(rowp + (((2 * st + g) ^ swz) * 8));
     } else {
@@ -706,15 +762,52 @@ __global__ void __launch_bounds__(WM* WN* kWave)
       return f;
     }
   };
+  // M/N-major fragment: column c0 .. c0+31 of the tile (this lane's column
+  // c0 + frow), k = 16 st + 8 g .. +7, from two transpose reads: lane i of a
+  // 16-lane group addresses row k + i / 4 at columns 4 (i % 4) .. +3 of the
+  // group's 16 columns.
+  const int tr_row = 8 * g + ((lane & 15) >> 2);
+  const int tr_col = (lane & 16) + 4 * (lane & 3);
+  auto frag_mn = [&](const T* tile, int row_elems, int c0, int st, auto op) {
+    typedef decltype(op) O;
+    const int col = c0 + tr_col;
+    const int r0 = 16 * st + tr_row;
+    const char* base = reinterpret_cast<const char*>(tile);
+    const int chunk = col / kVec, half = (col / 4) & 1;
+    const pf_v4i16 lo =
+        lds_read_tr16(base + r0 * (row_elems * 2) + ((chunk ^ O::key(r0)) * 16) + half * 8);
+    const pf_v4i16 hi =
+        lds_read_tr16(base + (r0 + 4) * (row_elems * 2) + ((chunk ^ O::key(r0 + 4)) * 16) + half * 8);
+    typename MM::frag f;
+    const auto l = __builtin_bit_cast(bf16x4, lo);
+    const auto h = __builtin_bit_cast(bf16x4, hi);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[e] = l[e];
+      f[e + 4] = h[e];
+    }
+    return f;
+  };
   typename MM::frag fa[2][S::kFM], fb[2][S::kFN];
   auto read_frags = [&](int tile, int st, int buf) {
     const T* cur = smem + (tile % NS) * D::kStage;
-    const T* sa = cur + (wm * S::kTM + frow) * BK;
-    const T* sb = cur + BM * BK + (wn * S::kTN + frow) * BK;
+    if constexpr (OA::kMN) {
 #pragma unroll
-    for (int i = 0; i < S::kFM; ++i) fa[buf][i] = frag(sa + i * 32 * BK, st);
+      for (int i = 0; i < S::kFM; ++i) fa[buf][i] = frag_mn(cur, BM, wm * S::kTM + i * 32, st, OA{});
+    } else {
+      const T* sa = cur + (wm * S::kTM + frow) * BK;
 #pragma unroll
-    for (int j = 0; j < S::kFN; ++j) fb[buf][j] = frag(sb + j * 32 * BK, st);
+      for (int i = 0; i < S::kFM; ++i) fa[buf][i] = frag_k(sa + i * 32 * BK, OA::key(frow), st);
+    }
+    const T* curb = cur + OA::kElems;
+    if constexpr (OB::kMN) {
+#pragma unroll
+      for (int j = 0; j < S::kFN; ++j) fb[buf][j] = frag_mn(curb, BN, wn * S::kTN + j * 32, st, OB{});
+    } else {
+      const T* sb = curb + (wn * S::kTN + frow) * BK;
+#pragma unroll
+      for (int j = 0; j < S::kFN; ++j) fb[buf][j] = frag_k(sb + j * 32 * BK, OB::key(frow), st);
+    }
   };
   auto mfmas = [&](int buf) {
 #pragma unroll
@@ -722,6 +815,8 @@ __global__ void __launch_bounds__(WM* WN* kWave)
 #pragma unroll
       for (int j = 0; j < S::kFN; ++j) acc[i][j] = MM::mma(fa[buf][i], fb[buf][j], acc[i][j]);
   };
+  // reads per k-step: one per K-major fragment, two per M/N-major one
+  constexpr int kReads = S::kFM * (OA::kMN ? 2 : 1) + S::kFN * (OB::kMN ? 2 : 1);
 
   // Ring of NS stages, tile t in stage t % NS. The hand-off to tile kt+1
   // happens before the last k-step of tile kt, whose fragments are already
@@ -743,7 +838,7 @@ __global__ void __launch_bounds__(WM* WN* kWave)
       read_frags(kt, st + 1, (st + 1) & 1);
       mfmas(st & 1);
     }
-    if constexpr (sizeof(T) == 2) pin_substeps<S::kFM + S::kFN, S::kFM * S::kFN, kSub - 1>();
+    if constexpr (sizeof(T) == 2) pin_substeps<kReads, S::kFM * S::kFN, kSub - 1>();
     // The last k-step's fragments are in registers on every path, so the
     // compiler sees no reason to make its MFMAs wait for the younger reads
     // of tile kt+1. The scheduling fence keeps the wait behind the MFMAs
@@ -901,13 +996,23 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   const bool aligned_split = (pr.a_ksplit >= pr.K || pr.a_ksplit % BK == 0) &&
                              (pr.b_ksplit >= pr.K || pr.b_ksplit % BK == 0) &&
                              (!pr.a2 || pr.lda2 == pr.lda) && (!pr.b2 || pr.ldb2 == pr.ldb);
+  // 256x256 tiles run as 8 waves of 128x64: two waves per SIMD, so one
+  // wave's MFMAs cover the other's load issue and barrier waits.
+  constexpr int DWN = (BM == 256 && BN == 256) ? 4 : WN;
   if constexpr (LA == LAYOUT_K && LB == LAYOUT_K) {
     if (aligned_split && pl.k_slice % BK == 0) {
-      // 256x256 tiles run as 8 waves of 128x64: two waves per SIMD, so one
-      // wave's MFMAs cover the other's load issue and barrier waits.
-      constexpr int DWN = (BM == 256 && BN == 256) ? 4 : WN;
       hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, DWN, 2, Epi>), grid, dim3(WM * DWN * kWave), 0,
                          stream, p, epi);
+      return hipGetLastError();
+    }
+  } else if constexpr (sizeof(T) == 2 && BM >= 128 && BN >= 128) {
+    // M/N-major operands through LDS transpose reads: rows of such an
+    // operand start 16-byte aligned and hold at least one tile width
+    const bool rows_ok = (LA == LAYOUT_K || (pr.lda % 8 == 0 && pr.lda >= BM)) &&
+                         (LB == LAYOUT_K || (pr.ldb % 8 == 0 && pr.ldb >= BN));
+    if (aligned_split && pl.k_slice % BK == 0 && rows_ok) {
+      hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, DWN, 2, Epi, LA, LB>), grid,
+                         dim3(WM * DWN * kWave), 0, stream, p, epi);
       return hipGetLastError();
     }
   }

@@ -177,6 +177,45 @@ __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* __restrict
   part[(int64_t)chunk * n + c] = s;
 }
 
+// The same partial sums, 8 columns per thread (16-byte loads; n and ld
+// multiples of 8) over four independent row streams combined in a fixed
+// order, so the sums stay deterministic.
+template <typename T>
+__global__ void __launch_bounds__(256) colsum_partial8_kernel(const T* __restrict__ in, int64_t rows, int n,
+                                                              int64_t ld, int64_t rows_per_chunk,
+                                                              float* __restrict__ part) {
+  const int c = (blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  const int chunk = blockIdx.y;
+  if (c >= n) return;
+  const int64_t r0 = (int64_t)chunk * rows_per_chunk;
+  const int64_t r1 = std::min<int64_t>(rows, r0 + rows_per_chunk);
+  float s[4][8];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[u][e] = 0.0f;
+  int64_t r = r0;
+  for (; r + 4 <= r1; r += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float v[8];
+      load8(in + (r + u) * ld + c, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[u][e] += v[e];
+    }
+  }
+  for (; r < r1; ++r) {
+    float v[8];
+    load8(in + r * ld + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[0][e] += v[e];
+  }
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (s[0][e] + s[1][e]) + (s[2][e] + s[3][e]);
+  store8(part + (int64_t)chunk * n + c, o);
+}
+
 __global__ void __launch_bounds__(256) colsum_final_kernel(const float* __restrict__ part, int chunks, int n,
                                                            float* __restrict__ out) {
   const int c = blockIdx.x * blockDim.x + threadIdx.x;
@@ -381,8 +420,12 @@ static void colsum(Runner& run, const char* label, const T* in, int64_t rows, in
   const int chunks = (int)std::max<int64_t>(1, std::min<int64_t>(kColsumChunks, (rows + 63) / 64));
   const int64_t rpc = (rows + chunks - 1) / chunks;
   run.launch(label, [&] {
-    hipLaunchKernelGGL((colsum_partial_kernel<T>), dim3((n + 255) / 256, chunks), dim3(256), 0, run.stream, in,
-                       rows, n, ld, rpc, part);
+    if (n % 8 == 0 && ld % 8 == 0)
+      hipLaunchKernelGGL((colsum_partial8_kernel<T>), dim3((n / 8 + 255) / 256, chunks), dim3(256), 0, run.stream,
+                         in, rows, n, ld, rpc, part);
+    else
+      hipLaunchKernelGGL((colsum_partial_kernel<T>), dim3((n + 255) / 256, chunks), dim3(256), 0, run.stream, in,
+                         rows, n, ld, rpc, part);
     hipLaunchKernelGGL(colsum_final_kernel, dim3((n + 255) / 256), dim3(256), 0, run.stream, part, chunks, n, out);
     return hipGetLastError();
   });
@@ -420,6 +463,18 @@ static void wgrad(Runner& run, const char* label, const T* a, int64_t lda, const
   pr.M = M;
   pr.N = N;
   pr.K = (int)rows;
+  if constexpr (sizeof(T) == 2) {
+    // bf16: the direct kernel reads both row-major operands through LDS
+    // transpose reads; no transposed copies
+    if (db) colsum<T>(run, "bias_colsum", a, rows, M, lda, part, db);
+    if (!out) return;
+    pr.a = a;
+    pr.lda = lda;
+    pr.b = b;
+    pr.ldb = ldb;
+    run.gemm<T, LAYOUT_MN, LAYOUT_MN>(label, pr, EpiF32{out, ldo, 0});
+    return;
+  }
   if (out && rows >= kTransposeMinRows && !a_t) {
     transpose<T>(run, "transpose", a, lda, rows, M, tr_a, round8(rows), db ? part : nullptr);
     if (db) colsum_final(run, "bias_colsum", rows, M, part, part2, db);
