@@ -56,9 +56,9 @@ hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, cons
 struct PrefillWs {
   size_t u;      // [B*T, d] RMSNorm output, later the attention output A
   size_t q, k;   // [B, h, T, dh]
-  size_t vt;     // [B, h, dh, ld_t] values of the chunk, token-contiguous
+  size_t vt;     // values of the chunk: bf16 [B, h, T, dh]; fp32 [B, h, dh, ld_t] (token-contiguous)
   size_t alpha;  // fp32 [B*T, h]
-  size_t vct;    // [B, h, dh, ld_c] cached values, row-contiguous
+  size_t vct;    // fp32 only: [B, h, dh, ld_c] cached values, row-contiguous (bf16: empty)
   size_t xc;     // [B, T/P*P, d] complete blocks, gathered when T % P != 0
   size_t gemm;   // split-K partials of the chunk's GEMMs
   size_t bytes;

@@ -94,7 +94,9 @@ struct GenAttnParams {
   const void* q;       // [B, h, T, dh]
   const void* k;       // [B, h, T, dh]
   const void* vt;      // [B, h, dh, ld_t], columns T .. ld_t-1 zero
+  const void* v;       // bf16: [B, h, T, dh] (in place of vt)
   const void* kc;      // [B, h, n_cap, dh] cache keys
+  const void* vc;      // bf16: [B, h, n_cap, dh] cached values (in place of vct)
   const void* vct;     // [B, h, dh, ld_c] cached values, columns n_keys .. ld_c-1 zero
   const float* alpha;  // [B*T, h]
   void* out;           // [B*T, h*dh] A = A_x + alpha * A_h
@@ -119,6 +121,16 @@ struct GenShape {
 };
 
 
+// Chunk swizzle of a row-major value tile read through LDS transpose reads:
+// a read pass covers 4 consecutive rows (keys) at 4 consecutive chunks, so
+// the key moves rows by 64 bytes within each 256-byte bank window.
+template <int NC>
+__device__ __forceinline__ int vtr_swz(int r, int c) {
+  static_assert(NC == 8 || NC >= 16, "rows of 128 bytes or of 256 bytes and more");
+  return NC == 8 ? c ^ (((r >> 1) & 1) * 4) : c ^ ((r & 3) * 4);
+}
+
+
 // One softmax over the keys lo .. hi (inclusive, per lane; hi < lo: none) of
 // the 64-key tiles t_first .. t_last. Keys come from kp (rows of DH, nkeys
 // readable rows), values from vtp (DH rows of stride ld_v). The wave's 32
@@ -127,7 +139,10 @@ struct GenShape {
 // masked. On return o holds the normalised result (zero without any key).
 // Follows the online softmax of the proxy attention forward; scores are the
 // transposed tile S^T = K Q^T, so a lane holds one query.
-template <typename T, int DH>
+// With VROW (bf16) the values are row-major like the keys (vtp: rows of DH,
+// nkeys readable rows; ld_v unused) and their MFMA operands come from LDS
+// transpose reads; otherwise vtp holds V^T (DH rows of stride ld_v).
+template <typename T, int DH, bool VROW = false>
 __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys, const char* vtp, int ld_v,
                                           int t_first, int t_last, int lo, int hi, int wlo_min, int wlo_max,
                                           int whi_min, int whi_max, const typename Mma<T>::frag (&qf)[DH / 16],
@@ -149,8 +164,10 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
     const int kt0 = (t_first + t) * S::kKT;
     char* st = smem + stage * S::kStage;
     const rsrc_t rk = make_rsrc_uniform(kp + (int64_t)kt0 * S::kRowBytes, (uint32_t)max(0, nkeys - kt0) * S::kRowBytes);
-    const rsrc_t rv = make_rsrc_uniform(vtp + (int64_t)kt0 * sizeof(T),
-                                        (uint32_t)((int64_t)DH * ld_v * sizeof(T) - (int64_t)kt0 * sizeof(T)));
+    const rsrc_t rv = VROW ? make_rsrc_uniform(vtp + (int64_t)kt0 * S::kRowBytes,
+                                               (uint32_t)max(0, nkeys - kt0) * S::kRowBytes)
+                           : make_rsrc_uniform(vtp + (int64_t)kt0 * sizeof(T),
+                                               (uint32_t)((int64_t)DH * ld_v * sizeof(T) - (int64_t)kt0 * sizeof(T)));
 #pragma unroll
     for (int j = 0; j < S::kInstsPerWave; ++j) {
       const int i = wave * S::kInstsPerWave + j;  // wave-uniform
@@ -161,6 +178,10 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
         r = rk;
         const int row = off / S::kRowBytes + lane / (S::kRowBytes / 16);
         vo = (uint32_t)(row * S::kRowBytes + lds_swz<S::kRowBytes / 16>(row, lane % (S::kRowBytes / 16)) * 16);
+      } else if constexpr (VROW) {  // V: row = key, like K
+        r = rv;
+        const int row = (off - S::kKTile) / S::kRowBytes + lane / (S::kRowBytes / 16);
+        vo = (uint32_t)(row * S::kRowBytes + vtr_swz<S::kRowBytes / 16>(row, lane % (S::kRowBytes / 16)) * 16);
       } else {  // V^T: row = channel, stride ld_v
         r = rv;
         const int row = (off - S::kKTile) / S::kVRowBytes + lane / (S::kVRowBytes / 16);
@@ -266,7 +287,23 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
           const int dd = cb * 32 + col;
           const char* vrow = sv + dd * S::kVRowBytes;
           typename MM::frag va;
-          if constexpr (sizeof(T) == 2) {
+          if constexpr (VROW) {
+            // keys c0 .. c0+7 of channel dd: two transpose reads, lane i of a
+            // 16-lane group addressing key c0 (+4) + i / 4 at channels
+            // 4 (i % 4) .. +3 of the group's 16
+            const int ch = cb * 32 + (lane & 16) + 4 * (lane & 3);
+            const int k1 = c0 + ((lane & 15) >> 2);
+            auto addr = [&](int key) {
+              return sv + key * S::kRowBytes + vtr_swz<S::kRowBytes / 16>(key, ch / 8) * 16 + ((ch / 4) & 1) * 8;
+            };
+            const auto lo = __builtin_bit_cast(bf16x4, lds_read_tr16(addr(k1)));
+            const auto hi = __builtin_bit_cast(bf16x4, lds_read_tr16(addr(k1 + 4)));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              va[e] = lo[e];
+              va[e + 4] = hi[e];
+            }
+          } else if constexpr (sizeof(T) == 2) {
             va = *reinterpret_cast<const typename MM::frag*>(vrow + lds_swz<S::kVRowBytes / 16>(dd, c0 / 8) * 16);
           } else {
             const f32x4 a = *reinterpret_cast<const f32x4*>(vrow + lds_swz<S::kVRowBytes / 16>(dd, c4 / 4) * 16);
@@ -296,6 +333,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DH == 
     gen_attn_kernel(const GenAttnParams p) {
   typedef GenShape<T, DH> S;
   typedef Mma<T> MM;
+  // bf16 values stay row-major and reach the MFMA through LDS transpose reads
+  constexpr bool kRow = sizeof(T) == 2;
   __shared__ __attribute__((aligned(1024))) char smem[S::kNS * S::kStage];
 
   // 1-D grid over (head, token tile); each XCD gets a contiguous run so the
@@ -330,18 +369,20 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DH == 
   f32x16 ox[DH / 32];
   {
     const char* kp = reinterpret_cast<const char*>(p.k) + (int64_t)bh * p.T * S::kRowBytes;
-    const char* vtp = reinterpret_cast<const char*>(p.vt) + (int64_t)bh * DH * p.ld_t * (int64_t)sizeof(T);
+    const char* vtp = kRow ? reinterpret_cast<const char*>(p.v) + (int64_t)bh * p.T * S::kRowBytes
+                           : reinterpret_cast<const char*>(p.vt) + (int64_t)bh * DH * p.ld_t * (int64_t)sizeof(T);
     const int lo = (qc / p.P) * p.P;
-    gen_phase<T, DH>(smem, kp, p.T, vtp, p.ld_t, ((q0 / p.P) * p.P) / S::kKT, q1c / S::kKT, lo, qc,
+    gen_phase<T, DH, kRow>(smem, kp, p.T, vtp, p.ld_t, ((q0 / p.P) * p.P) / S::kKT, q1c / S::kKT, lo, qc,
                      (qw0c / p.P) * p.P, (qw1c / p.P) * p.P, qw0c, qw1c, qf, p.scale_log2, ox);
   }
   // cache phase: rows 0 .. n0 + blk(t) - 1
   f32x16 oc[DH / 32];
   {
     const char* kp = reinterpret_cast<const char*>(p.kc) + (int64_t)bh * p.n_cap * S::kRowBytes;
-    const char* vtp = reinterpret_cast<const char*>(p.vct) + (int64_t)bh * DH * p.ld_c * (int64_t)sizeof(T);
+    const char* vtp = kRow ? reinterpret_cast<const char*>(p.vc) + (int64_t)bh * p.n_cap * S::kRowBytes
+                           : reinterpret_cast<const char*>(p.vct) + (int64_t)bh * DH * p.ld_c * (int64_t)sizeof(T);
     const int hmax = p.n0 + q1c / p.P - 1;
-    gen_phase<T, DH>(smem, kp, p.n_keys, vtp, p.ld_c, 0, hmax >= 0 ? hmax / S::kKT : -1, 0, p.n0 + qc / p.P - 1, 0,
+    gen_phase<T, DH, kRow>(smem, kp, p.n_keys, vtp, p.ld_c, 0, hmax >= 0 ? hmax / S::kKT : -1, 0, p.n0 + qc / p.P - 1, 0,
                      0, p.n0 + qw0c / p.P - 1, p.n0 + qw1c / p.P - 1, qf, p.scale_log2, oc);
   }
   if (myq < p.T) {
@@ -354,14 +395,15 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DH == 
 }
 
 // Tokens start .. start+rem-1 of every sequence into the local slots 0 ..
-// rem-1: x into x_blk [B, P, d], K into k_loc and V (from its
-// token-contiguous copy) into v_loc [B, h, P, dh].
+// rem-1: x into x_blk [B, P, d], K into k_loc and V into v_loc [B, h, P, dh].
+// Value (bh, t, e) sits at v[bh * v_bh + t * v_t + e * v_e] (per-head rows,
+// or the token-contiguous transposed copy).
 template <typename T>
 __global__ void __launch_bounds__(256) prefill_tail_kernel(const T* __restrict__ x, const T* __restrict__ k,
-                                                           const T* __restrict__ vt, T* __restrict__ x_blk,
+                                                           const T* __restrict__ v, T* __restrict__ x_blk,
                                                            T* __restrict__ k_loc, T* __restrict__ v_loc, int B,
                                                            int T_, int nh, int dh, int64_t P, int start, int rem,
-                                                           int64_t ld_t) {
+                                                           int64_t v_bh, int64_t v_t, int64_t v_e) {
   const int d = nh * dh;
   const int64_t total = (int64_t)B * rem * d;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
@@ -372,7 +414,7 @@ __global__ void __launch_bounds__(256) prefill_tail_kernel(const T* __restrict__
     const int64_t bh = (int64_t)b * nh + h;
     x_blk[((int64_t)b * P + s) * d + c] = x[((int64_t)b * T_ + start + s) * d + c];
     k_loc[(bh * P + s) * dh + e] = k[(bh * T_ + start + s) * dh + e];
-    v_loc[(bh * P + s) * dh + e] = vt[(bh * dh + e) * ld_t + start + s];
+    v_loc[(bh * P + s) * dh + e] = v[bh * v_bh + (start + s) * v_t + e * v_e];
   }
 }
 
@@ -389,7 +431,7 @@ const char* prefill_limits(const DecodeDims& d, int64_t T, int64_t n_cap) {
   if ((int64_t)d.dh * round64(T) * es >= ((int64_t)1 << 31))
     return "one head's token-contiguous values (head_dim * n_tokens) must stay below 2 GiB";
   if ((int64_t)d.dh * round64(std::max<int64_t>(n_cap, 1)) * es >= ((int64_t)1 << 31))
-    return "one head's transposed cache values (head_dim * n_cap) must stay below 2 GiB";
+    return "one head's cached keys or values (head_dim * n_cap) must stay below 2 GiB";
   return nullptr;
 }
 
@@ -423,9 +465,12 @@ PrefillWs prefill_ws(const DecodeDims& d, int64_t T, int64_t n_cap) {
   w.u = take(rows * d.d * es);
   w.q = take(rows * d.d * es);
   w.k = take(rows * d.d * es);
-  w.vt = take((size_t)d.B * d.nh * d.dh * w.ld_t * es);
+  // bf16 keeps V per head in rows and reads the cached values in place; fp32
+  // keeps V^T and a transposed copy of the cached values
+  const bool vrow = d.esize == 2;
+  w.vt = take(vrow ? rows * d.d * es : (size_t)d.B * d.nh * d.dh * w.ld_t * es);
   w.alpha = take(rows * d.nh * 4);
-  w.vct = take((size_t)d.B * d.nh * d.dh * w.ld_c * es);
+  w.vct = take(vrow ? 0 : (size_t)d.B * d.nh * d.dh * w.ld_c * es);
   const int64_t nblk = T / d.P;
   w.xc = take(nblk > 0 && T % d.P != 0 ? (size_t)d.B * nblk * d.P * d.d * es : 0);
   w.gemm = off;
@@ -456,14 +501,16 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
     return hipGetLastError();
   });
 
-  // 2. projections: Q, K per head (row tensors), V token-contiguous, alpha
-  if (W.ld_t != Tn) {  // padding columns of V^T must read as zero
+  // 2. projections: Q, K per head (row tensors), V per head (bf16) or
+  //    token-contiguous (fp32), alpha
+  constexpr bool vrow = sizeof(T) == 2;
+  if (!vrow && W.ld_t != Tn) {  // padding columns of V^T must read as zero
     const size_t tb = (size_t)d.B * d.nh * d.dh * W.ld_t * sizeof(T);
     run.launch("fill_zero", [&] { return fill_zero(vt, tb, run.stream); });
   }
   const pf_linear* proj[3] = {&w->q, &w->k, &w->v};
-  T* outs[3] = {q, k, nullptr};
-  T* outs_t[3] = {nullptr, nullptr, vt};
+  T* outs[3] = {q, k, vrow ? vt : nullptr};
+  T* outs_t[3] = {nullptr, nullptr, vrow ? nullptr : vt};
   for (int i = 0; i < 3; ++i) {
     GemmProblem pr{};
     pr.a = u;
@@ -507,12 +554,12 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
     }
   }
 
-  // 4. cached values of rows 0 .. n_keys-1, transposed with row stride ld_c
-  //    (the columns up to the next multiple of 64 are zeros; W.ld_c, sized
-  //    from the capacity, bounds it)
+  // 4. fp32: cached values of rows 0 .. n_keys-1, transposed with row stride
+  //    ld_c (the columns up to the next multiple of 64 are zeros; W.ld_c,
+  //    sized from the capacity, bounds it)
   const int64_t n_keys = st.n + nblk;
   const int64_t ld_c = round64(std::max<int64_t>(n_keys, 1));
-  if (n_keys > 0) {
+  if (!vrow && n_keys > 0) {
     run.launch("prefill_cache_vt", [&] {
       const dim3 grid((d.dh + 63) / 64, (unsigned)(ld_c / 64), (unsigned)(d.B * d.nh));
       hipLaunchKernelGGL((transpose_kernel<T>), grid, dim3(256), 0, run.stream,
@@ -526,9 +573,11 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
   GenAttnParams ap{};
   ap.q = q;
   ap.k = k;
-  ap.vt = vt;
+  ap.vt = vrow ? nullptr : vt;
+  ap.v = vrow ? vt : nullptr;
   ap.kc = st.k_cache;
-  ap.vct = vct;
+  ap.vc = vrow ? st.v_cache : nullptr;
+  ap.vct = vrow ? nullptr : vct;
   ap.alpha = alpha;
   ap.out = u;
   ap.T = Tn;
@@ -558,7 +607,9 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
       const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
       hipLaunchKernelGGL((prefill_tail_kernel<T>), dim3(blocks), dim3(256), 0, run.stream, xin, k, vt,
                          reinterpret_cast<T*>(st.x_blk), reinterpret_cast<T*>(st.k_loc),
-                         reinterpret_cast<T*>(st.v_loc), d.B, Tn, d.nh, d.dh, d.P, (int)(nblk * d.P), rem, W.ld_t);
+                         reinterpret_cast<T*>(st.v_loc), d.B, Tn, d.nh, d.dh, d.P, (int)(nblk * d.P), rem,
+                         vrow ? (int64_t)Tn * d.dh : (int64_t)d.dh * W.ld_t, vrow ? (int64_t)d.dh : (int64_t)1,
+                         vrow ? (int64_t)1 : W.ld_t);
       return hipGetLastError();
     });
   }

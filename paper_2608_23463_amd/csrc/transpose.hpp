@@ -1,5 +1,5 @@
 // out[c, r] = in[r, c] through 64x64 LDS tiles (shared by the backward's
-// operand transposes and the decode prefill's transposed cache values).
+// operand transposes and the fp32 prefill's transposed cache values).
 #pragma once
 
 #include "common.hpp"
