@@ -117,18 +117,28 @@ template <typename T>
 __global__ void __launch_bounds__(256) head_gate_combine_kernel(const T* __restrict__ x, const T* __restrict__ delta,
                                                                 const float* __restrict__ gh, T* __restrict__ y,
                                                                 int64_t rows, int d, int nh) {
-  const int64_t n8 = rows * d / 8;
+  // A row is tpr runs of 8; a block covers rpb rows at a time (one row in
+  // passes of 256 runs when tpr > 256). The run and its head are fixed per
+  // thread, so the loop carries no division.
+  const int tpr = d / 8;
+  const int rpb = tpr <= 256 ? 256 / tpr : 1;
+  const int lr = tpr <= 256 ? (int)threadIdx.x / tpr : 0;
+  if (lr >= rpb) return;
+  const int j0 = tpr <= 256 ? (int)threadIdx.x - lr * tpr : (int)threadIdx.x;
   const int gs = d / nh;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (int64_t)gridDim.x * 256) {
-    const int64_t e0 = i * 8, r = e0 / d;
-    const int c = (int)(e0 - r * d);
-    const float s = sigmoidf(gh[r * nh + c / gs]);
-    float a[8], b[8], o[8];
-    load8(x + e0, a);
-    load8(delta + e0, b);
+  for (int64_t r = (int64_t)blockIdx.x * rpb + lr; r < rows; r += (int64_t)gridDim.x * rpb) {
+    const T* xr = x + r * d;
+    const T* dr = delta + r * d;
+    T* yr = y + r * d;
+    for (int j = j0; j < tpr; j += 256) {
+      const float s = sigmoidf(gh[r * nh + (j * 8) / gs]);
+      float a[8], b[8], o[8];
+      load8(xr + j * 8, a);
+      load8(dr + j * 8, b);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = fmaf(s, b[e], a[e]);
-    store8(y + e0, o);
+      for (int e = 0; e < 8; ++e) o[e] = fmaf(s, b[e], a[e]);
+      store8(yr + j * 8, o);
+    }
   }
 }
 
@@ -536,8 +546,8 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.K = 2 * d.d_f;
     run.gemm<T, LAYOUT_K, LAYOUT_K>("head_gate_gemm", pr, EpiBiasF32<T>{gh, d.nh, reinterpret_cast<const T*>(w->gate.b)});
     run.launch("head_gate_combine", [&] {
-      const int64_t n8 = rows * d.d_f / 8;
-      hipLaunchKernelGGL((head_gate_combine_kernel<T>), dim3((unsigned)std::min<int64_t>((n8 + 255) / 256, 16384)),
+      const int tpr = d.d_f / 8, rpb = tpr <= 256 ? 256 / tpr : 1;
+      hipLaunchKernelGGL((head_gate_combine_kernel<T>), dim3((unsigned)std::min<int64_t>((rows + rpb - 1) / rpb, 16384)),
                          dim3(256), 0, run.stream, reinterpret_cast<const T*>(x), P(A.delta), gh,
                          reinterpret_cast<T*>(x_out), rows, d.d_f, d.nh);
       return hipGetLastError();
