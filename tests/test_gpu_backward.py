@@ -98,6 +98,9 @@ CASES = {
                                True),
     "fp32_inject_gated_head": (LayerShape(2, 8 * 37, 64, 128, 2, 64, (2, 4), level_dims=(96,), dtype="fp32",
                                           injection=synth.INJECT_GATED_HEAD), False),
+    # d_fine = 3072 (768 channels per head): head sums over 96 runs of 8 per head
+    "bf16_gated_head_wide": (LayerShape(1, 16 * 24, 3072, 256, 4, 64, (16,), injection=synth.INJECT_GATED_HEAD),
+                             False),
     # partial last block (L % P != 0): zero-padded inside the library, dY = 0 on the padding
     "bf16_tc_partial_block": (LayerShape(2, 16 * 37 + 9, 192, 192, 3, 64, (16,)), True),
     "fp32_bi_partial_block_factorised": (LayerShape(1, 8 * 37 + 5, 64, 128, 2, 64, (2, 4), level_dims=(96,),

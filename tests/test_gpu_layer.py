@@ -44,6 +44,9 @@ SMALL = {
                                               injection=synth.INJECT_GATED_HEAD), False),
     "bf16_gated_head_lm_shape": (LayerShape(1, 64 * 300, 64, 512, 8, 64, (64,), injection=synth.INJECT_GATED_HEAD),
                                  False),
+    # d_fine = 3072: a row is 384 runs of 8, more than one combine block covers at a time
+    "bf16_gated_head_wide": (LayerShape(1, 16 * 24, 3072, 256, 4, 64, (16,), injection=synth.INJECT_GATED_HEAD),
+                             False),
     # partial last block (L % P != 0, m = ceil(L / P), zero-padded, Sec. 3.1)
     "bf16_partial_block_tc": (LayerShape(2, 37 * 16 + 5, 192, 192, 3, 64, (16,)), True),
     "fp32_partial_block_factorised_bi": (LayerShape(1, 8 * 40 + 3, 64, 128, 1, 128, (2, 4), level_dims=(48,),
