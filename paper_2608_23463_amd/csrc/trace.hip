@@ -44,8 +44,16 @@ bool trace_on() { return g_on; }
 void trace_begin(const char* label, hipStream_t stream) {
   std::lock_guard<std::mutex> lk(g_mu);
   Pending p{label, get_event(), get_event()};
-  if (!p.start || !p.stop) return;
-  hipEventRecord(p.start, stream);
+  if (!p.start || !p.stop) {
+    if (p.start) g_pool.push_back(p.start);
+    if (p.stop) g_pool.push_back(p.stop);
+    return;
+  }
+  if (hipEventRecord(p.start, stream) != hipSuccess) {  // not traced: events back to the pool
+    g_pool.push_back(p.start);
+    g_pool.push_back(p.stop);
+    return;
+  }
   g_pending.push_back(p);
   g_open = (int)g_pending.size() - 1;
 }
@@ -53,7 +61,12 @@ void trace_begin(const char* label, hipStream_t stream) {
 void trace_end(hipStream_t stream) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (g_open < 0 || g_open >= (int)g_pending.size()) return;
-  hipEventRecord(g_pending[g_open].stop, stream);
+  if (hipEventRecord(g_pending[g_open].stop, stream) != hipSuccess) {
+    // an unrecorded stop event would never complete: drop the launch from the trace
+    g_pool.push_back(g_pending[g_open].start);
+    g_pool.push_back(g_pending[g_open].stop);
+    g_pending.erase(g_pending.begin() + g_open);
+  }
   g_open = -1;
 }
 
@@ -102,7 +115,7 @@ int proxy_trace_get(int i, char* label, size_t label_cap, int64_t* launches, dou
 void proxy_trace_reset(void) {
   std::lock_guard<std::mutex> lk(g_mu);
   for (Pending& p : g_pending) {
-    hipEventSynchronize(p.stop);
+    (void)hipEventSynchronize(p.stop);  // discarded either way
     g_pool.push_back(p.start);
     g_pool.push_back(p.stop);
   }
