@@ -11,7 +11,8 @@ Extra objects on the same line:
                (a second pass over K calls) and achieved TFLOP/s or GB/s
   variants     the same forward with residual-add injection (Eq. 11), affine
                modulation (Eq. 13) and the per-head gate
-  ceilings     a 1 GiB device copy (achievable HBM rate) beside the vendor peaks
+  ceilings     a 1 GiB device copy (achievable HBM rate) and an MFMA-only loop
+               (achievable dense bf16 rate) beside the vendor peaks
   roofline     the dominant kernel against the MI355X peak of its bound
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
                rows each, 256 new tokens per sequence including the 4
@@ -275,6 +276,28 @@ def hbm_copy_ceiling():
     del a, b
     torch.cuda.empty_cache()
     return round(2 * n / (best * 1e-3) / 1e9, 1)
+
+
+def mfma_ceiling():
+    """Achievable dense bf16 MFMA rate on this device: the library's MFMA-only
+    loop (1,024 workgroups of four waves, no memory traffic), best of three."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    n_wg, iters = 1024, 20000
+    out = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda")
+    B.ceiling_mfma(out, n_wg, 100)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(3):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        B.ceiling_mfma(out, n_wg, iters)
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop)
+        best = ms if best is None else min(best, ms)
+    flops = n_wg * 4 * iters * 8 * 32768
+    return round(flops / (best * 1e-3) / 1e12, 1)
 
 
 def bench_decode(workload=DECODE_WORKLOAD):
@@ -587,6 +610,7 @@ def main():
         "kernels": kernels,
         "variants": variants,
         "ceilings": {"hbm_copy_gbs": hbm_copy_ceiling(), "hbm_peak_gbs": PEAK_HBM_GBS,
+                     "mfma_loop_bf16_tflops": mfma_ceiling(),
                      "mfma_bf16_peak_tflops": PEAK_BF16_TFLOPS},
     }
     if not args.no_decode:

@@ -286,6 +286,18 @@ int proxy_trace_collect(void);
 int proxy_trace_get(int i, char* label, size_t label_cap, int64_t* launches, double* total_ms);
 void proxy_trace_reset(void);
 
+/* Matrix-core ceiling (measurement aid, not part of the layer): enqueues
+ * n_workgroups workgroups of four waves on `stream`; every wave issues
+ * iters x 8 independent v_mfma_f32_32x32x16_bf16 (32x32x16 multiply-adds,
+ * 32,768 flops each) on register operands and touches no memory until it
+ * writes one float per thread to out. out: caller-owned device buffer of
+ * n_workgroups * 256 floats. Flops per call:
+ * n_workgroups * 4 * iters * 8 * 32768; timing the call with events on the
+ * same stream gives the achievable dense bf16 rate of the device.
+ * PF_ERR_INVALID_ARG for a NULL out, n_workgroups outside [1, 2^20] or
+ * iters < 1 (nothing enqueued); PF_ERR_HIP if the launch fails. */
+int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* stream);
+
 /* Message of the last non-OK status on the calling thread. */
 const char* proxy_last_error(void);
 

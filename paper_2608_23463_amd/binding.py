@@ -33,6 +33,7 @@ EXPORTS = (
     "proxy_cache_append", "proxy_prefill_workspace_size", "proxy_decode_prefill",
     "proxy_last_error", "proxy_version",
     "proxy_trace_enable", "proxy_trace_collect", "proxy_trace_get", "proxy_trace_reset",
+    "proxy_ceiling_mfma",
 )
 
 c_void_p = ctypes.c_void_p
@@ -145,6 +146,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.proxy_trace_get.restype = c_int32
     lib.proxy_trace_reset.argtypes = []
     lib.proxy_trace_reset.restype = None
+    lib.proxy_ceiling_mfma.argtypes = [c_void_p, c_int64, c_int32, c_void_p]
+    lib.proxy_ceiling_mfma.restype = c_int32
     _lib = lib
     return lib
 
@@ -156,6 +159,17 @@ def last_error() -> str:
 def _check(status: int):
     if status != PF_OK:
         raise ProxyFormerError(status, last_error())
+
+
+def ceiling_mfma(out, n_workgroups: int, iters: int, stream=None) -> None:
+    """Enqueue the matrix-core ceiling loop (see proxy_ceiling_mfma) on
+    `stream` (torch's current stream if None); out is a device float32
+    tensor of n_workgroups * 256 elements."""
+    if out.numel() < n_workgroups * 256 or out.dtype.itemsize != 4 or not out.is_cuda:
+        raise ValueError("out must be a device float32 tensor of n_workgroups * 256 elements")
+    st = load().proxy_ceiling_mfma(c_void_p(out.data_ptr()), n_workgroups, iters, c_void_p(_stream(stream)))
+    if st != PF_OK:
+        raise ProxyFormerError(st, "proxy_ceiling_mfma: invalid arguments or launch failure")
 
 
 def trace_enable(on: bool) -> bool:

@@ -84,6 +84,40 @@ def test_forward_parity_small(gpu, name):
     assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
 
 
+# Four sequences x 16 heads over 1,000-1,024 proxies (a grid of 512
+# attention workgroups, more than the chip holds at once); m = 1000 leaves a
+# ragged last query tile and a partial last key tile.
+INJECTED = {
+    "bf16_many_heads_tc": LayerShape(4, 16 * 1000, 64, 1024, 16, 64, (16,)),
+    "bf16_many_heads_bc": LayerShape(4, 16 * 1024, 64, 1024, 16, 64, (16,), mask=synth.BLOCK_CAUSAL),
+    "bf16_many_heads_bi": LayerShape(4, 16 * 1000, 64, 1024, 16, 64, (16,), mask=synth.BIDIRECTIONAL),
+}
+
+
+@pytest.mark.parametrize("name", list(INJECTED))
+def test_forward_parity_injected_signal(gpu, name):
+    """The injected signal X_out - X (which carries the attention output
+    through W_o and the decompression) is compared as well as X_out, so an
+    attention error cannot hide behind the residual. W_o is scaled by 8 (exact
+    in bf16) so that signal is as large as X: otherwise the bf16 rounding of
+    X_out alone (half a unit in the last place of |X_out| ~ 5) is a few
+    percent of it."""
+    shape = INJECTED[name]
+    print(f"[case {name}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, seed=zlib.crc32(name.encode()) % 1000, with_h_in=True)
+    for key in ("q", "k"):  # logits with std of a few units: attention neither uniform nor one-hot
+        wq, bq = inp["weights"][key]
+        inp["weights"][key] = (synth.bf16_round(wq * 2), bq)
+    wo, bo = inp["weights"]["o"]
+    inp["weights"]["o"] = (wo * 8, bo)
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask, inp["h_in"])
+    x = inp["x"].astype(np.float64)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+    assert_close(host(x_out) - x, ref["x_out"] - x, shape.dtype, f"{name} x_out - x")
+
+
 @pytest.mark.parametrize("name", ["layer_fp32_L4k_d256", "layer_bf16_L64k_d1024"])
 def test_forward_parity_workload(gpu, name):
     shape = synth.WORKLOADS[name]
