@@ -167,9 +167,7 @@ def ceiling_mfma(out, n_workgroups: int, iters: int, stream=None) -> None:
     tensor of n_workgroups * 256 elements."""
     if out.numel() < n_workgroups * 256 or out.dtype.itemsize != 4 or not out.is_cuda:
         raise ValueError("out must be a device float32 tensor of n_workgroups * 256 elements")
-    st = load().proxy_ceiling_mfma(c_void_p(out.data_ptr()), n_workgroups, iters, c_void_p(_stream(stream)))
-    if st != PF_OK:
-        raise ProxyFormerError(st, "proxy_ceiling_mfma: invalid arguments or launch failure")
+    _check(load().proxy_ceiling_mfma(c_void_p(out.data_ptr()), n_workgroups, iters, c_void_p(_stream(stream))))
 
 
 def trace_enable(on: bool) -> bool:

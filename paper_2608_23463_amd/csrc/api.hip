@@ -6,6 +6,7 @@
 #include <cstring>
 #include <string>
 
+#include "ceiling.hpp"
 #include "common.hpp"
 #include "decode.hpp"
 #include "layer.hpp"
@@ -48,6 +49,15 @@ static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 extern "C" {
 
 int proxy_version(void) { return 100; }
+
+int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* stream) {
+  if (!out) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_mfma: out is NULL");
+  if (n_workgroups < 1 || n_workgroups > (1 << 20))
+    return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_mfma: n_workgroups must be in [1, 2^20]");
+  if (iters < 1) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_mfma: iters must be >= 1");
+  return hip_status(launch_mfma_ceiling(static_cast<float*>(out), n_workgroups, iters, (hipStream_t)stream),
+                    "proxy_ceiling_mfma");
+}
 
 const char* proxy_last_error(void) { return g_last_error.c_str(); }
 

@@ -4,7 +4,7 @@
 // reach at best on this device, next to the vendor's dense bf16 peak.
 #include <hip/hip_runtime.h>
 
-#include "../../include/proxyformer.h"
+#include "ceiling.hpp"
 #include "common.hpp"
 
 namespace pf {
@@ -36,11 +36,10 @@ __global__ void __launch_bounds__(256) mfma_ceiling_kernel(float* __restrict__ o
   out[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
+hipError_t launch_mfma_ceiling(float* out, int64_t n_workgroups, int iters, hipStream_t stream) {
+  hipLaunchKernelGGL(mfma_ceiling_kernel, dim3((unsigned)n_workgroups), dim3(256), 0, stream, out, iters);
+  return hipGetLastError();
+}
+
 }  // namespace pf
 
-extern "C" int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* stream) {
-  if (!out || n_workgroups < 1 || n_workgroups > (1 << 20) || iters < 1) return PF_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(pf::mfma_ceiling_kernel, dim3((unsigned)n_workgroups), dim3(256), 0,
-                     (hipStream_t)stream, (float*)out, (int)iters);
-  return hipGetLastError() == hipSuccess ? PF_OK : PF_ERR_HIP;
-}

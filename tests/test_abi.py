@@ -263,6 +263,7 @@ def test_per_head_gate_shape_limits(lib):
 def test_mfma_ceiling_rejects_bad_arguments(lib):
     """The ceiling probe validates on the host before it launches anything."""
     assert lib.proxy_ceiling_mfma(None, 16, 10, None) == B.PF_ERR_INVALID_ARG
+    assert "out is NULL" in lib.proxy_last_error().decode()
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), 0, 10, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), (1 << 20) + 1, 10, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), 16, 0, None) == B.PF_ERR_INVALID_ARG
