@@ -13,7 +13,9 @@ Extra objects on the same line:
                modulation (Eq. 13) and the per-head gate
   ceilings     a 1 GiB device copy (achievable HBM rate) and an MFMA-only loop
                (achievable dense bf16 rate) beside the vendor peaks
-  roofline     the dominant kernel against the MI355X peak of its bound
+  roofline     the dominant kernel against the MI355X peak of its bound, with
+               its matrix-core busy fraction and clock from the committed
+               counter summary (while the kernel sources are unchanged)
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
                rows each, 256 new tokens per sequence including the 4
                block-triggered appends
@@ -51,6 +53,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 CPU_SAMPLE_TOKENS = 393216
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_bf16_L1M_d1024_decode_bf16_B32_n16k.txt")
+MFMA_FILE = os.path.join(ROOT, "profiles", "mfma_counters_layer_bf16_L1M_d1024_decode_bf16_B32_n16k.txt")
 KERNEL_SOURCES = ["paper_2608_23463_amd/csrc/gemm.hpp", "paper_2608_23463_amd/csrc/epilogues.hpp",
                   "paper_2608_23463_amd/csrc/common.hpp", "paper_2608_23463_amd/csrc/attention.hpp",
                   "paper_2608_23463_amd/csrc/attention_fwd.hip", "paper_2608_23463_amd/csrc/layer_fwd.hip",
@@ -69,20 +72,33 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(label: str):
-    """HBM bytes per launch of `label` from the committed counter summary, or
-    None when the summary is missing or the kernel sources changed since."""
-    if not os.path.exists(TRAFFIC_FILE):
+def counter_value(path: str, key: str):
+    """Value of `key` in a committed counter summary, or None when the summary
+    is missing or the kernel sources changed since the counters were taken."""
+    if not os.path.exists(path):
         return None
     vals = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     if vals.get("kernel_source_hash") != kernel_source_hash():
         return None
-    v = vals.get(f"{label}_bytes_per_launch")
+    v = vals.get(key)
     return float(v) if v else None
+
+
+def measured_traffic(label: str):
+    """HBM bytes per launch of `label` (FETCH_SIZE and WRITE_SIZE passes)."""
+    return counter_value(TRAFFIC_FILE, f"{label}_bytes_per_launch")
+
+
+def measured_mfma(label: str):
+    """Matrix-core busy fraction of `label` at the clock it ran at, and that
+    clock in GHz (SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE pass)."""
+    util = counter_value(MFMA_FILE, f"{label}_mfma_util")
+    clk = counter_value(MFMA_FILE, f"{label}_clock_ghz")
+    return (util, clk) if util is not None and clk is not None else None
 
 
 def layer_flops(shape):
@@ -180,6 +196,9 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
         hbm = measured_traffic(label) if workload == LAYER_WORKLOAD else None
         if hbm:  # measured HBM bytes per launch over this run's duration
             ent["hbm_gbs"] = round(hbm / (avg * 1e-3) / 1e9, 1)
+        mf = measured_mfma(label) if workload == LAYER_WORKLOAD else None
+        if mf:  # counters: matrix cores busy at the clock the kernel ran at
+            ent["mfma_util_counters"], ent["clock_ghz_counters"] = mf
         kernels[label] = ent
     dom = max((k for k in tr if k in flops), key=lambda k: tr[k][1])
     dom_ms = tr[dom][1] / tr[dom][0]
@@ -250,6 +269,9 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
+    mf = measured_mfma(dom) if workload == LAYER_WORKLOAD else None
+    if mf:
+        roof["mfma_util_counters"], roof["clock_ghz_counters"] = mf
     del x, x_out, h_out, ws, w
     torch.cuda.empty_cache()
     return shape, ms, kernels, roof, sample, variants
