@@ -579,13 +579,17 @@ struct DirectOp {
   static_assert(!kMN || sizeof(T) == 2, "transpose reads take 16-bit elements");
   static_assert(kMN ? kCpr >= 16 : (kCpr == 8 || kCpr == 4), "swizzle covers these row widths");
   static_assert(kInsts >= 1 && kTileRows % (kRowsPerInst * WAVES) == 0, "tile rows split evenly over waves");
-  // Physical chunk of logical chunk c in row r is c ^ key(r). K-major: any 8
-  // consecutive rows read at one logical chunk cover all 32 LDS banks.
-  // M/N-major: a transpose-read pass touches 4 consecutive rows (k) at 4
-  // consecutive chunks; the key moves each row by 64 bytes.
+  // Physical chunk of logical chunk c in row r is c ^ key(r). K-major: a
+  // 16-byte read pass serves 16 lanes (16 consecutive rows at one logical
+  // chunk) over 64 banks, i.e. 16 slots of 16 bytes; rows of 8 chunks put
+  // two rows in each 256-byte span, so the key steps every second row and
+  // the 16 rows land on 16 distinct slots (a key of r & 7 would put rows r
+  // and r + 8 on one slot). M/N-major: a transpose-read pass touches 4
+  // consecutive rows (k) at 4 consecutive chunks; the key moves each row by
+  // 64 bytes.
   static __device__ __forceinline__ int key(int r) {
     if constexpr (kMN) return (r & 3) * 4;
-    return kCpr == 8 ? (r & 7) : ((r >> 1) & 3);
+    return kCpr == 8 ? ((r >> 1) & 7) : ((r >> 2) & 3);
   }
 };
 
