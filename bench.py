@@ -502,20 +502,34 @@ def bench_train(steps):
     return out
 
 
+def cpu_model() -> str:
+    """Model name of the host CPU (first entry of /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(shape, sample):
     import oracle
-    try:
+    nproc = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    try:  # the threads numpy's BLAS runs the oracle's matrix products on
         from threadpoolctl import threadpool_info
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        cores = os.cpu_count() or 1
+        cores = nproc
     log(f"oracle on {CPU_SAMPLE_TOKENS} tokens")
     t0 = time.perf_counter()
     oracle.layer_forward(sample["x"], sample["weights"], shape.factors, shape.n_heads, shape.mask)
     dt = time.perf_counter() - t0
     return {"value": round(CPU_SAMPLE_TOKENS / dt, 1), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "nproc": nproc, "cpu_count": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": f"full layer forward (fp64) over the first {CPU_SAMPLE_TOKENS} tokens "
-                      f"({CPU_SAMPLE_TOKENS // shape.block} blocks) of the 1M-token workload",
+                      f"({CPU_SAMPLE_TOKENS // shape.block} blocks) of the 1M-token workload; cores = BLAS "
+                      f"threads of the oracle's matrix products, nproc = CPUs this process may run on",
             "seconds": round(dt, 2)}
 
 

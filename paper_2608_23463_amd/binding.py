@@ -88,6 +88,34 @@ class PfDecodeState(ctypes.Structure):
 
 _lib = None
 
+# Allocation policy of the helpers below (a test aid): when on, every buffer
+# they allocate for the library to write (outputs, gradients, saved
+# activations, workspace, decode state slots) starts as all-ones bytes, a NaN
+# in both bf16 and fp32, and the decode and prefill workspaces are refilled
+# before every call. An element the library fails to write then cannot pass
+# a comparison on stale memory that happens to hold a correct value.
+_poison = False
+
+
+def set_poison(on: bool) -> bool:
+    """Turn NaN-filled allocation on or off; returns the previous setting."""
+    global _poison
+    prev, _poison = _poison, bool(on)
+    return prev
+
+
+def _fresh(t):
+    """Apply the allocation policy to a new (contiguous) buffer; returns it."""
+    if _poison:
+        import torch
+        t.view(torch.uint8).fill_(255)
+    return t
+
+
+def _empty(shape, dtype, device):
+    import torch
+    return _fresh(torch.empty(shape, dtype=dtype, device=device))
+
 
 class ProxyFormerError(RuntimeError):
     def __init__(self, status: int, msg: str):
@@ -266,7 +294,7 @@ def layer_saved_size(cfg: PfLayerConfig) -> int:
 
 def _bytes(n: int, device):
     import torch
-    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+    return _fresh(torch.empty(max(n, 256), dtype=torch.uint8, device=device))
 
 
 def layer_forward_raw(cfg, wstruct, x, h_in, x_out, h_out, saved, workspace, stream=None):
@@ -282,8 +310,8 @@ def layer_forward(cfg: PfLayerConfig, weights: Dict[str, object], x, h_in=None, 
     """Allocate outputs (and workspace), run the forward; returns (x_out, h_out, saved)."""
     import torch
     m = -(-cfg.seq_len // _block(cfg))  # ceil(L / P): a partial last block has a proxy
-    x_out = torch.empty_like(x)
-    h_out = torch.empty((cfg.batch, m, cfg.d_proxy), dtype=x.dtype, device=x.device)
+    x_out = _empty(x.shape, x.dtype, x.device)
+    h_out = _empty((cfg.batch, m, cfg.d_proxy), x.dtype, x.device)
     saved = _bytes(layer_saved_size(cfg), x.device) if save else None
     if workspace is None:
         workspace = _bytes(layer_workspace_size(cfg, False), x.device)
@@ -321,13 +349,12 @@ def layer_backward(cfg: PfLayerConfig, weights: Dict[str, object], x, h_in, save
     """Run the backward; returns (dx, dh_in, grads) with fp32 weight gradients."""
     import torch
     dev = x.device
-    dx = torch.empty_like(x)
-    dh_in = torch.empty_like(h_in) if h_in is not None else None
+    dx = _empty(x.shape, x.dtype, dev)
+    dh_in = _empty(h_in.shape, h_in.dtype, dev) if h_in is not None else None
 
     def g_like(pair):
         w, b = pair
-        return (torch.empty(w.shape, dtype=torch.float32, device=dev),
-                torch.empty(w.shape[0], dtype=torch.float32, device=dev))
+        return (_empty(w.shape, torch.float32, dev), _empty((w.shape[0],), torch.float32, dev))
 
     grads = {"compress": [g_like(p) for p in weights["compress"]],
              "decompress": [g_like(p) for p in weights["decompress"]]}
@@ -390,9 +417,10 @@ class DecodeSession:
         dt = k_cache.dtype
         self.k_cache = k_cache
         self.v_cache = v_cache
-        self.x_blk = torch.zeros((cfg.batch, p, cfg.d_model), dtype=dt, device=device)
-        self.k_loc = torch.zeros((cfg.batch, cfg.n_heads, p, cfg.head_dim), dtype=dt, device=device)
-        self.v_loc = torch.zeros_like(self.k_loc)
+        # slots at or past j are never read: they start as NaN under poisoning
+        self.x_blk = _fresh(torch.zeros((cfg.batch, p, cfg.d_model), dtype=dt, device=device))
+        self.k_loc = _fresh(torch.zeros((cfg.batch, cfg.n_heads, p, cfg.head_dim), dtype=dt, device=device))
+        self.v_loc = _fresh(torch.zeros_like(self.k_loc))
         self.state = PfDecodeState(k_cache.data_ptr(), v_cache.data_ptr(), k_cache.shape[2], n,
                                    self.x_blk.data_ptr(), self.k_loc.data_ptr(), self.v_loc.data_ptr(), 0)
         self.n_seq = self.j_seq = None
@@ -414,9 +442,9 @@ class DecodeSession:
         return int(self.state.j)
 
     def step(self, x_t, y_t=None, stream=None):
-        import torch
         if y_t is None:
-            y_t = torch.empty_like(x_t)
+            y_t = _empty(x_t.shape, x_t.dtype, x_t.device)
+        _fresh(self.workspace)
         _check(load().proxy_decode_step(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),
                                         ctypes.byref(self.state), _ptr(x_t), _ptr(y_t),
                                         _ptr(self.workspace), self.workspace.numel(), _stream(stream)))
@@ -426,21 +454,22 @@ class DecodeSession:
         """Parallel form of the generation block over x [B, T, d] (the next T
         tokens of every sequence, from a block boundary); returns y [B, T, d].
         The prefill workspace is allocated on first use and grown as needed."""
-        import torch
         if y is None:
-            y = torch.empty_like(x)
+            y = _empty(x.shape, x.dtype, x.device)
         lib = load()
         need = int(lib.proxy_prefill_workspace_size(ctypes.byref(self.cfg), x.shape[1], self.state.n_cap))
         if need == 0:
             raise ProxyFormerError(-2, "prefill sizes beyond the library's limits")
         if getattr(self, "prefill_ws", None) is None or self.prefill_ws.numel() < need:
             self.prefill_ws = _bytes(need, x.device)
+        _fresh(self.prefill_ws)
         _check(lib.proxy_decode_prefill(ctypes.byref(self.cfg), ctypes.byref(self.wstruct), ctypes.byref(self.state),
                                         _ptr(x), x.shape[1], _ptr(y), _ptr(self.prefill_ws),
                                         self.prefill_ws.numel(), _stream(stream)))
         return y
 
     def append(self, x_blocks, nblk: int, stream=None):
+        _fresh(self.workspace)
         _check(load().proxy_cache_append(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),
                                          ctypes.byref(self.state), _ptr(x_blocks), nblk,
                                          _ptr(self.workspace), self.workspace.numel(), _stream(stream)))

@@ -189,7 +189,6 @@ int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w, 
   e = cfg->dtype == PF_BF16
           ? layer_backward_run<bf16>(d, cfg, w, xk, h_in, sv, dyk, dh_out, dxk, dh_in, grads, ws, s)
           : layer_backward_run<float>(d, cfg, w, xk, h_in, sv, dyk, dh_out, dxk, dh_in, grads, ws, s);
-  if (e == hipErrorNotSupported) return fail(PF_ERR_UNSUPPORTED, "backward not available for this config");
   if (e == hipSuccess && d.staged())
     e = d.img_w ? permute_patches(dxk, dx, d.B, d.L, d.img_w, d.patch, row_bytes, true, s)
                 : unpad_rows(dxk, dx, d.B, d.L_in, d.L, row_bytes, s);

@@ -543,9 +543,7 @@ static void launch_bwd_cfg(const AttnBwdParams& p, int batch, hipStream_t stream
 
 template <typename T>
 hipError_t launch_attention_bwd(const AttnBwdParams& p, int batch, int head_dim, hipStream_t stream) {
-  if (p.m <= 0) return hipSuccess;
-  // 32-bit buffer offsets: one head's transposed operands stay below 2 GiB
-  if ((int64_t)head_dim * p.ld_t * (int64_t)sizeof(T) >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  if (p.m <= 0) return hipSuccess;  // one head's tensors are below 2 GiB (checked by layer_dims)
   const int64_t rows = (int64_t)batch * p.n_heads * p.m;
   const dim3 dgrid((unsigned)((rows + 3) / 4));
   const bool split = sizeof(T) == 2 && p.q_lo && p.k_lo;

@@ -13,8 +13,10 @@
 //  3. the append of the chunk's complete blocks (the decode path's
 //     compression and K/V proxy GEMMs), so the cache holds every row a token
 //     of the chunk may see.
-//  4. a transposed copy of the cached values (rows 0 .. n0 + T/P - 1), the
-//     operand layout the attention kernel reads with 16-byte chunks.
+//  4. fp32 only: a transposed copy of the cached values (rows 0 .. n0 +
+//     T/P - 1), the operand layout the fp32 value product reads with 16-byte
+//     chunks. The bf16 path reads the cached values in place, row-major like
+//     the keys, through LDS transpose reads.
 //  5. gen_attn_kernel: per (sequence, head, 128 tokens), the local phase
 //     then the cache phase, each a flash-style loop over 64-key tiles staged
 //     through LDS; A = A_x + alpha * A_h.

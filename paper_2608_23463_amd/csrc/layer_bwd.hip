@@ -14,10 +14,13 @@
 //     + dV W_v accumulated in fp32, rounded once (this is dH_in, Eq. 8).
 //  6. compression levels M..1 (reverse of Eq. 16): dW_cj = dZ_j^T V_j and
 //     dV_j = dZ_j W_cj; level 1 adds into the fp32 dX and rounds it once.
-// Bias gradients are column sums, reduced in two fixed-order stages. Every
-// GEMM whose reduction runs over tokens (the weight gradients) uses operands
-// contiguous along the output dimensions (LAYOUT_MN), transposed in registers
-// on the way to LDS, so no transposed copy of any activation is made.
+// Bias gradients are column sums, reduced in two fixed-order stages. In bf16
+// every GEMM whose reduction runs over tokens (the weight gradients) reads its
+// token-major operands as they are, through LDS transpose reads, so no
+// transposed copy of an activation is made. In fp32 those operands are
+// transposed once into workspace when they have kTransposeMinRows rows or
+// more (the transpose of the output-gradient operand also leaves the bias
+// column sums), and read through the register-transposing GEMM below that.
 #include <algorithm>
 
 #include "attention.hpp"

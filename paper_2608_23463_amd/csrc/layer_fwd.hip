@@ -206,9 +206,13 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   d->R[0] = d->L;
   for (int j = 1; j <= d->M; ++j) d->R[j] = d->R[j - 1] / d->k[j - 1];
   d->m = d->R[d->M];
+  if ((int64_t)d->B * d->L > INT32_MAX) return *why = "batch * seq_len exceeds 2^31 - 1 rows", PF_ERR_UNSUPPORTED;
   d->ld_t = (int)((d->m + 63) / 64 * 64);
   d->esize = c->dtype == PF_BF16 ? 2 : 4;
-  if ((int64_t)d->B * d->L > INT32_MAX) return *why = "batch * seq_len exceeds 2^31 - 1 rows", PF_ERR_UNSUPPORTED;
+  // the attention kernels address one head's tensors ([m, d_head] rows,
+  // [d_head, ld_t] transposed) through 32-bit buffer offsets
+  if ((int64_t)d->ld_t * c->head_dim * d->esize >= ((int64_t)1 << 31))
+    return *why = "one head's proxy tensors exceed 2 GiB (m * head_dim * element size)", PF_ERR_UNSUPPORTED;
   for (int j = 0; j <= d->M; ++j)
     if (d->d[j] % 8 != 0) return *why = "every channel width must be a multiple of 8", PF_ERR_UNSUPPORTED;
   for (int j = 0; j < d->M; ++j)

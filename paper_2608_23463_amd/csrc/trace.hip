@@ -85,10 +85,18 @@ int proxy_trace_enable(int on) {
 
 int proxy_trace_collect(void) {
   std::lock_guard<std::mutex> lk(g_mu);
-  for (Pending& p : g_pending) {
-    if (hipEventSynchronize(p.stop) != hipSuccess) return PF_ERR_HIP;
+  // Launches are folded in order; each one leaves g_pending as it is counted,
+  // so after a failure the launches already counted are not counted again and
+  // their events (back in the pool) are referenced by nothing pending.
+  size_t done = 0;
+  int status = 0;
+  for (; done < g_pending.size(); ++done) {
+    Pending& p = g_pending[done];
     float ms = 0.0f;
-    if (hipEventElapsedTime(&ms, p.start, p.stop) != hipSuccess) return PF_ERR_HIP;
+    if (hipEventSynchronize(p.stop) != hipSuccess || hipEventElapsedTime(&ms, p.start, p.stop) != hipSuccess) {
+      status = PF_ERR_HIP;
+      break;
+    }
     if (!g_agg.count(p.label)) g_order.push_back(p.label);
     Agg& a = g_agg[p.label];
     a.launches += 1;
@@ -96,8 +104,8 @@ int proxy_trace_collect(void) {
     g_pool.push_back(p.start);
     g_pool.push_back(p.stop);
   }
-  g_pending.clear();
-  return (int)g_order.size();
+  g_pending.erase(g_pending.begin(), g_pending.begin() + done);
+  return status ? status : (int)g_order.size();
 }
 
 int proxy_trace_get(int i, char* label, size_t label_cap, int64_t* launches, double* total_ms) {

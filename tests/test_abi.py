@@ -90,6 +90,23 @@ def test_forward_rejects_bad_config(lib, bad, status):
     assert B.last_error()
 
 
+def test_forward_rejects_oversize_head_before_any_launch(lib):
+    # P = 1 and 2^23 tokens: one head of 128 bf16 channels over 2^23 proxies is
+    # 2 GiB, beyond the attention kernels' 32-bit buffer offsets. The forward
+    # and backward refuse it on the host (pointers are never dereferenced)
+    cfg = _cfg(seq_len=1 << 23, d_fine=8, d_proxy=128, n_heads=1, head_dim=128, factors=(1,))
+    assert _fwd(lib, cfg, _weights_struct()) == B.PF_ERR_UNSUPPORTED
+    assert "2 GiB" in B.last_error()
+    assert B.layer_workspace_size(cfg) == 0 and B.layer_saved_size(cfg) == 0
+    g = B.PfLayerGrads()
+    st = lib.proxy_layer_backward(ctypes.byref(cfg), ctypes.byref(_weights_struct()), 0x20000, None, 0x70000,
+                                  0x30000, None, 0x40000, None, ctypes.byref(g), 0x50000, 1 << 40, None)
+    assert st == B.PF_ERR_UNSUPPORTED
+    # one proxy fewer (2^23 - 64 tokens) fits
+    ok = _cfg(seq_len=(1 << 23) - 64, d_fine=8, d_proxy=128, n_heads=1, head_dim=128, factors=(1,))
+    assert B.layer_workspace_size(ok) > 0
+
+
 def test_partial_last_block_sizes(lib):
     # L = 4000 with P = 64: m = 63 blocks, the last zero-padded (Sec. 3.1)
     ragged, whole = _cfg(seq_len=4000), _cfg(seq_len=63 * 64)

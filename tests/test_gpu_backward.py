@@ -146,6 +146,42 @@ def test_backward_parity_factorised_workload_reduced_L(gpu):
     compare(shape, inp, res, ref, "L8192_d2048_f8x8")
 
 
+@pytest.mark.timeout(400)
+def test_backward_parity_factorised_workload_widths_many_tiles(gpu):
+    """The 256K-token factorised workload's widths, heads and factors (d = 2048,
+    16 x 128, P = 8 x 8) over 650 proxies: six 128-row query and key
+    workgroups per head in the attention backward (the last one ragged) and
+    full-size level GEMMs, every gradient compared. The oracle takes about a
+    minute here."""
+    full = synth.WORKLOADS["layer_bf16_L256k_d2048_f8x8"]
+    shape = LayerShape(1, 64 * 650, full.d_fine, full.d_proxy, full.n_heads, full.head_dim, full.factors)
+    print(f"[workload widths, m = 650] {shape}: generating inputs", flush=True)
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS["layer_bf16_L256k_d2048_f8x8"] + 1, with_dy=True)
+    res = run_gpu_backward(shape, inp)
+    print("[workload widths, m = 650] oracle backward", flush=True)
+    ref = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask)
+    compare(shape, inp, res, ref, "L41600_d2048_f8x8")
+
+
+@pytest.mark.parametrize("mask", [synth.TOKEN_CAUSAL, synth.BLOCK_CAUSAL, synth.BIDIRECTIONAL])
+def test_backward_parity_dh128_many_tiles(gpu, mask):
+    """16 heads of 128 over 1,000 proxies (eight query and key workgroups per
+    head, the last ragged) with a narrow local stream, attention sharpened,
+    every gradient compared."""
+    shape = LayerShape(1, 64 * 1000, 64, 2048, 16, 128, (8, 8), mask=mask)
+    print(f"[case dh128 m = 1000 mask {mask}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, 600 + mask, with_dy=True, with_h_in=True)
+    for key in ("q", "k"):
+        wq, bq = inp["weights"][key]
+        inp["weights"][key] = (synth.bf16_round(wq * 2), bq)
+    rng = np.random.default_rng(5)
+    dh_out = synth.bf16_round(rng.standard_normal((1, shape.n_proxies, shape.d_proxy)).astype(np.float32))
+    res = run_gpu_backward(shape, inp, dh_out)
+    ref = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask,
+                                inp["h_in"], dh_out)
+    compare(shape, inp, res, ref, f"dh128_m1000_mask{mask}")
+
+
 def test_backward_dual_causality_bitwise(gpu):
     """Token-causal layer: dY[t] cannot reach dX[s] for s > t."""
     import torch

@@ -4,11 +4,23 @@ The HIP path and the oracle decode the same seeded token stream from the same
 initial cache; outputs of every step, the appended cache rows and the
 counters n, j are compared (infinity-norm relative error, 1e-4 fp32, 2e-2
 bf16). At the full 32 x 16,384-row workload the oracle follows a sample of
-the sequences (sequences are independent).
+the sequences (sequences are independent). Cache rows past n start as NaN
+and must stay untouched (the outputs, workspace and local slots start as NaN
+too: the gpu fixture turns on the binding's NaN-filled allocation).
+
+The cache-sensitive cases (`cache_cases`) make the cached read alpha * A_h
+of Eq. 19-20 carry the output and also compare the sublayer output y - x;
+planted mistakes in the oracle (the cached read dropped, one slice of 1,024
+cached rows left out) move y - x by at least five times the tolerance
+(`test_parity_sensitivity.py`). With the workload's own weights y - x is
+small next to x and its bf16 rounding alone would exceed the tolerance, so
+the other cases compare y.
 """
 import numpy as np
 import pytest
 
+import cache_cases as cc
+from cache_cases import oracle_state
 import oracle
 from paper_2608_23463_amd import synth
 from paper_2608_23463_amd.synth import DecodeShape
@@ -24,16 +36,17 @@ def make_session(shape, inp):
     w = dev_weights(inp["weights"], shape.dtype)
     kc = dev(inp["k_cache"], shape.dtype)
     vc = dev(inp["v_cache"], shape.dtype)
+    # capacity past the valid rows is never read: it starts as NaN
+    kc[:, :, inp["n0"]:] = float("nan")
+    vc[:, :, inp["n0"]:] = float("nan")
     return B.DecodeSession(cfg, w, kc, vc, n=inp["n0"])
 
 
-def oracle_state(shape, inp, seqs):
-    st = oracle.DecodeState.empty(len(seqs), shape.n_heads, shape.head_dim, shape.block, shape.capacity,
-                                  shape.d_model)
-    st.k_cache[:] = inp["k_cache"][seqs]
-    st.v_cache[:] = inp["v_cache"][seqs]
-    st.n = inp["n0"]
-    return st
+def assert_rows_untouched(sess, seqs, n):
+    """Cache rows at or past n were not written (they still hold NaN)."""
+    import torch
+    for c in (sess.k_cache, sess.v_cache):
+        assert bool(torch.isnan(c[seqs][:, :, n:].float()).all()), "a cache row past n was written"
 
 
 def run_and_compare(shape, inp, seqs=None, label=""):
@@ -56,6 +69,7 @@ def run_and_compare(shape, inp, seqs=None, label=""):
         vc = host(sess.v_cache)[seqs][:, :, n0:st.n]
         assert_close(kc, st.k_cache[:, :, n0:st.n], shape.dtype, f"{label} appended K rows")
         assert_close(vc, st.v_cache[:, :, n0:st.n], shape.dtype, f"{label} appended V rows")
+    assert_rows_untouched(sess, seqs, st.n)
     return sess
 
 
@@ -180,4 +194,84 @@ def test_ragged_mode_with_equal_positions_is_lockstep_bitwise(gpu):
         torch.cuda.synchronize()
         assert torch.equal(ya, yb), t
     assert all(b.n_seq == a.n) and all(b.j_seq == a.j)
-    assert torch.equal(a.k_cache, b.k_cache) and torch.equal(a.v_cache, b.v_cache)
+    n = a.n  # rows past n are not state (a's start as NaN)
+    assert torch.equal(a.k_cache[:, :, :n], b.k_cache[:, :, :n]) and torch.equal(a.v_cache[:, :, :n], b.v_cache[:, :, :n])
+
+
+def run_gpu_steps(shape, inp):
+    import torch
+    sess = make_session(shape, inp)
+    ys = [sess.step(dev(inp["x"][t], shape.dtype)) for t in range(shape.steps)]
+    torch.cuda.synchronize()
+    return sess, np.stack([host(y) for y in ys])
+
+
+@pytest.mark.parametrize("name", list(cc.DECODE_CASES))
+def test_decode_parity_cache_sensitive(gpu, name):
+    """17 cache slices; y and y - x against the oracle, appended rows, counters."""
+    shape = cc.DECODE_CASES[name]
+    print(f"[cache-sensitive decode {name}] {shape}", flush=True)
+    inp = cc.build(shape, name, cc.decode_seed(name))
+    sess, got = run_gpu_steps(shape, inp)
+    ref, st = cc.oracle_decode(shape, inp)
+    x = inp["x"].astype(np.float64)
+    assert_close(got, ref, shape.dtype, f"{name} y")
+    assert_close(got - x, ref - x, shape.dtype, f"{name} y - x")
+    assert sess.n == st.n and sess.j == st.j
+    n0 = inp["n0"]
+    assert st.n > n0
+    assert_close(host(sess.k_cache)[:, :, n0:st.n], st.k_cache[:, :, n0:st.n], shape.dtype, f"{name} appended K")
+    assert_close(host(sess.v_cache)[:, :, n0:st.n], st.v_cache[:, :, n0:st.n], shape.dtype, f"{name} appended V")
+    assert_rows_untouched(sess, list(range(shape.batch)), st.n)
+
+
+def test_decode_alpha_off_ignores_the_cache(gpu):
+    """b_alpha = -40 gives alpha < 1e-16 (Eq. 20): the output must equal the
+    oracle decoding from an EMPTY initial cache, whatever the 16,500 cached
+    rows hold (the block appended on the way is compared as well)."""
+    shape = cc.DECODE_CASES["sharp"]
+    inp = cc.build(shape, "sharp", cc.decode_seed("sharp") + 1)
+    inp["weights"]["alpha"] = (inp["weights"]["alpha"][0], np.full(shape.n_heads, -40.0, np.float32))
+    sess, got = run_gpu_steps(shape, inp)
+    empty = dict(inp)
+    empty["k_cache"] = np.zeros_like(inp["k_cache"])
+    empty["v_cache"] = np.zeros_like(inp["v_cache"])
+    empty["n0"] = 0
+    ref, st = cc.oracle_decode(shape, empty)
+    x = inp["x"].astype(np.float64)
+    assert_close(got, ref, shape.dtype, "alpha off: y")
+    assert_close(got - x, ref - x, shape.dtype, "alpha off: y - x")
+    assert sess.n == inp["n0"] + st.n and sess.j == st.j
+    n0 = inp["n0"]
+    assert_close(host(sess.k_cache)[:, :, n0:n0 + st.n], st.k_cache[:, :, :st.n], shape.dtype, "alpha off: appended K")
+
+
+def test_decode_constant_cached_values_closed_form(gpu):
+    """Every cached value row of (sequence, head) equal to one vector c gives
+    A_h = c whatever the attention weights (softmax rows sum to 1), so
+    y = y_without_cache + (alpha * c) W_o^T over all 17 slices; alpha is
+    sigmoid(RMSNorm(x) W_alpha^T + b_alpha) (Eq. 20). No block completes."""
+    base = cc.DECODE_CASES["sharp"]
+    shape = DecodeShape(base.batch, base.d_model, base.n_heads, base.head_dim, base.factors, n0=base.n0,
+                        steps=base.block - 1)
+    inp = cc.build(shape, "sharp", cc.decode_seed("sharp") + 2)
+    rng = np.random.default_rng(3)
+    c = synth.bf16_round(rng.standard_normal((shape.batch, shape.n_heads, 1, shape.head_dim)).astype(np.float32))
+    inp["v_cache"][:, :, :shape.n0] = c
+    sess, got = run_gpu_steps(shape, inp)
+    empty = dict(inp)
+    empty["n0"] = 0
+    y0, _ = cc.oracle_decode(shape, empty)
+    w = {k: v for k, v in inp["weights"].items()}
+    wa, ba = (np.asarray(a, np.float64) for a in w["alpha"])
+    wo = np.asarray(w["o"][0], np.float64)
+    ref = np.zeros_like(y0)
+    for t in range(shape.steps):
+        u = oracle.rms_norm(inp["x"][t], w["rms_gamma"], shape.rms_eps)
+        alpha = oracle.sigmoid(u @ wa.T + ba)                                   # [B, h]
+        ah = (alpha[:, :, None] * c[:, :, 0, :]).reshape(shape.batch, shape.d_model)
+        ref[t] = y0[t] + ah @ wo.T
+    x = inp["x"].astype(np.float64)
+    assert_close(got, ref, shape.dtype, "constant V: y")
+    assert_close(got - x, ref - x, shape.dtype, "constant V: y - x")
+    assert sess.n == shape.n0 and sess.j == shape.steps

@@ -91,6 +91,11 @@ INJECTED = {
     "bf16_many_heads_tc": LayerShape(4, 16 * 1000, 64, 1024, 16, 64, (16,)),
     "bf16_many_heads_bc": LayerShape(4, 16 * 1024, 64, 1024, 16, 64, (16,), mask=synth.BLOCK_CAUSAL),
     "bf16_many_heads_bi": LayerShape(4, 16 * 1000, 64, 1024, 16, 64, (16,), mask=synth.BIDIRECTIONAL),
+    # the factorised 256K-token workload's heads (16 x 128, d_proxy = 2048, P = 8 x 8) over
+    # 1,000 proxies: eight 128-query workgroups per head, the last one ragged
+    "bf16_dh128_heads_tc": LayerShape(2, 64 * 1000, 64, 2048, 16, 128, (8, 8)),
+    "bf16_dh128_heads_bc": LayerShape(2, 64 * 1000, 64, 2048, 16, 128, (8, 8), mask=synth.BLOCK_CAUSAL),
+    "bf16_dh128_heads_bi": LayerShape(2, 64 * 1000, 64, 2048, 16, 128, (8, 8), mask=synth.BIDIRECTIONAL),
 }
 
 
@@ -129,9 +134,12 @@ def test_forward_parity_workload(gpu, name):
     assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
 
 
-@pytest.mark.parametrize("name", ["layer_bf16_L1M_d1024", "layer_bf16_L1M_lm_df64_dp512"])
+@pytest.mark.parametrize("name", ["layer_bf16_L1M_d1024", "layer_bf16_L1M_lm_df64_dp512",
+                                  "layer_bf16_L256k_d2048_f8x8"])
 def test_forward_parity_L1M_sampled(gpu, name):
-    """Full-size 1M-token layers: every proxy, and 64 sampled blocks of X_out."""
+    """Full-size layers (1M tokens; the factorised 256K-token workload with
+    4,096 proxies over 16 heads of 128): every proxy, and 64 sampled blocks
+    of X_out."""
     shape = synth.WORKLOADS[name]
     print(f"[workload {name}] generating inputs", flush=True)
     inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])

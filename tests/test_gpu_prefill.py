@@ -7,15 +7,23 @@ unfinished last block and the counters n, j are compared (infinity-norm
 relative error, 1e-4 fp32, 2e-2 bf16); then both decode a few more tokens
 from the prefilled state. At the full 32 x 4,096-token chunk the oracle
 follows two sequences at sampled tokens (sequences are independent).
+Cache rows past n start as NaN and must stay untouched.
+
+The cache-sensitive cases (`cache_cases`: 16,500 cached rows, 258 key tiles
+per head) also compare y - x; planted mistakes in the oracle (the cached
+read dropped, one slice or one 64-key tile of cached rows left out) move it
+by at least five times the tolerance (`test_parity_sensitivity.py`).
 """
 import numpy as np
 import pytest
 
+import cache_cases as cc
 import oracle
 from paper_2608_23463_amd import synth
 from paper_2608_23463_amd.synth import DecodeShape
 from helpers import assert_close, dev, host
-from test_gpu_decode import make_session, oracle_state
+from cache_cases import oracle_state
+from test_gpu_decode import assert_rows_untouched, make_session
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +58,7 @@ def compare_state(sess, st, shape, seqs, n0, label):
         assert_close(host(sess.x_blk)[seqs][:, :j], st.x_blk[:, :j], shape.dtype, f"{label} x_blk")
         assert_close(host(sess.k_loc)[seqs][:, :, :j], st.k_loc[:, :, :j], shape.dtype, f"{label} k_loc")
         assert_close(host(sess.v_loc)[seqs][:, :, :j], st.v_loc[:, :, :j], shape.dtype, f"{label} v_loc")
+    assert_rows_untouched(sess, seqs, st.n)
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -91,7 +100,8 @@ def test_prefill_in_whole_block_chunks_equals_one_chunk(gpu):
     torch.cuda.synchronize()
     assert torch.equal(ya, torch.cat([y1, y2], dim=1))
     assert (a.n, a.j) == (b.n, b.j) == (40 + 6, 0)
-    assert torch.equal(a.k_cache, b.k_cache) and torch.equal(a.v_cache, b.v_cache)
+    n = a.n  # rows past n start as NaN and are not state
+    assert torch.equal(a.k_cache[:, :, :n], b.k_cache[:, :, :n]) and torch.equal(a.v_cache[:, :, :n], b.v_cache[:, :, :n])
 
 
 @pytest.mark.parametrize("name", ["prefill_bf16_B32_T4096_n16k"])
@@ -114,4 +124,23 @@ def test_prefill_parity_full_workload_sampled(gpu, name):
     print(f"[workload {name}] oracle on sequences {seqs}, tokens {toks}", flush=True)
     ref = oracle.prefill(st, inp["weights"], shape.factors, xs[seqs], shape.rms_eps, tokens=toks)
     assert_close(got, ref, shape.dtype, f"{name} y (sampled)")
+    compare_state(sess, st, shape, seqs, inp["n0"], name)
+
+
+@pytest.mark.parametrize("name", list(cc.PREFILL_CASES))
+def test_prefill_parity_cache_sensitive(gpu, name):
+    """Every output (y and y - x), appended rows, local slots and counters."""
+    import torch
+    shape = cc.PREFILL_CASES[name]
+    print(f"[cache-sensitive prefill {name}] {shape}", flush=True)
+    inp = cc.build(shape, name, cc.prefill_seed(name))
+    xs = cc.chunk(inp)
+    sess = make_session(shape, inp)
+    y = sess.prefill(dev(xs, shape.dtype))
+    torch.cuda.synchronize()
+    seqs = list(range(shape.batch))
+    ref, st = cc.oracle_prefill(shape, inp)
+    got = host(y)
+    assert_close(got, ref, shape.dtype, f"{name} y")
+    assert_close(got - xs, ref - xs, shape.dtype, f"{name} y - x")
     compare_state(sess, st, shape, seqs, inp["n0"], name)
