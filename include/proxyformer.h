@@ -11,7 +11,9 @@
  *  - Tensor arguments are DEVICE pointers owned by the caller: contiguous,
  *    row-major, 16-byte aligned. The library never allocates or frees device
  *    memory; scratch space is the caller's `workspace` (size from the
- *    matching *_workspace_size query, alignment 256 bytes).
+ *    matching *_workspace_size query, alignment 256 bytes). The one
+ *    exception is proxy_decode_step_static, whose scratch is a fixed array
+ *    in the library's own device memory.
  *  - Activations and weights use the dtype of the config (PF_BF16: bfloat16,
  *    PF_FP32: float). Accumulation is always fp32. Weight gradients are
  *    always fp32.
@@ -235,6 +237,24 @@ size_t proxy_decode_workspace_size(const pf_decode_config* cfg);
 int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w,
                       pf_decode_state* st, const void* x_t, void* y_t,
                       void* workspace, size_t ws_bytes, void* stream);
+
+/* proxy_decode_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). Same arguments, kernels and results as
+ * proxy_decode_step; the scratch is a fixed 64 MiB array in the library's
+ * device memory, one per GPU, held until the process ends. It calls no
+ * allocation routine; its device address is looked up once per device on the
+ * first call there (with that device current).
+ *  A step needs about B * n_heads * (head_dim + 2) * 4 bytes per 1,024 cached
+ *  rows of its longest sequence, plus the append of one block per sequence
+ *  (about 5 MiB at 32 sequences x 16,384 rows, d_model 1024); a step needing
+ *  more than 64 MiB returns PF_ERR_UNSUPPORTED before any launch.
+ *  Every call on one GPU uses that GPU's one array: calls that overlap on one
+ *  GPU (other streams, other threads) race and corrupt each other's results.
+ *  Nothing in the array needs to start at zero; it keeps the last call's
+ *  contents. */
+int proxy_decode_step_static(const pf_decode_config* cfg, const pf_decode_weights* w,
+                             pf_decode_state* st, const void* x_t, void* y_t, void* stream);
 
 /* Append nblk whole blocks to the cache (prefill path and the streaming
  * update of Sec. 3.8): for each block h = C(x_block) (Eq. 7 / 16), then

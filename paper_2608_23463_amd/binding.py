@@ -33,7 +33,7 @@ EXPORTS = (
     "proxy_cache_append", "proxy_prefill_workspace_size", "proxy_decode_prefill",
     "proxy_last_error", "proxy_version",
     "proxy_trace_enable", "proxy_trace_collect", "proxy_trace_get", "proxy_trace_reset",
-    "proxy_ceiling_mfma",
+    "proxy_ceiling_mfma", "proxy_decode_step_static",
 )
 
 c_void_p = ctypes.c_void_p
@@ -176,6 +176,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.proxy_trace_reset.restype = None
     lib.proxy_ceiling_mfma.argtypes = [c_void_p, c_int64, c_int32, c_void_p]
     lib.proxy_ceiling_mfma.restype = c_int32
+    lib.proxy_decode_step_static.argtypes = [P(PfDecodeConfig), P(PfDecodeWeights), P(PfDecodeState), c_void_p,
+                                             c_void_p, c_void_p]
+    lib.proxy_decode_step_static.restype = c_int32
     _lib = lib
     return lib
 
@@ -448,6 +451,14 @@ class DecodeSession:
         _check(load().proxy_decode_step(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),
                                         ctypes.byref(self.state), _ptr(x_t), _ptr(y_t),
                                         _ptr(self.workspace), self.workspace.numel(), _stream(stream)))
+        return y_t
+
+    def step_static(self, x_t, y_t=None, stream=None):
+        """The same step through proxy_decode_step_static (no workspace)."""
+        if y_t is None:
+            y_t = _empty(x_t.shape, x_t.dtype, x_t.device)
+        _check(load().proxy_decode_step_static(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),
+                                               ctypes.byref(self.state), _ptr(x_t), _ptr(y_t), _stream(stream)))
         return y_t
 
     def prefill(self, x, y=None, stream=None):

@@ -1,9 +1,11 @@
 // C-ABI entry points: argument validation on the host, then dispatch to the
 // dtype-specific launch sequences. Nothing is enqueued unless every check
 // passes.
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "ceiling.hpp"
@@ -205,8 +207,10 @@ size_t proxy_decode_workspace_size(const pf_decode_config* cfg) {
 }
 
 // prefill_tokens >= 0: the workspace is checked against a prefill of that many tokens
+// check_ws = false: the caller brings no workspace (the static-scratch step)
 static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weights* w, const pf_decode_state* st,
-                               DecodeDims* d, void* workspace, size_t ws_bytes, int64_t prefill_tokens = -1) {
+                               DecodeDims* d, void* workspace, size_t ws_bytes, int64_t prefill_tokens = -1,
+                               bool check_ws = true) {
   const char* why;
   int s = decode_dims(cfg, d, &why);
   if (s != PF_OK) return fail(s, "invalid decode config: %s", why);
@@ -242,6 +246,7 @@ static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weig
     if (st->n < 0 || st->n > st->n_cap) return fail(PF_ERR_INVALID_ARG, "state n must be in 0..n_cap");
     if (st->j < 0 || st->j >= d->P) return fail(PF_ERR_INVALID_ARG, "state j must be in 0..P-1");
   }
+  if (!check_ws) return PF_OK;
   size_t need;
   if (prefill_tokens >= 0) {
     if (const char* lim = prefill_limits(*d, prefill_tokens, st->n_cap))
@@ -255,17 +260,11 @@ static int check_decode_common(const pf_decode_config* cfg, const pf_decode_weig
   return PF_OK;
 }
 
-int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, pf_decode_state* st, const void* x_t,
-                      void* y_t, void* workspace, size_t ws_bytes, void* stream) {
-  DecodeDims d;
-  int s = check_decode_common(cfg, w, st, &d, workspace, ws_bytes);
-  if (s != PF_OK) return s;
-  if (!x_t || !y_t) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be non-NULL");
-  if (!aligned16(x_t) || !aligned16(y_t)) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be 16-byte aligned");
-  if (overlaps(x_t, (size_t)d.B * d.d * d.esize, y_t, (size_t)d.B * d.d * d.esize))
-    return fail(PF_ERR_INVALID_ARG, "y_t must not alias x_t");
-  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  char* ws = reinterpret_cast<char*>(workspace);
+// One decode step on validated arguments with the scratch layout W inside
+// ws: the step's launches, then the append of the blocks the token
+// completes, then the host counters.
+static int decode_step_on(const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w, pf_decode_state* st,
+                          const void* x_t, void* y_t, char* ws, hipStream_t hs, const char* who) {
   DecodePos pos{};
   if (st->n_seq) {
     // per-sequence positions: the blocks that complete in this step are
@@ -277,18 +276,18 @@ int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, p
       pos.j[b] = st->j_seq[b];
       if (st->j_seq[b] + 1 == d.P) {
         if (st->n_seq[b] + 1 > st->n_cap)
-          return fail(PF_ERR_CAPACITY, "proxy cache of sequence %d full: n = %lld, n_cap = %lld", b,
+          return fail(PF_ERR_CAPACITY, "%s: proxy cache of sequence %d full: n = %lld, n_cap = %lld", who, b,
                       (long long)st->n_seq[b], (long long)st->n_cap);
         pos.write |= (uint64_t)1 << b;
       }
     }
-    hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, w, *st, pos, x_t, y_t, ws, hs)
-                                : decode_step_run<float>(d, w, *st, pos, x_t, y_t, ws, hs);
-    if (e != hipSuccess) return hip_status(e, "proxy_decode_step launch");
+    hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, W, w, *st, pos, x_t, y_t, ws, hs)
+                                : decode_step_run<float>(d, W, w, *st, pos, x_t, y_t, ws, hs);
+    if (e != hipSuccess) return hip_status(e, who);
     if (pos.write) {
-      e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, pos, st->x_blk, 1, ws, hs)
-                       : cache_append_run<float>(d, w, *st, pos, st->x_blk, 1, ws, hs);
-      if (e != hipSuccess) return hip_status(e, "proxy_decode_step append launch");
+      e = d.esize == 2 ? cache_append_run<bf16>(d, W, w, *st, pos, st->x_blk, 1, ws, hs)
+                       : cache_append_run<float>(d, W, w, *st, pos, st->x_blk, 1, ws, hs);
+      if (e != hipSuccess) return hip_status(e, who);
     }
     for (int b = 0; b < d.B; ++b) {
       if ((pos.write >> b) & 1) {
@@ -302,20 +301,91 @@ int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, p
   }
   const bool completes = st->j + 1 == d.P;
   if (completes && st->n + 1 > st->n_cap)
-    return fail(PF_ERR_CAPACITY, "proxy cache full: n = %lld, n_cap = %lld", (long long)st->n, (long long)st->n_cap);
-  hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, w, *st, pos, x_t, y_t, ws, hs)
-                              : decode_step_run<float>(d, w, *st, pos, x_t, y_t, ws, hs);
-  if (e != hipSuccess) return hip_status(e, "proxy_decode_step launch");
+    return fail(PF_ERR_CAPACITY, "%s: proxy cache full: n = %lld, n_cap = %lld", who, (long long)st->n,
+                (long long)st->n_cap);
+  hipError_t e = d.esize == 2 ? decode_step_run<bf16>(d, W, w, *st, pos, x_t, y_t, ws, hs)
+                              : decode_step_run<float>(d, W, w, *st, pos, x_t, y_t, ws, hs);
+  if (e != hipSuccess) return hip_status(e, who);
   if (completes) {
-    e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, pos, st->x_blk, 1, ws, hs)
-                     : cache_append_run<float>(d, w, *st, pos, st->x_blk, 1, ws, hs);
-    if (e != hipSuccess) return hip_status(e, "proxy_decode_step append launch");
+    e = d.esize == 2 ? cache_append_run<bf16>(d, W, w, *st, pos, st->x_blk, 1, ws, hs)
+                     : cache_append_run<float>(d, W, w, *st, pos, st->x_blk, 1, ws, hs);
+    if (e != hipSuccess) return hip_status(e, who);
     st->n += 1;
     st->j = 0;
   } else {
     st->j += 1;
   }
   return PF_OK;
+}
+
+static int check_step_io(const DecodeDims& d, const void* x_t, void* y_t) {
+  if (!x_t || !y_t) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be non-NULL");
+  if (!aligned16(x_t) || !aligned16(y_t)) return fail(PF_ERR_INVALID_ARG, "x_t and y_t must be 16-byte aligned");
+  if (overlaps(x_t, (size_t)d.B * d.d * d.esize, y_t, (size_t)d.B * d.d * d.esize))
+    return fail(PF_ERR_INVALID_ARG, "y_t must not alias x_t");
+  return PF_OK;
+}
+
+int proxy_decode_step(const pf_decode_config* cfg, const pf_decode_weights* w, pf_decode_state* st, const void* x_t,
+                      void* y_t, void* workspace, size_t ws_bytes, void* stream) {
+  DecodeDims d;
+  int s = check_decode_common(cfg, w, st, &d, workspace, ws_bytes);
+  if (s != PF_OK) return s;
+  if ((s = check_step_io(d, x_t, y_t)) != PF_OK) return s;
+  return decode_step_on(d, decode_ws(d), w, st, x_t, y_t, reinterpret_cast<char*>(workspace),
+                        reinterpret_cast<hipStream_t>(stream), "proxy_decode_step");
+}
+
+// ---------------------------------------------------------------- decode step without allocation
+
+// Scratch of proxy_decode_step_static: one array on every device the library
+// runs on, held until the process ends. In host code `scratch` only names the
+// array; its device address comes from hipGetSymbolAddress, looked up once per
+// device (with that device current) on the first call there.
+static constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static constexpr int kMaxDevices = 64;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+static int static_scratch(void** out) {
+  static std::mutex mu;
+  static void* ptr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "proxy_decode_step_static: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(PF_ERR_UNSUPPORTED, "proxy_decode_step_static: device %d beyond the %d devices it tracks", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "proxy_decode_step_static: hipGetSymbolAddress(scratch)");
+    ptr[dev] = p;
+  }
+  *out = ptr[dev];
+  return PF_OK;
+}
+
+int proxy_decode_step_static(const pf_decode_config* cfg, const pf_decode_weights* w, pf_decode_state* st,
+                             const void* x_t, void* y_t, void* stream) {
+  DecodeDims d;
+  int s = check_decode_common(cfg, w, st, &d, nullptr, 0, -1, false);
+  if (s != PF_OK) return s;
+  if ((s = check_step_io(d, x_t, y_t)) != PF_OK) return s;
+  int64_t n_max = st->n;  // the slices cover the longest cache of the batch
+  if (st->n_seq) {
+    n_max = 0;
+    for (int b = 0; b < d.B; ++b) n_max = std::max<int64_t>(n_max, st->n_seq[b]);
+  }
+  const DecodeWs W = decode_step_ws(d, n_max);
+  if (W.bytes > kStaticScratchBytes)
+    return fail(PF_ERR_UNSUPPORTED,
+                "proxy_decode_step_static: this step needs %zu bytes of scratch, the static scratch holds %zu "
+                "(use proxy_decode_step with a workspace)", W.bytes, kStaticScratchBytes);
+  void* ptr = nullptr;
+  if ((s = static_scratch(&ptr)) != PF_OK) return s;
+  return decode_step_on(d, W, w, st, x_t, y_t, reinterpret_cast<char*>(ptr), reinterpret_cast<hipStream_t>(stream),
+                        "proxy_decode_step_static");
 }
 
 size_t proxy_prefill_workspace_size(const pf_decode_config* cfg, int64_t n_tokens, int64_t n_cap) {
@@ -378,8 +448,9 @@ int proxy_cache_append(const pf_decode_config* cfg, const pf_decode_weights* w, 
   }
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   char* ws = reinterpret_cast<char*>(workspace);
-  hipError_t e = d.esize == 2 ? cache_append_run<bf16>(d, w, *st, pos, x_blocks, nblk, ws, hs)
-                              : cache_append_run<float>(d, w, *st, pos, x_blocks, nblk, ws, hs);
+  const DecodeWs W = decode_ws(d);
+  hipError_t e = d.esize == 2 ? cache_append_run<bf16>(d, W, w, *st, pos, x_blocks, nblk, ws, hs)
+                              : cache_append_run<float>(d, W, w, *st, pos, x_blocks, nblk, ws, hs);
   if (e != hipSuccess) return hip_status(e, "proxy_cache_append launch");
   if (st->n_seq) {
     for (int b = 0; b < d.B; ++b) st->n_seq[b] += nblk;

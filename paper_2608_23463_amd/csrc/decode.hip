@@ -68,9 +68,13 @@ int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why) {
   return PF_OK;
 }
 
-// Offsets of every scratch buffer except the split-K partials.
-static DecodeWs decode_ws_layout(const DecodeDims& d) {
+// Offsets of every scratch buffer except the split-K partials: the slice
+// partials of up to splits_cap cache slices per (sequence, head), and the
+// append's level outputs for up to rows_cap (sequence, block) rows per chunk.
+static DecodeWs decode_ws_layout(const DecodeDims& d, int splits_cap, int rows_cap) {
   DecodeWs w{};
+  w.splits_cap = splits_cap;
+  w.rows_cap = rows_cap;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -81,14 +85,14 @@ static DecodeWs decode_ws_layout(const DecodeDims& d) {
   w.q = take((size_t)d.B * d.d * es);
   w.alpha = take((size_t)d.B * d.nh * 4);
   w.attn = take((size_t)d.B * d.d * es);
-  const size_t nparts = (size_t)d.B * d.nh * (kDecodeMaxSplits + 1);
+  const size_t nparts = (size_t)d.B * d.nh * (splits_cap + 1);
   w.part_m = take(nparts * 4);
   w.part_l = take(nparts * 4);
   w.part_acc = take(nparts * d.dh * 4);
   int64_t per_block = d.P;  // rows of level j per block
   for (int j = 1; j <= d.M; ++j) {
     per_block /= d.k[j - 1];
-    w.z[j] = take((size_t)d.append_rows * per_block * d.dl[j] * es);
+    w.z[j] = take((size_t)rows_cap * per_block * d.dl[j] * es);
   }
   w.gemm = off;
   w.bytes = off;
@@ -510,13 +514,12 @@ struct EpiCache {
 // ---- launch sequences ---------------------------------------------------------
 
 template <typename T>
-static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                        const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws) {
-  const DecodeWs W = decode_ws_layout(d);
+static void append_impl(Runner& run, const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w,
+                        const pf_decode_state& st, const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws) {
   const int64_t total = (int64_t)d.B * nblk;   // (sequence, block) rows of the [B*nblk, P*d] view
   const int64_t row_elems = d.P * d.d;
-  for (int64_t r0 = 0; r0 < total; r0 += d.append_rows) {
-    const int rows = (int)std::min<int64_t>(d.append_rows, total - r0);
+  for (int64_t r0 = 0; r0 < total; r0 += W.rows_cap) {
+    const int rows = (int)std::min<int64_t>(W.rows_cap, total - r0);
     const T* zin = reinterpret_cast<const T*>(x_blocks) + r0 * row_elems;
     int64_t lvl_rows = (int64_t)rows * d.P;
     for (int j = 0; j < d.M; ++j) {  // compression C (Eq. 7, 16)
@@ -552,7 +555,7 @@ static void append_impl(Runner& run, const DecodeDims& d, const pf_decode_weight
   }
 }
 
-static void split_plan(int64_t n, int* splits, int* chunk) {
+void split_plan(int64_t n, int* splits, int* chunk) {
   if (n <= 0) {
     *splits = 0;
     *chunk = kDecodeRowsPerSplit;
@@ -597,9 +600,8 @@ static hipError_t launch_small_gemm(dim3 grid, const DecodeProjParams& pp, hipSt
 }
 
 template <typename T>
-static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                      const DecodePos& pos, const void* x_t, void* y_t, char* ws) {
-  const DecodeWs W = decode_ws_layout(d);
+static void step_impl(Runner& run, const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w,
+                      const pf_decode_state& st, const DecodePos& pos, const void* x_t, void* y_t, char* ws) {
   T* q = reinterpret_cast<T*>(ws + W.q);
   float* alpha = reinterpret_cast<float*>(ws + W.alpha);
   T* attn = reinterpret_cast<T*>(ws + W.attn);
@@ -694,25 +696,25 @@ static void step_impl(Runner& run, const DecodeDims& d, const pf_decode_weights*
 }
 
 // Split-K need of every GEMM a step or an append can issue (any chunk size).
-static size_t decode_gemm_need(const DecodeDims& d) {
+static size_t decode_gemm_need(const DecodeDims& d, const DecodeWs& W) {
   Runner dry(true);
   pf_decode_weights nw{};
   pf_decode_state ns{};
   ns.n_cap = 1;
   const DecodePos np{};
-  for (int rows = 1; rows <= d.append_rows; ++rows) {
+  for (int rows = 1; rows <= W.rows_cap; ++rows) {
     // one append of `rows` blocks of a single sequence exercises every chunk size
     DecodeDims d1 = d;
     d1.B = 1;
     if (d.esize == 2)
-      append_impl<bf16>(dry, d1, &nw, ns, np, nullptr, rows, nullptr);
+      append_impl<bf16>(dry, d1, W, &nw, ns, np, nullptr, rows, nullptr);
     else
-      append_impl<float>(dry, d1, &nw, ns, np, nullptr, rows, nullptr);
+      append_impl<float>(dry, d1, W, &nw, ns, np, nullptr, rows, nullptr);
   }
   if (d.esize == 2)
-    step_impl<bf16>(dry, d, &nw, ns, np, nullptr, nullptr, nullptr);
+    step_impl<bf16>(dry, d, W, &nw, ns, np, nullptr, nullptr, nullptr);
   else
-    step_impl<float>(dry, d, &nw, ns, np, nullptr, nullptr, nullptr);
+    step_impl<float>(dry, d, W, &nw, ns, np, nullptr, nullptr, nullptr);
   return dry.gemm_need;
 }
 
@@ -721,12 +723,12 @@ DecodeWs decode_ws(const DecodeDims& d) {
   static thread_local DecodeDims last{};
   static thread_local size_t last_need = 0;
   static thread_local bool have = false;
-  DecodeWs w = decode_ws_layout(d);
+  DecodeWs w = decode_ws_layout(d, kDecodeMaxSplits, d.append_rows);
   size_t need;
   if (have && memcmp(&last, &d, sizeof(d)) == 0) {
     need = last_need;
   } else {
-    need = decode_gemm_need(d);
+    need = decode_gemm_need(d, w);
     last = d;
     last_need = need;
     have = true;
@@ -735,31 +737,57 @@ DecodeWs decode_ws(const DecodeDims& d) {
   return w;
 }
 
+DecodeWs decode_step_ws(const DecodeDims& d, int64_t n_max) {
+  int splits, chunk;
+  split_plan(n_max, &splits, &chunk);
+  // the step appends at most one block per sequence: B rows
+  DecodeWs w = decode_ws_layout(d, splits, (int)std::min<int64_t>(d.append_rows, d.B));
+  Runner dry(true);
+  pf_decode_weights nw{};
+  pf_decode_state ns{};
+  ns.n_cap = 1;
+  ns.n = n_max;
+  const DecodePos np{};
+  if (d.esize == 2) {
+    append_impl<bf16>(dry, d, w, &nw, ns, np, nullptr, 1, nullptr);
+    step_impl<bf16>(dry, d, w, &nw, ns, np, nullptr, nullptr, nullptr);
+  } else {
+    append_impl<float>(dry, d, w, &nw, ns, np, nullptr, 1, nullptr);
+    step_impl<float>(dry, d, w, &nw, ns, np, nullptr, nullptr, nullptr);
+  }
+  w.bytes = w.gemm + align256(dry.gemm_need);
+  return w;
+}
+
 template <typename T>
-hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                           const DecodePos& pos, const void* x_t, void* y_t, char* ws, hipStream_t stream) {
-  const DecodeWs W = decode_ws_layout(d);
+hipError_t decode_step_run(const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w,
+                           const pf_decode_state& st, const DecodePos& pos, const void* x_t, void* y_t, char* ws,
+                           hipStream_t stream) {
   Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
-  step_impl<T>(run, d, w, st, pos, x_t, y_t, ws);
+  step_impl<T>(run, d, W, w, st, pos, x_t, y_t, ws);
   return run.err;
 }
 
 template <typename T>
-hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                            const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream) {
-  const DecodeWs W = decode_ws_layout(d);
+hipError_t cache_append_run(const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w,
+                            const pf_decode_state& st, const DecodePos& pos, const void* x_blocks, int64_t nblk,
+                            char* ws, hipStream_t stream) {
   Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
-  append_impl<T>(run, d, w, st, pos, x_blocks, nblk, ws);
+  append_impl<T>(run, d, W, w, st, pos, x_blocks, nblk, ws);
   return run.err;
 }
 
-template hipError_t decode_step_run<bf16>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                          const DecodePos&, const void*, void*, char*, hipStream_t);
-template hipError_t decode_step_run<float>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                           const DecodePos&, const void*, void*, char*, hipStream_t);
-template hipError_t cache_append_run<bf16>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                           const DecodePos&, const void*, int64_t, char*, hipStream_t);
-template hipError_t cache_append_run<float>(const DecodeDims&, const pf_decode_weights*, const pf_decode_state&,
-                                            const DecodePos&, const void*, int64_t, char*, hipStream_t);
+template hipError_t decode_step_run<bf16>(const DecodeDims&, const DecodeWs&, const pf_decode_weights*,
+                                          const pf_decode_state&, const DecodePos&, const void*, void*, char*,
+                                          hipStream_t);
+template hipError_t decode_step_run<float>(const DecodeDims&, const DecodeWs&, const pf_decode_weights*,
+                                           const pf_decode_state&, const DecodePos&, const void*, void*, char*,
+                                           hipStream_t);
+template hipError_t cache_append_run<bf16>(const DecodeDims&, const DecodeWs&, const pf_decode_weights*,
+                                           const pf_decode_state&, const DecodePos&, const void*, int64_t, char*,
+                                           hipStream_t);
+template hipError_t cache_append_run<float>(const DecodeDims&, const DecodeWs&, const pf_decode_weights*,
+                                            const pf_decode_state&, const DecodePos&, const void*, int64_t, char*,
+                                            hipStream_t);
 
 }  // namespace pf

@@ -36,6 +36,8 @@ constexpr int kDecodeMaxSplits = 256;   // cache-row slices per (sequence, head)
 constexpr int kDecodeRowsPerSplit = 1024;
 
 struct DecodeWs {
+  int splits_cap;                   // cache slices per (sequence, head) the partials hold
+  int rows_cap;                     // (sequence, block) rows per append chunk
   size_t q, alpha, attn;            // [B, d], fp32 [B, h], [B, d]
   size_t part_m, part_l, part_acc;  // fp32 partial softmax states
   size_t z[PF_MAX_LEVELS];          // append: compression level outputs (j = 1..M)
@@ -44,12 +46,21 @@ struct DecodeWs {
 };
 
 int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why);
+// Workspace of every decode call (steps and appends of any size).
 DecodeWs decode_ws(const DecodeDims& d);
+// Scratch of one decode step whose longest cache holds n_max rows: its own
+// slice partials and the append of one block per sequence (smaller than
+// decode_ws; the layout differs, the kernels are the same).
+DecodeWs decode_step_ws(const DecodeDims& d, int64_t n_max);
+// Cache slices the decode attention cuts n rows into, and their length.
+void split_plan(int64_t n, int* splits, int* chunk);
 
-// `pos` carries the per-sequence positions when st.n_seq / st.j_seq are set.
+// `pos` carries the per-sequence positions when st.n_seq / st.j_seq are set;
+// W is the scratch layout inside ws.
 template <typename T>
-hipError_t decode_step_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                           const DecodePos& pos, const void* x_t, void* y_t, char* ws, hipStream_t stream);
+hipError_t decode_step_run(const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w,
+                           const pf_decode_state& st, const DecodePos& pos, const void* x_t, void* y_t, char* ws,
+                           hipStream_t stream);
 
 // Prefill (parallel form of the generation block over a chunk of T tokens):
 // buffers placed after the decode workspace, which the chunk's append uses.
@@ -74,7 +85,8 @@ hipError_t prefill_run(const DecodeDims& d, const pf_decode_weights* w, const pf
                        int64_t n_tok, void* y, char* ws, hipStream_t stream);
 
 template <typename T>
-hipError_t cache_append_run(const DecodeDims& d, const pf_decode_weights* w, const pf_decode_state& st,
-                            const DecodePos& pos, const void* x_blocks, int64_t nblk, char* ws, hipStream_t stream);
+hipError_t cache_append_run(const DecodeDims& d, const DecodeWs& W, const pf_decode_weights* w,
+                            const pf_decode_state& st, const DecodePos& pos, const void* x_blocks, int64_t nblk,
+                            char* ws, hipStream_t stream);
 
 }  // namespace pf

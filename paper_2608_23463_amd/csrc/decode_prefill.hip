@@ -552,7 +552,7 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
     }
     if (run.ok()) {
       const DecodePos np{};
-      run.err = cache_append_run<T>(d, w, st, np, xb, nblk, ws, run.stream);
+      run.err = cache_append_run<T>(d, decode_ws(d), w, st, np, xb, nblk, ws, run.stream);
     }
   }
 

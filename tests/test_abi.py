@@ -284,3 +284,24 @@ def test_mfma_ceiling_rejects_bad_arguments(lib):
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), 0, 10, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), (1 << 20) + 1, 10, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), 16, 0, None) == B.PF_ERR_INVALID_ARG
+
+
+def test_static_decode_step_rejects_before_any_launch(lib):
+    """proxy_decode_step_static validates on the host: bad arguments, and a
+    step whose scratch would exceed the fixed 64 MiB array (64 sequences of
+    16 x 128 channels over 2^20 cached rows: 256 slices of partials)."""
+    cfg = B.decode_config(64, 2048, 16, 128, (64,))
+    w = B.PfDecodeWeights()
+    fake = 0x10000
+    w.rms_gamma = fake
+    for name in ("q", "k", "v", "o", "alpha", "k_proxy", "v_proxy"):
+        setattr(w, name, B.PfLinear(fake, None))
+    w.compress[0] = B.PfLinear(fake, None)
+    st = B.PfDecodeState(fake, fake, 1 << 20, 1 << 20, fake, fake, fake, 0)
+    step = lib.proxy_decode_step_static
+    assert step(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), 1 << 40, 2 << 40, None) == B.PF_ERR_UNSUPPORTED
+    assert "static scratch" in B.last_error()
+    assert st.n == 1 << 20 and st.j == 0  # nothing advanced
+    assert step(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), None, 2 << 40, None) == B.PF_ERR_INVALID_ARG
+    st.j = 64  # j must be below P
+    assert step(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(st), 1 << 40, 2 << 40, None) == B.PF_ERR_INVALID_ARG
