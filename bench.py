@@ -141,15 +141,78 @@ def dev_weights(w, dt):
     return out
 
 
+def time_calls(call, steps, warmup):
+    """Average milliseconds of `call` over `steps` timed calls after `warmup`
+    untimed ones (HIP events on torch's current stream, which the library's
+    launches use)."""
+    import torch
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        call()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps
+
+
+def trace_calls(call, steps):
+    """{label: (launches, total_ms)} of the library's launches over `steps` calls."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    B.trace_reset()
+    B.trace_enable(True)
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    tr = B.trace_collect()
+    B.trace_enable(False)
+    return tr
+
+
+def attention_roofline(tr, flops, steps):
+    """The proxy attention's algorithmic TFLOP/s from a trace."""
+    cnt, tot = tr["attention_fwd"]
+    avg = tot / cnt
+    tf = flops["attention_fwd"] / (avg * 1e-3) / 1e12
+    return {"kernel": "attention_fwd", "bound": "mfma", "achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4), "avg_ms": round(avg, 4),
+            "work_per_launch": flops["attention_fwd"]}
+
+
+def kernel_table(tr, flops, steps, counters: bool):
+    """Per-kernel entries of a trace: launches per call, average duration,
+    algorithmic TFLOP/s, and (for the headline workload, while the kernel
+    sources match the committed summaries) counter HBM rate and matrix-core
+    busy fraction."""
+    kernels = {}
+    for label, (cnt, tot) in tr.items():
+        avg = tot / cnt
+        ent = {"launches_per_step": cnt / steps, "avg_ms": round(avg, 4)}
+        if label in flops:
+            ent["tflops"] = round(flops[label] / (avg * 1e-3) / 1e12, 1)
+        hbm = measured_traffic(label) if counters else None
+        if hbm:  # measured HBM bytes per launch over this run's duration
+            ent["hbm_gbs"] = round(hbm / (avg * 1e-3) / 1e9, 1)
+        mf = measured_mfma(label) if counters else None
+        if mf:  # counters: matrix cores busy at the clock the kernel ran at
+            ent["mfma_util_counters"], ent["clock_ghz_counters"] = mf
+        kernels[label] = ent
+    return kernels
+
+
 def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     import torch
     from paper_2608_23463_amd import binding as B
     from paper_2608_23463_amd import synth
     shape = synth.WORKLOADS[workload]
+    headline = workload == LAYER_WORKLOAD
     log(f"generating {workload} inputs")
     inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[workload])
     sample = None
-    if workload == LAYER_WORKLOAD:
+    if headline:
         sample = {"x": inp["x"][:, :CPU_SAMPLE_TOKENS].copy(), "weights": inp["weights"]}
     x = to_dev(inp["x"], shape.dtype)
     del inp["x"]
@@ -160,68 +223,48 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     x_out = torch.empty_like(x)
     h_out = torch.empty((1, m, shape.d_proxy), dtype=x.dtype, device="cuda")
     wst = B.layer_weights(w)
+    tokens = shape.seq_len * shape.batch
 
-    def call():
-        B.layer_forward_raw(cfg, wst, x, None, x_out, h_out, None, ws)
+    def forward(c, weights=wst, workspace=ws):
+        return lambda: B.layer_forward_raw(c, weights, x, None, x_out, h_out, None, workspace)
 
-    log(f"warmup {warmup}")
-    for _ in range(warmup):
-        call()
-    torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    log(f"timing {steps} forward calls")
-    start.record()
-    for _ in range(steps):
-        call()
-    stop.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / steps
-
+    log(f"timing {steps} forward calls after {warmup} warmup calls")
+    ms = time_calls(forward(cfg), steps, warmup)
     log("tracing per-kernel durations")
-    B.trace_reset()
-    B.trace_enable(True)
-    for _ in range(steps):
-        call()
-    torch.cuda.synchronize()
-    tr = B.trace_collect()
-    B.trace_enable(False)
+    tr = trace_calls(forward(cfg), steps)
     flops = layer_flops(shape)
-    kernels = {}
-    for label, (cnt, tot) in tr.items():
-        per_call = cnt / steps
-        avg = tot / cnt
-        ent = {"launches_per_step": per_call, "avg_ms": round(avg, 4)}
-        if label in flops:
-            ent["tflops"] = round(flops[label] / (avg * 1e-3) / 1e12, 1)
-        hbm = measured_traffic(label) if workload == LAYER_WORKLOAD else None
-        if hbm:  # measured HBM bytes per launch over this run's duration
-            ent["hbm_gbs"] = round(hbm / (avg * 1e-3) / 1e9, 1)
-        mf = measured_mfma(label) if workload == LAYER_WORKLOAD else None
-        if mf:  # counters: matrix cores busy at the clock the kernel ran at
-            ent["mfma_util_counters"], ent["clock_ghz_counters"] = mf
-        kernels[label] = ent
+    kernels = kernel_table(tr, flops, steps, headline)
     dom = max((k for k in tr if k in flops), key=lambda k: tr[k][1])
     dom_ms = tr[dom][1] / tr[dom][0]
     achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
     # the committed counter summary covers the headline workload only
-    traffic = measured_traffic(dom) if workload == LAYER_WORKLOAD else None
-    variants = {}
-    if workload == LAYER_WORKLOAD:
+    traffic = measured_traffic(dom) if headline else None
+    roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
+    mf = measured_mfma(dom) if headline else None
+    if mf:
+        roof["mfma_util_counters"], roof["clock_ghz_counters"] = mf
+
+    def entry(ms_v, **extra):
+        return {"ms_per_step": round(ms_v, 4), "value": round(tokens / (ms_v * 1e-3), 1), "unit": "tokens/s",
+                **extra}
+
+    variants = {"attention_extended": attention_roofline(tr, flops, steps)}
+    # plain bf16 H, Q, K (PF_PRECISION_BF16): one score MFMA per tile step
+    cfg_p = B.config_from_shape(shape)
+    cfg_p.precision = B.PF_PRECISION_BF16
+    ws_p = torch.empty(B.layer_workspace_size(cfg_p), dtype=torch.uint8, device="cuda")
+    ms_p = time_calls(forward(cfg_p, workspace=ws_p), steps, warmup)
+    tr_p = trace_calls(forward(cfg_p, workspace=ws_p), steps)
+    variants["precision_bf16"] = entry(ms_p, attention=attention_roofline(tr_p, flops, steps),
+                                       kernels=kernel_table(tr_p, flops, steps, False))
+    del ws_p
+    if headline:
         # the same inputs with residual-add injection (Eq. 11): no gate GEMM
         cfg_add = B.config_from_shape(shape)
         cfg_add.injection = B.PF_INJECT_ADD
-        for _ in range(warmup):
-            B.layer_forward_raw(cfg_add, wst, x, None, x_out, h_out, None, ws)
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(steps):
-            B.layer_forward_raw(cfg_add, wst, x, None, x_out, h_out, None, ws)
-        stop.record()
-        torch.cuda.synchronize()
-        ms_add = start.elapsed_time(stop) / steps
-        variants["inject_add"] = {"ms_per_step": round(ms_add, 4),
-                                  "value": round(shape.seq_len * shape.batch / (ms_add * 1e-3), 1),
-                                  "unit": "tokens/s"}
+        variants["inject_add"] = entry(time_calls(forward(cfg_add), steps, warmup))
         # affine modulation (Eq. 13): [S | T] GEMM (N = 2 d_fine, K = d_fine) instead of the gate
         cfg_aff = B.config_from_shape(shape)
         cfg_aff.injection = B.PF_INJECT_AFFINE
@@ -230,48 +273,20 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
         w_aff = dict(w)
         w_aff["affine"] = ((torch.randn(2 * shape.d_fine, shape.d_fine, generator=gen, device="cuda") * 0.02)
                            .to(x.dtype), torch.zeros(2 * shape.d_fine, dtype=x.dtype, device="cuda"))
-        wst_aff = B.layer_weights(w_aff)
         ws_aff = torch.empty(B.layer_workspace_size(cfg_aff), dtype=torch.uint8, device="cuda")
-        for _ in range(warmup):
-            B.layer_forward_raw(cfg_aff, wst_aff, x, None, x_out, h_out, None, ws_aff)
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(steps):
-            B.layer_forward_raw(cfg_aff, wst_aff, x, None, x_out, h_out, None, ws_aff)
-        stop.record()
-        torch.cuda.synchronize()
-        ms_aff = start.elapsed_time(stop) / steps
-        variants["inject_affine"] = {"ms_per_step": round(ms_aff, 4),
-                                     "value": round(shape.seq_len * shape.batch / (ms_aff * 1e-3), 1),
-                                     "unit": "tokens/s"}
-        del ws_aff, w_aff, wst_aff
+        variants["inject_affine"] = entry(time_calls(forward(cfg_aff, B.layer_weights(w_aff), ws_aff), steps,
+                                                     warmup))
+        del ws_aff, w_aff
         # per-head gate (Eq. 12 with one gate per head): N = n_heads gate GEMM and a combine pass
         cfg_gh = B.config_from_shape(shape)
         cfg_gh.injection = B.PF_INJECT_GATED_HEAD
         w_gh = dict(w)
         w_gh["gate"] = ((torch.randn(shape.n_heads, 2 * shape.d_fine, generator=gen, device="cuda") * 0.02)
                         .to(x.dtype), torch.zeros(shape.n_heads, dtype=x.dtype, device="cuda"))
-        wst_gh = B.layer_weights(w_gh)
         ws_gh = torch.empty(B.layer_workspace_size(cfg_gh), dtype=torch.uint8, device="cuda")
-        for _ in range(warmup):
-            B.layer_forward_raw(cfg_gh, wst_gh, x, None, x_out, h_out, None, ws_gh)
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(steps):
-            B.layer_forward_raw(cfg_gh, wst_gh, x, None, x_out, h_out, None, ws_gh)
-        stop.record()
-        torch.cuda.synchronize()
-        ms_gh = start.elapsed_time(stop) / steps
-        variants["inject_gated_head"] = {"ms_per_step": round(ms_gh, 4),
-                                         "value": round(shape.seq_len * shape.batch / (ms_gh * 1e-3), 1),
-                                         "unit": "tokens/s"}
-        del ws_gh, w_gh, wst_gh
-    roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic, "work_per_launch": flops[dom], "avg_ms": round(dom_ms, 4)}
-    mf = measured_mfma(dom) if workload == LAYER_WORKLOAD else None
-    if mf:
-        roof["mfma_util_counters"], roof["clock_ghz_counters"] = mf
+        variants["inject_gated_head"] = entry(time_calls(forward(cfg_gh, B.layer_weights(w_gh), ws_gh), steps,
+                                                         warmup))
+        del ws_gh, w_gh
     del x, x_out, h_out, ws, w
     torch.cuda.empty_cache()
     return shape, ms, kernels, roof, sample, variants
@@ -641,6 +656,7 @@ def main():
         "config": {"workload": LAYER_WORKLOAD, "batch": shape.batch, "seq_len": shape.seq_len,
                    "d_fine": shape.d_fine, "d_proxy": shape.d_proxy, "n_heads": shape.n_heads,
                    "head_dim": shape.head_dim, "P": shape.block, "levels": list(shape.factors),
+                   "proxy_precision": "extended (bf16 hi/lo parts of H, Q, K)",
                    "parallelism": "single GPU"},
         "roofline": roof,
         "kernels": kernels,
@@ -656,12 +672,12 @@ def main():
     if not args.no_prefill:
         result["prefill"] = bench_prefill()
     if not args.no_lm:
-        lshape, lms, lkernels, lroof, _, _ = bench_layer(args.steps, args.warmup, LM_LAYER_WORKLOAD)
+        lshape, lms, lkernels, lroof, _, lvariants = bench_layer(args.steps, args.warmup, LM_LAYER_WORKLOAD)
         result["lm"] = {"metric": "layer fwd tokens/s (language-model shape)",
                         "value": round(lshape.seq_len * lshape.batch / (lms * 1e-3), 1), "unit": "tokens/s",
                         "ms_per_step": round(lms, 4), "workload": LM_LAYER_WORKLOAD, "d_fine": lshape.d_fine,
                         "d_proxy": lshape.d_proxy, "n_heads": lshape.n_heads, "roofline": lroof,
-                        "kernels": lkernels}
+                        "kernels": lkernels, "variants": lvariants}
         if not args.no_decode:
             result["lm"]["decode"] = bench_decode(LM_DECODE_WORKLOAD)
     if not args.no_cpu_baseline:

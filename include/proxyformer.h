@@ -71,6 +71,19 @@ enum pf_mask { PF_TOKEN_CAUSAL = 0, PF_BLOCK_CAUSAL = 1, PF_BIDIRECTIONAL = 2 };
  *   c / (d_fine / n_heads); d_fine / n_heads must be a multiple of 8. */
 enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1, PF_INJECT_AFFINE = 2, PF_INJECT_GATED_HEAD = 3 };
 
+/* Arithmetic of the proxy path upstream of the attention logits in bf16 mode
+ * (ignored in fp32 mode). Accumulation is fp32 in both.
+ * PF_PRECISION_EXTENDED (default): H, the level outputs Z_j, Q and K keep a
+ *   bf16 low part next to their bf16 value (v = hi + lo, about 16 mantissa
+ *   bits); the projections read [hi | lo] and the logits are
+ *   Qh Kh + Ql Kh + Qh Kl. A proxy sums P * d_fine products, so with wide
+ *   layers the logits are large and one bf16 rounding of Q and K moves a
+ *   sharp softmax by several percent; this keeps such layers (and their
+ *   backward) within the bf16 tolerance. Twice the attention's score work.
+ * PF_PRECISION_BF16: H, Q and K are plain bf16 values (the bf16 training the
+ *   paper reports): the score product is one MFMA per tile step. */
+enum pf_precision { PF_PRECISION_EXTENDED = 0, PF_PRECISION_BF16 = 1 };
+
 typedef struct {
   const void* w; /* [out, in] */
   const void* b; /* [out] or NULL */
@@ -90,7 +103,8 @@ typedef struct {
  *  level_dims[j] = d_{j+1} for j < M-1 (0 -> d_proxy); level_dims[M-1] is
  *            ignored (d_M = d_proxy).
  *  head_dim  64 or 128.
- *  dtype     pf_dtype; mask pf_mask; injection pf_injection.
+ *  dtype     pf_dtype; mask pf_mask; injection pf_injection;
+ *            precision pf_precision (bf16 mode).
  *  image_width  0: the tokens are a sequence and a block is P consecutive
  *            tokens. > 0: 2-D partition of the vision instantiation
  *            (Sec. 3.9): the tokens are a raster-order image of this width
@@ -109,6 +123,7 @@ typedef struct {
   int32_t dtype, mask;
   int32_t injection;
   int32_t image_width;
+  int32_t precision; /* pf_precision */
 } pf_layer_config;
 
 /* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)
@@ -321,7 +336,8 @@ int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* str
 /* Message of the last non-OK status on the calling thread. */
 const char* proxy_last_error(void);
 
-/* Library ABI version (major * 100 + minor). */
+/* Library ABI version (major * 100 + minor): 101 adds pf_layer_config.precision
+ * and proxy_decode_step_static. */
 int proxy_version(void);
 
 #ifdef __cplusplus

@@ -26,6 +26,8 @@ PF_INJECT_GATED = 0
 PF_INJECT_ADD = 1
 PF_INJECT_AFFINE = 2
 PF_INJECT_GATED_HEAD = 3
+PF_PRECISION_EXTENDED = 0
+PF_PRECISION_BF16 = 1
 
 EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
@@ -50,7 +52,8 @@ class PfLayerConfig(ctypes.Structure):
     _fields_ = [("batch", c_int32), ("seq_len", c_int64), ("d_fine", c_int32), ("d_proxy", c_int32),
                 ("n_heads", c_int32), ("head_dim", c_int32), ("n_levels", c_int32),
                 ("factors", c_int32 * MAX_LEVELS), ("level_dims", c_int32 * MAX_LEVELS),
-                ("dtype", c_int32), ("mask", c_int32), ("injection", c_int32), ("image_width", c_int32)]
+                ("dtype", c_int32), ("mask", c_int32), ("injection", c_int32), ("image_width", c_int32),
+                ("precision", c_int32)]
 
 
 class PfLayerWeights(ctypes.Structure):
@@ -240,7 +243,7 @@ def _stream(stream) -> Optional[int]:
 
 def layer_config(batch: int, seq_len: int, d_fine: int, d_proxy: int, n_heads: int, head_dim: int,
                  factors: Sequence[int], level_dims: Sequence[int] = (), dtype: str = "bf16",
-                 mask: int = 0, injection: int = 0, image_width: int = 0) -> PfLayerConfig:
+                 mask: int = 0, injection: int = 0, image_width: int = 0, precision: int = 0) -> PfLayerConfig:
     c = PfLayerConfig()
     c.batch = batch
     c.seq_len = seq_len
@@ -257,6 +260,7 @@ def layer_config(batch: int, seq_len: int, d_fine: int, d_proxy: int, n_heads: i
     c.mask = mask
     c.injection = injection
     c.image_width = image_width
+    c.precision = precision
     return c
 
 
@@ -265,7 +269,8 @@ def config_from_shape(shape) -> PfLayerConfig:
     dims = list(shape.level_dims) if shape.level_dims else []
     return layer_config(shape.batch, shape.seq_len, shape.d_fine, shape.d_proxy, shape.n_heads,
                         shape.head_dim, shape.factors, dims, shape.dtype, shape.mask,
-                        getattr(shape, "injection", 0), getattr(shape, "image_width", 0))
+                        getattr(shape, "injection", 0), getattr(shape, "image_width", 0),
+                        getattr(shape, "precision", 0))
 
 
 def _lin(pair) -> PfLinear:

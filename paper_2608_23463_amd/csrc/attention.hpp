@@ -57,16 +57,15 @@ __device__ __forceinline__ bf16x8 pt_frag_bf16(const f32x16& s, int s2) {
 // index contiguous with row stride ld_t >= m, a multiple of 64 whose padding
 // columns hold zeros).
 struct AttnParams {
-  const void* q;    // [B, h, m, dh]
+  const void* q;    // [B, h, m, dh], pre-scaled by log2(e) / sqrt(dh)
   const void* k;    // [B, h, m, dh]
-  const void* q_lo; // optional low parts of the two-term split of Q and K
-  const void* k_lo; //   (bf16 only): logits use Qh Kh + Ql Kh + Qh Kl
+  const void* q_lo; // optional low parts of the two-term split of (scaled) Q
+  const void* k_lo; //   and K (bf16 only): logits use Qh Kh + Ql Kh + Qh Kl
   const void* vt;   // [B, h, dh, ld_t]
   void* o;          // [B*m, h*dh] row-major (heads are column slices)
-  float* lse;       // [B, h, m] natural-log log-sum-exp of the scaled scores
+  float* lse;       // [B, h, m] natural-log log-sum-exp of the scores Q.K / sqrt(dh)
   int m, n_heads, ld_t;
   int causal;       // 1: key j visible to query i iff j <= i
-  float scale_log2; // log2(e) / sqrt(dh)
 };
 
 template <typename T>

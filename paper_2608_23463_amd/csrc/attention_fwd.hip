@@ -6,15 +6,16 @@
 // chunks, so fragment reads are conflict-free 16-byte reads. A wave computes
 // the transposed score tile S^T = K Q^T with MFMA, so each lane holds one
 // query column: the online-softmax statistics of a query live in one lane
-// pair (lane, lane ^ 32) and the running maximum needs one cross-half
-// exchange per tile. The running maximum is only moved (and O rescaled) when
-// some score exceeds it by more than 2^8 in exp2 units; until then the stale
-// maximum is used, which leaves the result unchanged and keeps every
-// exponential below 2^8. P^T stays in registers: one v_permlane32_swap per
+// pair (lane, lane ^ 32). Q arrives pre-scaled by log2(e)/sqrt(d_head), so
+// scores are in exp2 units; the score MFMAs start their accumulators at
+// minus the query's reference maximum, so each probability is one exp2 of an
+// MFMA result, with no per-score scaling or shift. The reference is a real
+// maximum taken on the wave's first tile and kept while the running sums stay
+// below 2^64 (no per-tile maximum); a tile that would exceed that is redone
+// against a new reference. P^T stays in registers: one v_permlane32_swap per
 // pair of packed values turns the accumulator layout (runs of 4 keys) into
 // MFMA operands of 8 consecutive keys, so V^T (key-contiguous, written
-// transposed by the producing GEMM) is read as 16-byte chunks. Exponentials
-// use exp2 with log2(e)/sqrt(d_head) folded into one FMA per score. With SPLIT,
+// transposed by the producing GEMM) is read as 16-byte chunks. With SPLIT,
 // Q and K arrive as bf16 hi/lo pairs and the scores are Kh Qh + Kl Qh + Kh Ql
 // (three MFMAs into one accumulator), so a sharp softmax is not moved by one
 // bf16 rounding of its logits. Masked scores are -inf and contribute exactly
@@ -127,9 +128,26 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
   for (int cb = 0; cb < DH / 32; ++cb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.0f;
-  float mrun = -INFINITY, lrun = 0.0f;
-  const float sc = p.scale_log2;
-  const float thr = 8.0f / sc;  // raw-score headroom of the stale maximum (2^8)
+  // Online softmax in exp2 units (Q arrives scaled by log2(e)/sqrt(d_head)).
+  // mref is the reference maximum of this lane's query, the same in both
+  // lanes of the pair; lrun the lane's partial sum of exp2(score - mref).
+  // negm holds -mref in every slot and starts the score accumulators, so the
+  // MFMAs deliver score - mref and each probability is one exp2. The
+  // reference is set from a real maximum on the wave's first tile and kept
+  // while the running sums stay below 2^64; a tile that would push one past
+  // it (a score more than ~64 above the reference) is redone with a new
+  // reference. Rescaling by a power of the reference shift is exact up to
+  // rounding, so the result does not depend on when it happens.
+  float lrun = 0.0f;
+  float mref = -INFINITY;
+  f32x16 negm, zero;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    negm[r] = 0.0f;
+    zero[r] = 0.0f;
+  }
+  bool have_ref = false;  // wave-uniform
+  constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
 
 #pragma unroll
   for (int s0 = 0; s0 < S::kNS - 1; ++s0)
@@ -152,81 +170,105 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
     const char* sv = sk + S::kKParts * S::kKTile;
     const bool active = !p.causal || kt0 <= qw0 + 31;  // uniform across the wave
     if (active) {
-      // S^T = K Q^T for 64 keys (two 32-key blocks) x this wave's 32 queries.
-      // The matrix phases run at raised wave priority, so the SIMD's other
-      // wave (in its softmax phase) fills the issue slots between MFMAs.
-      __builtin_amdgcn_s_setprio(1);
-      f32x16 s[2];
+      const bool need_mask = (p.causal && kt0 + S::kKT - 1 > qw0) || kt0 + S::kKT > p.m;  // wave-uniform
+      const int klim = p.causal ? min(myq, p.m - 1) : p.m - 1;  // last visible key
+      // S^T = K Q^T + c0 for 64 keys (two 32-key blocks) x this wave's 32
+      // queries, masked entries -inf. The matrix phases run at raised wave
+      // priority, so the SIMD's other wave (in its softmax phase) fills the
+      // issue slots between MFMAs.
+      auto scores = [&](f32x16 (&s)[2], const f32x16& c0) {
+        // every fragment read is issued before the first MFMA
+        typename MM::frag kh[2][DH / 16], kl[2][SPLIT ? DH / 16 : 1];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+        for (int kb = 0; kb < 2; ++kb) {
+          const int kr = kb * 32 + col;  // key row of this lane's A fragment
+          const char* krow = sk + kr * S::kRowBytes;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
-        const int kr = kb * 32 + col;  // key row of this lane's A fragment
-        const char* krow = sk + kr * S::kRowBytes;
+          for (int kk = 0; kk < DH / 16; ++kk) {
+            if constexpr (sizeof(T) == 2) {
+              const int off = lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16;
+              kh[kb][kk] = *reinterpret_cast<const typename MM::frag*>(krow + off);
+              if constexpr (SPLIT) kl[kb][kk] = *reinterpret_cast<const typename MM::frag*>(krow + S::kKTile + off);
+            } else {
+              const int c0i = kk * 4 + g * 2;
+              const f32x4 lo = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0i) * 16);
+              const f32x4 hi = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0i + 1) * 16);
 #pragma unroll
-        for (int kk = 0; kk < DH / 16; ++kk) {
-          typename MM::frag kh, kl;
-          if constexpr (sizeof(T) == 2) {
-            const int off = lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16;
-            kh = *reinterpret_cast<const typename MM::frag*>(krow + off);
-            if constexpr (SPLIT) kl = *reinterpret_cast<const typename MM::frag*>(krow + S::kKTile + off);
-          } else {
-            const int c0 = kk * 4 + g * 2;
-            const f32x4 lo = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0) * 16);
-            const f32x4 hi = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0 + 1) * 16);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              kh[e] = lo[e];
-              kh[e + 4] = hi[e];
+              for (int e = 0; e < 4; ++e) {
+                kh[kb][kk][e] = lo[e];
+                kh[kb][kk][e + 4] = hi[e];
+              }
             }
           }
-          s[kb] = MM::mma(kh, qf[kk], s[kb]);
-          if constexpr (SPLIT) {
-            s[kb] = MM::mma(kl, qf[kk], s[kb]);
-            s[kb] = MM::mma(kh, qfl[kk], s[kb]);
-          }
         }
-      }
-      __builtin_amdgcn_s_setprio(0);
-      // online softmax on raw scores; masked entries are -inf
-      const bool need_mask = (p.causal && kt0 + S::kKT - 1 > qw0) || kt0 + S::kKT > p.m;
-      if (need_mask) {  // wave-uniform; selects, no per-element branches
-        const int klim = p.causal ? min(myq, p.m - 1) : p.m - 1;  // last visible key
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int kk = 0; kk < DH / 16; ++kk)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb) {
+            s[kb] = MM::mma(kh[kb][kk], qf[kk], kk == 0 ? c0 : s[kb]);
+            if constexpr (SPLIT) {
+              s[kb] = MM::mma(kl[kb][kk], qf[kk], s[kb]);
+              s[kb] = MM::mma(kh[kb][kk], qfl[kk], s[kb]);
+            }
+          }
+        __builtin_amdgcn_s_setprio(0);
+        if (need_mask) {  // selects, no per-element branches
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int key = kt0 + kb * 32 + acc_row(r, lane);
+              s[kb][r] = key > klim ? -INFINITY : s[kb][r];
+            }
+        }
+      };
+      // probabilities in place, summed in four chains
+      auto exponentiate = [&](f32x16 (&s)[2], float shift) {
+        float ls[4];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int key = kt0 + kb * 32 + acc_row(r, lane);
-            s[kb][r] = key > klim ? -INFINITY : s[kb][r];
+            const float e = fast_exp2(s[kb][r] - shift);
+            s[kb][r] = e;
+            ls[r & 3] = kb == 0 && r < 4 ? e : ls[r & 3] + e;
           }
+        return (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      };
+      f32x16 s[2];
+      float tsum = 0.0f;
+      bool redo = !have_ref;
+      if (have_ref) {
+        scores(s, negm);
+        tsum = exponentiate(s, 0.0f);
+        redo = __builtin_amdgcn_ballot_w64(!(lrun + tsum <= kSumLimit)) != 0;
       }
-      float mt = -INFINITY;
+      if (redo) {  // wave-uniform: first tile, or a sum past the limit
+        scores(s, zero);
+        float mt = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
-      mt = fmaxf(mt, other_half(mt));
-      const float mnew = fmaxf(mrun, mt);
-      if (__builtin_amdgcn_ballot_w64(mnew > mrun + thr) != 0) {
-        const float alpha = fast_exp2((mrun - mnew) * sc);  // 0 on the first tile
+          for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+        mt = fmaxf(mt, other_half(mt));
+        // the pair's sum so far in reference units: a shift by its
+        // exponent brings it back near 1 when no score of this tile does
+        const float ltot = lrun + other_half(lrun);
+        const float mnew = fmaxf(mt, mref + fmaxf(0.0f, __log2f(ltot)));
+        const float alpha = fast_exp2(mref - mnew);  // 0 while there is no reference
         lrun *= alpha;
 #pragma unroll
         for (int cb = 0; cb < DH / 32; ++cb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
-        mrun = mnew;
+        mref = mnew;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) negm[r] = -mnew;
+        have_ref = true;
+        tsum = exponentiate(s, mnew);
       }
-      const float mb = mrun * sc;
-      float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // four partial sums: no serial add chain
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = fast_exp2(fmaf(s[kb][r], sc, -mb));
-          s[kb][r] = e;
-          ls[r & 3] += e;
-        }
-      lrun += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      lrun += tsum;
       __builtin_amdgcn_s_setprio(1);
       // O^T += V^T P^T, 16 keys per MFMA
 #pragma unroll
@@ -276,7 +318,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
     for (int cb = 0; cb < DH / 32; ++cb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) orow[cb * 32 + acc_row(r, lane)] = from_f32<T>(oacc[cb][r] * inv);
-    if (g == 0) p.lse[(int64_t)bh * p.m + myq] = (mrun * sc + __log2f(ltot)) * 0.69314718055994531f;
+    if (g == 0) p.lse[(int64_t)bh * p.m + myq] = (mref + __log2f(ltot)) * 0.69314718055994531f;
   }
 }
 

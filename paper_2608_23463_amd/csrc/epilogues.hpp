@@ -83,6 +83,8 @@ struct EpiLinear {
 
 // Splits a [B*m, h*dh] projection into per-head tensors: row r = b*m + i,
 // column c = head*dh + e. `out` is [B, h, m, dh], `out_t` is [B, h, dh, ld_t].
+// Optionally also a scaled copy (v * scale) in the row layout, `outs`, with
+// its own low part `outs_lo` (the split of the scaled value).
 template <typename T>
 struct EpiHeads {
   T* out;
@@ -90,6 +92,9 @@ struct EpiHeads {
   const T* bias;
   int m, dh, n_heads, ld_t;
   T* out_lo;  // optional low part of the split, row layout
+  T* outs = nullptr;
+  T* outs_lo = nullptr;
+  float scale = 1.0f;
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     if (bias) v += to_f32(bias[c]);
     const T o = from_f32<T>(v);
@@ -99,6 +104,8 @@ struct EpiHeads {
     if (out) out[(bh * m + i) * dh + e] = o;
     if (out_t) out_t[(bh * dh + e) * ld_t + i] = o;
     if (out_lo) out_lo[(bh * m + i) * dh + e] = from_f32<T>(split_lo(v));
+    if (outs) outs[(bh * m + i) * dh + e] = from_f32<T>(v * scale);
+    if (outs_lo) outs_lo[(bh * m + i) * dh + e] = from_f32<T>(split_lo(v * scale));
   }
   struct Col {
     Raw8<T> b;
@@ -133,6 +140,16 @@ struct EpiHeads {
 #pragma unroll
       for (int e = 0; e < 8; ++e) t[e] = split_lo(v[e]);
       store8(out_lo + (bh * m + i) * dh + e0, t);
+    }
+    if (outs) {
+      float s[8], t[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        s[e] = v[e] * scale;
+        t[e] = split_lo(s[e]);
+      }
+      store8(outs + (bh * m + i) * dh + e0, s);
+      if (outs_lo) store8(outs_lo + (bh * m + i) * dh + e0, t);
     }
     if (out_t) {
 #pragma unroll

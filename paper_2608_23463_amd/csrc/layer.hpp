@@ -29,17 +29,19 @@ struct LayerDims {
   int esize;        // bytes per activation element
   int img_w, patch; // 2-D partition: image width and patch side (0 for sequences)
   int inject;       // pf_injection
+  bool split;       // bf16 low parts on the proxy path (PF_PRECISION_EXTENDED in bf16 mode)
   // the caller's token tensors go through workspace copies (padded or patch-ordered)
   bool staged() const { return L_in != L || img_w > 0; }
 };
 
 // Byte offsets of every activation inside the region that holds them
 // (the caller's `saved` buffer, or the workspace when saved is NULL).
-// In bf16 mode the proxy path upstream of the attention logits (Z_j, H, Q, K)
-// also keeps the low part of a two-term bf16 split (the *_lo buffers): a
-// proxy sums P * d_fine products, so its magnitude, and the logits', grow
-// with the compression fan-in, and one bf16 rounding there moves a sharp
-// softmax by several percent. In fp32 mode the *_lo buffers are empty.
+// With PF_PRECISION_EXTENDED in bf16 mode the proxy path upstream of the
+// attention logits (Z_j, H, Q, K) also keeps the low part of a two-term bf16
+// split (the *_lo buffers): a proxy sums P * d_fine products, so its
+// magnitude, and the logits', grow with the compression fan-in, and one bf16
+// rounding there moves a sharp softmax by several percent. In fp32 mode and
+// with PF_PRECISION_BF16 the *_lo buffers are empty.
 struct LayerActs {
   size_t z[PF_MAX_LEVELS];    // Z_j, j = 1..M-1: compression level outputs [B*R_j, d_j]
   size_t z_lo[PF_MAX_LEVELS];
@@ -47,6 +49,8 @@ struct LayerActs {
   size_t h_lo;
   size_t q, k, v;             // [B, h, m, dh]
   size_t q_lo, k_lo;
+  size_t qs, qs_lo;           // Q * log2(e)/sqrt(d_head) for the forward attention [B, h, m, dh]
+                              // (the same buffers as q, q_lo unless activations are saved)
   size_t qt, kt, vt;          // [B, h, dh, ld_t]
   size_t o;                   // [B*m, d_p]
   size_t lse;                 // [B, h, m] fp32

@@ -632,8 +632,8 @@ static void backward_impl(Runner& run, const LayerDims& d, const pf_layer_config
   AttnBwdParams ap{};
   ap.q = S(A.q);
   ap.k = S(A.k);
-  ap.q_lo = sizeof(T) == 2 ? S(A.q_lo) : nullptr;
-  ap.k_lo = sizeof(T) == 2 ? S(A.k_lo) : nullptr;
+  ap.q_lo = d.split ? S(A.q_lo) : nullptr;
+  ap.k_lo = d.split ? S(A.k_lo) : nullptr;
   ap.v = S(A.v);
   ap.qt = S(A.qt);
   ap.kt = S(A.kt);

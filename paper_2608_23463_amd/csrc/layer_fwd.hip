@@ -5,9 +5,10 @@
 //     Eq. 2 and the grouping of Eq. 16 are zero-copy views of row-major data,
 //     and the last level's epilogue adds b_c and H_in (Eq. 8) and writes H.
 //  2. Q, K, V projections of H, written per head (V key-contiguous). In bf16
-//     mode H, the level outputs Z_j, Q and K keep a bf16 low part as well
-//     (two-term split), and the GEMMs that read them multiply [hi | lo] by
-//     [W | W]: the attention logits then carry ~16 mantissa bits.
+//     mode with extended precision H, the level outputs Z_j, Q and K keep a
+//     bf16 low part as well (two-term split), and the GEMMs that read them
+//     multiply [hi | lo] by [W | W]: the attention logits then carry ~16
+//     mantissa bits.
 //  3. causal flash attention over the m proxies (Eq. 9).
 //  4. output map W_o -> contextualised proxies S.
 //  5. decompression, one GEMM per level from level M down to 1 (Eq. 10, 17),
@@ -163,6 +164,8 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   if (c->mask < PF_TOKEN_CAUSAL || c->mask > PF_BIDIRECTIONAL) return *why = "unknown mask mode", PF_ERR_INVALID_ARG;
   if (c->injection < PF_INJECT_GATED || c->injection > PF_INJECT_GATED_HEAD)
     return *why = "unknown injection mode", PF_ERR_INVALID_ARG;
+  if (c->precision != PF_PRECISION_EXTENDED && c->precision != PF_PRECISION_BF16)
+    return *why = "precision must be PF_PRECISION_EXTENDED or PF_PRECISION_BF16", PF_ERR_INVALID_ARG;
   if (c->batch < 1 || c->seq_len < 1) return *why = "batch and seq_len must be >= 1", PF_ERR_INVALID_ARG;
   if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
   if (c->d_fine < 1 || c->d_proxy < 1 || c->n_heads < 1 || c->head_dim < 1)
@@ -209,6 +212,7 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   if ((int64_t)d->B * d->L > INT32_MAX) return *why = "batch * seq_len exceeds 2^31 - 1 rows", PF_ERR_UNSUPPORTED;
   d->ld_t = (int)((d->m + 63) / 64 * 64);
   d->esize = c->dtype == PF_BF16 ? 2 : 4;
+  d->split = d->esize == 2 && c->precision == PF_PRECISION_EXTENDED;
   // the attention kernels address one head's tensors ([m, d_head] rows,
   // [d_head, ld_t] transposed) through 32-bit buffer offsets
   if ((int64_t)d->ld_t * c->head_dim * d->esize >= ((int64_t)1 << 31))
@@ -236,7 +240,7 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   };
   const size_t prox = (size_t)d.B * d.m * d.d_p * es;
   const size_t headt = (size_t)d.B * d.nh * d.dh * d.ld_t * es;
-  const bool split = d.esize == 2;
+  const bool split = d.split;
   for (int j = 1; j < d.M; ++j) {
     a.z[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
     a.z_lo[j] = take(split ? (size_t)d.B * d.R[j] * d.d[j] * es : 0);
@@ -247,6 +251,9 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   a.k = take(prox);
   a.q_lo = take(split ? prox : 0);
   a.k_lo = take(split ? prox : 0);
+  // the forward attention reads Q pre-scaled; the backward reads Q itself
+  a.qs = bwd ? take(prox) : a.q;
+  a.qs_lo = bwd ? take(split ? prox : 0) : a.q_lo;
   a.v = bwd ? take(prox) : 0;
   a.qt = bwd ? take(headt) : 0;
   a.kt = bwd ? take(headt) : 0;
@@ -359,7 +366,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   auto P = [&](size_t off) { return reinterpret_cast<T*>(act + off); };
   const int64_t rows_m = (int64_t)d.B * d.m;
 
-  const bool split = sizeof(T) == 2;
+  const bool split = d.split;
 
   // 1. compression cascade (Eq. 7, 16) and the residual proxy update (Eq. 8).
   //    Levels after the first read their input as [hi | lo] against [W | W].
@@ -416,9 +423,12 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     }
   }
   const pf_linear* proj[3] = {&w->q, &w->k, &w->v};
-  T* outs[3] = {P(A.q), P(A.k), saving ? P(A.v) : nullptr};
+  // Q goes to the attention pre-scaled by log2(e)/sqrt(d_head) (scores in
+  // exp2 units); the unscaled Q is kept only for the backward
+  const float qscale = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+  T* outs[3] = {saving ? P(A.q) : nullptr, P(A.k), saving ? P(A.v) : nullptr};
   T* outs_t[3] = {saving ? P(A.qt) : nullptr, saving ? P(A.kt) : nullptr, P(A.vt)};
-  T* outs_lo[3] = {split ? P(A.q_lo) : nullptr, split ? P(A.k_lo) : nullptr, nullptr};
+  T* outs_lo[3] = {split && saving ? P(A.q_lo) : nullptr, split ? P(A.k_lo) : nullptr, nullptr};
   for (int i = 0; i < 3; ++i) {
     GemmProblem pr{};
     pr.a = hbuf;
@@ -428,7 +438,7 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     pr.M = (int)rows_m;
     pr.N = d.d_p;
     pr.K = d.d_p;
-    if (outs_lo[i]) {
+    if (split && i < 2) {  // Q and K read H as [hi | lo]
       pr.a2 = P(A.h_lo);
       pr.lda2 = d.d_p;
       pr.a_ksplit = d.d_p;
@@ -439,14 +449,19 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     }
     EpiHeads<T> e{outs[i], outs_t[i], reinterpret_cast<const T*>(proj[i]->b), (int)d.m, d.dh, d.nh, d.ld_t,
                   outs_lo[i]};
+    if (i == 0) {
+      e.outs = P(A.qs);
+      e.outs_lo = split ? P(A.qs_lo) : nullptr;
+      e.scale = qscale;
+    }
     run.gemm<T, LAYOUT_K, LAYOUT_K>("qkv_gemm", pr, e);
   }
 
   // 3. attention over the proxies (Eq. 9)
   AttnParams ap{};
-  ap.q = P(A.q);
+  ap.q = P(A.qs);
   ap.k = P(A.k);
-  ap.q_lo = split ? P(A.q_lo) : nullptr;
+  ap.q_lo = split ? P(A.qs_lo) : nullptr;
   ap.k_lo = split ? P(A.k_lo) : nullptr;
   ap.vt = P(A.vt);
   ap.o = P(A.o);
@@ -455,7 +470,6 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   ap.n_heads = d.nh;
   ap.ld_t = d.ld_t;
   ap.causal = cfg->mask != PF_BIDIRECTIONAL;
-  ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   run.launch("attention_fwd", [&] { return launch_attention_fwd<T>(ap, d.B, d.dh, run.stream); });
 
   // 4. output map of the interaction; in token-causal mode its epilogue also

@@ -34,6 +34,11 @@ INJECT_ADD = 1    # Eq. 11
 INJECT_AFFINE = 2  # Eq. 13
 INJECT_GATED_HEAD = 3  # Eq. 12 with one gate per head (Eq. 20's per-head weighting)
 
+# arithmetic of the GPU's proxy path in bf16 mode (pf_precision of the C ABI);
+# not an input property, carried here so a shape names one complete call
+PRECISION_EXTENDED = 0
+PRECISION_BF16 = 1
+
 WEIGHT_STD = 0.02
 
 
@@ -53,6 +58,7 @@ class LayerShape:
     mask: int = TOKEN_CAUSAL
     injection: int = INJECT_GATED
     image_width: int = 0              # > 0: raster-order image, blocks are p x p patches (Sec. 3.9)
+    precision: int = PRECISION_EXTENDED
 
     @property
     def block(self) -> int:

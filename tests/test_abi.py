@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.proxy_version() == 100
+    assert lib.proxy_version() == 101
 
 
 def _cfg(**kw):
@@ -81,6 +81,7 @@ def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 
     (dict(n_heads=8), B.PF_ERR_INVALID_ARG),
     (dict(mask=5), B.PF_ERR_INVALID_ARG),
     (dict(injection=4), B.PF_ERR_INVALID_ARG),
+    (dict(precision=2), B.PF_ERR_INVALID_ARG),
     (dict(head_dim=32, n_heads=8), B.PF_ERR_UNSUPPORTED),
     (dict(d_fine=100), B.PF_ERR_UNSUPPORTED),
 ])
@@ -105,6 +106,17 @@ def test_forward_rejects_oversize_head_before_any_launch(lib):
     # one proxy fewer (2^23 - 64 tokens) fits
     ok = _cfg(seq_len=(1 << 23) - 64, d_fine=8, d_proxy=128, n_heads=1, head_dim=128, factors=(1,))
     assert B.layer_workspace_size(ok) > 0
+
+
+def test_plain_bf16_precision_drops_the_low_parts(lib):
+    # the low parts of H, Q and K (and the doubled K of the Q/K GEMMs) exist
+    # only with PF_PRECISION_EXTENDED in bf16 mode
+    ext, plain = _cfg(), _cfg(precision=B.PF_PRECISION_BF16)
+    m, dp = 4096 // 64, 256
+    assert B.layer_saved_size(ext) - B.layer_saved_size(plain) >= 3 * m * dp * 2
+    f32 = _cfg(dtype="fp32")
+    f32p = _cfg(dtype="fp32", precision=B.PF_PRECISION_BF16)
+    assert B.layer_saved_size(f32) == B.layer_saved_size(f32p)
 
 
 def test_partial_last_block_sizes(lib):

@@ -84,6 +84,10 @@ CASES = {
     # the language-model shape (64-wide local stream, 512-wide proxies, 8 x 64, P = 64) over
     # 10,240 tokens: 160 proxies, and enough token rows for the transposed weight-gradient path
     "bf16_lm_shape": (LayerShape(1, 64 * 160, 64, 512, 8, 64, (64,)), True),
+    # the same with plain bf16 H, Q, K (PF_PRECISION_BF16) and the drawn Q/K weights (with 4x
+    # sharpened logits plain bf16 puts dW_q at 2.2e-2: the extended precision is the default)
+    "bf16_lm_shape_plain": (LayerShape(1, 64 * 160, 64, 512, 8, 64, (64,), precision=synth.PRECISION_BF16), True,
+                            False),
     # residual-add injection (Eq. 11); level 1 groups pairs of 16,384 tokens, so its weight
     # gradients (8,192 rows) take the transposed path with column sums from the transpose
     "bf16_inject_add": (LayerShape(1, 16384, 128, 256, 4, 64, (2, 8), injection=synth.INJECT_ADD), True),

@@ -155,6 +155,28 @@ def test_forward_parity_L1M_sampled(gpu, name):
     assert_close(got, ref["x_out"], shape.dtype, f"{name} x_out (sampled blocks)")
 
 
+@pytest.mark.parametrize("name", ["layer_bf16_L64k_d1024", "layer_bf16_L1M_d1024", "layer_bf16_L1M_lm_df64_dp512"])
+def test_forward_parity_plain_bf16_precision(gpu, name):
+    """PF_PRECISION_BF16: H, Q and K as plain bf16 values (one score MFMA per
+    tile step). The 64K-token layer in full; the 1M-token layers on every
+    proxy and 64 sampled blocks."""
+    import dataclasses
+    shape = dataclasses.replace(synth.WORKLOADS[name], precision=synth.PRECISION_BF16)
+    print(f"[workload {name}, plain bf16] generating inputs", flush=True)
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
+    x_out, h_out = run_gpu(shape, inp)
+    m = shape.n_proxies
+    blocks = None
+    if shape.seq_len > 65536:
+        rng = np.random.default_rng(321)
+        blocks = sorted(set([0, 1, m - 2, m - 1] + list(rng.choice(np.arange(2, m - 2), 60, replace=False))))
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask,
+                               sample_blocks=blocks)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} plain bf16 h_out")
+    got = host(x_out) if blocks is None else host(x_out.reshape(1, m, shape.block, shape.d_fine)[:, blocks])
+    assert_close(got, ref["x_out"], shape.dtype, f"{name} plain bf16 x_out")
+
+
 def test_zero_decompression_is_identity_bitwise(gpu):
     shape = synth.WORKLOADS["layer_bf16_L64k_d1024"]
     inp = synth.layer_inputs(shape, 5)
