@@ -119,6 +119,10 @@ def layer_flops(shape):
         "o_gemm": 2 * B * m * dp * dp,
         "decompress_gemm": comp / len(shape.factors),
         "gate_gemm": 2 * B * L * df * 2 * df,
+        # PF_GATE_FUSED: D = S W_d[p]^T and G = S C[p]^T + X_p W_gx^T per token,
+        # after the fold C[p] = W_gd W_d[p] for the k_1 positions
+        "fused_gate": 2 * B * L * df * (2 * dims[1] + df),
+        "gate_fold_gemm": 2 * shape.factors[0] * df * df * dims[1],
     }
 
 
@@ -261,10 +265,21 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
                                        kernels=kernel_table(tr_p, flops, steps, False))
     del ws_p
     if headline:
+        # PF_GATE_FUSED: level-1 decompression, gate and residual in one kernel
+        # (Delta stays in registers) after the per-position weight fold
+        cfg_f = B.config_from_shape(shape)
+        cfg_f.gate_fusion = B.PF_GATE_FUSED
+        ws_f = torch.empty(B.layer_workspace_size(cfg_f), dtype=torch.uint8, device="cuda")
+        ms_f = time_calls(forward(cfg_f, workspace=ws_f), steps, warmup)
+        tr_f = trace_calls(forward(cfg_f, workspace=ws_f), steps)
+        variants["gate_fused"] = entry(ms_f, kernels=kernel_table(tr_f, flops, steps, False))
+        del ws_f
         # the same inputs with residual-add injection (Eq. 11): no gate GEMM
         cfg_add = B.config_from_shape(shape)
         cfg_add.injection = B.PF_INJECT_ADD
-        variants["inject_add"] = entry(time_calls(forward(cfg_add), steps, warmup))
+        ws_add = torch.empty(B.layer_workspace_size(cfg_add), dtype=torch.uint8, device="cuda")
+        variants["inject_add"] = entry(time_calls(forward(cfg_add, workspace=ws_add), steps, warmup))
+        del ws_add
         # affine modulation (Eq. 13): [S | T] GEMM (N = 2 d_fine, K = d_fine) instead of the gate
         cfg_aff = B.config_from_shape(shape)
         cfg_aff.injection = B.PF_INJECT_AFFINE

@@ -84,6 +84,20 @@ enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1, PF_INJECT_AFFINE = 2
  *   paper reports): the score product is one MFMA per tile step. */
 enum pf_precision { PF_PRECISION_EXTENDED = 0, PF_PRECISION_BF16 = 1 };
 
+/* Kernels of the level-1 decompression and the gated injection (Eq. 10 with
+ * Eq. 12), bf16 layers with PF_INJECT_GATED.
+ * PF_GATE_SEPARATE: the decompression GEMM writes Delta to the workspace and
+ *   the gate GEMM reads [X, Delta] back (default).
+ * PF_GATE_FUSED: one kernel per call forms Delta for a tile of tokens in
+ *   registers and applies the gate and the residual there (the gate weight is
+ *   folded into the decompression weight per block position once per call),
+ *   so Delta never reaches HBM in a forward without saved activations. It
+ *   moves less memory but keeps fewer matrix operations in flight per LDS
+ *   byte than the two GEMMs; it applies where d_fine is a multiple of 128,
+ *   d_1 a multiple of 64 and at least 128, and otherwise the separate
+ *   kernels run. Results agree with PF_GATE_SEPARATE to bf16 rounding. */
+enum pf_gate_fusion { PF_GATE_SEPARATE = 0, PF_GATE_FUSED = 1 };
+
 typedef struct {
   const void* w; /* [out, in] */
   const void* b; /* [out] or NULL */
@@ -104,7 +118,7 @@ typedef struct {
  *            ignored (d_M = d_proxy).
  *  head_dim  64 or 128.
  *  dtype     pf_dtype; mask pf_mask; injection pf_injection;
- *            precision pf_precision (bf16 mode).
+ *            precision pf_precision (bf16 mode); gate_fusion pf_gate_fusion.
  *  image_width  0: the tokens are a sequence and a block is P consecutive
  *            tokens. > 0: 2-D partition of the vision instantiation
  *            (Sec. 3.9): the tokens are a raster-order image of this width
@@ -124,6 +138,7 @@ typedef struct {
   int32_t injection;
   int32_t image_width;
   int32_t precision; /* pf_precision */
+  int32_t gate_fusion; /* pf_gate_fusion */
 } pf_layer_config;
 
 /* compress[j]: W [d_{j+1}, k_{j+1} d_j]  (Eq. 7, Eq. 16)
@@ -337,7 +352,7 @@ int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* str
 const char* proxy_last_error(void);
 
 /* Library ABI version (major * 100 + minor): 101 adds pf_layer_config.precision
- * and proxy_decode_step_static. */
+ * and proxy_decode_step_static; 102 adds pf_layer_config.gate_fusion. */
 int proxy_version(void);
 
 #ifdef __cplusplus

@@ -28,6 +28,8 @@ PF_INJECT_AFFINE = 2
 PF_INJECT_GATED_HEAD = 3
 PF_PRECISION_EXTENDED = 0
 PF_PRECISION_BF16 = 1
+PF_GATE_SEPARATE = 0
+PF_GATE_FUSED = 1
 
 EXPORTS = (
     "proxy_layer_workspace_size", "proxy_layer_saved_size", "proxy_layer_forward",
@@ -53,7 +55,7 @@ class PfLayerConfig(ctypes.Structure):
                 ("n_heads", c_int32), ("head_dim", c_int32), ("n_levels", c_int32),
                 ("factors", c_int32 * MAX_LEVELS), ("level_dims", c_int32 * MAX_LEVELS),
                 ("dtype", c_int32), ("mask", c_int32), ("injection", c_int32), ("image_width", c_int32),
-                ("precision", c_int32)]
+                ("precision", c_int32), ("gate_fusion", c_int32)]
 
 
 class PfLayerWeights(ctypes.Structure):
@@ -243,7 +245,8 @@ def _stream(stream) -> Optional[int]:
 
 def layer_config(batch: int, seq_len: int, d_fine: int, d_proxy: int, n_heads: int, head_dim: int,
                  factors: Sequence[int], level_dims: Sequence[int] = (), dtype: str = "bf16",
-                 mask: int = 0, injection: int = 0, image_width: int = 0, precision: int = 0) -> PfLayerConfig:
+                 mask: int = 0, injection: int = 0, image_width: int = 0, precision: int = 0,
+                 gate_fusion: int = 0) -> PfLayerConfig:
     c = PfLayerConfig()
     c.batch = batch
     c.seq_len = seq_len
@@ -261,6 +264,7 @@ def layer_config(batch: int, seq_len: int, d_fine: int, d_proxy: int, n_heads: i
     c.injection = injection
     c.image_width = image_width
     c.precision = precision
+    c.gate_fusion = gate_fusion
     return c
 
 
@@ -270,7 +274,7 @@ def config_from_shape(shape) -> PfLayerConfig:
     return layer_config(shape.batch, shape.seq_len, shape.d_fine, shape.d_proxy, shape.n_heads,
                         shape.head_dim, shape.factors, dims, shape.dtype, shape.mask,
                         getattr(shape, "injection", 0), getattr(shape, "image_width", 0),
-                        getattr(shape, "precision", 0))
+                        getattr(shape, "precision", 0), getattr(shape, "gate_fusion", 0))
 
 
 def _lin(pair) -> PfLinear:

@@ -50,7 +50,7 @@ static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 extern "C" {
 
-int proxy_version(void) { return 101; }
+int proxy_version(void) { return 102; }
 
 int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* stream) {
   if (!out) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_mfma: out is NULL");

@@ -269,6 +269,21 @@ struct EpiGate {
   }
 };
 
+// out[(z M + r) ldo + c] = acc for batch z = blockIdx.y of a batched GEMM:
+// the batches' [M, N] results stacked along rows.
+template <typename T>
+struct EpiStacked {
+  T* out;
+  int64_t ldo;
+  int M;
+  __device__ __forceinline__ void operator()(int r, int c, float v) const {
+    out[((int64_t)blockIdx.y * M + r) * ldo + c] = from_f32<T>(v);
+  }
+  __device__ __forceinline__ void vec8(int r, int c, const float* v) const {
+    store8(out + ((int64_t)blockIdx.y * M + r) * ldo + c, v);
+  }
+};
+
 // fp32 out[r, c] = acc + bias[c] (bias in the activation type, optional).
 template <typename T>
 struct EpiBiasF32 {

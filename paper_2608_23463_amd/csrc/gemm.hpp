@@ -52,6 +52,7 @@ struct GemmParams {
   int k_slice;         // reduction length per gridDim.z slice (multiple of BK)
   int tiles_m, tiles_n;
   int group_m;
+  int64_t batch_a, batch_b;  // element offsets of batch blockIdx.y in A and B (direct kernel)
 };
 
 template <typename T, int BM, int BN, int BK, int WM, int WN>
@@ -682,10 +683,13 @@ __global__ void __launch_bounds__(WM* WN* kWave)
   // each row. M/N-major: the tile is BK rows of the operand starting at row
   // k0, each read from column m0 (n0); only the rows below kend and the
   // columns below M (N) of the last row are in range.
-  const char* a1 = reinterpret_cast<const char*>(p.a) + (OA::kMN ? m0 * (int64_t)sizeof(T) : m0 * lda_b);
+  // batch blockIdx.y of a batched problem starts at its own A and B
+  const char* a1 = reinterpret_cast<const char*>(p.a) + (int64_t)blockIdx.y * p.batch_a * (int64_t)sizeof(T) +
+                   (OA::kMN ? m0 * (int64_t)sizeof(T) : m0 * lda_b);
   const char* a2 = p.a2 ? reinterpret_cast<const char*>(p.a2) + (OA::kMN ? m0 * (int64_t)sizeof(T) : m0 * lda_b)
                         : nullptr;
-  const char* b1 = reinterpret_cast<const char*>(p.b) + (OB::kMN ? n0 * (int64_t)sizeof(T) : n0 * ldb_b);
+  const char* b1 = reinterpret_cast<const char*>(p.b) + (int64_t)blockIdx.y * p.batch_b * (int64_t)sizeof(T) +
+                   (OB::kMN ? n0 * (int64_t)sizeof(T) : n0 * ldb_b);
   const char* b2 = p.b2 ? reinterpret_cast<const char*>(p.b2) + (OB::kMN ? n0 * (int64_t)sizeof(T) : n0 * ldb_b)
                         : nullptr;
   const uint32_t a_rows = (uint32_t)(max(0, min(BM, p.M - m0)) * lda_b);
@@ -927,6 +931,11 @@ struct GemmProblem {
   int64_t ldb2 = 0;
   int b_ksplit = 1 << 30;
   int M, N, K;
+  // batched problem (direct kernel only, A2/B2 unused): `batch` independent
+  // products, batch z reading A at z * batch_a and B at z * batch_b
+  // (elements); the epilogue finds z in blockIdx.y
+  int batch = 1;
+  int64_t batch_a = 0, batch_b = 0;
 };
 
 // Tile configuration chosen for a problem.
@@ -963,12 +972,12 @@ inline GemmPlan plan_gemm(const GemmProblem& pr, int num_cu) {
     pl.bm = pl.bn = 64;
     pl.bk = 64;
   }
-  const int64_t tiles = (int64_t)((pr.M + pl.bm - 1) / pl.bm) * ((pr.N + pl.bn - 1) / pl.bn);
+  const int64_t tiles = (int64_t)((pr.M + pl.bm - 1) / pl.bm) * ((pr.N + pl.bn - 1) / pl.bn) * pr.batch;
   const int kblocks = (pr.K + pl.bk - 1) / pl.bk;
   int splits = 1;
   // Deterministic split-K when the tile grid cannot fill the chip and the
   // reduction is long enough for each slice to stay efficient.
-  while (tiles * splits < num_cu && kblocks / (splits * 2) >= 8) splits *= 2;
+  while (pr.batch == 1 && tiles * splits < num_cu && kblocks / (splits * 2) >= 8) splits *= 2;
   const int kb_per = (kblocks + splits - 1) / splits;
   pl.k_slice = kb_per * pl.bk;
   pl.splits = (kblocks + kb_per - 1) / kb_per;
@@ -996,7 +1005,9 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   p.tiles_m = (pr.M + BM - 1) / BM;
   p.tiles_n = (pr.N + BN - 1) / BN;
   p.group_m = 8;
-  dim3 grid(p.tiles_m * p.tiles_n, 1, pl.splits);
+  p.batch_a = pr.batch_a;
+  p.batch_b = pr.batch_b;
+  dim3 grid(p.tiles_m * p.tiles_n, pr.batch, pl.splits);
   const bool aligned_split = (pr.a_ksplit >= pr.K || pr.a_ksplit % BK == 0) &&
                              (pr.b_ksplit >= pr.K || pr.b_ksplit % BK == 0) &&
                              (!pr.a2 || pr.lda2 == pr.lda) && (!pr.b2 || pr.ldb2 == pr.ldb);
@@ -1020,6 +1031,7 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
       return hipGetLastError();
     }
   }
+  if (pr.batch != 1) return hipErrorInvalidValue;  // batches run on the direct kernel only
   hipLaunchKernelGGL((gemm_kernel<T, BM, BN, BK, WM, WN, LA, LB, Epi>), grid,
                      dim3(WM * WN * kWave), 0, stream, p, epi);
   return hipGetLastError();

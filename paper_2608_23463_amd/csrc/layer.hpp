@@ -30,6 +30,7 @@ struct LayerDims {
   int img_w, patch; // 2-D partition: image width and patch side (0 for sequences)
   int inject;       // pf_injection
   bool split;       // bf16 low parts on the proxy path (PF_PRECISION_EXTENDED in bf16 mode)
+  bool fused_gate;  // level-1 decompression and the gate run as one kernel (bf16, gated injection)
   // the caller's token tensors go through workspace copies (padded or patch-ordered)
   bool staged() const { return L_in != L || img_w > 0; }
 };
@@ -56,7 +57,7 @@ struct LayerActs {
   size_t lse;                 // [B, h, m] fp32
   size_t s;                   // S [B*m, d_p]: the contextualised proxy each block receives
   size_t u[PF_MAX_LEVELS];    // U_j, j = 1..M-1: decompression level outputs [B*R_j, d_j]
-  size_t delta;               // [B*L, d_f]
+  size_t delta;               // [B*L, d_f] (absent for residual addition, and in a forward with the fused gate)
   size_t g;                   // gate pre-activation G, or s of Eq. 13 [B*L, d_f]
   size_t rstd;                // Eq. 13: 1 / RMS of every X row, fp32 [B*L]
   size_t gh;                  // per-head gate pre-activation, fp32 [B*L, n_heads]
@@ -65,6 +66,7 @@ struct LayerActs {
 };
 
 struct LayerWs {
+  size_t gate_c, gate_b;     // fused gate: C [k_1 d_f, d_1] and b' [k_1, d_f] fp32
   size_t acts;      // forward activations when saved == NULL
   size_t gemm;      // split-K partials
   // backward scratch

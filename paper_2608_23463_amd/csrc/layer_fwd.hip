@@ -20,6 +20,7 @@
 
 #include "attention.hpp"
 #include "epilogues.hpp"
+#include "fused_gate.hpp"
 #include "layer.hpp"
 #include "runner.hpp"
 
@@ -36,6 +37,16 @@ hipError_t fill_zero(void* p, size_t bytes, hipStream_t stream) {
   const int blocks = (int)std::min<size_t>((n16 + 255) / 256, 4096);
   hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, reinterpret_cast<u32x4*>(p), n16);
   return hipGetLastError();
+}
+
+// b'[p][n] = b_g[n] (or 0) for every position p: the fused gate's bias when
+// the decompression has no bias.
+template <typename T>
+__global__ void __launch_bounds__(256) gate_bias_broadcast_kernel(const T* __restrict__ bg, float* __restrict__ out,
+                                                                   int k, int n) {
+  const int64_t total = (int64_t)k * n;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256)
+    out[i] = bg ? to_f32(bg[i % n]) : 0.0f;
 }
 
 __global__ void pad_rows_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst, int64_t L_in,
@@ -166,6 +177,8 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
     return *why = "unknown injection mode", PF_ERR_INVALID_ARG;
   if (c->precision != PF_PRECISION_EXTENDED && c->precision != PF_PRECISION_BF16)
     return *why = "precision must be PF_PRECISION_EXTENDED or PF_PRECISION_BF16", PF_ERR_INVALID_ARG;
+  if (c->gate_fusion != PF_GATE_SEPARATE && c->gate_fusion != PF_GATE_FUSED)
+    return *why = "gate_fusion must be PF_GATE_SEPARATE or PF_GATE_FUSED", PF_ERR_INVALID_ARG;
   if (c->batch < 1 || c->seq_len < 1) return *why = "batch and seq_len must be >= 1", PF_ERR_INVALID_ARG;
   if (c->n_levels < 1 || c->n_levels > PF_MAX_LEVELS) return *why = "n_levels must be in 1..4", PF_ERR_INVALID_ARG;
   if (c->d_fine < 1 || c->d_proxy < 1 || c->n_heads < 1 || c->head_dim < 1)
@@ -213,6 +226,7 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   d->ld_t = (int)((d->m + 63) / 64 * 64);
   d->esize = c->dtype == PF_BF16 ? 2 : 4;
   d->split = d->esize == 2 && c->precision == PF_PRECISION_EXTENDED;
+  d->fused_gate = false;  // set below once the level widths are known
   // the attention kernels address one head's tensors ([m, d_head] rows,
   // [d_head, ld_t] transposed) through 32-bit buffer offsets
   if ((int64_t)d->ld_t * c->head_dim * d->esize >= ((int64_t)1 << 31))
@@ -222,6 +236,8 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
   for (int j = 0; j < d->M; ++j)
     if ((int64_t)d->k[j] * d->d[j] > INT32_MAX / 2) return *why = "k_j * d_j too large", PF_ERR_UNSUPPORTED;
   if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
+  d->fused_gate = c->gate_fusion == PF_GATE_FUSED && d->esize == 2 && c->injection == PF_INJECT_GATED &&
+                  fused_gate_supported(d->d_f, d->d[1]);
   if (c->injection == PF_INJECT_GATED_HEAD && (d->d_f % d->nh != 0 || (d->d_f / d->nh) % 8 != 0))
     return *why = "the per-head gate needs d_fine / n_heads to be a multiple of 8", PF_ERR_UNSUPPORTED;
   if (c->injection == PF_INJECT_GATED_HEAD && (d->d_f > 4096 || d->nh > 64))
@@ -262,7 +278,11 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   a.lse = take((size_t)d.B * d.nh * d.m * 4);
   a.s = take(prox);
   for (int j = 1; j < d.M; ++j) a.u[j] = take((size_t)d.B * d.R[j] * d.d[j] * es);
-  a.delta = take((size_t)d.B * d.L * d.d_f * es);
+  // Delta is materialised for the injections that read it after the
+  // decompression, and for the backward; residual addition writes Y from the
+  // decompression's epilogue, and the fused gate keeps Delta in registers
+  const bool need_delta = d.inject != PF_INJECT_ADD && (bwd || !d.fused_gate);
+  a.delta = take(need_delta ? (size_t)d.B * d.L * d.d_f * es : 0);
   a.g = bwd && (d.inject == PF_INJECT_GATED || d.inject == PF_INJECT_AFFINE) ? take((size_t)d.B * d.L * d.d_f * es)
                                                                                : 0;
   const bool affine = d.inject == PF_INJECT_AFFINE;
@@ -287,6 +307,8 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
   const size_t tok = (size_t)d.B * d.L * d.d_f * es;
   if (!bwd) {
     w.acts = take(layer_acts(d, false).bytes);
+    w.gate_c = take(d.fused_gate ? (size_t)d.k[0] * d.d_f * d.d[1] * es : 0);
+    w.gate_b = take(d.fused_gate ? (size_t)d.k[0] * d.d_f * 4 : 0);
   } else {
     const size_t prox32 = (size_t)d.B * d.m * d.d_p * 4;
     w.dg = take(tok);
@@ -361,7 +383,8 @@ LayerWs layer_ws(const LayerDims& d, bool bwd) {
 
 template <typename T>
 static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config* cfg, const pf_layer_weights* w,
-                         const void* x, const void* h_in, void* x_out, void* h_out, char* act, bool saving) {
+                         const void* x, const void* h_in, void* x_out, void* h_out, char* act, bool saving,
+                         char* ws) {
   const LayerActs A = layer_acts(d, saving);
   auto P = [&](size_t off) { return reinterpret_cast<T*>(act + off); };
   const int64_t rows_m = (int64_t)d.B * d.m;
@@ -495,7 +518,8 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   // injection (Eq. 11) the last level's epilogue adds X and writes Y itself:
   // its [B R_1, k_1 d_fine] output is X_out byte for byte.
   const bool add_inject = cfg->injection == PF_INJECT_ADD;
-  for (int j = d.M - 1; j >= 0; --j) {
+  const bool fuse = d.fused_gate;
+  for (int j = d.M - 1; j >= (fuse ? 1 : 0); --j) {  // a fused level 1 runs with the gate below
     GemmProblem pr{};
     pr.a = j == d.M - 1 ? P(A.s) : P(A.u[j + 1]);
     pr.lda = d.d[j + 1];
@@ -573,6 +597,73 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
     return;
   }
 
+  // 5+6. level-1 decompression fused with the gated injection (Eq. 10, 12):
+  //    C[p] = W_gd W_d1[p] and b'[p] = b_g + W_gd b_d1[p] for every position
+  //    p < k_1, then one kernel forms Delta and G per tile and writes Y
+  if constexpr (sizeof(T) == 2) {
+    if (fuse) {
+      const LayerWs W = layer_ws_layout(d, false);
+      const int k1 = d.k[0], d1 = d.d[1];
+      const T* wg = reinterpret_cast<const T*>(w->gate.w);
+      T* cmat = reinterpret_cast<T*>(ws ? ws + W.gate_c : nullptr);
+      float* bprime = reinterpret_cast<float*>(ws ? ws + W.gate_b : nullptr);
+      {
+        GemmProblem pc{};
+        pc.a = wg ? wg + d.d_f : nullptr;  // W_gd: columns d_f .. 2 d_f of W_g
+        pc.lda = 2 * d.d_f;
+        pc.b = w->decompress[0].w;  // W_d1[p] read [c][n] (contiguous along n)
+        pc.ldb = d1;
+        pc.M = d.d_f;
+        pc.N = d1;
+        pc.K = d.d_f;
+        pc.batch = k1;
+        pc.batch_b = (int64_t)d.d_f * d1;
+        run.gemm<T, LAYOUT_K, LAYOUT_MN>("gate_fold_gemm", pc, EpiStacked<T>{cmat, d1, d.d_f});
+      }
+      const T* bg = reinterpret_cast<const T*>(w->gate.b);
+      const bool have_bd = w->decompress[0].b != nullptr;
+      if (have_bd || run.dry) {  // the sizing run plans this GEMM whatever the bias
+        GemmProblem pb{};
+        pb.a = w->decompress[0].b;  // b_d1 viewed [k_1, d_f]
+        pb.lda = d.d_f;
+        pb.b = wg ? wg + d.d_f : nullptr;
+        pb.ldb = 2 * d.d_f;
+        pb.M = k1;
+        pb.N = d.d_f;
+        pb.K = d.d_f;
+        run.gemm<T, LAYOUT_K, LAYOUT_K>("gate_fold_bias_gemm", pb, EpiBiasF32<T>{bprime, d.d_f, bg});
+      }
+      if (!have_bd) {
+        run.launch("gate_fold_bias", [&] {
+          const int64_t total = (int64_t)k1 * d.d_f;
+          hipLaunchKernelGGL((gate_bias_broadcast_kernel<T>), dim3((unsigned)std::min<int64_t>((total + 255) / 256, 1024)),
+                             dim3(256), 0, run.stream, bg, bprime, k1, d.d_f);
+          return hipGetLastError();
+        });
+      }
+      FusedGateParams fp{};
+      fp.s = reinterpret_cast<const bf16*>(d.M == 1 ? P(A.s) : P(A.u[1]));
+      fp.x = reinterpret_cast<const bf16*>(x);
+      fp.wc = reinterpret_cast<const bf16*>(cmat);
+      fp.wd = reinterpret_cast<const bf16*>(w->decompress[0].w);
+      fp.wg = reinterpret_cast<const bf16*>(wg);
+      fp.bias_g = bprime;
+      fp.bias_d = reinterpret_cast<const bf16*>(w->decompress[0].b);
+      fp.y = reinterpret_cast<bf16*>(x_out);
+      fp.delta_out = saving ? reinterpret_cast<bf16*>(P(A.delta)) : nullptr;
+      fp.g_out = saving ? reinterpret_cast<bf16*>(P(A.g)) : nullptr;
+      fp.M = (int)(d.B * d.R[1]);
+      fp.k = k1;
+      fp.N = d.d_f;
+      fp.Ks = d1;
+      fp.lda_s = d1;
+      fp.lda_x = (int64_t)k1 * d.d_f;
+      fp.ldb_g = 2 * (int64_t)d.d_f;
+      run.launch("fused_gate", [&] { return launch_fused_gate(fp, run.stream); });
+      return;
+    }
+  }
+
   // 6. gated injection (Eq. 12)
   if (!add_inject) {
     GemmProblem pr{};
@@ -598,7 +689,7 @@ hipError_t layer_forward_run(const LayerDims& d, const pf_layer_config* cfg, con
                              char* ws, hipStream_t stream) {
   const LayerWs W = layer_ws(d, false);
   Runner run(false, stream, reinterpret_cast<float*>(ws + W.gemm));
-  forward_impl<T>(run, d, cfg, w, x, h_in, x_out, h_out, acts, saving);
+  forward_impl<T>(run, d, cfg, w, x, h_in, x_out, h_out, acts, saving, ws);
   return run.err;
 }
 
@@ -609,9 +700,9 @@ size_t layer_forward_gemm_ws(const LayerDims& d) {
   pf_layer_weights w{};
   Runner run(true);
   if (d.esize == 2)
-    forward_impl<bf16>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, true);
+    forward_impl<bf16>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, true, nullptr);
   else
-    forward_impl<float>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, true);
+    forward_impl<float>(run, d, &cfg, &w, nullptr, nullptr, nullptr, nullptr, nullptr, true, nullptr);
   return run.gemm_need;
 }
 

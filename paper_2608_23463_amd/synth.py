@@ -38,6 +38,10 @@ INJECT_GATED_HEAD = 3  # Eq. 12 with one gate per head (Eq. 20's per-head weight
 # not an input property, carried here so a shape names one complete call
 PRECISION_EXTENDED = 0
 PRECISION_BF16 = 1
+# kernels of the level-1 decompression and the gated injection (pf_gate_fusion):
+# also a property of the call, not of the inputs
+GATE_SEPARATE = 0
+GATE_FUSED = 1
 
 WEIGHT_STD = 0.02
 
@@ -59,6 +63,7 @@ class LayerShape:
     injection: int = INJECT_GATED
     image_width: int = 0              # > 0: raster-order image, blocks are p x p patches (Sec. 3.9)
     precision: int = PRECISION_EXTENDED
+    gate_fusion: int = GATE_SEPARATE
 
     @property
     def block(self) -> int:

@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.proxy_version() == 101
+    assert lib.proxy_version() == 102
 
 
 def _cfg(**kw):
@@ -82,6 +82,7 @@ def _fwd(lib, cfg, w, x=2 << 32, xo=3 << 32, ho=4 << 32, ws=5 << 32, ws_bytes=1 
     (dict(mask=5), B.PF_ERR_INVALID_ARG),
     (dict(injection=4), B.PF_ERR_INVALID_ARG),
     (dict(precision=2), B.PF_ERR_INVALID_ARG),
+    (dict(gate_fusion=2), B.PF_ERR_INVALID_ARG),
     (dict(head_dim=32, n_heads=8), B.PF_ERR_UNSUPPORTED),
     (dict(d_fine=100), B.PF_ERR_UNSUPPORTED),
 ])
@@ -117,6 +118,20 @@ def test_plain_bf16_precision_drops_the_low_parts(lib):
     f32 = _cfg(dtype="fp32")
     f32p = _cfg(dtype="fp32", precision=B.PF_PRECISION_BF16)
     assert B.layer_saved_size(f32) == B.layer_saved_size(f32p)
+
+
+def test_gate_fusion_workspace(lib):
+    # fused (bf16, gated, d_fine a multiple of 128): the forward workspace
+    # holds the folded weight C[p] and bias b'[p] per block position instead
+    # of Delta; where the fused kernel does not apply the option changes nothing
+    L, P, df, d1 = 1 << 16, 64, 256, 256
+    sep, fus = _cfg(seq_len=L), _cfg(seq_len=L, gate_fusion=B.PF_GATE_FUSED)
+    delta, fold = L * df * 2, P * df * d1 * 2 + P * df * 4
+    assert B.layer_workspace_size(sep) - B.layer_workspace_size(fus) >= delta - fold - 4096
+    assert B.layer_workspace_size(sep) - B.layer_workspace_size(fus) <= delta - fold + 4096
+    for kw in (dict(dtype="fp32"), dict(d_fine=192), dict(injection=B.PF_INJECT_ADD)):
+        assert B.layer_workspace_size(_cfg(seq_len=L, **kw)) == \
+            B.layer_workspace_size(_cfg(seq_len=L, gate_fusion=B.PF_GATE_FUSED, **kw)), kw
 
 
 def test_partial_last_block_sizes(lib):

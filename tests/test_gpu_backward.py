@@ -110,6 +110,8 @@ CASES = {
                                         injection=synth.INJECT_GATED_HEAD), False),
     "bf16_gated_head_wide": (LayerShape(1, 16 * 24, 3072, 256, 4, 64, (16,), injection=synth.INJECT_GATED_HEAD),
                              False, False),
+    # the fused decompression + gate forward (d_fine 256) writes the saved Delta and G
+    "bf16_fused_gate": (LayerShape(1, 16 * 130, 256, 256, 4, 64, (16,), gate_fusion=synth.GATE_FUSED), True),
     # partial last block (L % P != 0): zero-padded inside the library, dY = 0 on the padding
     "bf16_tc_partial_block": (LayerShape(2, 16 * 37 + 9, 192, 192, 3, 64, (16,)), True),
     "fp32_bi_partial_block_factorised": (LayerShape(1, 8 * 37 + 5, 64, 128, 2, 64, (2, 4), level_dims=(96,),

@@ -52,6 +52,13 @@ SMALL = {
     "fp32_partial_block_factorised_bi": (LayerShape(1, 8 * 40 + 3, 64, 128, 1, 128, (2, 4), level_dims=(48,),
                                                     dtype="fp32", mask=synth.BIDIRECTIONAL), False),
     "bf16_shorter_than_one_block": (LayerShape(1, 40, 128, 128, 2, 64, (64,), mask=synth.BLOCK_CAUSAL), True),
+    # the fused decompression + gate kernel (bf16, gated, d_fine a multiple of 128, level-1
+    # input width a multiple of 64): 74 ragged rows of 16 positions; a factorised cascade
+    # whose level 1 (k_1 = 4, d_1 = 128) runs fused after two unfused levels
+    "bf16_fused_gate_ragged_tc": (LayerShape(2, 37 * 16, 256, 192, 3, 64, (16,), gate_fusion=synth.GATE_FUSED),
+                                  True),
+    "bf16_fused_gate_factorised_bi": (LayerShape(1, 64 * 70, 128, 256, 2, 128, (4, 2, 8), level_dims=(128, 192),
+                                                 mask=synth.BIDIRECTIONAL, gate_fusion=synth.GATE_FUSED), True),
 }
 
 
@@ -82,6 +89,49 @@ def test_forward_parity_small(gpu, name):
                                injection=shape.injection)
     assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
     assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+
+
+BIASED = {
+    # fused gate (d_fine 256) and unfused (d_fine 192; fp32) with every bias drawn
+    "bf16_fused_gate": LayerShape(2, 29 * 16, 256, 128, 2, 64, (16,), gate_fusion=synth.GATE_FUSED),
+    "bf16_fused_gate_factorised": LayerShape(1, 40 * 8, 128, 128, 2, 64, (2, 4), level_dims=(128,),
+                                             gate_fusion=synth.GATE_FUSED),
+    "bf16_separate_gate": LayerShape(2, 29 * 16, 256, 128, 2, 64, (16,)),
+    "bf16_unfused": LayerShape(2, 29 * 16, 192, 128, 2, 64, (16,)),
+    "fp32_unfused": LayerShape(1, 29 * 16, 128, 128, 2, 64, (16,), dtype="fp32"),
+}
+
+
+def draw_biases(shape, inp, seed):
+    """Non-zero biases (std 0.5) in every linear map (the workloads' are zero)
+    and W_o scaled by 8 (exact in bf16), so the injected signal X_out - X is
+    as large as X and a dropped decompression or gate bias moves it by a few
+    percent."""
+    rng = np.random.default_rng(seed)
+    w = inp["weights"]
+    w["o"] = (w["o"][0] * np.float32(8), w["o"][1])
+
+    def b(n):
+        v = (rng.standard_normal(n) * 0.5).astype(np.float32)
+        return synth.bf16_round(v) if shape.dtype == "bf16" else v
+    for key in ("compress", "decompress"):
+        w[key] = [(wm, b(wm.shape[0])) for wm, _ in w[key]]
+    for key in ("q", "k", "v", "o", "gate"):
+        w[key] = (w[key][0], b(w[key][0].shape[0]))
+
+
+@pytest.mark.parametrize("name", list(BIASED))
+def test_forward_parity_with_biases(gpu, name):
+    shape = BIASED[name]
+    print(f"[case {name}, biases drawn] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, zlib.crc32(name.encode()) % 1000, with_h_in=True)
+    draw_biases(shape, inp, 17)
+    x_out, h_out = run_gpu(shape, inp)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask, inp["h_in"])
+    x = inp["x"].astype(np.float64)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} x_out")
+    assert_close(host(x_out) - x, ref["x_out"] - x, shape.dtype, f"{name} x_out - x")
 
 
 # Four sequences x 16 heads over 1,000-1,024 proxies (a grid of 512
@@ -175,6 +225,27 @@ def test_forward_parity_plain_bf16_precision(gpu, name):
     assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} plain bf16 h_out")
     got = host(x_out) if blocks is None else host(x_out.reshape(1, m, shape.block, shape.d_fine)[:, blocks])
     assert_close(got, ref["x_out"], shape.dtype, f"{name} plain bf16 x_out")
+
+
+@pytest.mark.parametrize("name", ["layer_bf16_L64k_d1024", "layer_bf16_L1M_d1024"])
+def test_forward_parity_fused_gate(gpu, name):
+    """PF_GATE_FUSED at the workload widths (d_fine 1024, P = 64): the 64K-token
+    layer in full, the 1M-token layer on every proxy and 64 sampled blocks."""
+    import dataclasses
+    shape = dataclasses.replace(synth.WORKLOADS[name], gate_fusion=synth.GATE_FUSED)
+    print(f"[workload {name}, fused gate] generating inputs", flush=True)
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
+    x_out, h_out = run_gpu(shape, inp)
+    m = shape.n_proxies
+    blocks = None
+    if shape.seq_len > 65536:
+        rng = np.random.default_rng(654)
+        blocks = sorted(set([0, 1, m - 2, m - 1] + list(rng.choice(np.arange(2, m - 2), 60, replace=False))))
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask,
+                               sample_blocks=blocks)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"{name} fused gate h_out")
+    got = host(x_out) if blocks is None else host(x_out.reshape(1, m, shape.block, shape.d_fine)[:, blocks])
+    assert_close(got, ref["x_out"], shape.dtype, f"{name} fused gate x_out")
 
 
 def test_zero_decompression_is_identity_bitwise(gpu):
