@@ -59,6 +59,10 @@ __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff) {
 __device__ __forceinline__ void buf_ld16_lds(rsrc_t r, uint32_t voff, void* lds_base) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, 0, 0, 0);
 }
+// The same with a wave-uniform byte offset soff added to every lane's address.
+__device__ __forceinline__ void buf_ld16_lds_so(rsrc_t r, uint32_t voff, uint32_t soff, void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0, 0);
+}
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
 // expcnt in 6:4, lgkmcnt in 11:8); a field at its maximum does not wait.
 // Issued through the builtin so the compiler's own wait insertion knows

@@ -634,8 +634,11 @@ __device__ __forceinline__ void wait_stages(int pending) {
   }
 }
 
+// FAST (K-major operands whose slices hold whole BK tiles): the buffer
+// descriptors of A, A2, B and B2 are built once per workgroup, their ranges
+// clamp the tile rows, and a K step only moves the scalar offset of the loads.
 template <typename T, int BM, int BN, int BK, int WM, int WN, int NS, class Epi, int LA = LAYOUT_K,
-          int LB = LAYOUT_K>
+          int LB = LAYOUT_K, bool FAST = false>
 __global__ void __launch_bounds__(WM* WN* kWave)
     __attribute__((amdgpu_waves_per_eu(WM* WN / 4, (BM >= 256 ? 1 : 2) * WM * WN / 4)))
     gemm_direct_kernel(const GemmParams p, const Epi epi) {
@@ -738,7 +741,27 @@ __global__ void __launch_bounds__(WM* WN* kWave)
         }
     }
   };
-  auto issue = [&](int k0, int stage) { issue_range(k0, stage, 0, D::kLoads); };
+  static_assert(!FAST || (!OA::kMN && !OB::kMN), "the fixed-descriptor loads take K-major operands");
+  const rsrc_t rsa1 = make_rsrc_uniform(a1, a_rows), rsb1 = make_rsrc_uniform(b1, b_rows);
+  const rsrc_t rsa2 = make_rsrc_uniform(a2 ? a2 : a1, a2 ? a_rows : 0u);
+  const rsrc_t rsb2 = make_rsrc_uniform(b2 ? b2 : b1, b2 ? b_rows : 0u);
+  auto issue = [&](int k0, int stage) {
+    if constexpr (FAST) {
+      // within a row: k0 + BK <= K, so a lane's offset stays inside its row
+      T* st = smem + stage * D::kStage;
+      const bool sa = k0 >= p.a_ksplit, sb = k0 >= p.b_ksplit;
+      const uint32_t soa = __builtin_amdgcn_readfirstlane((uint32_t)((sa ? k0 - p.a_ksplit : k0) * (int)sizeof(T)));
+      const uint32_t sob = __builtin_amdgcn_readfirstlane((uint32_t)((sb ? k0 - p.b_ksplit : k0) * (int)sizeof(T)));
+#pragma unroll
+      for (int i = 0; i < OA::kInsts; ++i)
+        buf_ld16_lds_so(sa ? rsa2 : rsa1, voa[i], soa, st + (wave * OA::kInsts + i) * 1024 / (int)sizeof(T));
+#pragma unroll
+      for (int i = 0; i < OB::kInsts; ++i)
+        buf_ld16_lds_so(sb ? rsb2 : rsb1, vob[i], sob, st + OA::kElems + (wave * OB::kInsts + i) * 1024 / (int)sizeof(T));
+    } else {
+      issue_range(k0, stage, 0, D::kLoads);
+    }
+  };
 
   f32x16 acc[S::kFM][S::kFN];
 #pragma unroll
@@ -829,9 +852,9 @@ __global__ void __launch_bounds__(WM* WN* kWave)
   // Ring of NS stages, tile t in stage t % NS. The hand-off to tile kt+1
   // happens before the last k-step of tile kt, whose fragments are already
   // in registers: after the barrier the first fragments of tile kt+1 are
-  // requested and the refill of stage kt % NS (tile kt+NS) is issued, and
-  // the last MFMAs of tile kt then run while both are in flight, so the
-  // matrix pipe does not drain at tile boundaries.
+  // requested, the last MFMAs of tile kt are queued, and the refill of stage
+  // kt % NS (tile kt+NS) is issued while they execute, so the matrix pipe
+  // does not drain at tile boundaries.
   if (nk > 0) {
 #pragma unroll
     for (int s0 = 0; s0 < NS; ++s0)
@@ -857,9 +880,9 @@ __global__ void __launch_bounds__(WM* WN* kWave)
       wait_stages<D::kLoads, NS - 2>(min(NS - 2, nk - 2 - kt));
       lds_barrier();  // tile kt+1 is in LDS; every wave is done reading tile kt
       read_frags(kt + 1, 0, 0);
-      if (kt + NS < nk) issue(kbeg + (kt + NS) * BK, kt % NS);
     }
     mfmas(1);
+    if (kt + NS < nk) issue(kbeg + (kt + NS) * BK, kt % NS);  // after the hand-off above
   }
   // Every direct load has landed (the last wait_stages drained them all).
   // The stage that held tile nk-2 is free on every wave: nothing reads it
@@ -1016,8 +1039,12 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   constexpr int DWN = (BM == 256 && BN == 256) ? 4 : WN;
   if constexpr (LA == LAYOUT_K && LB == LAYOUT_K) {
     if (aligned_split && pl.k_slice % BK == 0) {
-      hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, DWN, 2, Epi>), grid, dim3(WM * DWN * kWave), 0,
-                         stream, p, epi);
+      if (pr.K % BK == 0)  // every slice holds whole tiles
+        hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, DWN, 2, Epi, LAYOUT_K, LAYOUT_K, true>), grid,
+                           dim3(WM * DWN * kWave), 0, stream, p, epi);
+      else
+        hipLaunchKernelGGL((gemm_direct_kernel<T, BM, BN, BK, WM, DWN, 2, Epi>), grid, dim3(WM * DWN * kWave), 0,
+                           stream, p, epi);
       return hipGetLastError();
     }
   } else if constexpr (sizeof(T) == 2 && BM >= 128 && BN >= 128) {
