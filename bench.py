@@ -565,7 +565,8 @@ def cpu_baseline(shape, sample):
 
 def pmc_pass():
     """Minimal dispatch sequence for hardware-counter runs: two layer forwards
-    on the 1M-token shape and two decode steps at the decode workload's shape
+    on the 1M-token shape, one more with the fused decompression + gate kernel,
+    and two decode steps at the decode workload's shape
     (random device data; traffic does not depend on the values), then one
     plain 1 GiB device-to-device copy whose FETCH_SIZE and WRITE_SIZE
     calibrate the counters (it must read and write 1 GiB)."""
@@ -595,6 +596,13 @@ def pmc_pass():
     for _ in range(2):
         B.layer_forward_raw(cfg, wst, x, None, x_out, h_out, None, ws)
         torch.cuda.synchronize()
+    del ws
+    # one forward through the fused decompression + gate kernel
+    cfg_f = B.config_from_shape(shape)
+    cfg_f.gate_fusion = B.PF_GATE_FUSED
+    ws = torch.empty(B.layer_workspace_size(cfg_f), dtype=torch.uint8, device="cuda")
+    B.layer_forward_raw(cfg_f, wst, x, None, x_out, h_out, None, ws)
+    torch.cuda.synchronize()
     del x, x_out, h_out, ws, w, wst
     torch.cuda.empty_cache()
     # two decode steps at the decode workload's shape (random device data)
@@ -624,7 +632,7 @@ def pmc_pass():
     torch.cuda.synchronize()
     b.copy_(a)
     torch.cuda.synchronize()
-    print("pmc pass done: 2 forwards, 2 decode steps, 1 GiB copy", flush=True)
+    print("pmc pass done: 2 forwards, 1 fused-gate forward, 2 decode steps, 1 GiB copy", flush=True)
 
 
 def main():

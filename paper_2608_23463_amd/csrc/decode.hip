@@ -317,37 +317,51 @@ struct DecodeAttnParams {
   DecodePos pos;       // per-sequence n and j when pos.ragged
 };
 
-// A[b, h, c] = A_x + alpha * A_h from the partials: cache slices merged in a
-// fixed order (A_h, zero without cached rows), local slice normalised (A_x).
-// A[b, h, c] = A_x + alpha * A_h from the partials: cache slices merged in a
-// fixed order with a running maximum (A_h, zero without cached rows), local
-// slice normalised (A_x). Loads go out eight slices at a time.
+// A[b, h, c] = A_x + alpha * A_h from the partials of one (sequence, head):
+// cache slices merged in a fixed order with a running maximum (A_h, zero
+// without cached rows), local slice normalised (A_x). A lane takes channels
+// c0, c0 + 64, ... (kC of them); the loads of up to kBatch slices, the local
+// part and alpha go out together before any is used, so a step with up to
+// kBatch slices waits for memory once.
 template <typename T, int DH>
-__device__ __forceinline__ void combine_partials(const DecodeAttnParams& p, int bh, int b, int h, int c) {
+__device__ __forceinline__ void combine_partials(const DecodeAttnParams& p, int bh, int b, int h, int c0) {
+  constexpr int kC = DH / 64, kBatch = 32;
   const int64_t base = (int64_t)bh * (p.splits + 1);
-  float mrun = -INFINITY, lrun = 0.0f, arun = 0.0f;
-  for (int s0 = 0; s0 < p.splits; s0 += 8) {
-    float m[8], l[8], a[8];
+  const float al = p.alpha[(int64_t)b * p.nh + h];
+  const float lx = p.part_l[base + p.splits];
+  float ax[kC];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+  for (int u = 0; u < kC; ++u) ax[u] = p.part_acc[(base + p.splits) * DH + c0 + 64 * u];
+  float mrun = -INFINITY, lrun = 0.0f, arun[kC];
+#pragma unroll
+  for (int u = 0; u < kC; ++u) arun[u] = 0.0f;
+  for (int s0 = 0; s0 < p.splits; s0 += kBatch) {
+    float m[kBatch], l[kBatch], a[kBatch][kC];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
       const int s = min(s0 + i, p.splits - 1);
       m[i] = p.part_m[base + s];
       l[i] = p.part_l[base + s];
-      a[i] = p.part_acc[(base + s) * DH + c];
+#pragma unroll
+      for (int u = 0; u < kC; ++u) a[i][u] = p.part_acc[(base + s) * DH + c0 + 64 * u];
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < kBatch; ++i) {
       if (s0 + i >= p.splits || m[i] == -INFINITY) continue;
       const float mn = fmaxf(mrun, m[i]);
       const float f0 = fast_exp2(mrun - mn), f1 = fast_exp2(m[i] - mn);
       lrun = lrun * f0 + l[i] * f1;
-      arun = arun * f0 + a[i] * f1;
+#pragma unroll
+      for (int u = 0; u < kC; ++u) arun[u] = arun[u] * f0 + a[i][u] * f1;
       mrun = mn;
     }
   }
-  const float ah = mrun == -INFINITY ? 0.0f : arun / lrun;
-  const float ax = p.part_acc[(base + p.splits) * DH + c] / p.part_l[base + p.splits];
-  reinterpret_cast<T*>(p.attn)[(int64_t)b * p.nh * DH + h * DH + c] = from_f32<T>(ax + p.alpha[(int64_t)b * p.nh + h] * ah);
+  T* out = reinterpret_cast<T*>(p.attn) + (int64_t)b * p.nh * DH + h * DH;
+#pragma unroll
+  for (int u = 0; u < kC; ++u) {
+    const float ah = mrun == -INFINITY ? 0.0f : arun[u] / lrun;
+    out[c0 + 64 * u] = from_f32<T>(ax[u] / lx + al * ah);
+  }
 }
 
 template <typename T, int DH>
@@ -470,8 +484,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(const DecodeAttnPar
   const int bh = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (bh >= nbh) return;
   const int b = bh / p.nh, h = bh % p.nh, lane = threadIdx.x & 63;
-#pragma unroll
-  for (int c = lane; c < DH; c += 64) combine_partials<T, DH>(p, bh, b, h, c);
+  combine_partials<T, DH>(p, bh, b, h, lane);
 }
 
 // Proxy K/V rows into the cache: row rr = r0 + r is (sequence rr / nblk,
