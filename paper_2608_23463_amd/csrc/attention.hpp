@@ -17,6 +17,16 @@ __device__ __forceinline__ int lds_swz(int r, int c) {
   return C >= 16 ? c ^ (r & 15) : c ^ ((r / (16 / C)) & (C - 1));
 }
 
+// acc + 2^-8 A B^T for one 32x32 block of fp8 e4m3 operands over 64 K
+// elements: lane l supplies row l % 32 of A and of B, bytes
+// [32 (l / 32), +32) of the block's 64 (the same convention on both sides,
+// so the products pair up whatever order the hardware takes them in; checked
+// on the device against a host product). The 2^-8 is B's block scale.
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f32x16 mfma_fp8_scaled(const i32x8& a, const i32x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 119);
+}
+
 // Value of lane l ^ 32 (the other half of the wave), through the VALU.
 __device__ __forceinline__ float other_half(float x) {
   const uint32_t u = __builtin_bit_cast(uint32_t, x);
@@ -59,8 +69,8 @@ __device__ __forceinline__ bf16x8 pt_frag_bf16(const f32x16& s, int s2) {
 struct AttnParams {
   const void* q;    // [B, h, m, dh], pre-scaled by log2(e) / sqrt(dh)
   const void* k;    // [B, h, m, dh]
-  const void* q_lo; // optional low parts of the two-term split of (scaled) Q
-  const void* k_lo; //   and K (bf16 only): logits use Qh Kh + Ql Kh + Qh Kl
+  const void* qx;   // optional (bf16 only): fp8 e4m3 correction rows [B, h, m, 2 dh]
+  const void* kx;   //   of the split logits, whose products are 256 (Ql Kh + Qh Kl)
   const void* vt;   // [B, h, dh, ld_t]
   void* o;          // [B*m, h*dh] row-major (heads are column slices)
   float* lse;       // [B, h, m] natural-log log-sum-exp of the scores Q.K / sqrt(dh)
@@ -79,7 +89,7 @@ hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hi
 struct AttnBwdParams {
   const void* q;
   const void* k;
-  const void* q_lo;  // optional, as in AttnParams
+  const void* q_lo;  // optional bf16 low parts of the split (logits Qh Kh + Ql Kh + Qh Kl)
   const void* k_lo;
   const void* v;
   const void* qt;

@@ -15,11 +15,17 @@
 // against a new reference. P^T stays in registers: one v_permlane32_swap per
 // pair of packed values turns the accumulator layout (runs of 4 keys) into
 // MFMA operands of 8 consecutive keys, so V^T (key-contiguous, written
-// transposed by the producing GEMM) is read as 16-byte chunks. With SPLIT,
-// Q and K arrive as bf16 hi/lo pairs and the scores are Kh Qh + Kl Qh + Kh Ql
-// (three MFMAs into one accumulator), so a sharp softmax is not moved by one
-// bf16 rounding of its logits. Masked scores are -inf and contribute exactly
-// zero, so a query never depends on later proxies (bit-exact causality).
+// transposed by the producing GEMM) is read as 16-byte chunks. With SPLIT
+// (bf16 extended precision) the scores are Kh Qh + (Kl Qh + Kh Ql) with Qh, Kh
+// the bf16 values and Ql, Kl their rounding remainders, so a sharp softmax is
+// not moved by one bf16 rounding of its logits. The correction products come
+// from fp8 e4m3 rows [256 Ql | Qh] and [Kh | 256 Kl] written by the Q and K
+// projections: per 32-key block one fp8 MFMA per 64 bytes of the row (half
+// the matrix time of two bf16 products), whose block scale removes the 256.
+// The correction is ~2^-8 of the logit, so its fp8 rounding (2^-4) leaves the
+// logits exact to ~2^-12 of |q||k| (one bf16 rounding: ~2^-8).
+// Masked scores are -inf and contribute exactly zero, so a query never
+// depends on later proxies (bit-exact causality).
 #include "attention.hpp"
 
 namespace pf {
@@ -44,6 +50,8 @@ struct AttnFwdShape {
 template <typename T, int DH, bool SPLIT, int NS, int OCC>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
     attn_fwd_kernel(const AttnParams p) {
+  static_assert(!SPLIT || sizeof(T) == 2, "the split takes bf16 operands");
+  constexpr int kXB = 2 * DH / 64;  // fp8 blocks of 64 bytes per correction row
   typedef AttnFwdShape<T, DH, SPLIT, NS> S;
   typedef Mma<T> MM;
   __shared__ __attribute__((aligned(1024))) char smem[S::kNS * S::kStage];
@@ -71,22 +79,35 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
   const int myq = qw0 + col;
 
   const char* kp = reinterpret_cast<const char*>(p.k) + (int64_t)bh * p.m * S::kRowBytes;
-  const char* klp = SPLIT ? reinterpret_cast<const char*>(p.k_lo) + (int64_t)bh * p.m * S::kRowBytes : nullptr;
+  // the second K tile (SPLIT): the fp8 correction rows, 2 dh bytes like a
+  // bf16 key row
+  const char* klp = SPLIT ? reinterpret_cast<const char*>(p.kx) + (int64_t)bh * p.m * S::kRowBytes : nullptr;
   const char* vtp = reinterpret_cast<const char*>(p.vt) + (int64_t)bh * DH * p.ld_t * (int64_t)sizeof(T);
   const T* qp = reinterpret_cast<const T*>(p.q) + (int64_t)bh * p.m * DH;
-  const T* qlp = SPLIT ? reinterpret_cast<const T*>(p.q_lo) + (int64_t)bh * p.m * DH : nullptr;
 
-  typename MM::frag qf[DH / 16], qfl[SPLIT ? DH / 16 : 1];
+  typename MM::frag qf[DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
     if (myq < p.m) {
       qf[kk] = MM::load(qp + (int64_t)myq * DH + kk * 16 + g * 8);
-      if constexpr (SPLIT) qfl[kk] = MM::load(qlp + (int64_t)myq * DH + kk * 16 + g * 8);
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        qf[kk][i] = (T)0.0f;
-        if constexpr (SPLIT) qfl[kk][i] = (T)0.0f;
+      for (int i = 0; i < 8; ++i) qf[kk][i] = (T)0.0f;
+    }
+  }
+  // fp8 correction operand of this lane's query: bytes [32 g, +32) of each
+  // 64-byte block of its row
+  i32x8 qx[SPLIT ? kXB : 1];
+  if constexpr (SPLIT) {
+    const char* qxr = reinterpret_cast<const char*>(p.qx) + ((int64_t)bh * p.m + (myq < p.m ? myq : 0)) * 2 * DH;
+#pragma unroll
+    for (int xb = 0; xb < kXB; ++xb) {
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(qxr + xb * 64 + 32 * g);
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(qxr + xb * 64 + 32 * g + 16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        qx[xb][e] = myq < p.m ? (int)lo[e] : 0;
+        qx[xb][e + 4] = myq < p.m ? (int)hi[e] : 0;
       }
     }
   }
@@ -178,17 +199,31 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
       // issue slots between MFMAs.
       auto scores = [&](f32x16 (&s)[2], const f32x16& c0) {
         // every fragment read is issued before the first MFMA
-        typename MM::frag kh[2][DH / 16], kl[2][SPLIT ? DH / 16 : 1];
+        typename MM::frag kh[2][DH / 16];
+        i32x8 kx[2][SPLIT ? kXB : 1];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
           const int kr = kb * 32 + col;  // key row of this lane's A fragment
           const char* krow = sk + kr * S::kRowBytes;
+          if constexpr (SPLIT) {
+#pragma unroll
+            for (int xb = 0; xb < kXB; ++xb) {
+              const u32x4 lo = *reinterpret_cast<const u32x4*>(
+                  krow + S::kKTile + lds_swz<S::kRowBytes / 16>(kr, xb * 4 + 2 * g) * 16);
+              const u32x4 hi = *reinterpret_cast<const u32x4*>(
+                  krow + S::kKTile + lds_swz<S::kRowBytes / 16>(kr, xb * 4 + 2 * g + 1) * 16);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                kx[kb][xb][e] = (int)lo[e];
+                kx[kb][xb][e + 4] = (int)hi[e];
+              }
+            }
+          }
 #pragma unroll
           for (int kk = 0; kk < DH / 16; ++kk) {
             if constexpr (sizeof(T) == 2) {
               const int off = lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16;
               kh[kb][kk] = *reinterpret_cast<const typename MM::frag*>(krow + off);
-              if constexpr (SPLIT) kl[kb][kk] = *reinterpret_cast<const typename MM::frag*>(krow + S::kKTile + off);
             } else {
               const int c0i = kk * 4 + g * 2;
               const f32x4 lo = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0i) * 16);
@@ -207,11 +242,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
 #pragma unroll
           for (int kb = 0; kb < 2; ++kb) {
             s[kb] = MM::mma(kh[kb][kk], qf[kk], kk == 0 ? c0 : s[kb]);
-            if constexpr (SPLIT) {
-              s[kb] = MM::mma(kl[kb][kk], qf[kk], s[kb]);
-              s[kb] = MM::mma(kh[kb][kk], qfl[kk], s[kb]);
-            }
           }
+        if constexpr (SPLIT) {
+#pragma unroll
+          for (int xb = 0; xb < kXB; ++xb)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) s[kb] = mfma_fp8_scaled(kx[kb][xb], qx[xb], s[kb]);
+        }
         __builtin_amdgcn_s_setprio(0);
         if (need_mask) {  // selects, no per-element branches
 #pragma unroll
@@ -338,15 +375,20 @@ static hipError_t launch_fwd_cfg(const AttnParams& p, dim3 grid, hipStream_t str
   return hipGetLastError();
 }
 
+template <typename T, int DH>
+static hipError_t launch_fwd_dh(const AttnParams& p, dim3 grid, hipStream_t stream) {
+  if constexpr (sizeof(T) == 2) {
+    if (p.qx && p.kx) return launch_fwd_cfg<T, DH, true>(p, grid, stream);
+  }
+  return launch_fwd_cfg<T, DH, false>(p, grid, stream);
+}
+
 template <typename T>
 hipError_t launch_attention_fwd(const AttnParams& p, int batch, int head_dim, hipStream_t stream) {
   if (p.m <= 0) return hipSuccess;  // one head's tensors are below 2 GiB (checked by layer_dims)
   dim3 grid(((p.m + 127) / 128) * batch * p.n_heads);
-  const bool split = sizeof(T) == 2 && p.q_lo && p.k_lo;
-  constexpr bool kSplit = sizeof(T) == 2;
-  if (head_dim == 64)
-    return split ? launch_fwd_cfg<T, 64, kSplit>(p, grid, stream) : launch_fwd_cfg<T, 64, false>(p, grid, stream);
-  return split ? launch_fwd_cfg<T, 128, kSplit>(p, grid, stream) : launch_fwd_cfg<T, 128, false>(p, grid, stream);
+  if (head_dim == 64) return launch_fwd_dh<T, 64>(p, grid, stream);
+  return launch_fwd_dh<T, 128>(p, grid, stream);
 }
 
 template hipError_t launch_attention_fwd<bf16>(const AttnParams&, int, int, hipStream_t);

@@ -93,7 +93,7 @@ struct EpiSigmoidF32 {
 // ---- attention over the two key sets ------------------------------------------------
 
 struct GenAttnParams {
-  const void* q;       // [B, h, T, dh]
+  const void* q;       // [B, h, T, dh], scaled by log2(e) / sqrt(dh)
   const void* k;       // [B, h, T, dh]
   const void* vt;      // [B, h, dh, ld_t], columns T .. ld_t-1 zero
   const void* v;       // bf16: [B, h, T, dh] (in place of vt)
@@ -106,7 +106,6 @@ struct GenAttnParams {
   int n0;              // cached rows before the chunk
   int n_keys;          // cached rows after the chunk's append
   int64_t n_cap;
-  float scale_log2;    // log2(e) / sqrt(dh)
 };
 
 template <typename T, int DH>
@@ -148,7 +147,7 @@ template <typename T, int DH, bool VROW = false>
 __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys, const char* vtp, int ld_v,
                                           int t_first, int t_last, int lo, int hi, int wlo_min, int wlo_max,
                                           int whi_min, int whi_max, const typename Mma<T>::frag (&qf)[DH / 16],
-                                          float sc, f32x16 (&o)[DH / 32]) {
+                                          f32x16 (&o)[DH / 32]) {
   typedef GenShape<T, DH> S;
   typedef Mma<T> MM;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -158,8 +157,20 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
   for (int cb = 0; cb < DH / 32; ++cb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[cb][r] = 0.0f;
-  float mrun = -INFINITY, lrun = 0.0f;
-  const float thr = 8.0f / sc;  // raw-score headroom of a stale maximum (2^8)
+  // Online softmax in exp2 units (Q arrives scaled by log2(e)/sqrt(d_head)),
+  // with the reference maximum of the proxy attention forward: mref is set
+  // from a real maximum on a lane pair's first tile with a visible key and
+  // kept while the running sums stay below 2^64; the score MFMAs start at
+  // -mref, so each probability is one exp2 of an MFMA result.
+  float mref = -INFINITY, lrun = 0.0f;
+  f32x16 negm, zero;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    negm[r] = 0.0f;
+    zero[r] = 0.0f;
+  }
+  bool have_ref = false;  // wave-uniform
+  constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
   const int ntiles = t_last - t_first + 1;
 
   auto issue = [&](int t, int stage) {
@@ -204,72 +215,92 @@ __device__ __forceinline__ void gen_phase(char* smem, const char* kp, int nkeys,
     const char* sv = sk + S::kKTile;
     const bool active = kt0 <= whi_max && kt0 + S::kKT - 1 >= wlo_min && whi_max >= wlo_min;
     if (!active) continue;  // wave-uniform
-    __builtin_amdgcn_s_setprio(1);
-    f32x16 s[2];
+    const bool need_mask = kt0 < wlo_max || kt0 + S::kKT - 1 > whi_min;  // some lane sees part of the tile
+    // S^T = K Q^T + c0 for the tile's 64 keys, keys outside [lo, hi] at -inf
+    auto scores = [&](f32x16 (&s)[2], const f32x16& c0) {
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb) {
+        s[kb] = c0;
+        const int kr = kb * 32 + col;
+        const char* krow = sk + kr * S::kRowBytes;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
-      const int kr = kb * 32 + col;
-      const char* krow = sk + kr * S::kRowBytes;
+        for (int kk = 0; kk < DH / 16; ++kk) {
+          typename MM::frag kh;
+          if constexpr (sizeof(T) == 2) {
+            kh = *reinterpret_cast<const typename MM::frag*>(krow + lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16);
+          } else {
+            const int c0i = kk * 4 + g * 2;
+            const f32x4 a = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0i) * 16);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0i + 1) * 16);
 #pragma unroll
-      for (int kk = 0; kk < DH / 16; ++kk) {
-        typename MM::frag kh;
-        if constexpr (sizeof(T) == 2) {
-          kh = *reinterpret_cast<const typename MM::frag*>(krow + lds_swz<S::kRowBytes / 16>(kr, kk * 2 + g) * 16);
-        } else {
-          const int c0 = kk * 4 + g * 2;
-          const f32x4 a = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0) * 16);
-          const f32x4 b = *reinterpret_cast<const f32x4*>(krow + lds_swz<S::kRowBytes / 16>(kr, c0 + 1) * 16);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            kh[e] = a[e];
-            kh[e + 4] = b[e];
+            for (int e = 0; e < 4; ++e) {
+              kh[e] = a[e];
+              kh[e + 4] = b[e];
+            }
           }
+          s[kb] = MM::mma(kh, qf[kk], s[kb]);
         }
-        s[kb] = MM::mma(kh, qf[kk], s[kb]);
       }
-    }
-    __builtin_amdgcn_s_setprio(0);
-    if (kt0 < wlo_max || kt0 + S::kKT - 1 > whi_min) {  // some lane sees only part of the tile
+      __builtin_amdgcn_s_setprio(0);
+      if (need_mask) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kt0 + kb * 32 + acc_row(r, lane);
+            s[kb][r] = (key < lo || key > hi) ? -INFINITY : s[kb][r];
+          }
+      }
+    };
+    // probabilities in place (exp2 of score - shift), summed in four chains
+    auto exponentiate = [&](f32x16 (&s)[2], float shift) {
+      float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = kt0 + kb * 32 + acc_row(r, lane);
-          s[kb][r] = (key < lo || key > hi) ? -INFINITY : s[kb][r];
+          const float e = fast_exp2(s[kb][r] - shift);
+          s[kb][r] = e;
+          ls[r & 3] += e;
         }
+      return (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    };
+    f32x16 s[2];
+    float tsum = 0.0f;
+    bool redo = !have_ref;
+    if (have_ref) {
+      scores(s, negm);
+      tsum = exponentiate(s, 0.0f);
+      redo = __builtin_amdgcn_ballot_w64(!(lrun + tsum <= kSumLimit)) != 0;
     }
-    float mt = -INFINITY;
+    if (redo) {  // wave-uniform: first active tile, a sum past the limit, or a lane's first key
+      scores(s, zero);
+      float mt = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
-    mt = fmaxf(mt, other_half(mt));
-    const float mnew = fmaxf(mrun, mt);
-    if (__builtin_amdgcn_ballot_w64(mnew > mrun + thr) != 0) {
-      // nothing has been accumulated while the maximum is -inf
-      const float a = mrun == -INFINITY ? 0.0f : fast_exp2((mrun - mnew) * sc);
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+      mt = fmaxf(mt, other_half(mt));
+      const float ltot = lrun + other_half(lrun);
+      const float mnew = fmaxf(mt, mref + fmaxf(0.0f, __log2f(ltot)));
+      // nothing is accumulated while a lane has no reference
+      const float a = mref == -INFINITY ? 0.0f : fast_exp2(mref - mnew);
       lrun *= a;
 #pragma unroll
       for (int cb = 0; cb < DH / 32; ++cb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[cb][r] *= a;
-      mrun = mnew;
+      mref = mnew;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) negm[r] = -mnew;
+      have_ref = true;
+      // a lane that has seen no key keeps mref = -inf: its scores are all
+      // -inf here (probability 0), and on a later tile its first visible key
+      // gives an infinite sum, which brings it back here
+      tsum = exponentiate(s, mnew == -INFINITY ? 0.0f : mnew);
     }
-    // a lane with no visible key so far has every score at -inf: exp2 of
-    // -inf is 0 with a zero offset
-    const float mb = mrun == -INFINITY ? 0.0f : mrun * sc;
-    float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = fast_exp2(fmaf(s[kb][r], sc, -mb));
-        s[kb][r] = e;
-        ls[r & 3] += e;
-      }
-    lrun += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    lrun += tsum;
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -375,7 +406,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DH == 
                            : reinterpret_cast<const char*>(p.vt) + (int64_t)bh * DH * p.ld_t * (int64_t)sizeof(T);
     const int lo = (qc / p.P) * p.P;
     gen_phase<T, DH, kRow>(smem, kp, p.T, vtp, p.ld_t, ((q0 / p.P) * p.P) / S::kKT, q1c / S::kKT, lo, qc,
-                     (qw0c / p.P) * p.P, (qw1c / p.P) * p.P, qw0c, qw1c, qf, p.scale_log2, ox);
+                     (qw0c / p.P) * p.P, (qw1c / p.P) * p.P, qw0c, qw1c, qf, ox);
   }
   // cache phase: rows 0 .. n0 + blk(t) - 1
   f32x16 oc[DH / 32];
@@ -385,7 +416,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DH == 
                            : reinterpret_cast<const char*>(p.vct) + (int64_t)bh * DH * p.ld_c * (int64_t)sizeof(T);
     const int hmax = p.n0 + q1c / p.P - 1;
     gen_phase<T, DH, kRow>(smem, kp, p.n_keys, vtp, p.ld_c, 0, hmax >= 0 ? hmax / S::kKT : -1, 0, p.n0 + qc / p.P - 1, 0,
-                     0, p.n0 + qw0c / p.P - 1, p.n0 + qw1c / p.P - 1, qf, p.scale_log2, oc);
+                     0, p.n0 + qw0c / p.P - 1, p.n0 + qw1c / p.P - 1, qf, oc);
   }
   if (myq < p.T) {
     T* orow = reinterpret_cast<T*>(p.out) + ((int64_t)b * p.T + myq) * ((int64_t)p.nh * DH) + h * DH;
@@ -511,7 +542,9 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
     run.launch("fill_zero", [&] { return fill_zero(vt, tb, run.stream); });
   }
   const pf_linear* proj[3] = {&w->q, &w->k, &w->v};
-  T* outs[3] = {q, k, vrow ? vt : nullptr};
+  // Q goes to the attention pre-scaled by log2(e)/sqrt(d_head): scores in
+  // exp2 units
+  T* outs[3] = {nullptr, k, vrow ? vt : nullptr};
   T* outs_t[3] = {nullptr, nullptr, vrow ? nullptr : vt};
   for (int i = 0; i < 3; ++i) {
     GemmProblem pr{};
@@ -523,6 +556,10 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
     pr.N = d.d;
     pr.K = d.d;
     EpiHeads<T> e{outs[i], outs_t[i], reinterpret_cast<const T*>(proj[i]->b), Tn, d.dh, d.nh, (int)W.ld_t, nullptr};
+    if (i == 0) {
+      e.outs = q;
+      e.scale = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
+    }
     run.gemm<T, LAYOUT_K, LAYOUT_K>("prefill_qkv_gemm", pr, e);
   }
   {
@@ -590,7 +627,6 @@ static void prefill_impl(Runner& run, const DecodeDims& d, const pf_decode_weigh
   ap.n0 = (int)st.n;
   ap.n_keys = (int)n_keys;
   ap.n_cap = st.n_cap;
-  ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   run.launch("prefill_attn", [&] {
     const dim3 grid((unsigned)(((Tn + 127) / 128) * d.B * d.nh));
     if (d.dh == 64)

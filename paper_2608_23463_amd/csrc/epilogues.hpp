@@ -83,8 +83,7 @@ struct EpiLinear {
 
 // Splits a [B*m, h*dh] projection into per-head tensors: row r = b*m + i,
 // column c = head*dh + e. `out` is [B, h, m, dh], `out_t` is [B, h, dh, ld_t].
-// Optionally also a scaled copy (v * scale) in the row layout, `outs`, with
-// its own low part `outs_lo` (the split of the scaled value).
+// Optionally also a scaled copy (v * scale) in the row layout, `outs`.
 template <typename T>
 struct EpiHeads {
   T* out;
@@ -93,8 +92,15 @@ struct EpiHeads {
   int m, dh, n_heads, ld_t;
   T* out_lo;  // optional low part of the split, row layout
   T* outs = nullptr;
-  T* outs_lo = nullptr;
   float scale = 1.0f;
+  // fp8 e4m3 operand of the attention's correction product, rows of 2 dh
+  // bytes [B, h, m, 2 dh] (bf16 only). With hi = bf16(x) and lo = x - hi of
+  // the value x the attention reads (x = v * scale for Q, v for K):
+  // xmode 1 writes [fp8(256 lo) | fp8(hi)], xmode 2 writes [fp8(hi) |
+  // fp8(256 lo)], so the dot product of a Q row and a K row is
+  // 256 (Ql Kh + Qh Kl).
+  uint8_t* outx = nullptr;
+  int xmode = 0;
   __device__ __forceinline__ void operator()(int r, int c, float v) const {
     if (bias) v += to_f32(bias[c]);
     const T o = from_f32<T>(v);
@@ -105,7 +111,13 @@ struct EpiHeads {
     if (out_t) out_t[(bh * dh + e) * ld_t + i] = o;
     if (out_lo) out_lo[(bh * m + i) * dh + e] = from_f32<T>(split_lo(v));
     if (outs) outs[(bh * m + i) * dh + e] = from_f32<T>(v * scale);
-    if (outs_lo) outs_lo[(bh * m + i) * dh + e] = from_f32<T>(split_lo(v * scale));
+    if (outx) {
+      const float x = xmode == 1 ? v * scale : v;
+      const float hi = (float)(bf16)x, lo = (x - hi) * 256.0f;
+      uint8_t* row = outx + (bh * m + i) * 2 * dh;
+      row[e] = (uint8_t)pack_fp8x4(xmode == 1 ? lo : hi, 0.0f, 0.0f, 0.0f);
+      row[dh + e] = (uint8_t)pack_fp8x4(xmode == 1 ? hi : lo, 0.0f, 0.0f, 0.0f);
+    }
   }
   struct Col {
     Raw8<T> b;
@@ -142,18 +154,31 @@ struct EpiHeads {
       store8(out_lo + (bh * m + i) * dh + e0, t);
     }
     if (outs) {
-      float s[8], t[8];
+      float s[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        s[e] = v[e] * scale;
-        t[e] = split_lo(s[e]);
-      }
+      for (int e = 0; e < 8; ++e) s[e] = v[e] * scale;
       store8(outs + (bh * m + i) * dh + e0, s);
-      if (outs_lo) store8(outs_lo + (bh * m + i) * dh + e0, t);
     }
     if (out_t) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) out_t[(bh * dh + e0 + e) * ld_t + i] = from_f32<T>(v[e]);
+    }
+    if (outx) {
+      float hi[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = xmode == 1 ? v[e] * scale : v[e];
+        hi[e] = (float)(bf16)x;
+        lo[e] = (x - hi[e]) * 256.0f;
+      }
+      const float* first = xmode == 1 ? lo : hi;
+      const float* second = xmode == 1 ? hi : lo;
+      uint8_t* row = outx + (bh * m + i) * 2 * dh;
+      typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+      *reinterpret_cast<u32x2_t*>(row + e0) =
+          u32x2_t{pack_fp8x4(first[0], first[1], first[2], first[3]), pack_fp8x4(first[4], first[5], first[6], first[7])};
+      *reinterpret_cast<u32x2_t*>(row + dh + e0) = u32x2_t{pack_fp8x4(second[0], second[1], second[2], second[3]),
+                                                           pack_fp8x4(second[4], second[5], second[6], second[7])};
     }
   }
 };

@@ -41,8 +41,10 @@ struct LayerDims {
 // attention logits (Z_j, H, Q, K) also keeps the low part of a two-term bf16
 // split (the *_lo buffers): a proxy sums P * d_fine products, so its
 // magnitude, and the logits', grow with the compression fan-in, and one bf16
-// rounding there moves a sharp softmax by several percent. In fp32 mode and
-// with PF_PRECISION_BF16 the *_lo buffers are empty.
+// rounding there moves a sharp softmax by several percent. The forward
+// attention reads the Q and K remainders as fp8 correction rows (qx, kx);
+// the bf16 low parts of Q and K are kept only for the backward. In fp32 mode
+// and with PF_PRECISION_BF16 the *_lo, qx and kx buffers are empty.
 struct LayerActs {
   size_t z[PF_MAX_LEVELS];    // Z_j, j = 1..M-1: compression level outputs [B*R_j, d_j]
   size_t z_lo[PF_MAX_LEVELS];
@@ -50,8 +52,10 @@ struct LayerActs {
   size_t h_lo;
   size_t q, k, v;             // [B, h, m, dh]
   size_t q_lo, k_lo;
-  size_t qs, qs_lo;           // Q * log2(e)/sqrt(d_head) for the forward attention [B, h, m, dh]
-                              // (the same buffers as q, q_lo unless activations are saved)
+  size_t qs;                  // Q * log2(e)/sqrt(d_head) for the forward attention [B, h, m, dh]
+                              // (the same buffer as q unless activations are saved)
+  size_t qx, kx;              // extended precision: fp8 correction rows of scaled Q and of K
+                              // [B, h, m, 2 dh] bytes (see EpiHeads)
   size_t qt, kt, vt;          // [B, h, dh, ld_t]
   size_t o;                   // [B*m, d_p]
   size_t lse;                 // [B, h, m] fp32

@@ -265,11 +265,14 @@ LayerActs layer_acts(const LayerDims& d, bool bwd) {
   a.h_lo = take(split ? prox : 0);
   a.q = take(prox);
   a.k = take(prox);
-  a.q_lo = take(split ? prox : 0);
-  a.k_lo = take(split ? prox : 0);
+  a.q_lo = take(split && bwd ? prox : 0);  // the backward's split logits
+  a.k_lo = take(split && bwd ? prox : 0);
   // the forward attention reads Q pre-scaled; the backward reads Q itself
   a.qs = bwd ? take(prox) : a.q;
-  a.qs_lo = bwd ? take(split ? prox : 0) : a.q_lo;
+  // the forward attention's fp8 correction rows: 2 dh bytes per head row,
+  // the size of a bf16 row
+  a.qx = take(split ? prox : 0);
+  a.kx = take(split ? prox : 0);
   a.v = bwd ? take(prox) : 0;
   a.qt = bwd ? take(headt) : 0;
   a.kt = bwd ? take(headt) : 0;
@@ -451,7 +454,9 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   const float qscale = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
   T* outs[3] = {saving ? P(A.q) : nullptr, P(A.k), saving ? P(A.v) : nullptr};
   T* outs_t[3] = {saving ? P(A.qt) : nullptr, saving ? P(A.kt) : nullptr, P(A.vt)};
-  T* outs_lo[3] = {split && saving ? P(A.q_lo) : nullptr, split ? P(A.k_lo) : nullptr, nullptr};
+  // the low parts of Q and K are kept for the backward; the forward
+  // attention reads the fp8 correction rows
+  T* outs_lo[3] = {split && saving ? P(A.q_lo) : nullptr, split && saving ? P(A.k_lo) : nullptr, nullptr};
   for (int i = 0; i < 3; ++i) {
     GemmProblem pr{};
     pr.a = hbuf;
@@ -474,8 +479,11 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
                   outs_lo[i]};
     if (i == 0) {
       e.outs = P(A.qs);
-      e.outs_lo = split ? P(A.qs_lo) : nullptr;
       e.scale = qscale;
+    }
+    if (split && i < 2) {
+      e.outx = reinterpret_cast<uint8_t*>(act + (i == 0 ? A.qx : A.kx));
+      e.xmode = i == 0 ? 1 : 2;
     }
     run.gemm<T, LAYOUT_K, LAYOUT_K>("qkv_gemm", pr, e);
   }
@@ -484,8 +492,8 @@ static void forward_impl(Runner& run, const LayerDims& d, const pf_layer_config*
   AttnParams ap{};
   ap.q = P(A.qs);
   ap.k = P(A.k);
-  ap.q_lo = split ? P(A.qs_lo) : nullptr;
-  ap.k_lo = split ? P(A.k_lo) : nullptr;
+  ap.qx = split ? act + A.qx : nullptr;
+  ap.kx = split ? act + A.kx : nullptr;
   ap.vt = P(A.vt);
   ap.o = P(A.o);
   ap.lse = reinterpret_cast<float*>(act + A.lse);
