@@ -1027,7 +1027,11 @@ inline hipError_t launch_gemm_tile(const GemmProblem& pr, const GemmPlan& pl, co
   p.k_slice = pl.k_slice;
   p.tiles_m = (pr.M + BM - 1) / BM;
   p.tiles_n = (pr.N + BN - 1) / BN;
-  p.group_m = 8;
+  // row tiles per column sweep: the sweep's A rows (group_m x BM rows of one
+  // K slice) fit about 4 MiB, one XCD's L2; 2 .. 8 (long reductions such as
+  // the compression take 2, K = 2048 takes 4, K = 1024 keeps 8)
+  p.group_m = (int)std::min<int64_t>(
+      8, std::max<int64_t>(2, ((int64_t)4 << 20) / ((int64_t)BM * std::max(pl.k_slice, BK) * (int64_t)sizeof(T))));
   p.batch_a = pr.batch_a;
   p.batch_b = pr.batch_b;
   dim3 grid(p.tiles_m * p.tiles_n, pr.batch, pl.splits);

@@ -227,6 +227,25 @@ def test_forward_parity_plain_bf16_precision(gpu, name):
     assert_close(got, ref["x_out"], shape.dtype, f"{name} plain bf16 x_out")
 
 
+def test_extended_precision_beats_plain_bf16(gpu):
+    """The correction products of PF_PRECISION_EXTENDED are applied: on the
+    64K-token layer (logit std ~11, where one bf16 rounding of Q and K moves
+    the softmax by percents) the extended output is at least twice as close
+    to the fp64 oracle as the plain-bf16 output of the same inputs. Both
+    pass 2e-2, so a correction that silently dropped out would pass every
+    tolerance check but not this one."""
+    import dataclasses
+    name = "layer_bf16_L64k_d1024"
+    shape = synth.WORKLOADS[name]
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask)
+    errs = {}
+    for prec in (synth.PRECISION_EXTENDED, synth.PRECISION_BF16):
+        x_out, _ = run_gpu(dataclasses.replace(shape, precision=prec), inp)
+        errs[prec] = assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} precision {prec} x_out")
+    assert errs[synth.PRECISION_EXTENDED] <= 0.5 * errs[synth.PRECISION_BF16], errs
+
+
 @pytest.mark.parametrize("name", ["layer_bf16_L64k_d1024", "layer_bf16_L1M_d1024"])
 def test_forward_parity_fused_gate(gpu, name):
     """PF_GATE_FUSED at the workload widths (d_fine 1024, P = 64): the 64K-token
