@@ -80,8 +80,8 @@ enum pf_injection { PF_INJECT_GATED = 0, PF_INJECT_ADD = 1, PF_INJECT_AFFINE = 2
  *   layers the logits are large and one bf16 rounding of Q and K moves a
  *   sharp softmax by several percent; this keeps such layers (and their
  *   backward) within the bf16 tolerance. The forward attention forms the two
- *   correction products from fp8 e4m3 copies of (Ql, Qh) and (Kh, Kl), which
- *   keeps the logits to about 2^-12 of |q||k| (one bf16 rounding: 2^-8) at
+ *   correction products from fp8 e5m2 copies of (Ql, Qh) and (Kh, Kl), which
+ *   keeps the logits to about 2^-11 of |q||k| (one bf16 rounding: 2^-8) at
  *   1.5x the score work of plain bf16; the backward uses the bf16 parts
  *   (three products). 
  * PF_PRECISION_BF16: H, Q and K are plain bf16 values (the bf16 training the

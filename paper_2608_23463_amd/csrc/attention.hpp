@@ -17,14 +17,14 @@ __device__ __forceinline__ int lds_swz(int r, int c) {
   return C >= 16 ? c ^ (r & 15) : c ^ ((r / (16 / C)) & (C - 1));
 }
 
-// acc + 2^-8 A B^T for one 32x32 block of fp8 e4m3 operands over 64 K
+// acc + 2^-8 A B^T for one 32x32 block of fp8 e5m2 operands over 64 K
 // elements: lane l supplies row l % 32 of A and of B, bytes
 // [32 (l / 32), +32) of the block's 64 (the same convention on both sides,
 // so the products pair up whatever order the hardware takes them in; checked
 // on the device against a host product). The 2^-8 is B's block scale.
 typedef int i32x8 __attribute__((ext_vector_type(8)));
-__device__ __forceinline__ f32x16 mfma_fp8_scaled(const i32x8& a, const i32x8& b, const f32x16& c) {
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 119);
+__device__ __forceinline__ f32x16 mfma_bf8_scaled(const i32x8& a, const i32x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 1, 1, 0, 127, 0, 119);
 }
 
 // Value of lane l ^ 32 (the other half of the wave), through the VALU.
@@ -69,7 +69,7 @@ __device__ __forceinline__ bf16x8 pt_frag_bf16(const f32x16& s, int s2) {
 struct AttnParams {
   const void* q;    // [B, h, m, dh], pre-scaled by log2(e) / sqrt(dh)
   const void* k;    // [B, h, m, dh]
-  const void* qx;   // optional (bf16 only): fp8 e4m3 correction rows [B, h, m, 2 dh]
+  const void* qx;   // optional (bf16 only): fp8 e5m2 correction rows [B, h, m, 2 dh]
   const void* kx;   //   of the split logits, whose products are 256 (Ql Kh + Qh Kl)
   const void* vt;   // [B, h, dh, ld_t]
   void* o;          // [B*m, h*dh] row-major (heads are column slices)

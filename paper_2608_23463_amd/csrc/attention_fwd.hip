@@ -19,11 +19,12 @@
 // (bf16 extended precision) the scores are Kh Qh + (Kl Qh + Kh Ql) with Qh, Kh
 // the bf16 values and Ql, Kl their rounding remainders, so a sharp softmax is
 // not moved by one bf16 rounding of its logits. The correction products come
-// from fp8 e4m3 rows [256 Ql | Qh] and [Kh | 256 Kl] written by the Q and K
+// from fp8 e5m2 rows [256 Ql | Qh] and [Kh | 256 Kl] written by the Q and K
 // projections: per 32-key block one fp8 MFMA per 64 bytes of the row (half
 // the matrix time of two bf16 products), whose block scale removes the 256.
-// The correction is ~2^-8 of the logit, so its fp8 rounding (2^-4) leaves the
-// logits exact to ~2^-12 of |q||k| (one bf16 rounding: ~2^-8).
+// The correction is ~2^-8 of the logit, so its fp8 rounding (2^-3) leaves the
+// logits exact to ~2^-11 of |q||k| (one bf16 rounding: ~2^-8); e5m2's range
+// (2^-14 .. 57344 normal) holds Q and K rows of any practical magnitude.
 // Masked scores are -inf and contribute exactly zero, so a query never
 // depends on later proxies (bit-exact causality).
 #include "attention.hpp"
@@ -247,7 +248,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC)))
 #pragma unroll
           for (int xb = 0; xb < kXB; ++xb)
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) s[kb] = mfma_fp8_scaled(kx[kb][xb], qx[xb], s[kb]);
+            for (int kb = 0; kb < 2; ++kb) s[kb] = mfma_bf8_scaled(kx[kb][xb], qx[xb], s[kb]);
         }
         __builtin_amdgcn_s_setprio(0);
         if (need_mask) {  // selects, no per-element branches

@@ -93,12 +93,13 @@ __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4
 // tensors there is no low part.
 __device__ __forceinline__ float split_lo(float v) { return (float)(bf16)(v - (float)(bf16)v); }
 
-// Four floats -> four fp8 e4m3 bytes (OCP encoding, round to nearest even,
-// hardware conversion), saturated to +-448 first; byte i holds the i-th value.
-__device__ __forceinline__ uint32_t pack_fp8x4(float a, float b, float c, float d) {
-  auto sat = [](float x) { return fminf(fmaxf(x, -448.0f), 448.0f); };
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(sat(a), sat(b), 0, false);
-  w = __builtin_amdgcn_cvt_pk_fp8_f32(sat(c), sat(d), w, true);
+// Four floats -> four fp8 e5m2 bytes (OCP "bf8" encoding, round to nearest
+// even, hardware conversion), saturated to the largest finite +-57344 first;
+// byte i holds the i-th value. Normal values span 2^-14 .. 57344.
+__device__ __forceinline__ uint32_t pack_bf8x4(float a, float b, float c, float d) {
+  auto sat = [](float x) { return fminf(fmaxf(x, -57344.0f), 57344.0f); };
+  int w = __builtin_amdgcn_cvt_pk_bf8_f32(sat(a), sat(b), 0, false);
+  w = __builtin_amdgcn_cvt_pk_bf8_f32(sat(c), sat(d), w, true);
   return (uint32_t)w;
 }
 

@@ -93,7 +93,7 @@ struct EpiHeads {
   T* out_lo;  // optional low part of the split, row layout
   T* outs = nullptr;
   float scale = 1.0f;
-  // fp8 e4m3 operand of the attention's correction product, rows of 2 dh
+  // fp8 (e5m2) operand of the attention's correction product, rows of 2 dh
   // bytes [B, h, m, 2 dh] (bf16 only). With hi = bf16(x) and lo = x - hi of
   // the value x the attention reads (x = v * scale for Q, v for K):
   // xmode 1 writes [fp8(256 lo) | fp8(hi)], xmode 2 writes [fp8(hi) |
@@ -115,8 +115,8 @@ struct EpiHeads {
       const float x = xmode == 1 ? v * scale : v;
       const float hi = (float)(bf16)x, lo = (x - hi) * 256.0f;
       uint8_t* row = outx + (bh * m + i) * 2 * dh;
-      row[e] = (uint8_t)pack_fp8x4(xmode == 1 ? lo : hi, 0.0f, 0.0f, 0.0f);
-      row[dh + e] = (uint8_t)pack_fp8x4(xmode == 1 ? hi : lo, 0.0f, 0.0f, 0.0f);
+      row[e] = (uint8_t)pack_bf8x4(xmode == 1 ? lo : hi, 0.0f, 0.0f, 0.0f);
+      row[dh + e] = (uint8_t)pack_bf8x4(xmode == 1 ? hi : lo, 0.0f, 0.0f, 0.0f);
     }
   }
   struct Col {
@@ -176,9 +176,9 @@ struct EpiHeads {
       uint8_t* row = outx + (bh * m + i) * 2 * dh;
       typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
       *reinterpret_cast<u32x2_t*>(row + e0) =
-          u32x2_t{pack_fp8x4(first[0], first[1], first[2], first[3]), pack_fp8x4(first[4], first[5], first[6], first[7])};
-      *reinterpret_cast<u32x2_t*>(row + dh + e0) = u32x2_t{pack_fp8x4(second[0], second[1], second[2], second[3]),
-                                                           pack_fp8x4(second[4], second[5], second[6], second[7])};
+          u32x2_t{pack_bf8x4(first[0], first[1], first[2], first[3]), pack_bf8x4(first[4], first[5], first[6], first[7])};
+      *reinterpret_cast<u32x2_t*>(row + dh + e0) = u32x2_t{pack_bf8x4(second[0], second[1], second[2], second[3]),
+                                                           pack_bf8x4(second[4], second[5], second[6], second[7])};
     }
   }
 };

@@ -246,6 +246,30 @@ def test_extended_precision_beats_plain_bf16(gpu):
     assert errs[synth.PRECISION_EXTENDED] <= 0.5 * errs[synth.PRECISION_BF16], errs
 
 
+def test_extended_precision_with_large_keys_and_small_queries(gpu):
+    """The correction rows cover the magnitudes Q and K take: with W_k scaled
+    by 256 and W_q by 1/256 (powers of two, so the bf16 weights stay exact)
+    every logit is the same as on the plain 64K-token layer, but the keys
+    reach ~1e3 and the scaled queries ~1e-3. Extended precision must still be
+    at least twice as close to the oracle as plain bf16 (an fp8 format of too
+    little range would saturate the keys or flush the queries and lose the
+    correction)."""
+    import dataclasses
+    name = "layer_bf16_L64k_d1024"
+    shape = synth.WORKLOADS[name]
+    inp = synth.layer_inputs(shape, synth.WORKLOAD_SEEDS[name])
+    wq, bq = inp["weights"]["q"]
+    wk, bk = inp["weights"]["k"]
+    inp["weights"]["q"] = (wq / 256.0, bq / 256.0)
+    inp["weights"]["k"] = (wk * 256.0, bk * 256.0)
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask)
+    errs = {}
+    for prec in (synth.PRECISION_EXTENDED, synth.PRECISION_BF16):
+        x_out, _ = run_gpu(dataclasses.replace(shape, precision=prec), inp)
+        errs[prec] = assert_close(host(x_out), ref["x_out"], shape.dtype, f"{name} K*256 Q/256 precision {prec} x_out")
+    assert errs[synth.PRECISION_EXTENDED] <= 0.5 * errs[synth.PRECISION_BF16], errs
+
+
 @pytest.mark.parametrize("name", ["layer_bf16_L64k_d1024", "layer_bf16_L1M_d1024"])
 def test_forward_parity_fused_gate(gpu, name):
     """PF_GATE_FUSED at the workload widths (d_fine 1024, P = 64): the 64K-token
