@@ -11,8 +11,9 @@ Extra objects on the same line:
                (a second pass over K calls) and achieved TFLOP/s or GB/s
   variants     the same forward with residual-add injection (Eq. 11), affine
                modulation (Eq. 13) and the per-head gate
-  ceilings     a 1 GiB device copy (achievable HBM rate) and an MFMA-only loop
-               (achievable dense bf16 rate) beside the vendor peaks
+  ceilings     a 1 GiB device copy and a 2 GiB read-only stream (achievable HBM
+               rates) and an MFMA-only loop (achievable dense bf16 rate) beside
+               the vendor peaks
   roofline     the dominant kernel against the MI355X peak of its bound, with
                its matrix-core busy fraction and clock from the committed
                counter summary (while the kernel sources are unchanged)
@@ -328,6 +329,32 @@ def hbm_copy_ceiling():
     del a, b
     torch.cuda.empty_cache()
     return round(2 * n / (best * 1e-3) / 1e9, 1)
+
+
+def hbm_read_ceiling():
+    """Achievable HBM read rate on this device: the library's read probe
+    (grid-strided 16-byte loads, nothing else) over a 2 GiB buffer, 4,096
+    workgroups, ten calls back to back, best of three."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    n, n_wg, calls = 2 << 30, 4096, 10
+    src = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    out = torch.empty(n_wg, dtype=torch.int32, device="cuda")
+    B.ceiling_read(src, out, n_wg)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(3):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(calls):
+            B.ceiling_read(src, out, n_wg)
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / calls
+        best = ms if best is None else min(best, ms)
+    del src, out
+    torch.cuda.empty_cache()
+    return round(n / (best * 1e-3) / 1e9, 1)
 
 
 def mfma_ceiling():
@@ -684,7 +711,8 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "variants": variants,
-        "ceilings": {"hbm_copy_gbs": hbm_copy_ceiling(), "hbm_peak_gbs": PEAK_HBM_GBS,
+        "ceilings": {"hbm_copy_gbs": hbm_copy_ceiling(), "hbm_read_gbs": hbm_read_ceiling(),
+                     "hbm_peak_gbs": PEAK_HBM_GBS,
                      "mfma_loop_bf16_tflops": mfma_ceiling(),
                      "mfma_bf16_peak_tflops": PEAK_BF16_TFLOPS},
     }

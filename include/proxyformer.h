@@ -352,11 +352,25 @@ void proxy_trace_reset(void);
  * iters < 1 (nothing enqueued); PF_ERR_HIP if the launch fails. */
 int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* stream);
 
+/* HBM read ceiling (measurement aid, not part of the layer): enqueues
+ * n_workgroups workgroups of four waves on `stream` that read the `bytes`
+ * bytes at src (device memory, 16-byte aligned, bytes a multiple of 16) with
+ * grid-strided 16-byte loads, four in flight per lane, and nothing else;
+ * workgroup w writes the XOR of every 32-bit word it read to out[w] (a
+ * caller-owned device buffer of n_workgroups uint32), so the XOR over out
+ * equals the XOR of the whole buffer. Timing the call with events on the same
+ * stream gives the read rate a streaming kernel can reach on the device.
+ * PF_ERR_INVALID_ARG for a NULL src or out, bytes zero or not a multiple of
+ * 16, or n_workgroups outside [1, 2^20] (nothing enqueued); PF_ERR_HIP if the
+ * launch fails. */
+int proxy_ceiling_read(const void* src, size_t bytes, void* out, int64_t n_workgroups, void* stream);
+
 /* Message of the last non-OK status on the calling thread. */
 const char* proxy_last_error(void);
 
 /* Library ABI version (major * 100 + minor): 101 adds pf_layer_config.precision
- * and proxy_decode_step_static; 102 adds pf_layer_config.gate_fusion. */
+ * and proxy_decode_step_static; 102 adds pf_layer_config.gate_fusion; 103 adds
+ * proxy_ceiling_read. */
 int proxy_version(void);
 
 #ifdef __cplusplus

@@ -37,7 +37,7 @@ EXPORTS = (
     "proxy_cache_append", "proxy_prefill_workspace_size", "proxy_decode_prefill",
     "proxy_last_error", "proxy_version",
     "proxy_trace_enable", "proxy_trace_collect", "proxy_trace_get", "proxy_trace_reset",
-    "proxy_ceiling_mfma", "proxy_decode_step_static",
+    "proxy_ceiling_mfma", "proxy_decode_step_static", "proxy_ceiling_read",
 )
 
 c_void_p = ctypes.c_void_p
@@ -181,6 +181,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.proxy_trace_reset.restype = None
     lib.proxy_ceiling_mfma.argtypes = [c_void_p, c_int64, c_int32, c_void_p]
     lib.proxy_ceiling_mfma.restype = c_int32
+    lib.proxy_ceiling_read.argtypes = [c_void_p, ctypes.c_size_t, c_void_p, c_int64, c_void_p]
+    lib.proxy_ceiling_read.restype = c_int32
     lib.proxy_decode_step_static.argtypes = [P(PfDecodeConfig), P(PfDecodeWeights), P(PfDecodeState), c_void_p,
                                              c_void_p, c_void_p]
     lib.proxy_decode_step_static.restype = c_int32
@@ -204,6 +206,18 @@ def ceiling_mfma(out, n_workgroups: int, iters: int, stream=None) -> None:
     if out.numel() < n_workgroups * 256 or out.dtype.itemsize != 4 or not out.is_cuda:
         raise ValueError("out must be a device float32 tensor of n_workgroups * 256 elements")
     _check(load().proxy_ceiling_mfma(c_void_p(out.data_ptr()), n_workgroups, iters, c_void_p(_stream(stream))))
+
+
+def ceiling_read(src, out, n_workgroups: int, stream=None) -> None:
+    """Enqueue the HBM read probe (see proxy_ceiling_read) over all bytes of
+    the device tensor src on `stream` (torch's current stream if None); out is
+    a device int32 tensor of at least n_workgroups elements."""
+    if not src.is_cuda or not src.is_contiguous() or (src.numel() * src.element_size()) % 16 != 0:
+        raise ValueError("src must be a contiguous device tensor whose size is a multiple of 16 bytes")
+    if out.numel() < n_workgroups or out.element_size() != 4 or not out.is_cuda:
+        raise ValueError("out must be a device 32-bit tensor of n_workgroups elements")
+    _check(load().proxy_ceiling_read(c_void_p(src.data_ptr()), src.numel() * src.element_size(),
+                                     c_void_p(out.data_ptr()), n_workgroups, c_void_p(_stream(stream))))
 
 
 def trace_enable(on: bool) -> bool:

@@ -50,7 +50,7 @@ static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 extern "C" {
 
-int proxy_version(void) { return 102; }
+int proxy_version(void) { return 103; }
 
 int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* stream) {
   if (!out) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_mfma: out is NULL");
@@ -59,6 +59,15 @@ int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* str
   if (iters < 1) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_mfma: iters must be >= 1");
   return hip_status(launch_mfma_ceiling(static_cast<float*>(out), n_workgroups, iters, (hipStream_t)stream),
                     "proxy_ceiling_mfma");
+}
+
+int proxy_ceiling_read(const void* src, size_t bytes, void* out, int64_t n_workgroups, void* stream) {
+  if (!src || !out) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: src or out is NULL");
+  if (bytes == 0 || bytes % 16 != 0) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: bytes must be a positive multiple of 16");
+  if (n_workgroups < 1 || n_workgroups > (1 << 20))
+    return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: n_workgroups must be in [1, 2^20]");
+  return hip_status(launch_read_ceiling(src, bytes, static_cast<unsigned*>(out), n_workgroups, (hipStream_t)stream),
+                    "proxy_ceiling_read");
 }
 
 const char* proxy_last_error(void) { return g_last_error.c_str(); }

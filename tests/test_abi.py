@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
     assert set(names) == set(B.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.proxy_version() == 102
+    assert lib.proxy_version() == 103
 
 
 def _cfg(**kw):
@@ -311,6 +311,20 @@ def test_mfma_ceiling_rejects_bad_arguments(lib):
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), 0, 10, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), (1 << 20) + 1, 10, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_mfma(ctypes.c_void_p(0x90000), 16, 0, None) == B.PF_ERR_INVALID_ARG
+
+
+def test_read_ceiling_rejects_bad_arguments(lib):
+    """The read probe validates on the host before it launches anything
+    (the pointers are never dereferenced)."""
+    p = ctypes.c_void_p(0x90000)
+    assert lib.proxy_ceiling_read(None, 1024, p, 16, None) == B.PF_ERR_INVALID_ARG
+    assert "NULL" in lib.proxy_last_error().decode()
+    assert lib.proxy_ceiling_read(p, 1024, None, 16, None) == B.PF_ERR_INVALID_ARG
+    assert lib.proxy_ceiling_read(p, 0, p, 16, None) == B.PF_ERR_INVALID_ARG
+    assert lib.proxy_ceiling_read(p, 1000, p, 16, None) == B.PF_ERR_INVALID_ARG
+    assert "multiple of 16" in lib.proxy_last_error().decode()
+    assert lib.proxy_ceiling_read(p, 1024, p, 0, None) == B.PF_ERR_INVALID_ARG
+    assert lib.proxy_ceiling_read(p, 1024, p, (1 << 20) + 1, None) == B.PF_ERR_INVALID_ARG
 
 
 def test_static_decode_step_rejects_before_any_launch(lib):

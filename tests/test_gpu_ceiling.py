@@ -1,4 +1,10 @@
-"""The matrix-core ceiling probe (proxy_ceiling_mfma) through the C ABI.
+"""The ceiling probes (proxy_ceiling_mfma, proxy_ceiling_read) through the C ABI.
+
+Read probe: the XOR over its per-workgroup outputs equals the XOR of every
+32-bit word of the buffer, which shows each word was read exactly once (a
+word read twice or skipped changes the XOR for almost every pattern).
+
+Matrix-core probe:
 
 Every thread's output is predictable on the CPU: each wave multiplies the
 same 32x16 by 16x32 bf16 tiles (lane l supplies row / column l % 32 and
@@ -48,3 +54,17 @@ def test_mfma_ceiling_matches_the_predicted_sums(gpu):
     assert np.isfinite(got).all()
     assert np.abs(got - ref).max() <= 1e-5 * np.abs(ref).max(), np.abs(got - ref).max()
     assert torch.equal(out, again)
+
+
+@pytest.mark.parametrize("words,n_wg", [(4 * 1000, 3), (4 * 256 * 4 * 7 + 12, 5), (1 << 20, 64)])
+def test_read_ceiling_reads_every_word_once(gpu, words, n_wg):
+    import torch
+    from paper_2608_23463_amd import binding as B
+    rng = np.random.default_rng(words + n_wg)
+    host = rng.integers(-(1 << 31), (1 << 31) - 1, size=words, dtype=np.int64).astype(np.int32)
+    src = torch.from_numpy(host).to("cuda")
+    out = torch.zeros(n_wg, dtype=torch.int32, device="cuda")
+    B.ceiling_read(src, out, n_wg)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32))
+    assert got == np.bitwise_xor.reduce(host.view(np.uint32))
