@@ -80,6 +80,8 @@ CASES = {
     "bf16_dh128_factorised": DecodeShape(2, 256, 2, 128, (2, 4), level_dims=(192,), n0=3000, steps=17),
     "bf16_many_splits": DecodeShape(4, 512, 8, 64, (16,), n0=5000, steps=33),
     "bf16_lm_shape": DecodeShape(3, 512, 8, 64, (64,), n0=1100, steps=70),
+    # 37 sequences: the projection kernel's second 32-row block holds 5 rows
+    "bf16_batch_over_32": DecodeShape(37, 128, 2, 64, (4,), n0=9, steps=6),
 }
 
 
