@@ -82,6 +82,10 @@ CASES = {
     "bf16_lm_shape": DecodeShape(3, 512, 8, 64, (64,), n0=1100, steps=70),
     # 37 sequences: the projection kernel's second 32-row block holds 5 rows
     "bf16_batch_over_32": DecodeShape(37, 128, 2, 64, (4,), n0=9, steps=6),
+    # the widest rows a step takes (d_model * element size = 4 KB): four 16-byte chunks per
+    # lane when the projection kernel stages x, and (bf16) a second chunk of weight fragments
+    "bf16_max_width": DecodeShape(2, 2048, 16, 128, (4,), n0=40, steps=9),
+    "fp32_max_width": DecodeShape(2, 1024, 8, 128, (4,), n0=40, steps=9, dtype="fp32"),
 }
 
 

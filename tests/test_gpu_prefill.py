@@ -39,6 +39,7 @@ CASES = {
     "bf16_large_blocks": DecodeShape(2, 256, 4, 64, (16, 16), n0=130, steps=700),
     "fp32_dh128": DecodeShape(2, 256, 2, 128, (8,), n0=70, steps=150, dtype="fp32"),
     "bf16_batch_over_32": DecodeShape(35, 128, 2, 64, (4,), n0=6, steps=9),
+    "bf16_max_width": DecodeShape(2, 2048, 16, 128, (4,), n0=20, steps=14),
 }
 
 
