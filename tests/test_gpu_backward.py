@@ -116,6 +116,9 @@ CASES = {
     "bf16_tc_partial_block": (LayerShape(2, 16 * 37 + 9, 192, 192, 3, 64, (16,)), True),
     "fp32_bi_partial_block_factorised": (LayerShape(1, 8 * 37 + 5, 64, 128, 2, 64, (2, 4), level_dims=(96,),
                                                     dtype="fp32", mask=synth.BIDIRECTIONAL), True),
+    # d_fine a multiple of 8 but not of the K tile: the [X | Delta] split inside a K tile
+    "bf16_odd_width": (LayerShape(2, 16 * 37, 72, 128, 2, 64, (16,)), True),
+    "fp32_odd_width": (LayerShape(1, 16 * 37, 40, 128, 2, 64, (16,), dtype="fp32"), True),
 }
 
 

@@ -59,6 +59,10 @@ SMALL = {
                                   True),
     "bf16_fused_gate_factorised_bi": (LayerShape(1, 64 * 70, 128, 256, 2, 128, (4, 2, 8), level_dims=(128, 192),
                                                  mask=synth.BIDIRECTIONAL, gate_fusion=synth.GATE_FUSED), True),
+    # d_fine a multiple of 8 but not of the K tile (72 bf16, 40 fp32): the gate's [X | Delta]
+    # split falls inside a K tile, and the gate GEMM (N = d_fine) has a partial column tile
+    "bf16_odd_width": (LayerShape(2, 37 * 16, 72, 128, 2, 64, (16,)), True),
+    "fp32_odd_width": (LayerShape(1, 37 * 16, 40, 128, 2, 64, (16,), dtype="fp32"), True),
 }
 
 
