@@ -119,7 +119,11 @@ typedef struct {
  *  d_proxy   proxy width d_M = n_heads * head_dim.
  *  n_levels  M in 1..4; factors[0..M-1] = k_1..k_M, P = prod k_j.
  *  level_dims[j] = d_{j+1} for j < M-1 (0 -> d_proxy); level_dims[M-1] is
- *            ignored (d_M = d_proxy).
+ *            ignored (d_M = d_proxy). Every width is a multiple of 8, and a
+ *            level's grouped row of k_j * d_{j-1} elements spans at most
+ *            8 MiB (bf16: k_j * d_{j-1} <= 4M); larger rows return
+ *            PF_ERR_UNSUPPORTED (a GEMM tile addresses 256 rows through one
+ *            32-bit range).
  *  head_dim  64 or 128.
  *  dtype     pf_dtype; mask pf_mask; injection pf_injection;
  *            precision pf_precision (bf16 mode); gate_fusion pf_gate_fusion.
@@ -211,9 +215,11 @@ int proxy_layer_backward(const pf_layer_config* cfg, const pf_layer_weights* w,
                          void* stream);
 
 /* Decode (generation block of Eq. 19-20 against the proxy cache of Eq. 21).
- *  d_model = n_heads * head_dim; head_dim 64 or 128.
+ *  d_model = n_heads * head_dim; head_dim 64 or 128; d_model * element size
+ *  at most 4096 bytes.
  *  n_levels/factors/level_dims describe the compression C of the append
- *  (as in pf_layer_config with d_fine = d_proxy = d_model). */
+ *  (as in pf_layer_config with d_fine = d_proxy = d_model, including the
+ *  8 MiB bound on a grouped row k_j * d_{j-1}). */
 typedef struct {
   int32_t batch, d_model, n_heads, head_dim, n_levels;
   int32_t factors[PF_MAX_LEVELS];

@@ -63,6 +63,11 @@ int decode_dims(const pf_decode_config* c, DecodeDims* d, const char** why) {
     return *why = "d_model * element size must be at most 4096 bytes (32 staged rows in LDS)", PF_ERR_UNSUPPORTED;
   for (int j = 0; j <= d->M; ++j)
     if (d->dl[j] % 8 != 0) return *why = "every channel width must be a multiple of 8", PF_ERR_UNSUPPORTED;
+  // the append's compression GEMMs take rows of k_j * d_{j-1} elements (at
+  // most 8 MiB: a GEMM tile's 256 rows share one 32-bit buffer range)
+  for (int j = 0; j < d->M; ++j)
+    if ((int64_t)d->k[j] * d->dl[j] * d->esize > kMaxGemmRowBytes)
+      return *why = "a grouped row k_j * d_{j-1} * element size exceeds 8 MiB", PF_ERR_UNSUPPORTED;
   const int64_t lvl1_rows_per_block = d->P / d->k[0];
   d->append_rows = (int)std::max<int64_t>(1, std::min<int64_t>(4096, 65536 / lvl1_rows_per_block));
   return PF_OK;

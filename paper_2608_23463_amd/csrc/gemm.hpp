@@ -37,6 +37,11 @@ namespace pf {
 
 enum { LAYOUT_K = 0, LAYOUT_MN = 1 };
 
+// Longest operand row (bytes) a GEMM takes: a tile addresses up to 256 rows
+// through one 32-bit buffer range that must stay below the out-of-range
+// offset kOOB = 2^31.
+constexpr int64_t kMaxGemmRowBytes = (int64_t)1 << 23;
+
 struct GemmParams {
   const void* a;
   int64_t lda;

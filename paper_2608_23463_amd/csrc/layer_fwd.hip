@@ -233,8 +233,15 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
     return *why = "one head's proxy tensors exceed 2 GiB (m * head_dim * element size)", PF_ERR_UNSUPPORTED;
   for (int j = 0; j <= d->M; ++j)
     if (d->d[j] % 8 != 0) return *why = "every channel width must be a multiple of 8", PF_ERR_UNSUPPORTED;
+  // A GEMM tile reaches up to 256 rows of an operand through one 32-bit
+  // buffer range whose out-of-range offset is 2^31, so an operand row (a
+  // level's grouped row of k_j * d_{j-1} elements, the gate's 2 * d_fine) may
+  // span at most 8 MiB.
   for (int j = 0; j < d->M; ++j)
-    if ((int64_t)d->k[j] * d->d[j] > INT32_MAX / 2) return *why = "k_j * d_j too large", PF_ERR_UNSUPPORTED;
+    if ((int64_t)d->k[j] * d->d[j] * d->esize > kMaxGemmRowBytes)
+      return *why = "a grouped row k_j * d_{j-1} * element size exceeds 8 MiB", PF_ERR_UNSUPPORTED;
+  if ((int64_t)2 * d->d_f * d->esize > kMaxGemmRowBytes)
+    return *why = "2 * d_fine * element size exceeds 8 MiB", PF_ERR_UNSUPPORTED;
   if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
   d->fused_gate = c->gate_fusion == PF_GATE_FUSED && d->esize == 2 && c->injection == PF_INJECT_GATED &&
                   fused_gate_supported(d->d_f, d->d[1]);

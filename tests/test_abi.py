@@ -109,6 +109,22 @@ def test_forward_rejects_oversize_head_before_any_launch(lib):
     assert B.layer_workspace_size(ok) > 0
 
 
+def test_grouped_rows_beyond_the_gemm_range_are_rejected(lib):
+    """A GEMM tile addresses 256 operand rows through one 32-bit range below
+    the 2^31 out-of-range offset: a level's grouped row (k_j * d_{j-1}
+    elements) may span at most 8 MiB. P * d_fine = 4M bf16 elements (8 MiB)
+    fits; 4M + 256 does not, nor 2M fp32 + 64, nor a second level's row."""
+    ok = _cfg(seq_len=4096 * 2, d_fine=1024, d_proxy=256, factors=(4096,))
+    assert B.layer_workspace_size(ok) > 0
+    for bad in (dict(seq_len=4096 * 2, d_fine=1024 + 8, d_proxy=256, factors=(4096,)),
+                dict(seq_len=2048 * 2, d_fine=1024 + 8, d_proxy=256, factors=(2048,), dtype="fp32"),
+                dict(seq_len=64 * 8192, d_fine=64, d_proxy=256, factors=(64, 8192), level_dims=(1032,))):
+        cfg = _cfg(**bad)
+        assert _fwd(lib, cfg, _weights_struct(len(bad["factors"]))) == B.PF_ERR_UNSUPPORTED, bad
+        assert "8 MiB" in B.last_error(), bad
+        assert B.layer_workspace_size(cfg) == 0 and B.layer_saved_size(cfg) == 0
+
+
 def test_plain_bf16_precision_drops_the_low_parts(lib):
     # the low parts of H, Q and K (and the doubled K of the Q/K GEMMs) exist
     # only with PF_PRECISION_EXTENDED in bf16 mode
@@ -197,6 +213,19 @@ def _dweights():
 
 def _dstate(n=0, n_cap=4, j=0):
     return B.PfDecodeState(0x20000, 0x30000, n_cap, n, 0x40000, 0x50000, 0x60000, j)
+
+
+def test_decode_rejects_grouped_rows_beyond_the_gemm_range(lib):
+    """The append's compression GEMMs take rows of k_j * d_{j-1} elements:
+    at most 8 MiB (P = 4096 at d_model 1024 in bf16 fits, P = 8192 does not)."""
+    ok = _dcfg(d_model=1024, n_heads=16, factors=(4096,))
+    assert int(lib.proxy_decode_workspace_size(ctypes.byref(ok))) > 0
+    bad = _dcfg(d_model=1024, n_heads=16, factors=(8192,))
+    assert int(lib.proxy_decode_workspace_size(ctypes.byref(bad))) == 0
+    st = _dstate()
+    assert lib.proxy_decode_step(ctypes.byref(bad), ctypes.byref(_dweights()), ctypes.byref(st), 0x70000, 0x80000,
+                                 0x90000, 1 << 40, None) == B.PF_ERR_UNSUPPORTED
+    assert "8 MiB" in B.last_error()
 
 
 def test_decode_validation(lib):
