@@ -341,8 +341,10 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
 
     Given dY = dL/dX_out [B, L, d_fine] and optionally dH_out [B, m, d_proxy],
     returns dx, dh_in (None when h_in is None), every weight and bias gradient
-    summed over the batch in the layout of the weights, and the gradients of
-    the projections Q, K, V per proxy ("proj_grads", [B, m, d_proxy] each).
+    summed over the batch in the layout of the weights, the gradients of
+    the projections Q, K, V per proxy ("proj_grads", [B, m, d_proxy] each),
+    and for the gated injections the per-column sums over tokens of |dG|
+    ("gate_abs"), the magnitude of the terms the gate bias gradient sums.
     """
     dy = _f64(dy)
     bsz, seq, d_f = dy.shape
@@ -374,6 +376,9 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
     d_p = weights["q"][0].shape[0]
     dh_in = None if h_in is None else np.zeros((bsz, m, d_p))
     proj_grads = {name: np.zeros((bsz, m, d_p)) for name in ("q", "k", "v")}
+    # per gate column, the sum over tokens of |dG|: the scale of the terms the
+    # gate's bias gradient adds up (its accuracy is relative to this scale)
+    gate_abs = np.zeros(_f64(weights["gate"][0]).shape[0]) if gr["gate"] is not None else None
     for b in range(bsz):
         kp = fwd["kept"][b]
         xb, delta, g = kp["x"], kp["delta"], kp["g"]
@@ -392,6 +397,7 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             dxb = dy[b] + dg @ wg[:, :d_f]
             gr["gate"][0] += dg.T @ np.concatenate([xb, delta], axis=1)
             gr["gate"][1] += dg.sum(axis=0)
+            gate_abs += np.abs(dg).sum(axis=0)
         elif injection == INJECT_AFFINE:
             # Eq. 13: Y = (1 + s) * N + t, N = X r, r = (mean(X^2) + eps)^(-1/2)
             wa = _f64(weights["affine"][0])
@@ -412,6 +418,7 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             dxb = dy[b] + dg @ wg[:, :d_f]
             gr["gate"][0] += dg.T @ np.concatenate([xb, delta], axis=1)
             gr["gate"][1] += dg.sum(axis=0)
+            gate_abs += np.abs(dg).sum(axis=0)
         # Eq. 17 in reverse: level j = 1..M (the forward ran M..1)
         du = ddelta
         for j in range(nlev):
@@ -447,7 +454,8 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             gr["compress"][j][1] += dz.sum(axis=0)
             dz = ungroup_rows(dz @ _f64(weights["compress"][j][0]), factors[j])
         dx[b] = dxb + dz
-    return {"dx": dx, "dh_in": dh_in, "grads": gr, "proj_grads": proj_grads}
+    return {"dx": dx, "dh_in": dh_in, "grads": gr, "proj_grads": proj_grads,
+            "gate_abs": gate_abs if injection in (INJECT_GATED, INJECT_GATED_HEAD) else None}
 
 
 def patch_order(height: int, width: int, p: int):
