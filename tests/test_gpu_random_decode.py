@@ -7,7 +7,9 @@ free middle widths, empty, short and long caches, and step counts that
 cross block boundaries (so appends happen mid-run), in bf16 and fp32. Decode
 outputs of every step, appended cache rows and the counters are compared with
 the oracle; prefill of the same stream in one call, its state, and three
-decode steps after it likewise.
+decode steps after it likewise; and batches with per-sequence positions
+(random cache lengths and block fill), each sequence against the oracle
+run on it alone.
 """
 import dataclasses
 import math
@@ -19,7 +21,7 @@ import oracle
 from cache_cases import oracle_state
 from paper_2608_23463_amd import synth
 from paper_2608_23463_amd.synth import DecodeShape
-from helpers import assert_close, dev, host
+from helpers import assert_close, dev, dev_weights, host
 from test_gpu_decode import make_session, run_and_compare
 from test_gpu_prefill import chunk, compare_state
 
@@ -88,3 +90,67 @@ def test_prefill_parity_random_shape(gpu, i):
     got = [host(sess.step(dev(more[t], shape.dtype))) for t in range(3)]
     want = [oracle.decode_step(st, inp["weights"], shape.factors, more[t], shape.rms_eps) for t in range(3)]
     assert_close(np.stack(got), np.stack(want), shape.dtype, f"random prefill {i} decode after prefill")
+
+
+N_RAGGED = 6
+
+
+def draw_ragged(i: int):
+    """A random batch with per-sequence positions: cache lengths 0..300,
+    local-block fill 0..P-1, 1-64 sequences (the per-sequence limit)."""
+    rng = np.random.default_rng(20261206 + i)
+    while True:
+        dtype = "fp32" if rng.random() < 0.3 else "bf16"
+        dh = int(rng.choice([64, 128]))
+        nh = int(rng.integers(1, 4))
+        factors = tuple(int(rng.choice([1, 2, 3, 4, 8])) for _ in range(int(rng.integers(1, 3))))
+        if math.prod(factors) <= 32:
+            break
+    P = math.prod(factors)
+    b = int(rng.integers(1, 65))
+    steps = int(rng.integers(1, 2 * P + 6))
+    n0 = rng.integers(0, 300, size=b).astype(np.int64)
+    n0[rng.random(b) < 0.2] = 0
+    j0 = rng.integers(0, P, size=b).astype(np.int32)
+    cap = int(n0.max()) + (steps + P) // P + 1
+    shape = DecodeShape(b, nh * dh, nh, dh, factors, n0=0, steps=steps, n_cap=cap, dtype=dtype)
+    return shape, n0, j0, rng
+
+
+@pytest.mark.parametrize("i", range(N_RAGGED))
+def test_ragged_decode_parity_random(gpu, i):
+    """Per-sequence positions drawn at random; each sequence must match the
+    oracle decoding that sequence alone, with its own appends."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    shape, n0, j0, rng = draw_ragged(i)
+    print(f"[random ragged {i}] {shape} n0={n0.tolist()} j0={j0.tolist()}", flush=True)
+    P, h, dh, d, b = shape.block, shape.n_heads, shape.head_dim, shape.d_model, shape.batch
+    inp = synth.decode_inputs(shape, 5000 + i)
+    rnd = (lambda a: synth.bf16_round(a)) if shape.dtype == "bf16" else (lambda a: a)
+    kc = rnd(rng.standard_normal((b, h, shape.capacity, dh)).astype(np.float32))
+    vc = rnd(rng.standard_normal((b, h, shape.capacity, dh)).astype(np.float32))
+    x_blk = rnd(rng.standard_normal((b, P, d)).astype(np.float32))
+    k_loc = rnd(rng.standard_normal((b, h, P, dh)).astype(np.float32))
+    v_loc = rnd(rng.standard_normal((b, h, P, dh)).astype(np.float32))
+    cfg = B.decode_config(b, d, h, dh, shape.factors, (), shape.dtype, shape.rms_eps)
+    sess = B.DecodeSession(cfg, dev_weights(inp["weights"], shape.dtype), dev(kc, shape.dtype),
+                           dev(vc, shape.dtype), ragged=True, n_seq=n0, j_seq=j0)
+    sess.x_blk.copy_(dev(x_blk, shape.dtype))
+    sess.k_loc.copy_(dev(k_loc, shape.dtype))
+    sess.v_loc.copy_(dev(v_loc, shape.dtype))
+    got = np.stack([host(sess.step(dev(inp["x"][t], shape.dtype))) for t in range(shape.steps)])
+    torch.cuda.synchronize()
+    kc_after, vc_after = host(sess.k_cache), host(sess.v_cache)
+    for s in range(b):
+        st = oracle.DecodeState(kc[s:s + 1].astype(np.float64), vc[s:s + 1].astype(np.float64), int(n0[s]),
+                                x_blk[s:s + 1].astype(np.float64), k_loc[s:s + 1].astype(np.float64),
+                                v_loc[s:s + 1].astype(np.float64), int(j0[s]))
+        ref = np.stack([oracle.decode_step(st, inp["weights"], shape.factors, inp["x"][t][s:s + 1], shape.rms_eps)
+                        for t in range(shape.steps)])
+        assert_close(got[:, s:s + 1], ref, shape.dtype, f"random ragged {i} sequence {s} y")
+        assert sess.n_seq[s] == st.n and sess.j_seq[s] == st.j, (s, sess.n_seq[s], sess.j_seq[s], st.n, st.j)
+        new = slice(int(n0[s]), st.n)
+        assert_close(kc_after[s:s + 1, :, new], st.k_cache[:, :, new], shape.dtype, f"ragged {i}/{s} K rows")
+        assert_close(vc_after[s:s + 1, :, new], st.v_cache[:, :, new], shape.dtype, f"ragged {i}/{s} V rows")
+        assert np.array_equal(kc_after[s, :, st.n:], kc[s, :, st.n:])
