@@ -7,7 +7,8 @@ the tiles, 1-3 heads of 64 or 128 channels, partial last blocks, all three
 masks, all four injections, both precisions and both gate kernels, one or two
 sequences, with and without H_in. Every shape is within the library's
 documented limits; forward outputs and (for a subset) every gradient are
-compared with the oracle at the usual tolerances.
+compared with the oracle at the usual tolerances. Random image layers (p x p
+patches, Sec. 3.9) are checked forward and backward as well.
 """
 import math
 
@@ -113,3 +114,48 @@ def test_backward_parity_random_shape(gpu, i):
     ref = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask,
                                 inp["h_in"], dh_out, injection=shape.injection)
     compare(shape, inp, res, ref, f"random {i}")
+
+
+N_IMAGES = 8
+
+
+def draw_image(i: int):
+    """A random image layer (Sec. 3.9): p x p patches (p in 1..8), a grid of
+    1..12 x 1..12 patches, random widths, heads, mask, injection and dtype."""
+    rng = np.random.default_rng(20261207 + i)
+    while True:
+        dtype = "fp32" if rng.random() < 0.3 else "bf16"
+        p = int(rng.integers(1, 9))
+        gw, gh = int(rng.integers(1, 13)), int(rng.integers(1, 13))
+        dh = int(rng.choice([64, 128]))
+        nh = int(rng.integers(1, 4))
+        d_f = 8 * int(rng.integers(1, 40))
+        injection = int(rng.integers(0, 4))
+        if injection == synth.INJECT_GATED_HEAD and (d_f % nh or (d_f // nh) % 8):
+            continue
+        return LayerShape(int(rng.integers(1, 3)), gw * p * gh * p, d_f, nh * dh, nh, dh, (p * p,), (), dtype,
+                          mask=int(rng.integers(0, 3)), injection=injection, image_width=gw * p,
+                          precision=int(rng.integers(0, 2)) if dtype == "bf16" else synth.PRECISION_EXTENDED)
+
+
+@pytest.mark.parametrize("i", range(N_IMAGES))
+def test_image_partition_parity_random(gpu, i):
+    """Forward and backward of a random image layer against the oracle's
+    gather -> layer -> scatter form."""
+    from paper_2608_23463_amd import binding as B
+    import torch
+    shape = draw_image(i)
+    print(f"[random image {i}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, 6000 + i, with_dy=True, with_h_in=True)
+    sharpen(shape, inp)
+    x_out, h_out, _ = B.layer_forward(B.config_from_shape(shape), dev_weights(inp["weights"], shape.dtype),
+                                      dev(inp["x"], shape.dtype), dev(inp["h_in"], shape.dtype))
+    torch.cuda.synchronize()
+    ref = oracle.layer_forward_2d(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.image_width,
+                                  shape.mask, inp["h_in"], injection=shape.injection)
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"random image {i} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"random image {i} x_out")
+    res = run_gpu_backward(shape, inp)
+    refb = oracle.layer_backward_2d(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.image_width,
+                                    inp["dy"], shape.mask, inp["h_in"], None, injection=shape.injection)
+    compare(shape, inp, res, refb, f"random image {i}")
