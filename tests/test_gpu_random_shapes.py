@@ -159,3 +159,50 @@ def test_image_partition_parity_random(gpu, i):
     refb = oracle.layer_backward_2d(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.image_width,
                                     inp["dy"], shape.mask, inp["h_in"], None, injection=shape.injection)
     compare(shape, inp, res, refb, f"random image {i}")
+
+
+N_FUSED = 8
+
+
+def draw_fused(i: int):
+    """A random layer that takes the fused decompression + gate kernel (bf16,
+    gated, d_fine a multiple of 128, level-1 input width a multiple of 64 and
+    at least 128): 1-2 levels, partial blocks, all masks, both precisions."""
+    rng = np.random.default_rng(20261208 + i)
+    while True:
+        levels = int(rng.integers(1, 3))
+        factors = tuple(int(rng.choice([1, 2, 3, 4, 8])) for _ in range(levels))
+        block = math.prod(factors)
+        if block <= 64:
+            break
+    dh = int(rng.choice([64, 128]))
+    nh = int(rng.integers(1, 4))
+    level_dims = tuple(64 * int(rng.integers(2, 6)) for _ in range(levels - 1))
+    m = int(rng.integers(1, 200))
+    tail = int(rng.integers(1, block)) if block > 1 and rng.random() < 0.4 else 0
+    return LayerShape(int(rng.integers(1, 3)), (m - 1) * block + tail if tail else m * block,
+                      128 * int(rng.integers(1, 5)), nh * dh, nh, dh, factors, level_dims, "bf16",
+                      mask=int(rng.integers(0, 3)), precision=int(rng.integers(0, 2)),
+                      gate_fusion=synth.GATE_FUSED)
+
+
+@pytest.mark.parametrize("i", range(N_FUSED))
+def test_fused_gate_parity_random(gpu, i):
+    """Forward and backward through the fused decompression + gate kernel
+    (the forward saves Delta and G for the backward)."""
+    from paper_2608_23463_amd import binding as B
+    import torch
+    shape = draw_fused(i)
+    print(f"[random fused {i}] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, 7000 + i, with_dy=True, with_h_in=i % 2 == 0)
+    sharpen(shape, inp)
+    x_out, h_out, _ = B.layer_forward(B.config_from_shape(shape), dev_weights(inp["weights"], shape.dtype),
+                                      dev(inp["x"], shape.dtype), dev(inp["h_in"], shape.dtype))
+    torch.cuda.synchronize()
+    ref = oracle.layer_forward(inp["x"], inp["weights"], shape.factors, shape.n_heads, shape.mask, inp["h_in"])
+    assert_close(host(h_out), ref["h_out"], shape.dtype, f"random fused {i} h_out")
+    assert_close(host(x_out), ref["x_out"], shape.dtype, f"random fused {i} x_out")
+    res = run_gpu_backward(shape, inp)
+    refb = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask,
+                                 inp["h_in"], None)
+    compare(shape, inp, res, refb, f"random fused {i}")
