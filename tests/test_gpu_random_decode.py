@@ -7,9 +7,10 @@ free middle widths, empty, short and long caches, and step counts that
 cross block boundaries (so appends happen mid-run), in bf16 and fp32. Decode
 outputs of every step, appended cache rows and the counters are compared with
 the oracle; prefill of the same stream in one call, its state, and three
-decode steps after it likewise; and batches with per-sequence positions
+decode steps after it likewise; batches with per-sequence positions
 (random cache lengths and block fill), each sequence against the oracle
-run on it alone.
+run on it alone; appends of many blocks at once; and a stream prefilled in
+random chunks against one prefill, bit for bit.
 """
 import dataclasses
 import math
@@ -154,3 +155,74 @@ def test_ragged_decode_parity_random(gpu, i):
         assert_close(kc_after[s:s + 1, :, new], st.k_cache[:, :, new], shape.dtype, f"ragged {i}/{s} K rows")
         assert_close(vc_after[s:s + 1, :, new], st.v_cache[:, :, new], shape.dtype, f"ragged {i}/{s} V rows")
         assert np.array_equal(kc_after[s, :, st.n:], kc[s, :, st.n:])
+
+
+N_APPEND = 6
+
+
+@pytest.mark.parametrize("i", range(N_APPEND))
+def test_append_parity_random(gpu, i):
+    """proxy_cache_append of 1-80 whole blocks per sequence at once (the
+    prefill of a history), random factorisation, widths and dtype."""
+    import torch
+    rng = np.random.default_rng(20261209 + i)
+    while True:
+        levels = int(rng.integers(1, 4))
+        factors = tuple(int(rng.choice([1, 2, 3, 4, 8])) for _ in range(levels))
+        if math.prod(factors) <= 64:
+            break
+    dtype = "fp32" if rng.random() < 0.3 else "bf16"
+    dh = int(rng.choice([64, 128]))
+    nh = int(rng.integers(1, 4))
+    nblk = int(rng.integers(1, 81))
+    n0 = int(rng.integers(0, 50))
+    shape = DecodeShape(int(rng.integers(1, 20)), nh * dh, nh, dh, factors,
+                        tuple(8 * int(rng.integers(2, 33)) for _ in range(levels - 1)),
+                        n0=n0, steps=0, n_cap=n0 + nblk + 1, dtype=dtype)
+    print(f"[random append {i}] {shape} nblk={nblk}", flush=True)
+    inp = synth.decode_inputs(shape, 8000 + i)
+    sess = make_session(shape, inp)
+    xb = rng.standard_normal((shape.batch, nblk * shape.block, shape.d_model)).astype(np.float32)
+    if dtype == "bf16":
+        xb = synth.bf16_round(xb)
+    sess.append(dev(xb, dtype), nblk)
+    torch.cuda.synchronize()
+    st = oracle_state(shape, inp, range(shape.batch))
+    oracle.cache_append(st, inp["weights"], shape.factors, xb)
+    assert sess.n == st.n == n0 + nblk
+    assert_close(host(sess.k_cache)[:, :, :st.n], st.k_cache[:, :, :st.n], dtype, f"random append {i} K")
+    assert_close(host(sess.v_cache)[:, :, :st.n], st.v_cache[:, :, :st.n], dtype, f"random append {i} V")
+
+
+N_CHUNKED = 4
+
+
+@pytest.mark.parametrize("i", range(N_CHUNKED))
+def test_chunked_prefill_random(gpu, i):
+    """A token stream prefilled in random chunks (whole blocks, then a ragged
+    tail) gives the same outputs and state as one prefill, bit for bit."""
+    import torch
+    rng = np.random.default_rng(20261210 + i)
+    factors = tuple(int(rng.choice([2, 4, 8])) for _ in range(int(rng.integers(1, 3))))
+    P = math.prod(factors)
+    nblocks = int(rng.integers(2, 12))
+    tail = int(rng.integers(0, P))
+    shape = DecodeShape(int(rng.integers(1, 6)), 128, 2, 64, factors, n0=int(rng.integers(0, 100)),
+                        steps=nblocks * P + tail)
+    print(f"[random chunked prefill {i}] {shape}", flush=True)
+    inp = synth.decode_inputs(shape, 9000 + i)
+    xs = dev(chunk(inp), shape.dtype)
+    a = make_session(shape, inp)
+    ya = a.prefill(xs)
+    b = make_session(shape, inp)
+    cuts = sorted(rng.choice(np.arange(1, nblocks), size=int(rng.integers(1, nblocks)), replace=False).tolist())
+    edges = [0] + [c * P for c in cuts] + [shape.steps]
+    parts = [b.prefill(xs[:, lo:hi].contiguous()) for lo, hi in zip(edges[:-1], edges[1:])]
+    torch.cuda.synchronize()
+    assert torch.equal(ya, torch.cat(parts, dim=1)), edges
+    assert (a.n, a.j) == (b.n, b.j)
+    n, j = a.n, a.j
+    assert torch.equal(a.k_cache[:, :, :n], b.k_cache[:, :, :n]) and torch.equal(a.v_cache[:, :, :n], b.v_cache[:, :, :n])
+    if j:
+        assert torch.equal(a.x_blk[:, :j], b.x_blk[:, :j])
+        assert torch.equal(a.k_loc[:, :, :j], b.k_loc[:, :, :j]) and torch.equal(a.v_loc[:, :, :j], b.v_loc[:, :, :j])
