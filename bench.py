@@ -16,7 +16,8 @@ Extra objects on the same line:
                the vendor peaks
   roofline     the dominant kernel against the MI355X peak of its bound, with
                its matrix-core busy fraction and clock from the committed
-               counter summary (while the kernel sources are unchanged)
+               counter summary (while the kernel sources are unchanged) and
+               the socket power under sustained forwards (amd-smi, if present)
   decode       proxy-KV decode tokens/s: 32 sequences, 16,384 cached proxy
                rows each, 256 new tokens per sequence including the 4
                block-triggered appends
@@ -208,6 +209,56 @@ def kernel_table(tr, flops, steps, counters: bool):
     return kernels
 
 
+def socket_power(call, seconds=2.5):
+    """Socket power of GPU 0 (W, from `amd-smi metric -p -g 0`) while `call`
+    runs back to back for about `seconds`: one reading before the load and
+    the median and maximum of the readings taken after the first 0.75 s of
+    load (the tool's figure lags by a few hundred milliseconds). None where
+    amd-smi is not available or prints no socket power."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+    import torch
+    exe = shutil.which("amd-smi")
+    if exe is None:
+        return None
+
+    def read():
+        try:
+            r = subprocess.run([exe, "metric", "-p", "-g", "0"], capture_output=True, text=True, timeout=10)
+        except (OSError, subprocess.SubprocessError):
+            return None
+        m = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", r.stdout)
+        return float(m.group(1)) if m else None
+
+    idle = read()
+    samples = []
+    stop = threading.Event()
+    t0 = time.time()
+
+    def sampler():
+        while not stop.is_set():
+            v = read()
+            if v is not None and time.time() - t0 > 0.75:
+                samples.append(v)
+            time.sleep(0.2)
+
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    while time.time() - t0 < seconds:
+        for _ in range(10):
+            call()
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=15)
+    if not samples:
+        return None
+    samples.sort()
+    return {"gpu": 0, "before_load_w": idle, "under_load_median_w": samples[len(samples) // 2],
+            "under_load_max_w": samples[-1], "readings": len(samples), "load": "layer forwards back to back"}
+
+
 def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     import torch
     from paper_2608_23463_amd import binding as B
@@ -250,6 +301,9 @@ def bench_layer(steps, warmup, workload=LAYER_WORKLOAD):
     mf = measured_mfma(dom) if headline else None
     if mf:
         roof["mfma_util_counters"], roof["clock_ghz_counters"] = mf
+    if headline:
+        log("sampling socket power under sustained forwards")
+        roof["socket_power"] = socket_power(forward(cfg))
 
     def entry(ms_v, **extra):
         return {"ms_per_step": round(ms_v, 4), "value": round(tokens / (ms_v * 1e-3), 1), "unit": "tokens/s",
