@@ -366,9 +366,9 @@ int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* str
  * caller-owned device buffer of n_workgroups uint32), so the XOR over out
  * equals the XOR of the whole buffer. Timing the call with events on the same
  * stream gives the read rate a streaming kernel can reach on the device.
- * PF_ERR_INVALID_ARG for a NULL src or out, bytes zero or not a multiple of
- * 16, or n_workgroups outside [1, 2^20] (nothing enqueued); PF_ERR_HIP if the
- * launch fails. */
+ * PF_ERR_INVALID_ARG for a NULL or misaligned src, a NULL out, bytes zero or
+ * not a multiple of 16, or n_workgroups outside [1, 2^20] (nothing enqueued);
+ * PF_ERR_HIP if the launch fails. */
 int proxy_ceiling_read(const void* src, size_t bytes, void* out, int64_t n_workgroups, void* stream);
 
 /* Message of the last non-OK status on the calling thread. */

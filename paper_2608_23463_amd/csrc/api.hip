@@ -63,6 +63,7 @@ int proxy_ceiling_mfma(void* out, int64_t n_workgroups, int32_t iters, void* str
 
 int proxy_ceiling_read(const void* src, size_t bytes, void* out, int64_t n_workgroups, void* stream) {
   if (!src || !out) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: src or out is NULL");
+  if (!aligned16(src)) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: src must be 16-byte aligned");
   if (bytes == 0 || bytes % 16 != 0) return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: bytes must be a positive multiple of 16");
   if (n_workgroups < 1 || n_workgroups > (1 << 20))
     return fail(PF_ERR_INVALID_ARG, "proxy_ceiling_read: n_workgroups must be in [1, 2^20]");

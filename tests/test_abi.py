@@ -349,6 +349,8 @@ def test_read_ceiling_rejects_bad_arguments(lib):
     assert lib.proxy_ceiling_read(None, 1024, p, 16, None) == B.PF_ERR_INVALID_ARG
     assert "NULL" in lib.proxy_last_error().decode()
     assert lib.proxy_ceiling_read(p, 1024, None, 16, None) == B.PF_ERR_INVALID_ARG
+    assert lib.proxy_ceiling_read(ctypes.c_void_p(0x90008), 1024, p, 16, None) == B.PF_ERR_INVALID_ARG
+    assert "aligned" in lib.proxy_last_error().decode()
     assert lib.proxy_ceiling_read(p, 0, p, 16, None) == B.PF_ERR_INVALID_ARG
     assert lib.proxy_ceiling_read(p, 1000, p, 16, None) == B.PF_ERR_INVALID_ARG
     assert "multiple of 16" in lib.proxy_last_error().decode()
