@@ -117,6 +117,16 @@ def _fresh(t):
     return t
 
 
+def _fresh_on(t, stream):
+    """_fresh with the fill enqueued on `stream` (the stream the library call
+    that reads the buffer runs on; None = the current stream)."""
+    if _poison and stream is not None:
+        import torch
+        with torch.cuda.stream(stream):
+            return _fresh(t)
+    return _fresh(t)
+
+
 def _empty(shape, dtype, device):
     import torch
     return _fresh(torch.empty(shape, dtype=dtype, device=device))
@@ -470,7 +480,7 @@ class DecodeSession:
     def step(self, x_t, y_t=None, stream=None):
         if y_t is None:
             y_t = _empty(x_t.shape, x_t.dtype, x_t.device)
-        _fresh(self.workspace)
+        _fresh_on(self.workspace, stream)
         _check(load().proxy_decode_step(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),
                                         ctypes.byref(self.state), _ptr(x_t), _ptr(y_t),
                                         _ptr(self.workspace), self.workspace.numel(), _stream(stream)))
@@ -496,14 +506,14 @@ class DecodeSession:
             raise ProxyFormerError(-2, "prefill sizes beyond the library's limits")
         if getattr(self, "prefill_ws", None) is None or self.prefill_ws.numel() < need:
             self.prefill_ws = _bytes(need, x.device)
-        _fresh(self.prefill_ws)
+        _fresh_on(self.prefill_ws, stream)
         _check(lib.proxy_decode_prefill(ctypes.byref(self.cfg), ctypes.byref(self.wstruct), ctypes.byref(self.state),
                                         _ptr(x), x.shape[1], _ptr(y), _ptr(self.prefill_ws),
                                         self.prefill_ws.numel(), _stream(stream)))
         return y
 
     def append(self, x_blocks, nblk: int, stream=None):
-        _fresh(self.workspace)
+        _fresh_on(self.workspace, stream)
         _check(load().proxy_cache_append(ctypes.byref(self.cfg), ctypes.byref(self.wstruct),
                                          ctypes.byref(self.state), _ptr(x_blocks), nblk,
                                          _ptr(self.workspace), self.workspace.numel(), _stream(stream)))

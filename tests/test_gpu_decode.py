@@ -204,6 +204,50 @@ def test_ragged_mode_with_equal_positions_is_lockstep_bitwise(gpu):
     assert torch.equal(a.k_cache[:, :, :n], b.k_cache[:, :, :n]) and torch.equal(a.v_cache[:, :, :n], b.v_cache[:, :, :n])
 
 
+
+@pytest.mark.parametrize("name,cut", [("bf16_batch_over_32", 32), ("bf16_batch_over_32", 17), ("fp32_small", 1),
+                                      ("bf16_lm_shape", 2)])
+def test_batch_split_is_bitwise_invariant(gpu, name, cut):
+    """Sequences are independent (Eq. 19-21 act per sequence): decoding the
+    batch as two sessions of cut and B - cut sequences, each on its own
+    stream and running concurrently, gives the one-session outputs and cache
+    rows bit for bit (appends included); a row of one sequence read or
+    written for another, or the 32-row blocks of the projections mixing
+    rows, would show here."""
+    import torch
+    from paper_2608_23463_amd import binding as B
+    shape = CASES[name]
+    inp = synth.decode_inputs(shape, 11)
+    full = make_session(shape, inp)
+    w = dev_weights(inp["weights"], shape.dtype)
+    kc, vc = full.k_cache.clone(), full.v_cache.clone()
+    halves = []
+    for lo, hi in ((0, cut), (cut, shape.batch)):
+        cfg = B.decode_config(hi - lo, shape.d_model, shape.n_heads, shape.head_dim, shape.factors,
+                              shape.level_dims, shape.dtype, shape.rms_eps)
+        halves.append((B.DecodeSession(cfg, w, kc[lo:hi], vc[lo:hi], n=inp["n0"]), lo, hi, torch.cuda.Stream()))
+    main = torch.cuda.current_stream()
+    for t in range(shape.steps):
+        x = dev(inp["x"][t], shape.dtype)
+        y_full = full.step(x)
+        y_split = torch.full_like(x, float("nan"))
+        start = torch.cuda.Event()
+        start.record(main)
+        for sess, lo, hi, stream in halves:
+            stream.wait_event(start)
+            with torch.cuda.stream(stream):
+                sess.step(x[lo:hi], y_split[lo:hi], stream=stream)
+        for _, _, _, stream in halves:
+            done = torch.cuda.Event()
+            done.record(stream)
+            main.wait_event(done)
+        torch.cuda.synchronize()
+        assert torch.equal(y_full, y_split), f"{name} cut {cut}: step {t}"
+    n = full.n
+    assert all(sess.n == n and sess.j == full.j for sess, _, _, _ in halves)
+    assert torch.equal(full.k_cache[:, :, :n], kc[:, :, :n]) and torch.equal(full.v_cache[:, :, :n], vc[:, :, :n])
+
+
 def run_gpu_steps(shape, inp):
     import torch
     sess = make_session(shape, inp)
