@@ -189,8 +189,9 @@ struct LoaderMN {
   }
 
   __device__ __forceinline__ void fetch(u32x4 (&r)[kLoads], int k0, int kend) const {
-    // K rows at or beyond kend fall outside the descriptor's range
-    const rsrc_t rs = make_rsrc(src + (int64_t)k0 * ld_bytes, (uint32_t)(max(0, kend - k0) * ld_bytes));
+    // the range covers this step's K rows below kend only, so it stays below
+    // kOOB (idle blocks) however long K is
+    const rsrc_t rs = make_rsrc(src + (int64_t)k0 * ld_bytes, (uint32_t)(max(0, min(BK, kend - k0)) * ld_bytes));
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) r[i] = buf_ld16(rs, voff[i]);
   }

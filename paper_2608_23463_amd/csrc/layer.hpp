@@ -102,6 +102,12 @@ constexpr int kColsumChunks = 512;
 // Weight and data gradients over at least this many rows run on transposed
 // (K-contiguous) operand copies through the direct GEMM kernel.
 constexpr int64_t kTransposeMinRows = 8192;
+// fp32 weight gradients: a transposed copy's rows are runs of `rows` tokens,
+// and a K-contiguous GEMM operand row may span at most 8 MiB (256 tile rows
+// in one 32-bit buffer range), so longer runs keep the M/N-contiguous loads.
+inline bool wgrad_transposes(int64_t rows, int64_t esize) {
+  return rows >= kTransposeMinRows && rows * esize <= ((int64_t)1 << 23);
+}
 inline int64_t round8(int64_t v) { return (v + 7) / 8 * 8; }
 
 // dst[b, t] = t < L_in ? src[b, t] : 0 for t < L_pad, rows of row_bytes (a

@@ -19,8 +19,9 @@
 // token-major operands as they are, through LDS transpose reads, so no
 // transposed copy of an activation is made. In fp32 those operands are
 // transposed once into workspace when they have kTransposeMinRows rows or
-// more (the transpose of the output-gradient operand also leaves the bias
-// column sums), and read through the register-transposing GEMM below that.
+// more and a transposed row of them spans at most 8 MiB (the transpose of the
+// output-gradient operand also leaves the bias column sums), and read through
+// the register-transposing GEMM otherwise.
 #include <algorithm>
 
 #include "attention.hpp"
@@ -478,14 +479,15 @@ static void wgrad(Runner& run, const char* label, const T* a, int64_t lda, const
     run.gemm<T, LAYOUT_MN, LAYOUT_MN>(label, pr, EpiF32{out, ldo, 0});
     return;
   }
-  if (out && rows >= kTransposeMinRows && !a_t) {
+  const bool tr = wgrad_transposes(rows, sizeof(T));
+  if (out && tr && !a_t) {
     transpose<T>(run, "transpose", a, lda, rows, M, tr_a, round8(rows), db ? part : nullptr);
     if (db) colsum_final(run, "bias_colsum", rows, M, part, part2, db);
   } else if (db) {
     colsum<T>(run, "bias_colsum", a, rows, M, lda, part, db);
   }
   if (!out) return;
-  if (rows >= kTransposeMinRows) {
+  if (tr) {
     const int64_t ldt = round8(rows);
     transpose<T>(run, "transpose", b, ldb, rows, N, tr_b, ldt);
     pr.a = tr_a;

@@ -242,6 +242,9 @@ int layer_dims(const pf_layer_config* c, LayerDims* d, const char** why) {
       return *why = "a grouped row k_j * d_{j-1} * element size exceeds 8 MiB", PF_ERR_UNSUPPORTED;
   if ((int64_t)2 * d->d_f * d->esize > kMaxGemmRowBytes)
     return *why = "2 * d_fine * element size exceeds 8 MiB", PF_ERR_UNSUPPORTED;
+  // the projections read H with its low part beside it ([H_hi | H_lo] rows)
+  if ((int64_t)2 * d->d_p * d->esize > kMaxGemmRowBytes)
+    return *why = "2 * d_proxy * element size exceeds 8 MiB", PF_ERR_UNSUPPORTED;
   if (d->dh != 64 && d->dh != 128) return *why = "head_dim must be 64 or 128", PF_ERR_UNSUPPORTED;
   d->fused_gate = c->gate_fusion == PF_GATE_FUSED && d->esize == 2 && c->injection == PF_INJECT_GATED &&
                   fused_gate_supported(d->d_f, d->d[1]);
@@ -342,7 +345,7 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     // when the column sums come out of a transpose
     size_t part = (size_t)kColsumChunks * widest;
     auto tp = [&](int64_t rows, int64_t cols) {
-      if (rows >= kTransposeMinRows) part = std::max(part, (size_t)((rows + 63) / 64 * cols));
+      if (wgrad_transposes(rows, es)) part = std::max(part, (size_t)((rows + 63) / 64 * cols));
     };
     tp((int64_t)d.B * d.L, d.d_f);
     for (int j = 0; j < d.M; ++j) {
@@ -356,7 +359,7 @@ LayerWs layer_ws_layout(const LayerDims& d, bool bwd) {
     // most [B*L, d_f] elements (plus row padding to a multiple of 8)
     size_t tr = 0, trw = 0;
     auto op = [&](int64_t rows, int64_t cols) {
-      if (rows >= kTransposeMinRows) tr = std::max(tr, (size_t)(round8(rows) * cols) * es);
+      if (wgrad_transposes(rows, es)) tr = std::max(tr, (size_t)(round8(rows) * cols) * es);
     };
     auto wt = [&](int64_t out, int64_t in) { trw = std::max(trw, (size_t)(out * in) * es); };
     op((int64_t)d.B * d.L, d.d_f);

@@ -125,6 +125,21 @@ def test_grouped_rows_beyond_the_gemm_range_are_rejected(lib):
         assert B.layer_workspace_size(cfg) == 0 and B.layer_saved_size(cfg) == 0
 
 
+def test_proxy_rows_beyond_the_gemm_range_are_rejected(lib):
+    """The projections read H with its low part beside it, rows of
+    2 * d_proxy elements, under the same 8 MiB row limit: 8,192 heads of 128
+    in fp32 (exactly 8 MiB) fit; one more head does not, nor 16,385 heads of
+    128 in bf16."""
+    ok = _cfg(seq_len=64, d_proxy=8192 * 128, n_heads=8192, head_dim=128, dtype="fp32")
+    assert B.layer_workspace_size(ok) > 0
+    for bad in (dict(seq_len=64, d_proxy=8193 * 128, n_heads=8193, head_dim=128, dtype="fp32"),
+                dict(seq_len=64, d_proxy=16385 * 128, n_heads=16385, head_dim=128)):
+        cfg = _cfg(**bad)
+        assert _fwd(lib, cfg, _weights_struct(1)) == B.PF_ERR_UNSUPPORTED, bad
+        assert "d_proxy" in B.last_error() and "8 MiB" in B.last_error(), bad
+        assert B.layer_workspace_size(cfg) == 0 and B.layer_saved_size(cfg) == 0
+
+
 def test_plain_bf16_precision_drops_the_low_parts(lib):
     # the low parts of H, Q and K (and the doubled K of the Q/K GEMMs) exist
     # only with PF_PRECISION_EXTENDED in bf16 mode

@@ -131,6 +131,9 @@ CASES = {
     # d_fine a multiple of 8 but not of the K tile: the [X | Delta] split inside a K tile
     "bf16_odd_width": (LayerShape(2, 16 * 37, 72, 128, 2, 64, (16,)), True),
     "fp32_odd_width": (LayerShape(1, 16 * 37, 40, 128, 2, 64, (16,), dtype="fp32"), True),
+    # fp32 over 16,384 token rows and 8,192 level-1 rows: the weight gradients run on
+    # transposed (K-contiguous) copies of their operands
+    "fp32_transposed_wgrad": (LayerShape(1, 16384, 64, 128, 2, 64, (2, 8), level_dims=(96,), dtype="fp32"), True),
 }
 
 
@@ -154,6 +157,25 @@ def test_backward_parity_small(gpu, name):
     ref = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask,
                                 inp["h_in"], dh_out, injection=shape.injection)
     compare(shape, inp, res, ref, name)
+
+
+@pytest.mark.timeout(300)
+def test_backward_parity_fp32_token_rows_past_the_transposes(gpu):
+    """fp32 over 2 x 1,050,624 tokens: the gate's weight and bias gradients
+    reduce over 2,101,248 token rows, whose transposed rows would pass the
+    8 MiB operand-row limit, so they read the token-major operands as they
+    are (K of two million rows); the level rows (8,208) still take the
+    transposed copies. Every gradient compared; the oracle takes seconds."""
+    shape = LayerShape(2, 1050624, 8, 64, 1, 64, (256,), dtype="fp32")
+    print(f"[fp32 2.1M token rows] {shape}", flush=True)
+    inp = synth.layer_inputs(shape, 77, with_dy=True, with_h_in=True)
+    for key in ("q", "k"):
+        wq, bq = inp["weights"][key]
+        inp["weights"][key] = (wq * 4, bq)
+    res = run_gpu_backward(shape, inp)
+    ref = oracle.layer_backward(inp["x"], inp["weights"], shape.factors, shape.n_heads, inp["dy"], shape.mask,
+                                inp["h_in"], None)
+    compare(shape, inp, res, ref, "fp32_2.1M_rows")
 
 
 def test_backward_parity_factorised_workload_reduced_L(gpu):
