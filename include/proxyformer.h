@@ -120,10 +120,10 @@ typedef struct {
  *  n_levels  M in 1..4; factors[0..M-1] = k_1..k_M, P = prod k_j.
  *  level_dims[j] = d_{j+1} for j < M-1 (0 -> d_proxy); level_dims[M-1] is
  *            ignored (d_M = d_proxy). Every width is a multiple of 8, and a
- *            level's grouped row of k_j * d_{j-1} elements spans at most
- *            8 MiB (bf16: k_j * d_{j-1} <= 4M); larger rows return
- *            PF_ERR_UNSUPPORTED (a GEMM tile addresses 256 rows through one
- *            32-bit range).
+ *            level's grouped row of k_j * d_{j-1} elements, 2 * d_fine and
+ *            2 * d_proxy elements each span at most 8 MiB (bf16:
+ *            k_j * d_{j-1} <= 4M); larger rows return PF_ERR_UNSUPPORTED (a
+ *            GEMM tile addresses 256 rows through one 32-bit range).
  *  head_dim  64 or 128.
  *  dtype     pf_dtype; mask pf_mask; injection pf_injection;
  *            precision pf_precision (bf16 mode); gate_fusion pf_gate_fusion.
