@@ -311,6 +311,11 @@ def _attention_backward(q, k, v, o, do, n_heads, mask):
     With P = softmax(S), S = Q K^T / sqrt(d_head) + M: dV = P^T dO,
     dP = dO V^T, dS = P * (dP - rowsum(dO * O)), dQ = dS K / sqrt(d_head),
     dK = dS^T Q / sqrt(d_head).
+
+    Also returns the magnitudes of the terms that cancel in dS carried to
+    dQ and dK: with |dS| := P * (|dP| + |rowsum(dO * O)|), |dQ| = |dS| |K|
+    / sqrt(d_head) and |dK| = |dS|^T |Q| / sqrt(d_head) (entrywise
+    absolute values; upper bounds of |dQ| and |dK|).
     """
     m, d = q.shape
     dh = d // n_heads
@@ -318,6 +323,8 @@ def _attention_backward(q, k, v, o, do, n_heads, mask):
     dq = np.zeros_like(q)
     dk = np.zeros_like(k)
     dv = np.zeros_like(v)
+    dq_abs = np.zeros_like(q)
+    dk_abs = np.zeros_like(k)
     for h in range(n_heads):
         cs = slice(h * dh, (h + 1) * dh)
         sc = (q[:, cs] @ k[:, cs].T) * scale
@@ -328,10 +335,14 @@ def _attention_backward(q, k, v, o, do, n_heads, mask):
         p /= p.sum(axis=1, keepdims=True)
         dv[:, cs] = p.T @ do[:, cs]
         dp = do[:, cs] @ v[:, cs].T
-        dsm = p * (dp - np.sum(do[:, cs] * o[:, cs], axis=1, keepdims=True))
+        rs = np.sum(do[:, cs] * o[:, cs], axis=1, keepdims=True)
+        dsm = p * (dp - rs)
         dq[:, cs] = (dsm @ k[:, cs]) * scale
         dk[:, cs] = (dsm.T @ q[:, cs]) * scale
-    return dq, dk, dv
+        dsm_abs = p * (np.abs(dp) + np.abs(rs))
+        dq_abs[:, cs] = (dsm_abs @ np.abs(k[:, cs])) * scale
+        dk_abs[:, cs] = (dsm_abs.T @ np.abs(q[:, cs])) * scale
+    return dq, dk, dv, dq_abs, dk_abs
 
 
 def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
@@ -345,6 +356,10 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
     the projections Q, K, V per proxy ("proj_grads", [B, m, d_proxy] each),
     and for the gated injections the per-column sums over tokens of |dG|
     ("gate_abs"), the magnitude of the terms the gate bias gradient sums.
+    "score_abs" holds, for the Q and K maps, entrywise bounds of their weight
+    and bias gradients built from the magnitudes of the terms that cancel in
+    the score gradient dS: the scale against which a gradient that cancels
+    to zero (one visible key per row, where a softmax is constant) is measured.
     """
     dy = _f64(dy)
     bsz, seq, d_f = dy.shape
@@ -376,6 +391,9 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
     d_p = weights["q"][0].shape[0]
     dh_in = None if h_in is None else np.zeros((bsz, m, d_p))
     proj_grads = {name: np.zeros((bsz, m, d_p)) for name in ("q", "k", "v")}
+    # entrywise bounds of the Q and K weight and bias gradients from the
+    # magnitudes of the terms that cancel in dS (see _attention_backward)
+    score_abs = {name: [np.zeros_like(gr[name][0]), np.zeros_like(gr[name][1])] for name in ("q", "k")}
     # per gate column, the sum over tokens of |dG|: the scale of the terms the
     # gate's bias gradient adds up (its accuracy is relative to this scale)
     gate_abs = np.zeros(_f64(weights["gate"][0]).shape[0]) if gr["gate"] is not None else None
@@ -437,13 +455,16 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
         gr["o"][0] += dhbar.T @ kp["o"]
         gr["o"][1] += dhbar.sum(axis=0)
         do = dhbar @ _f64(weights["o"][0])
-        dq, dk, dv = _attention_backward(kp["q"], kp["k"], kp["v"], kp["o"], do, n_heads, mask)
+        dq, dk, dv, dq_abs, dk_abs = _attention_backward(kp["q"], kp["k"], kp["v"], kp["o"], do, n_heads, mask)
         dh = np.zeros_like(kp["h"]) if dh_out is None else _f64(dh_out)[b].copy()
         for name, dz in (("q", dq), ("k", dk), ("v", dv)):
             proj_grads[name][b] = dz
             gr[name][0] += dz.T @ kp["h"]
             gr[name][1] += dz.sum(axis=0)
             dh += dz @ _f64(weights[name][0])
+        for name, dz_abs in (("q", dq_abs), ("k", dk_abs)):
+            score_abs[name][0] += dz_abs.T @ np.abs(kp["h"])
+            score_abs[name][1] += dz_abs.sum(axis=0)
         if dh_in is not None:
             dh_in[b] = dh
         # Eq. 8 passes dH to c unchanged; then Eq. 16 in reverse, level M..1
@@ -455,7 +476,8 @@ def layer_backward(x, weights, factors: Sequence[int], n_heads: int, dy,
             dz = ungroup_rows(dz @ _f64(weights["compress"][j][0]), factors[j])
         dx[b] = dxb + dz
     return {"dx": dx, "dh_in": dh_in, "grads": gr, "proj_grads": proj_grads,
-            "gate_abs": gate_abs if injection in (INJECT_GATED, INJECT_GATED_HEAD) else None}
+            "gate_abs": gate_abs if injection in (INJECT_GATED, INJECT_GATED_HEAD) else None,
+            "score_abs": score_abs}
 
 
 def patch_order(height: int, width: int, p: int):

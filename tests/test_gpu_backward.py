@@ -42,7 +42,10 @@ def compare(shape, inp, res, ref, label):
     max_c sum_rows |dK[row, c]| (oracle), instead of its own ~0 magnitude.
     The per-head gate's bias gradient (n_heads columns, each a sum of
     cancelling terms over every token) is measured the same way, against
-    max_c sum_rows |dG[row, c]|.
+    max_c sum_rows |dG[row, c]|. With a single proxy the Q and K weight and
+    bias gradients are zero (a softmax over one key is constant) and are
+    measured against the oracle's bounds built from the terms that cancel
+    in dS ("score_abs").
     """
     from helpers import TOL
     dx, dh_in, grads = res
@@ -66,6 +69,14 @@ def compare(shape, inp, res, ref, label):
     for name in ("q", "k", "v", "o", "gate", "affine"):
         if rg.get(name) is None:  # the gate (or the affine map) only with its injection mode
             assert grads.get(name) is None
+            continue
+        if name in ("q", "k") and shape.n_proxies == 1:
+            # one proxy: every row's softmax has one key and is constant, so the Q and K maps get
+            # no gradient; what is left on either side is rounding of the terms that cancel in
+            # dS, measured against their magnitude
+            sa = ref["score_abs"][name]
+            chk(host(grads[name][0]), rg[name][0], f"dW_{name}", float(np.max(sa[0])))
+            chk(host(grads[name][1]), rg[name][1], f"db_{name}", float(np.max(sa[1])))
             continue
         chk(host(grads[name][0]), rg[name][0], f"dW_{name}")
         if name == "k":
@@ -131,6 +142,11 @@ CASES = {
     # d_fine a multiple of 8 but not of the K tile: the [X | Delta] split inside a K tile
     "bf16_odd_width": (LayerShape(2, 16 * 37, 72, 128, 2, 64, (16,)), True),
     "fp32_odd_width": (LayerShape(1, 16 * 37, 40, 128, 2, 64, (16,), dtype="fp32"), True),
+    # one proxy (a full block, and a partial one) in the masks where it feeds its own block: the
+    # Q and K maps get no gradient
+    "bf16_single_proxy_bidirectional": (LayerShape(2, 5, 80, 192, 3, 64, (8,), mask=synth.BIDIRECTIONAL), True),
+    "fp32_single_proxy_block_causal": (LayerShape(1, 8, 64, 128, 1, 128, (2, 4), level_dims=(96,),
+                                                  mask=synth.BLOCK_CAUSAL, dtype="fp32"), True),
     # fp32 over 16,384 token rows and 8,192 level-1 rows: the weight gradients run on
     # transposed (K-contiguous) copies of their operands
     "fp32_transposed_wgrad": (LayerShape(1, 16384, 64, 128, 2, 64, (2, 8), level_dims=(96,), dtype="fp32"), True),

@@ -187,6 +187,52 @@ def test_key_bias_gradient_vanishes():
         np.testing.assert_allclose(res["grads"]["k"][1], res["proj_grads"]["k"].sum(axis=(0, 1)), atol=1e-14)
 
 
+
+def test_score_gradient_bounds():
+    """score_abs bounds the Q and K weight and bias gradients entrywise (the
+    triangle inequality over the terms of dS and of the products after it),
+    in every mask, and is of the gradients' own order where they do not
+    cancel (the weight gradients here)."""
+    rng = np.random.default_rng(33)
+    d_f, d_p, nh, L = 4, 6, 2, 24
+    w = rand_weights(rng, d_f, d_p, (4,), std=0.5)
+    x = rng.standard_normal((2, L, d_f))
+    dy = rng.standard_normal((2, L, d_f))
+    for mask in (0, 1, 2):
+        res = oracle.layer_backward(x, w, (4,), nh, dy, mask)
+        for name in ("q", "k"):
+            for i in (0, 1):
+                g, bound = np.abs(res["grads"][name][i]), res["score_abs"][name][i]
+                assert np.all(g <= bound * (1 + 1e-12) + 1e-15), (mask, name, i)
+            assert np.max(np.abs(res["grads"][name][0])) > 1e-2 * np.max(res["score_abs"][name][0]), (mask, name)
+
+
+@pytest.mark.parametrize("mask", [oracle.BLOCK_CAUSAL, oracle.BIDIRECTIONAL])
+@pytest.mark.parametrize("L", [8, 5])
+def test_single_proxy_score_gradients_vanish(mask, L):
+    """One proxy (L <= P = 8): every attention row sees one key, and a
+    softmax over one key is constant (Eq. 9), so the loss does not depend on
+    W_q, b_q, W_k, b_k. Central differences in those weights are zero; the
+    oracle's gradients are zero up to rounding, against a score_abs that is
+    not (in these masks the proxy feeds its own block, so dO != 0)."""
+    rng = np.random.default_rng(34 + L + mask)
+    d_f, d_p, nh = 4, 6, 2
+    w = rand_weights(rng, d_f, d_p, (8,), std=0.5)
+    x = rng.standard_normal((1, L, d_f))
+    dy = rng.standard_normal((1, L, d_f))
+    res = oracle.layer_backward(x, w, (8,), nh, dy, mask)
+    eps = 1e-4
+    for name in ("q", "k"):
+        for i in (0, 1):
+            path = ((name, i),)
+            v = rng.standard_normal(np.shape(_get(w, path)))
+            num = (_loss(x, _set(w, path, _get(w, path) + eps * v), (8,), nh, mask, None, dy, None)
+                   - _loss(x, _set(w, path, _get(w, path) - eps * v), (8,), nh, mask, None, dy, None)) / (2 * eps)
+            assert abs(num) < 1e-9, (name, i, num)
+            scale = np.max(res["score_abs"][name][i])
+            assert scale > 1e-3, (name, i)
+            assert np.max(np.abs(res["grads"][name][i])) < 1e-12 * scale, (name, i)
+
 @pytest.mark.parametrize("mask", [oracle.TOKEN_CAUSAL, oracle.BIDIRECTIONAL])
 def test_backward_finite_differences_partial_last_block(mask):
     """L % P != 0: the zero-padded last block (Sec. 3.1) in the backward."""
